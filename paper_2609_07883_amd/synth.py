@@ -1,0 +1,131 @@
+"""Seeded synthetic inputs for the mixed iteration.
+
+This module only draws random numbers and rounds them to bf16; it holds none
+of the method's arithmetic.  Tests, the benchmark and the smoke check call it
+to make the inputs that both the HIP path and the reference oracle consume.
+
+Recipe (all numpy PCG64 ``default_rng``):
+  * weights of layer l: seed ``weight_seed + 1000 * l``; linear weights
+    N(0, 0.02), norm gains 1 + N(0, 0.02), drawn in the order
+    Wqkv, Wo, Wgu, Wd, g1, g2 as float32 and rounded to bf16 (RNE);
+  * a "sharp" variant draws the q and k rows of Wqkv at std 0.16 so that
+    attention is far from uniform;
+  * token embeddings (the iteration's input rows): N(0, 1), bf16;
+  * pre-existing cached K/V (decode contexts, prefill prefixes): N(0, 1),
+    bf16, one independent stream per (layer, sequence);
+  * context and prompt lengths: uniform or clipped log-normal integers.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+def bf16_bits(a) -> np.ndarray:
+    """Round float32 values to bf16 (round to nearest, ties to even); returns uint16 bits."""
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    u = a.view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
+    nan = np.isnan(a)
+    if nan.any():
+        r[nan] = 0x7FC0
+    return r
+
+
+def bf16_to_f64(bits) -> np.ndarray:
+    """Exact float64 value of bf16 bit patterns."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def round_bf16(a) -> tuple[np.ndarray, np.ndarray]:
+    """(bits, exact float64 values) of a rounded to bf16."""
+    bits = bf16_bits(a)
+    return bits, bf16_to_f64(bits)
+
+
+@dataclass(frozen=True)
+class ModelShape:
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn_dim: int
+    rms_eps: float = 1e-5
+    rope_theta: float = 10000.0
+    block_size: int = 16
+    max_pos: int = 32768
+
+
+TINY = ModelShape(n_layers=1, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64,
+                  ffn_dim=704, rms_eps=1e-5, rope_theta=10000.0, max_pos=4096)
+LLAMA8B_LAYER = ModelShape(n_layers=1, d_model=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                           ffn_dim=14336, rms_eps=1e-5, rope_theta=500000.0, max_pos=32768)
+
+
+def with_layers(shape: ModelShape, n_layers: int) -> ModelShape:
+    return ModelShape(n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                      shape.ffn_dim, shape.rms_eps, shape.rope_theta, shape.block_size,
+                      shape.max_pos)
+
+
+@dataclass
+class LayerBits:
+    """bf16 bit patterns of one layer's weights (row-major [out][in])."""
+
+    wqkv: np.ndarray
+    wo: np.ndarray
+    wgu: np.ndarray
+    wd: np.ndarray
+    g1: np.ndarray
+    g2: np.ndarray
+
+    def as_f64(self) -> dict:
+        return {k: bf16_to_f64(getattr(self, k)) for k in ("wqkv", "wo", "wgu", "wd", "g1", "g2")}
+
+
+def layer_weights(shape: ModelShape, layer: int = 0, weight_seed: int = 0,
+                  std: float = 0.02, qk_std: float | None = None) -> LayerBits:
+    rng = np.random.default_rng(weight_seed + 1000 * layer)
+    d, hq, hkv, hd, f = (shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                         shape.ffn_dim)
+    nqkv = (hq + 2 * hkv) * hd
+    wqkv = rng.standard_normal((nqkv, d), dtype=np.float32) * np.float32(std)
+    if qk_std is not None:
+        wqkv[: (hq + hkv) * hd] *= np.float32(qk_std / std)
+    wo = rng.standard_normal((d, hq * hd), dtype=np.float32) * np.float32(std)
+    wgu = rng.standard_normal((2 * f, d), dtype=np.float32) * np.float32(std)
+    wd = rng.standard_normal((d, f), dtype=np.float32) * np.float32(std)
+    g1 = 1.0 + rng.standard_normal(d, dtype=np.float32) * np.float32(std)
+    g2 = 1.0 + rng.standard_normal(d, dtype=np.float32) * np.float32(std)
+    return LayerBits(bf16_bits(wqkv), bf16_bits(wo), bf16_bits(wgu), bf16_bits(wd),
+                     bf16_bits(g1), bf16_bits(g2))
+
+
+def embeddings(rows: int, d: int, seed: int = 1, stream: int = 0) -> np.ndarray:
+    """bf16 bits of N(0,1) input rows."""
+    rng = np.random.default_rng([seed, stream])
+    return bf16_bits(rng.standard_normal((rows, d), dtype=np.float32))
+
+
+def cached_kv(length: int, n_kv_heads: int, head_dim: int, seed: int, layer: int, seq: int):
+    """bf16 bits of N(0,1) K and V, [length][Hkv][hd] each, for a pre-existing context."""
+    rng = np.random.default_rng([seed, layer, seq])
+    k = rng.standard_normal((length, n_kv_heads, head_dim), dtype=np.float32)
+    v = rng.standard_normal((length, n_kv_heads, head_dim), dtype=np.float32)
+    return bf16_bits(k), bf16_bits(v)
+
+
+def uniform_lengths(n: int, lo: int, hi: int, seed: int = 2) -> np.ndarray:
+    """n integers uniform in [lo, hi] (inclusive)."""
+    return np.random.default_rng(seed).integers(lo, hi + 1, size=n).astype(np.int64)
+
+
+def lognormal_lengths(n: int, median: float, sigma: float, cap: int, seed: int = 2,
+                      floor: int = 1) -> np.ndarray:
+    """n integers min(cap, max(floor, round(median * exp(sigma z))))."""
+    z = np.random.default_rng(seed).standard_normal(n)
+    return np.clip(np.rint(median * np.exp(sigma * z)), floor, cap).astype(np.int64)

@@ -1,0 +1,233 @@
+"""Pins for the controller, cost-table and block-manager oracles (CPU only).
+
+Pinned against: the analytic cost model's closed-form chunk choices
+(tests/golden/analytic_cost_model.txt, Sec. 4.1 and Eq. 1), a brute-force
+linear scan of Eq. 1, Proposition 1's safety and maximality, numpy's
+nearest-rank ("inverted_cdf") percentile and running maximum, exact rational
+interpolation, and a hand-worked allocation scenario
+(tests/golden/block_manager_scenario.txt).
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import paging, schedule as S
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    rows = []
+    with open(os.path.join(GOLD, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                rows.append(line.split())
+    return rows
+
+
+def test_analytic_model_matches_paper_coefficients_and_values():
+    rows = _golden("analytic_cost_model.txt")
+    coeff = [int(v) for v in next(r for r in rows if r[0] == "coeff")[1:]]
+    assert coeff == [350000, 900000, 55000, 400000, 6000]
+    for r in rows:
+        if r[0] == "value":
+            n, c, t = map(int, r[1:])
+            assert S.analytic_cost_ns(n, c) == t
+
+
+def _closed_form(n, budget, c_max, remaining):
+    t0 = S.analytic_cost_ns(n, 0)
+    if n == 0:
+        return min(c_max, remaining)
+    if S.analytic_cost_ns(n, 1) > budget:
+        return 0
+    return max(0, min(c_max, remaining, (budget - t0 - 400_000) // 6_000))
+
+
+def test_select_chunk_worked_examples():
+    for r in _golden("analytic_cost_model.txt"):
+        if r[0] != "choice":
+            continue
+        n, budget, want = map(int, r[1:])
+        now = 1_000_000_000
+        deadlines = [now + budget + 7 * i for i in range(n)]   # earliest one binds
+        c, flags, _ = S.select_chunk(S.analytic_cost_ns, deadlines, now, 100_000, 4096)
+        assert c == want == _closed_form(n, budget, 4096, 100_000)
+        if want == 0:
+            assert flags & S.DECODE_INFEASIBLE
+
+
+@settings(max_examples=300, deadline=None)
+@given(n=st.integers(0, 300), budget=st.integers(-1_000_000, 60_000_000),
+       c_max=st.integers(0, 5000), remaining=st.integers(-3, 9000), margin=st.integers(0, 2_000_000))
+def test_select_chunk_equals_brute_force_and_closed_form(n, budget, c_max, remaining, margin):
+    now = 5_000_000
+    deadlines = [now + budget + 1000 * i for i in range(n)]
+    c, flags, lookups = S.select_chunk(S.analytic_cost_ns, deadlines, now, remaining, c_max, margin)
+    if remaining <= 0:
+        assert (c, flags) == (0, S.NO_PENDING)
+        return
+    cap = min(c_max, remaining)
+    if n == 0:
+        assert c == cap and flags & S.NO_ACTIVE
+        return
+    feasible = [x for x in range(cap + 1) if S.analytic_cost_ns(n, x) + margin <= budget]
+    brute = max(feasible) if feasible else 0
+    assert c == brute
+    assert c == _closed_form(n, budget - margin, c_max, remaining)
+    # Proposition 1: safe when decode-only is feasible, and maximal
+    if S.analytic_cost_ns(n, 0) + margin <= budget:
+        assert S.analytic_cost_ns(n, c) + margin <= budget
+        assert c == cap or S.analytic_cost_ns(n, c + 1) + margin > budget
+        assert not flags & S.DECODE_INFEASIBLE
+    else:
+        assert c == 0 and flags & S.DECODE_INFEASIBLE
+    assert lookups <= math.ceil(math.log2(cap + 1)) + 1
+
+
+def test_nearest_rank_matches_numpy_inverted_cdf():
+    rng = np.random.default_rng(0)
+    for k in [1, 2, 3, 7, 99, 100, 101, 250]:
+        xs = rng.integers(0, 10**9, size=k)
+        for num, den in [(1, 2), (99, 100), (9, 10), (1, 1)]:
+            ref = np.percentile(xs, 100.0 * num / den, method="inverted_cdf")
+            assert S.nearest_rank(xs, num, den) == int(ref)
+
+
+def test_cummax_matches_numpy():
+    rng = np.random.default_rng(1)
+    row = rng.integers(0, 100, size=50)
+    assert S.cummax(list(row)) == list(np.maximum.accumulate(row))
+
+
+def _random_table(rng, nb=4, nc=6, reps=5):
+    c_grid = [0] + sorted(rng.choice(np.arange(1, 5000), size=nc - 1, replace=False).tolist())
+    b_grid = sorted(rng.choice(np.arange(0, 300), size=nb, replace=False).tolist())
+    samples = rng.integers(1_000_000, 30_000_000, size=(nb, nc, reps)).tolist()
+    return S.CostTable(c_grid, b_grid, samples)
+
+
+def test_table_lookup_interpolates_with_ceiling_exactly():
+    rng = np.random.default_rng(2)
+    for _ in range(20):
+        t = _random_table(rng)
+        for i, b in enumerate(t.b_grid):
+            row = t.t_hat[i]
+            assert t.lookup(b, 0) == row[0]
+            for j in range(1, len(t.c_grid)):
+                assert t.lookup(b, t.c_grid[j]) == row[j]
+            for c in rng.integers(1, t.c_grid[-1] + 1, size=40):
+                c = int(c)
+                j = next(j for j in range(1, len(t.c_grid)) if t.c_grid[j] >= c)
+                if j == 1:
+                    want = row[1]
+                else:
+                    frac = Fraction(row[j] - row[j - 1]) * (c - t.c_grid[j - 1]) / (
+                        t.c_grid[j] - t.c_grid[j - 1])
+                    want = row[j - 1] + math.ceil(frac)
+                assert t.lookup(b, c) == want
+            vals = [t.lookup(b, c) for c in range(0, t.c_grid[-1] + 1, 7)]
+            assert all(x <= y for x, y in zip(vals, vals[1:]))       # monotone in c
+        # n rounds up to the next grid point
+        for n in range(0, t.b_grid[-1] + 1, 13):
+            i = next(i for i, b in enumerate(t.b_grid) if b >= n)
+            assert t.lookup(n, 0) == t.t_hat[i][0]
+        with pytest.raises(IndexError):
+            t.lookup(t.b_grid[-1] + 1, 0)
+
+
+def test_table_statistics_from_samples():
+    rng = np.random.default_rng(3)
+    t = _random_table(rng, reps=100)
+    for i in range(len(t.b_grid)):
+        for j in range(len(t.c_grid)):
+            xs = np.sort(t.samples[i][j])
+            assert t.p99[i][j] == xs[98] and t.p50[i][j] == xs[49]
+        assert t.t_hat[i] == list(np.maximum.accumulate(t.p99[i]))
+
+
+def test_select_over_table_caps_at_grid_and_matches_scan():
+    rng = np.random.default_rng(4)
+    for _ in range(30):
+        t = _random_table(rng)
+        n = int(rng.integers(1, t.b_grid[-1] + 1)) if t.b_grid[-1] > 0 else 0
+        now = 0
+        budget = int(rng.integers(0, 40_000_000))
+        c_max = int(rng.integers(0, 6000))
+        rem = int(rng.integers(1, 6000))
+        c, flags, _ = S.select_chunk_table(t, [budget] * n, now, rem, c_max)
+        cap = min(c_max, rem, t.c_grid[-1])
+        if n == 0:
+            assert c == cap
+            continue
+        feas = [x for x in range(cap + 1) if t.lookup(n, x) <= budget]
+        assert c == (max(feas) if feas else 0)
+        assert bool(flags & S.CAPPED_BY_GRID) == (t.c_grid[-1] < min(c_max, rem))
+
+
+def test_block_manager_hand_worked_scenario():
+    m = paging.BlockManager(8, 16)
+    for r in _golden("block_manager_scenario.txt"):
+        op = r[0]
+        if op == "create":
+            m.create(int(r[1]))
+        elif op == "reserve":
+            try:
+                m.reserve(int(r[1]), int(r[2]))
+                last_enomem = False
+            except paging.OutOfBlocks:
+                last_enomem = True
+        elif op == "enomem":
+            assert last_enomem
+        elif op == "expect":
+            assert m.block_table(int(r[1])) == [int(v) for v in r[2:]]
+        elif op == "free":
+            m.free(int(r[1]))
+        elif op == "slot":
+            assert m.slot(int(r[1]), int(r[2])) == int(r[3])
+
+
+@settings(max_examples=100, deadline=None)
+@given(st.lists(st.tuples(st.sampled_from(["create", "reserve", "free"]), st.integers(0, 5),
+                          st.integers(0, 120)), max_size=60))
+def test_block_manager_invariants(ops):
+    m = paging.BlockManager(20, 16)
+    live = set()
+    for op, sid, n in ops:
+        if op == "create" and sid not in live:
+            m.create(sid)
+            live.add(sid)
+        elif op == "reserve" and sid in live:
+            before = {s: m.block_table(s) for s in live}
+            free_before = m.free_count()
+            try:
+                m.reserve(sid, n)
+            except paging.OutOfBlocks:
+                assert {s: m.block_table(s) for s in live} == before
+                assert m.free_count() == free_before
+        elif op == "free" and sid in live:
+            m.free(sid)
+            live.discard(sid)
+        used = [b for s in live for b in m.block_table(s)]
+        assert len(used) == len(set(used))                      # no block shared
+        assert len(used) + m.free_count() == 20
+        for s in live:
+            assert len(m.block_table(s)) == -(-m.reserved(s) // 16)
+
+
+def test_iteration_metadata_all_or_nothing():
+    m = paging.BlockManager(4, 16)
+    for s in (1, 2, 3):
+        m.create(s)
+    m.reserve(2, 16)
+    m.reserve(3, 16)
+    with pytest.raises(paging.OutOfBlocks):
+        paging.iteration_metadata(m, 40, 1, 0, [2, 3], [16, 16])  # needs 3 + 1 + 1 > 2 free
+    assert m.block_table(1) == [] and m.free_count() == 2
+    slots, tables = paging.iteration_metadata(m, 10, 1, 0, [2], [15])
+    assert tables[1] == [2] and slots == [32 + j for j in range(10)] + [0 * 16 + 15]
