@@ -171,8 +171,12 @@ def select_chunk(predict, deadlines_ns, now_ns: int, remaining: int, c_max: int,
 
 
 def select_chunk_table(table: CostTable, deadlines_ns, now_ns, remaining, c_max, margin_ns=0):
-    """Alg. 1 over a measured table (the capped, interpolated lookup)."""
-    if len(deadlines_ns) > 0:
+    """Alg. 1 over a measured table (the capped, interpolated lookup).
+
+    Alg. 1 returns before any cost query when nothing is pending or nothing
+    is active; only then can the decode count fall outside the table.
+    """
+    if remaining > 0 and len(deadlines_ns) > 0:
         table.row_for(len(deadlines_ns))          # raises for n above the grid
     return select_chunk(table.lookup, deadlines_ns, now_ns, remaining, c_max, margin_ns,
                         c_last=table.c_grid[-1])
