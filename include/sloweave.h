@@ -1,0 +1,292 @@
+/*
+ * sloweave.h -- C ABI of libsloweave.so, an MI355X (gfx950) implementation of
+ * the mixed prefill+decode iteration that SLOWeave schedules (arXiv
+ * 2609.07883), the profiler that prices it, and the controller that sizes
+ * each iteration's prefill chunk.
+ *
+ * Conventions
+ *   - Every call returns SLW_OK (0) or a negative SLW_E* code; the message of
+ *     the last failure on the calling thread is returned by slw_last_error().
+ *     No C++ exception crosses this boundary.
+ *   - "device" pointers are HIP device memory on the current device; "host"
+ *     pointers are ordinary CPU memory.  The library never allocates device
+ *     memory: weights, KV pools, activations and the workspace all belong to
+ *     the caller.  It owns only host state (sequence tables, cost tables) plus
+ *     a small pinned host staging ring and HIP events, created on first use.
+ *   - Streams are passed as void* holding a hipStream_t (NULL = the null
+ *     stream).  Device work is enqueued asynchronously; kernel faults surface
+ *     at the caller's next synchronisation.
+ *   - bf16 is the 16-bit brain-float format stored as uint16 bit patterns.
+ *   - A context is not thread-safe; slw_select_chunk and the cost-table
+ *     queries are pure and may be called from any thread.
+ */
+#ifndef SLOWEAVE_H
+#define SLOWEAVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SLW_OK 0
+#define SLW_EINVAL (-1)       /* bad argument or inconsistent state            */
+#define SLW_ERANGE (-2)       /* argument outside a grid or a capacity          */
+#define SLW_ENOMEM (-3)       /* KV block pool or workspace too small           */
+#define SLW_EHIP (-4)         /* a HIP runtime call failed                      */
+#define SLW_EUNSUPPORTED (-5) /* shape outside what the kernels implement      */
+
+/* flags reported by slw_select_chunk */
+#define SLW_FLAG_NO_PENDING 1u         /* no pending prefill: chunk 0          */
+#define SLW_FLAG_NO_ACTIVE 2u          /* empty active set: chunk = cap        */
+#define SLW_FLAG_DECODE_INFEASIBLE 4u  /* even a decode-only iteration misses  */
+#define SLW_FLAG_CAPPED_BY_GRID 8u     /* cap lowered to the last profiled C   */
+
+typedef struct slw_ctx slw_ctx;
+typedef struct slw_cost_table slw_cost_table;
+
+/* Thread-local message describing the last failure ("" if none). */
+const char* slw_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* Model                                                                     */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Shape of the decoder stack the iteration runs.  The paper schedules an
+ * unmodified dense decoder (Sec. 5.1, Sec. 5.2); the block is the standard
+ * pre-norm one: RMSNorm, QKV projection, rotate-half RoPE, grouped-query
+ * causal attention over the paged cache, output projection + residual,
+ * RMSNorm, SwiGLU MLP + residual.
+ * Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with group
+ * n_q_heads / n_kv_heads <= 16; d_model and ffn_dim multiples of 64;
+ * block_size == 16; 1 <= max_pos <= 1048576.
+ */
+typedef struct slw_model_cfg {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t ffn_dim;
+    float rms_eps;      /* RMSNorm epsilon                                      */
+    float rope_theta;   /* RoPE base: angle(p, i) = p * theta^(-2i/head_dim)    */
+    int32_t block_size; /* KV positions per block; must be 16                  */
+    int32_t max_pos;    /* largest sequence length any call may reach          */
+} slw_model_cfg;
+
+/*
+ * Device pointers to one layer's bf16 weights, row-major [out][in]:
+ *   wqkv [(Hq + 2 Hkv) * hd][d]   q rows, then k rows, then v rows
+ *   wo   [d][Hq * hd]
+ *   wgu  [2 F][d]                 gate rows, then up rows
+ *   wd   [d][F]
+ *   g1, g2 [d]                    RMSNorm gains (before attention / MLP)
+ * The caller keeps the memory alive while the context uses it.
+ */
+typedef struct slw_layer_weights {
+    const void* wqkv;
+    const void* wo;
+    const void* wgu;
+    const void* wd;
+    const void* g1;
+    const void* g2;
+} slw_layer_weights;
+
+/* Create a context for cfg (host state only; touches no GPU).  *out owns it. */
+int slw_create(const slw_model_cfg* cfg, slw_ctx** out);
+/* Destroy a context (waits for nothing: synchronise your streams first). */
+int slw_destroy(slw_ctx* ctx);
+/* Register layer `layer`'s weights (0 <= layer < n_layers). */
+int slw_set_layer_weights(slw_ctx* ctx, int32_t layer, const slw_layer_weights* w);
+
+/* ------------------------------------------------------------------------ */
+/* Paged KV cache (Table 1, "KV manager": layout unchanged, blocks allocated */
+/* as chunks are processed)                                                  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Attach caller-owned KV pools of num_blocks blocks each (device, bf16):
+ *   k_pool  [n_layers][num_blocks][Hkv][hd/32][16][32]
+ *           element (token t of the block, dim d) at (d/32)*512 + t*32 + d%32
+ *           within the (layer, block, head) page of 16*hd values;
+ *   v_pool  [n_layers][num_blocks][Hkv][hd][16]
+ *           element (t, d) at d*16 + t within the page.
+ * Resets the block manager (all sequences are forgotten).
+ */
+int slw_kv_init(slw_ctx* ctx, void* k_pool, void* v_pool, int32_t num_blocks);
+/* Number of free blocks. */
+int slw_kv_free_blocks(slw_ctx* ctx, int32_t* n_free);
+
+/*
+ * Sequences.  A sequence grows by whole blocks, always taking the
+ * lowest-numbered free block first; slw_seq_reserve(id, n) makes room for
+ * positions 0..n-1 (a no-op if already there).  A reservation the pool cannot
+ * cover returns SLW_ENOMEM and changes nothing.  slw_seq_free returns all the
+ * sequence's blocks.  Ids below -2^62 are reserved for the profiler.
+ */
+int slw_seq_create(slw_ctx* ctx, int64_t id);
+int slw_seq_free(slw_ctx* ctx, int64_t id);
+int slw_seq_reserve(slw_ctx* ctx, int64_t id, int32_t new_len);
+/* Copy the sequence's block table (host int32, at most cap entries) and its length to *n. */
+int slw_seq_block_table(slw_ctx* ctx, int64_t id, int32_t* out, int32_t cap, int32_t* n);
+
+/* ------------------------------------------------------------------------ */
+/* The mixed iteration (Sec. 3: one prefill chunk plus one decode token per */
+/* active request; Sec. 5.1: the chunk rides in ordinary sequence metadata)  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One iteration's batch (host memory):
+ *   C             prefill-chunk tokens (0: decode-only iteration)
+ *   prefill_seq   sequence the chunk belongs to (ignored when C == 0)
+ *   prefix_len    tokens of prefill_seq already cached; the chunk occupies
+ *                 positions prefix_len .. prefix_len + C - 1
+ *   B             decode requests (0: prefill-only iteration)
+ *   decode_seqs   [B] sequence ids, distinct and different from prefill_seq
+ *   context_lens  [B] tokens cached for each decode BEFORE this iteration; the
+ *                 decode token sits at position context_lens[b] and attends to
+ *                 context_lens[b] + 1 keys
+ */
+typedef struct slw_batch {
+    int32_t C;
+    int64_t prefill_seq;
+    int32_t prefix_len;
+    int32_t B;
+    const int64_t* decode_seqs;
+    const int32_t* context_lens;
+} slw_batch;
+
+/*
+ * Device workspace bytes needed by any iteration with C <= max_C and
+ * B <= max_B (activations, split partials, per-iteration metadata).
+ */
+int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes);
+
+/*
+ * Run all n_layers layers over the batch (asynchronous on `stream`).
+ *   x_in   device bf16 [C + B][d]: chunk rows first, then decode rows
+ *   x_out  device bf16 [C + B][d]; may equal x_in
+ *   ws     device workspace of ws_bytes >= slw_workspace_size(ctx, C, B)
+ * Reserves KV room (prefill_seq up to prefix_len + C, each decode up to
+ * context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
+ * it), builds the slot mapping and block tables on the host, uploads them
+ * through a pinned staging ring, then enqueues per layer: RMSNorm, QKV GEMM,
+ * RoPE with KV append, chunk attention and split decode attention, output
+ * GEMM + residual, RMSNorm, gate/up GEMM with SiLU*mul, down GEMM + residual.
+ * Each row's K/V is written at slot(seq, pos) = bt[pos/16]*16 + pos%16 of its
+ * sequence in every layer.  C == 0 and B == 0 together is a no-op.
+ */
+int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const void* x_in, void* x_out,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Slot of every row of the last slw_mixed_iteration (host int32, chunk rows first). */
+int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n);
+
+/*
+ * Where an intermediate of the LAST layer of an iteration with (C, B) lives
+ * in the workspace, for inspection after the stream is synchronised:
+ *   SLW_VIEW_QKV   bf16 [C+B][(Hq+2Hkv)*hd] (q and k after RoPE)
+ *   SLW_VIEW_ATTN  bf16 [C+B][Hq*hd] attention output
+ *   SLW_VIEW_H     bf16 [C+B][d] residual stream after attention
+ *   SLW_VIEW_ACT   bf16 [C+B][F] silu(gate) * up
+ */
+#define SLW_VIEW_QKV 0
+#define SLW_VIEW_ATTN 1
+#define SLW_VIEW_H 2
+#define SLW_VIEW_ACT 3
+int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_t B, size_t* offset,
+                       size_t* bytes);
+
+/* ------------------------------------------------------------------------ */
+/* Cost table (Sec. 5.1 profiler: P50/P99 per grid point, cumulative max    */
+/* along the chunk axis; Sec. 6.4: profile at start-up, interpolate)         */
+/* ------------------------------------------------------------------------ */
+
+typedef struct slw_profile_opts {
+    int32_t prefix_len;   /* cached tokens of the profiled prefill sequence           */
+    int32_t ctx_lo;       /* decode contexts uniform in [ctx_lo, ctx_hi]               */
+    int32_t ctx_hi;
+    uint64_t seed;        /* seed of the context draw                                 */
+    int32_t warmup;       /* untimed iterations per grid point (>= 0)                 */
+    int32_t repeats;      /* timed iterations per grid point (>= 1)                   */
+    void* flush_buf;      /* device buffer overwritten before every timed iteration   */
+    size_t flush_bytes;   /* (flushes the last-level cache); 0 = no flush             */
+    const void* x_in;     /* device bf16 [max C + max B][d] input rows                */
+    void* x_out;          /* device bf16 [max C + max B][d]                           */
+    void* ws;             /* device workspace for (max C, max B)                      */
+    size_t ws_bytes;
+    void* stream;
+} slw_profile_opts;
+
+/*
+ * Time slw_mixed_iteration over every (b, c) of b_grid x c_grid and build the
+ * table (synchronous).  Grids strictly increase; c_grid[0] must be 0 (the
+ * decode-only column); b_grid values are >= 0.  Each repeat is timed on the
+ * host clock from the call to the end of a stream synchronisation, so launch
+ * overhead is part of T.  Temporary sequences (one prefill sequence, max(b)
+ * decodes) are reserved from the pool and freed before returning; KV contents
+ * are whatever the pool holds.  *out receives a new table (slw_cost_table_free).
+ */
+int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                         int32_t nb, const slw_profile_opts* opts, slw_cost_table** out);
+
+/* Build a table from raw samples, host int64 ns [nb][nc][repeats] (e.g. an analytic model). */
+int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                int32_t nb, const int64_t* samples, int32_t repeats,
+                                slw_cost_table** out);
+void slw_cost_table_free(slw_cost_table* t);
+int slw_cost_table_dims(const slw_cost_table* t, int32_t* nc, int32_t* nb, int32_t* repeats);
+int slw_cost_table_grids(const slw_cost_table* t, int32_t* c_grid, int32_t* b_grid);
+
+/*
+ * Copy a table view to host int64:
+ *   SLW_TABLE_SAMPLES [nb][nc][repeats] raw ns; SLW_TABLE_P50 / SLW_TABLE_P99 [nb][nc]
+ *   nearest-rank percentiles sorted[ceil(k*q)-1]; SLW_TABLE_THAT [nb][nc] the P99 with
+ *   a running maximum along c (the table the controller reads).
+ */
+#define SLW_TABLE_SAMPLES 0
+#define SLW_TABLE_P50 1
+#define SLW_TABLE_P99 2
+#define SLW_TABLE_THAT 3
+int slw_cost_table_values(const slw_cost_table* t, int32_t which, int64_t* out, size_t cap);
+
+/*
+ * Predicted time T_hat(n, c) in ns.  n rounds up to the next b_grid point
+ * (SLW_ERANGE above the last); c = 0 reads column 0; 0 < c <= c_1 reads c_1;
+ * c_j < c <= c_{j+1} interpolates T_hat_j + ceil((T_hat_{j+1}-T_hat_j)(c-c_j)/(c_{j+1}-c_j));
+ * c above the last grid point is SLW_ERANGE.
+ */
+int slw_cost_table_lookup(const slw_cost_table* t, int32_t n, int32_t c, int64_t* t_ns);
+/* Raw P99 decreases along c before the running maximum: count and largest drop (ns). */
+int slw_cost_table_monotone(const slw_cost_table* t, int32_t* violations, int64_t* worst_ns);
+/* Text save / load of grids and raw samples (percentiles are recomputed on load). */
+int slw_cost_table_save(const slw_cost_table* t, const char* path);
+int slw_cost_table_load(const char* path, slw_cost_table** out);
+
+/* ------------------------------------------------------------------------ */
+/* Controller (Eq. 1 by the binary search of Alg. 1, margin of Sec. 3.3)    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Largest chunk c <= min(c_max, remaining, last grid C) with
+ * T_hat(n_active, c) + margin_ns <= min_i deadlines_ns[i] - now_ns.
+ *   deadlines_ns  host [n_active] absolute next-token deadlines d_i = l_i + D_i
+ *   remaining     remaining prompt tokens of the oldest pending prefill (<= 0: none)
+ * remaining <= 0 gives 0 (NO_PENDING); n_active == 0 gives the cap (NO_ACTIVE);
+ * when no chunk fits the result is 0 (a decode-only iteration) and
+ * DECODE_INFEASIBLE tells whether decode-only itself misses the budget.
+ * n_active above the last b_grid point is SLW_ERANGE with *chunk = 0.
+ * n_lookups (may be NULL) receives the number of table lookups made.
+ * Pure, no allocation, thread-safe.
+ */
+int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
+                     int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
+                     int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLOWEAVE_H */

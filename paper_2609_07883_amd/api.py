@@ -1,0 +1,328 @@
+"""ctypes binding of libsloweave.so (argument marshalling only).
+
+Every computation happens in the library: the mixed iteration in its gfx950
+kernels, the block manager, profiler and controller in its host code.  This
+module converts Python values to the C ABI of ``include/sloweave.h`` and
+raises ``SloweaveError`` for every negative return code.  Device buffers are
+passed as integer addresses (``tensor.data_ptr()``) and streams as integer
+handles (``torch.cuda.current_stream().cuda_stream``).
+
+A missing library is an error, never a fallback: build it with
+``python -m paper_2609_07883_amd.build``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsloweave.so")
+
+OK, EINVAL, ERANGE, ENOMEM, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+FLAG_NO_PENDING, FLAG_NO_ACTIVE, FLAG_DECODE_INFEASIBLE, FLAG_CAPPED_BY_GRID = 1, 2, 4, 8
+VIEW_QKV, VIEW_ATTN, VIEW_H, VIEW_ACT = 0, 1, 2, 3
+TABLE_SAMPLES, TABLE_P50, TABLE_P99, TABLE_THAT = 0, 1, 2, 3
+
+EXPORTS = (
+    "slw_last_error", "slw_create", "slw_destroy", "slw_set_layer_weights", "slw_kv_init",
+    "slw_kv_free_blocks", "slw_seq_create", "slw_seq_free", "slw_seq_reserve",
+    "slw_seq_block_table", "slw_workspace_size", "slw_mixed_iteration", "slw_last_slots",
+    "slw_workspace_view", "slw_build_cost_table", "slw_cost_table_from_samples",
+    "slw_cost_table_free", "slw_cost_table_dims", "slw_cost_table_grids", "slw_cost_table_values",
+    "slw_cost_table_lookup", "slw_cost_table_monotone", "slw_cost_table_save",
+    "slw_cost_table_load", "slw_select_chunk",
+)
+
+
+class SloweaveError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"sloweave error {code}: {msg}")
+        self.code = code
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
+                ("rms_eps", C.c_float), ("rope_theta", C.c_float), ("block_size", C.c_int32),
+                ("max_pos", C.c_int32)]
+
+
+class LayerWeightsC(C.Structure):
+    _fields_ = [("wqkv", C.c_void_p), ("wo", C.c_void_p), ("wgu", C.c_void_p), ("wd", C.c_void_p),
+                ("g1", C.c_void_p), ("g2", C.c_void_p)]
+
+
+class BatchC(C.Structure):
+    _fields_ = [("C", C.c_int32), ("prefill_seq", C.c_int64), ("prefix_len", C.c_int32),
+                ("B", C.c_int32), ("decode_seqs", C.POINTER(C.c_int64)),
+                ("context_lens", C.POINTER(C.c_int32))]
+
+
+class ProfileOpts(C.Structure):
+    _fields_ = [("prefix_len", C.c_int32), ("ctx_lo", C.c_int32), ("ctx_hi", C.c_int32),
+                ("seed", C.c_uint64), ("warmup", C.c_int32), ("repeats", C.c_int32),
+                ("flush_buf", C.c_void_p), ("flush_bytes", C.c_size_t), ("x_in", C.c_void_p),
+                ("x_out", C.c_void_p), ("ws", C.c_void_p), ("ws_bytes", C.c_size_t),
+                ("stream", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2609_07883_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    i32, i64, u32, vp, sz = C.c_int32, C.c_int64, C.c_uint32, C.c_void_p, C.c_size_t
+    P = C.POINTER
+    sig = {
+        "slw_last_error": ([], C.c_char_p),
+        "slw_create": ([P(ModelCfg), P(vp)], C.c_int),
+        "slw_destroy": ([vp], C.c_int),
+        "slw_set_layer_weights": ([vp, i32, P(LayerWeightsC)], C.c_int),
+        "slw_kv_init": ([vp, vp, vp, i32], C.c_int),
+        "slw_kv_free_blocks": ([vp, P(i32)], C.c_int),
+        "slw_seq_create": ([vp, i64], C.c_int),
+        "slw_seq_free": ([vp, i64], C.c_int),
+        "slw_seq_reserve": ([vp, i64, i32], C.c_int),
+        "slw_seq_block_table": ([vp, i64, P(i32), i32, P(i32)], C.c_int),
+        "slw_workspace_size": ([vp, i32, i32, P(sz)], C.c_int),
+        "slw_mixed_iteration": ([vp, P(BatchC), vp, vp, vp, sz, vp], C.c_int),
+        "slw_last_slots": ([vp, P(i32), i32, P(i32)], C.c_int),
+        "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
+        "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
+        "slw_cost_table_from_samples": ([P(i32), i32, P(i32), i32, P(i64), i32, P(vp)], C.c_int),
+        "slw_cost_table_free": ([vp], None),
+        "slw_cost_table_dims": ([vp, P(i32), P(i32), P(i32)], C.c_int),
+        "slw_cost_table_grids": ([vp, P(i32), P(i32)], C.c_int),
+        "slw_cost_table_values": ([vp, i32, P(i64), sz], C.c_int),
+        "slw_cost_table_lookup": ([vp, i32, i32, P(i64)], C.c_int),
+        "slw_cost_table_monotone": ([vp, P(i32), P(i64)], C.c_int),
+        "slw_cost_table_save": ([vp, C.c_char_p], C.c_int),
+        "slw_cost_table_load": ([C.c_char_p, P(vp)], C.c_int),
+        "slw_select_chunk": ([vp, P(i64), i32, i64, i32, i32, i64, P(i32), P(u32), P(i32)], C.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _check(rc: int) -> None:
+    if rc != OK:
+        raise SloweaveError(rc, lib().slw_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _i64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int64))
+
+
+def _ptr(a: np.ndarray, ct):
+    return a.ctypes.data_as(C.POINTER(ct))
+
+
+# ---------------------------------------------------------------------------
+# Cost table and controller
+# ---------------------------------------------------------------------------
+
+class CostTable:
+    """Owns a slw_cost_table*."""
+
+    def __init__(self, handle: int):
+        self._h = C.c_void_p(handle)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value and _lib is not None:
+            _lib.slw_cost_table_free(self._h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    @classmethod
+    def from_samples(cls, c_grid, b_grid, samples) -> "CostTable":
+        cg, bg = _i32(c_grid), _i32(b_grid)
+        s = _i64(samples)
+        if s.ndim == 2:
+            s = s[:, :, None]
+        assert s.shape[:2] == (len(bg), len(cg))
+        h = C.c_void_p()
+        _check(lib().slw_cost_table_from_samples(_ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
+                                                 len(bg), _ptr(s, C.c_int64), s.shape[2], C.byref(h)))
+        return cls(h.value)
+
+    @classmethod
+    def load(cls, path: str) -> "CostTable":
+        h = C.c_void_p()
+        _check(lib().slw_cost_table_load(path.encode(), C.byref(h)))
+        return cls(h.value)
+
+    def save(self, path: str) -> None:
+        _check(lib().slw_cost_table_save(self._h, path.encode()))
+
+    def dims(self):
+        nc, nb, r = C.c_int32(), C.c_int32(), C.c_int32()
+        _check(lib().slw_cost_table_dims(self._h, C.byref(nc), C.byref(nb), C.byref(r)))
+        return nc.value, nb.value, r.value
+
+    def grids(self):
+        nc, nb, _ = self.dims()
+        cg = np.zeros(nc, np.int32)
+        bg = np.zeros(nb, np.int32)
+        _check(lib().slw_cost_table_grids(self._h, _ptr(cg, C.c_int32), _ptr(bg, C.c_int32)))
+        return cg, bg
+
+    def values(self, which: int) -> np.ndarray:
+        nc, nb, r = self.dims()
+        shape = (nb, nc, r) if which == TABLE_SAMPLES else (nb, nc)
+        out = np.zeros(shape, np.int64)
+        _check(lib().slw_cost_table_values(self._h, which, _ptr(out, C.c_int64), out.size))
+        return out
+
+    def lookup(self, n: int, c: int) -> int:
+        t = C.c_int64()
+        _check(lib().slw_cost_table_lookup(self._h, n, c, C.byref(t)))
+        return t.value
+
+    def monotone(self):
+        v, w = C.c_int32(), C.c_int64()
+        _check(lib().slw_cost_table_monotone(self._h, C.byref(v), C.byref(w)))
+        return v.value, w.value
+
+
+def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_max: int,
+                 margin_ns: int = 0):
+    """(chunk, flags, n_lookups) from slw_select_chunk (Alg. 1)."""
+    d = _i64(deadlines_ns)
+    ch, fl, nl = C.c_int32(), C.c_uint32(), C.c_int32()
+    _check(lib().slw_select_chunk(table.handle, _ptr(d, C.c_int64), len(d), int(now_ns), int(remaining),
+                                  int(c_max), int(margin_ns), C.byref(ch), C.byref(fl), C.byref(nl)))
+    return ch.value, fl.value, nl.value
+
+
+# ---------------------------------------------------------------------------
+# Context
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Batch:
+    chunk: int
+    prefill_seq: int
+    prefix_len: int
+    decode_seqs: list
+    context_lens: list
+
+    @property
+    def rows(self) -> int:
+        return self.chunk + len(self.decode_seqs)
+
+
+class Context:
+    """Owns a slw_ctx*.  Pointers passed in stay owned by the caller."""
+
+    def __init__(self, n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, rms_eps,
+                 rope_theta, max_pos, block_size=16):
+        cfg = ModelCfg(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, rms_eps,
+                       rope_theta, block_size, max_pos)
+        h = C.c_void_p()
+        _check(lib().slw_create(C.byref(cfg), C.byref(h)))
+        self._h = h
+        self.cfg = cfg
+
+    @classmethod
+    def from_shape(cls, shape) -> "Context":
+        return cls(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                   shape.ffn_dim, shape.rms_eps, shape.rope_theta, shape.max_pos, shape.block_size)
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().slw_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # weights and pools
+    def set_layer_weights(self, layer: int, wqkv: int, wo: int, wgu: int, wd: int, g1: int, g2: int):
+        w = LayerWeightsC(wqkv, wo, wgu, wd, g1, g2)
+        _check(lib().slw_set_layer_weights(self._h, layer, C.byref(w)))
+
+    def kv_init(self, k_pool: int, v_pool: int, num_blocks: int):
+        _check(lib().slw_kv_init(self._h, C.c_void_p(k_pool), C.c_void_p(v_pool), num_blocks))
+
+    def free_blocks(self) -> int:
+        n = C.c_int32()
+        _check(lib().slw_kv_free_blocks(self._h, C.byref(n)))
+        return n.value
+
+    def seq_create(self, sid: int):
+        _check(lib().slw_seq_create(self._h, sid))
+
+    def seq_free(self, sid: int):
+        _check(lib().slw_seq_free(self._h, sid))
+
+    def seq_reserve(self, sid: int, new_len: int):
+        _check(lib().slw_seq_reserve(self._h, sid, new_len))
+
+    def block_table(self, sid: int) -> list:
+        n = C.c_int32()
+        _check(lib().slw_seq_block_table(self._h, sid, None, 0, C.byref(n)))
+        out = np.zeros(max(n.value, 1), np.int32)
+        _check(lib().slw_seq_block_table(self._h, sid, _ptr(out, C.c_int32), len(out), C.byref(n)))
+        return out[: n.value].tolist()
+
+    # iteration
+    def workspace_size(self, max_c: int, max_b: int) -> int:
+        b = C.c_size_t()
+        _check(lib().slw_workspace_size(self._h, max_c, max_b, C.byref(b)))
+        return b.value
+
+    def workspace_view(self, which: int, c: int, b: int):
+        off, nb = C.c_size_t(), C.c_size_t()
+        _check(lib().slw_workspace_view(self._h, which, c, b, C.byref(off), C.byref(nb)))
+        return off.value, nb.value
+
+    def mixed_iteration(self, batch: Batch, x_in: int, x_out: int, ws: int, ws_bytes: int,
+                        stream: int = 0):
+        ds = _i64(batch.decode_seqs)
+        cl = _i32(batch.context_lens)
+        bc = BatchC(batch.chunk, batch.prefill_seq, batch.prefix_len, len(ds),
+                    _ptr(ds, C.c_int64), _ptr(cl, C.c_int32))
+        _check(lib().slw_mixed_iteration(self._h, C.byref(bc), C.c_void_p(x_in), C.c_void_p(x_out),
+                                         C.c_void_p(ws), ws_bytes, C.c_void_p(stream)))
+
+    def last_slots(self) -> list:
+        n = C.c_int32()
+        _check(lib().slw_last_slots(self._h, None, 0, C.byref(n)))
+        out = np.zeros(max(n.value, 1), np.int32)
+        _check(lib().slw_last_slots(self._h, _ptr(out, C.c_int32), len(out), C.byref(n)))
+        return out[: n.value].tolist()
+
+    def build_cost_table(self, c_grid, b_grid, *, prefix_len: int, ctx_lo: int, ctx_hi: int,
+                         seed: int, warmup: int, repeats: int, x_in: int, x_out: int, ws: int,
+                         ws_bytes: int, flush_buf: int = 0, flush_bytes: int = 0,
+                         stream: int = 0) -> CostTable:
+        cg, bg = _i32(c_grid), _i32(b_grid)
+        o = ProfileOpts(prefix_len, ctx_lo, ctx_hi, seed, warmup, repeats, flush_buf or None,
+                        flush_bytes, x_in, x_out, ws, ws_bytes, stream or None)
+        h = C.c_void_p()
+        _check(lib().slw_build_cost_table(self._h, _ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
+                                          len(bg), C.byref(o), C.byref(h)))
+        return CostTable(h.value)

@@ -1,0 +1,426 @@
+// Paged attention on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16).
+//
+// Both kernels compute transposed scores S^T = K Q^T: K (16 tokens of a page)
+// is the A operand and Q^T the B operand, so lane l holds, for query (or
+// head) l % 16, the scores of tokens 4 (l / 16) .. 4 (l / 16) + 3 of the page.
+// Those four scores from two pages are exactly the eight k-values lane l must
+// supply as the A operand (P) of the P V product, whose k index runs over the
+// same tokens; the V operand reads the matching tokens of one head dimension,
+// which are contiguous in the dim-major V page.  The softmax is online
+// (running max and sum per query, base-2 exponentials) in fp32.
+//
+// Page layouts (one (layer, block, kv head) page of 16 tokens):
+//   K: [hd/32][16][32]  element (t, d) at (d/32)*512 + t*32 + d%32
+//   V: [hd][16]         element (t, d) at d*16 + t
+#include <math.h>
+
+#include "device.h"
+#include "kernels.h"
+
+namespace slw {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ bf16x8 cat44(bf16x4 lo, bf16x4 hi) {
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+__device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
+    bf16x8 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        r[e] = f2bf(lo[e]);
+        r[4 + e] = f2bf(hi[e]);
+    }
+    return r;
+}
+
+// ---------------------------------------------------------------------------
+// Chunk attention: C queries at positions P..P+C-1 of one sequence attend to
+// its keys 0..P+C-1 under the causal mask.
+// ---------------------------------------------------------------------------
+
+// LDS swizzles: K rows (64 B = four 16-byte chunks) and V rows (32 B = four
+// 8-byte groups of four tokens).
+__device__ __forceinline__ int kswz(int t, int sub) { return sub ^ ((t >> 1) & 3); }
+__device__ __forceinline__ int vswz(int d, int grp) { return grp ^ ((d >> 2) & 3); }
+
+template <int HD>
+__global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a, int heads_per_wg,
+                                                         int span) {
+    constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
+    constexpr int CHUNKS = 4 * PAGE / 8;                 // 16-byte chunks per K (or V) tile
+    constexpr int PER_THREAD = 2 * CHUNKS / 256;
+    __shared__ __attribute__((aligned(16))) bf16 Ks[2][4 * PAGE];
+    __shared__ __attribute__((aligned(16))) bf16 Vs[2][4 * PAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = lane >> 4, col = lane & 15;
+    const int group = a.hq / a.hkv;
+    const int head = blockIdx.y * heads_per_wg + (wave % heads_per_wg);
+    const int kvh = head / group;
+    const int q0 = blockIdx.x * span + (wave / heads_per_wg) * 32;
+    const int key_end = min(a.prefix + a.c, a.prefix + (int)blockIdx.x * span + span);
+    const int n_tiles = (key_end + 63) / 64;
+    const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
+
+    const bf16* kpool = static_cast<const bf16*>(a.k_pool);
+    const bf16* vpool = static_cast<const bf16*>(a.v_pool);
+
+    // Q^T operand: query col of sub-tile qt, dims kk*32 + grp*8 .. +8
+    bf16x8 qf[2][KK];
+    const bf16* qkv = static_cast<const bf16*>(a.qkv);
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        const int qi = q0 + qt * 16 + col;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qf[qt][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
+                                        qkv + static_cast<size_t>(qi) * a.ld_qkv + head * HD + kk * 32 + grp * 8)
+                                  : bf16x8{};
+    }
+
+    // staging: thread handles PER_THREAD 16-byte chunks of the K and V tiles
+    bf16x8 stage[PER_THREAD];
+    auto load_tile = [&](int t) {
+#pragma unroll
+        for (int j = 0; j < PER_THREAD; ++j) {
+            const int c = tid + j * 256;
+            const bool is_v = c >= CHUNKS;
+            const int cc = is_v ? c - CHUNKS : c;
+            const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
+            const int pg = 4 * t + p;
+            bf16x8 v = {};
+            if (pg * 16 < key_end) {
+                const size_t blk = a.bt[pg];
+                const bf16* src = (is_v ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + q * 8;
+                v = *reinterpret_cast<const bf16x8*>(src);
+                if (is_v) {  // zero tokens at or past key_end (unwritten slots)
+                    const int tok0 = pg * 16 + (q & 1) * 8;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (tok0 + e >= key_end) v[e] = bf16(0.0f);
+                }
+            }
+            stage[j] = v;
+        }
+    };
+    auto store_tile = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < PER_THREAD; ++j) {
+            const int c = tid + j * 256;
+            const bool is_v = c >= CHUNKS;
+            const int cc = is_v ? c - CHUNKS : c;
+            const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
+            if (!is_v) {
+                const int kk = q / 64, t = (q % 64) / 4, sub = q % 4;
+                *reinterpret_cast<bf16x8*>(&Ks[buf][p * PAGE + kk * 512 + t * 32 + kswz(t, sub) * 8]) = stage[j];
+            } else {
+                const int d = q / 2, h = q % 2;
+                bf16* row = &Vs[buf][p * PAGE + d * 16];
+                const bf16x4 lo = {stage[j][0], stage[j][1], stage[j][2], stage[j][3]};
+                const bf16x4 hi = {stage[j][4], stage[j][5], stage[j][6], stage[j][7]};
+                *reinterpret_cast<bf16x4*>(row + vswz(d, 2 * h) * 4) = lo;
+                *reinterpret_cast<bf16x4*>(row + vswz(d, 2 * h + 1) * 4) = hi;
+            }
+        }
+    };
+
+    f32x4 o[2][NT];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) o[qt][nt] = f32x4{};
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+    load_tile(0);
+    store_tile(0);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < n_tiles) load_tile(t + 1);
+
+        f32x4 s[4][2];
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) s[p][qt] = f32x4{};
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+                    &Ks[buf][p * PAGE + kk * 512 + col * 32 + kswz(col, grp) * 8]);
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt) s[p][qt] = mfma16(kf, qf[qt][kk], s[p][qt]);
+            }
+
+        const int key0 = t * 64;
+        const bool need_mask = key0 + 63 > a.prefix + q0 || key0 + 63 >= key_end;
+        f32x4 pr[4][2];
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const int qpos = a.prefix + q0 + qt * 16 + col;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float x = s[p][qt][e] * sl2;
+                    if (need_mask) {
+                        const int kpos = key0 + p * 16 + grp * 4 + e;
+                        x = (kpos <= qpos && kpos < key_end) ? x : -INFINITY;
+                    }
+                    s[p][qt][e] = x;
+                    mx = fmaxf(mx, x);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float m_new = fmaxf(m_run[qt], mx);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2f(m_run[qt] - m_use);
+            float ls = 0.f;
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = exp2f(s[p][qt][e] - m_use);
+                    pr[p][qt][e] = v;
+                    ls += v;
+                }
+            l_run[qt] = l_run[qt] * alpha + ls;
+            m_run[qt] = m_new;
+            // rescale the output rows (query grp*4 + e) by their alpha
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) o[qt][nt][e] *= ae;
+            }
+        }
+
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            bf16x8 pf[2];
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) pf[qt] = to_bf16x8(pr[2 * j][qt], pr[2 * j + 1][qt]);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int d = nt * 16 + col;
+                const int off = d * 16 + vswz(d, grp) * 4;
+                const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
+                const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
+                const bf16x8 vf = cat44(lo, hi);
+#pragma unroll
+                for (int qt = 0; qt < 2; ++qt) o[qt][nt] = mfma16(pf[qt], vf, o[qt][nt]);
+            }
+        }
+
+        if (t + 1 < n_tiles) store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    bf16* out = static_cast<bf16*>(a.out);
+    const int ldo = a.hq * HD;
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        float l = l_run[qt];
+        l += __shfl_xor(l, 16, 64);
+        l += __shfl_xor(l, 32, 64);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float le = __shfl(l, grp * 4 + e, 64);
+            const int qi = q0 + qt * 16 + grp * 4 + e;
+            if (qi < a.c) {
+                const float inv = 1.0f / le;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    out[static_cast<size_t>(qi) * ldo + head * HD + nt * 16 + col] = f2bf(o[qt][nt][e] * inv);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Decode attention, split over the key axis: one wave per (work item, kv
+// head); a work item is one split of `split_tokens` keys of one decode.  All
+// q heads of the kv head's group (<= 16) are the columns of Q^T.
+// ---------------------------------------------------------------------------
+template <int HD>
+__global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
+    constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
+    const int lane = threadIdx.x, grp = lane >> 4, col = lane & 15;
+    const int w = blockIdx.x, kvh = blockIdx.y;
+    const int b = a.work_b[w], split = a.work_s[w];
+    const int group = a.hq / a.hkv;
+    const int kv_len = a.kv_len[b];
+    const int tok0 = split * a.split_tokens;
+    const int tok1 = min(tok0 + a.split_tokens, kv_len);
+    const int* bt = a.bt + a.bt_off[b];
+    const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
+
+    const bf16* kpool = static_cast<const bf16*>(a.k_pool);
+    const bf16* vpool = static_cast<const bf16*>(a.v_pool);
+
+    bf16x8 qf[KK];
+    {
+        const bf16* q = static_cast<const bf16*>(a.q) + static_cast<size_t>(b) * a.ld_q;
+        const int h = kvh * group + col;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+            qf[kk] = col < group ? *reinterpret_cast<const bf16x8*>(q + h * HD + kk * 32 + grp * 8)
+                                 : bf16x8{};
+    }
+
+    f32x4 o[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    for (int c0 = tok0; c0 < tok1; c0 += 64) {
+        bf16x8 kf[4][KK];
+        bf16x4 vf[4][NT];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const int pg = (c0 >> 4) + p;
+            if (pg * 16 < tok1) {
+                const size_t page = (static_cast<size_t>(bt[pg]) * a.hkv + kvh) * PAGE;
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk)
+                    kf[p][kk] = *reinterpret_cast<const bf16x8*>(kpool + page + kk * 512 + col * 32 + grp * 8);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    vf[p][nt] = *reinterpret_cast<const bf16x4*>(vpool + page + (nt * 16 + col) * 16 + grp * 4);
+            } else {
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk) kf[p][kk] = bf16x8{};
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) vf[p][nt] = bf16x4{};
+            }
+        }
+        const bool tail = c0 + 64 > tok1;
+        if (tail) {  // zero V of tokens past the split (possibly unwritten slots)
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (c0 + p * 16 + grp * 4 + e >= tok1)
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt) vf[p][nt][e] = bf16(0.0f);
+        }
+
+        f32x4 s[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            s[p] = f32x4{};
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) s[p] = mfma16(kf[p][kk], qf[kk], s[p]);
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float x = s[p][e] * sl2;
+                if (tail && c0 + p * 16 + grp * 4 + e >= tok1) x = -INFINITY;
+                s[p][e] = x;
+                mx = fmaxf(mx, x);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m_run - m_use);
+        float ls = 0.f;
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float v = exp2f(s[p][e] - m_use);
+                s[p][e] = v;
+                ls += v;
+            }
+        l_run = l_run * alpha + ls;
+        m_run = m_new;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) o[nt][e] *= ae;
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const bf16x8 pf = to_bf16x8(s[2 * j], s[2 * j + 1]);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, cat44(vf[2 * j][nt], vf[2 * j + 1][nt]), o[nt]);
+        }
+    }
+
+    float l = l_run;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const size_t hbase = static_cast<size_t>(w) * a.hq + kvh * group;
+    if (grp == 0 && col < group) {
+        a.part_ml[(hbase + col) * 2 + 0] = m_run;
+        a.part_ml[(hbase + col) * 2 + 1] = l;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int h = grp * 4 + e;
+        if (h < group) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) a.part_o[(hbase + h) * HD + nt * 16 + col] = o[nt][e];
+        }
+    }
+}
+
+// Merge the splits of one (decode, q head): weights 2^(m_s - max m).
+template <int HD>
+__global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
+    const int b = blockIdx.x, h = blockIdx.y;
+    const int w0 = a.work_off[b], w1 = a.work_off[b + 1];
+    float mmax = -INFINITY;
+    for (int w = w0; w < w1; ++w) mmax = fmaxf(mmax, a.part_ml[(static_cast<size_t>(w) * a.hq + h) * 2]);
+    float lsum = 0.f;
+    constexpr int PER = HD / 64;
+    float acc[PER] = {};
+    for (int w = w0; w < w1; ++w) {
+        const size_t r = static_cast<size_t>(w) * a.hq + h;
+        const float sc = exp2f(a.part_ml[r * 2] - mmax);
+        lsum += sc * a.part_ml[r * 2 + 1];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) acc[j] += sc * a.part_o[r * HD + threadIdx.x + 64 * j];
+    }
+    bf16* out = static_cast<bf16*>(a.out) + static_cast<size_t>(b) * a.hq * HD + h * HD;
+    const float inv = 1.0f / lsum;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
+}
+
+}  // namespace
+
+void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s) {
+    if (a.c <= 0) return;
+    const int group = a.hq / a.hkv;
+    const int heads_per_wg = group >= 4 ? 4 : group;
+    const int span = 32 * (4 / heads_per_wg);
+    dim3 grid((a.c + span - 1) / span, a.hq / heads_per_wg);
+    if (a.hd == 128) chunk_attn_kernel<128><<<grid, 256, 0, s>>>(a, heads_per_wg, span);
+    else chunk_attn_kernel<64><<<grid, 256, 0, s>>>(a, heads_per_wg, span);
+}
+
+void launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s) {
+    if (a.b <= 0) return;
+    dim3 grid(a.n_work, a.hkv);
+    dim3 mgrid(a.b, a.hq);
+    if (a.hd == 128) {
+        decode_attn_kernel<128><<<grid, 64, 0, s>>>(a);
+        decode_merge_kernel<128><<<mgrid, 64, 0, s>>>(a);
+    } else {
+        decode_attn_kernel<64><<<grid, 64, 0, s>>>(a);
+        decode_merge_kernel<64><<<mgrid, 64, 0, s>>>(a);
+    }
+}
+
+}  // namespace slw

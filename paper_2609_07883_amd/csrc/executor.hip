@@ -1,0 +1,590 @@
+// Context, paged-KV bookkeeping, the mixed iteration and the cost profiler.
+//
+// A mixed iteration (Sec. 3: one prefill chunk plus one token for every
+// active decode; Sec. 5.1: the chunk arrives through ordinary sequence
+// metadata) is: host-side reservation and slot mapping, one upload of the
+// per-iteration metadata through a pinned staging ring, then per layer nine
+// launches on the caller's stream.
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <memory>
+#include <random>
+#include <unordered_set>
+#include <vector>
+
+#include "common.h"
+#include "cost_table.h"
+#include "kernels.h"
+#include "kv_manager.h"
+
+using namespace slw;
+
+namespace {
+
+constexpr int kRing = 4;                 // pinned staging buffers in flight
+constexpr int kDecodeTargetWaves = 2048; // decode work-groups aimed for per iteration
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+#define HIP_TRY(expr)                                                                      \
+    do {                                                                                   \
+        hipError_t e_ = (expr);                                                            \
+        if (e_ != hipSuccess) return fail(SLW_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+}  // namespace
+
+struct slw_ctx {
+    slw_model_cfg cfg{};
+    std::vector<slw_layer_weights> w;
+    std::vector<char> have_w;
+    void* k_pool = nullptr;
+    void* v_pool = nullptr;
+    KvManager kv;
+    bool kv_ready = false;
+    std::vector<int32_t> last_slots;
+    std::vector<int32_t> meta;  // host build area
+
+    // HIP resources, created on first device use
+    bool hip_ready = false;
+    int32_t* staging[kRing] = {};
+    size_t staging_cap[kRing] = {};
+    hipEvent_t staged[kRing] = {};
+    int ring = 0;
+
+    ~slw_ctx() {
+        if (!hip_ready) return;
+        for (int i = 0; i < kRing; ++i) {
+            if (staged[i]) {
+                (void)hipEventSynchronize(staged[i]);
+                (void)hipEventDestroy(staged[i]);
+            }
+            if (staging[i]) (void)hipHostFree(staging[i]);
+        }
+    }
+};
+
+namespace {
+
+int qkv_width(const slw_model_cfg& c) { return (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim; }
+int max_blocks(const slw_model_cfg& c) { return static_cast<int>(ceil_div(c.max_pos, 16)); }
+int decode_work_cap(const slw_model_cfg& c, int B) {
+    return std::max(1, kDecodeTargetWaves / c.n_kv_heads) + B + 1;
+}
+
+// Keys per split: a multiple of 64 chosen so that about kDecodeTargetWaves
+// work-groups cover all decodes' keys.
+int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
+    const int64_t per_head = std::max(1, kDecodeTargetWaves / c.n_kv_heads);
+    int64_t s = ceil_div(total_keys, per_head);
+    s = ceil_div(std::max<int64_t>(s, 64), 64) * 64;
+    return static_cast<int>(s);
+}
+
+size_t meta_ints(const slw_model_cfg& c, int C, int B) {
+    const int M = C + B;
+    const size_t mb = static_cast<size_t>(max_blocks(c));
+    return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + mb +
+           2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1);
+}
+
+struct Layout {
+    size_t xn, qkv, attn, h, act, meta, part_o, part_ml, gemm_part, end_fixed;
+};
+
+Layout layout(const slw_model_cfg& c, int C, int B) {
+    const size_t M = static_cast<size_t>(C) + B;
+    const int W = decode_work_cap(c, B);
+    Layout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    L.xn = take(M * c.d_model * 2);
+    L.qkv = take(M * qkv_width(c) * 2);
+    L.attn = take(M * c.n_q_heads * c.head_dim * 2);
+    L.h = take(M * c.d_model * 2);
+    L.act = take(M * c.ffn_dim * 2);
+    L.meta = take(meta_ints(c, C, B) * 4);
+    L.part_o = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * c.head_dim * 4 : 0);
+    L.part_ml = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * 2 * 4 : 0);
+    L.gemm_part = off;  // split-K partials take the rest of the workspace
+    L.end_fixed = off;
+    return L;
+}
+
+size_t gemm_partial_bytes(const slw_model_cfg& c, int M) {
+    size_t b = 0;
+    b = std::max(b, plan_gemm(M, qkv_width(c), c.d_model).partial_bytes);
+    b = std::max(b, plan_gemm(M, c.d_model, c.n_q_heads * c.head_dim).partial_bytes);
+    b = std::max(b, plan_gemm(M, 2 * c.ffn_dim, c.d_model).partial_bytes);
+    b = std::max(b, plan_gemm(M, c.d_model, c.ffn_dim).partial_bytes);
+    return b;
+}
+
+int check_cfg(const slw_model_cfg& c) {
+    if (c.n_layers < 1) return fail(SLW_EINVAL, "n_layers must be >= 1");
+    if (c.head_dim != 64 && c.head_dim != 128) return fail(SLW_EUNSUPPORTED, "head_dim must be 64 or 128");
+    if (c.n_q_heads < 1 || c.n_kv_heads < 1 || c.n_q_heads % c.n_kv_heads)
+        return fail(SLW_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
+    const int group = c.n_q_heads / c.n_kv_heads;
+    if (group > 16 || (group & (group - 1))) return fail(SLW_EUNSUPPORTED, "GQA group must be 1, 2, 4, 8 or 16");
+    if (c.d_model < 128 || c.d_model % 128 || c.d_model > 8192)
+        return fail(SLW_EUNSUPPORTED, "d_model must be a multiple of 128 in [128, 8192]");
+    if (c.ffn_dim < 64 || c.ffn_dim % 64) return fail(SLW_EUNSUPPORTED, "ffn_dim must be a multiple of 64");
+    if (qkv_width(c) % 128) return fail(SLW_EUNSUPPORTED, "(Hq + 2 Hkv) * hd must be a multiple of 128");
+    if ((c.n_q_heads * c.head_dim) % 64) return fail(SLW_EUNSUPPORTED, "Hq * hd must be a multiple of 64");
+    if (c.block_size != 16) return fail(SLW_EUNSUPPORTED, "block_size must be 16");
+    if (c.max_pos < 1 || c.max_pos > (1 << 20)) return fail(SLW_EINVAL, "max_pos out of range");
+    if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f)) return fail(SLW_EINVAL, "rms_eps and rope_theta must be > 0");
+    return SLW_OK;
+}
+
+int ensure_hip(slw_ctx* ctx) {
+    if (ctx->hip_ready) return SLW_OK;
+    for (int i = 0; i < kRing; ++i) HIP_TRY(hipEventCreateWithFlags(&ctx->staged[i], hipEventDisableTiming));
+    ctx->hip_ready = true;
+    return SLW_OK;
+}
+
+// Pinned buffer of the next ring slot with room for n ints (waits for its last copy).
+int next_staging(slw_ctx* ctx, size_t n, int32_t** buf, int* slot_out) {
+    const int slot = ctx->ring;
+    ctx->ring = (ctx->ring + 1) % kRing;
+    HIP_TRY(hipEventSynchronize(ctx->staged[slot]));
+    if (ctx->staging_cap[slot] < n) {
+        if (ctx->staging[slot]) HIP_TRY(hipHostFree(ctx->staging[slot]));
+        ctx->staging[slot] = nullptr;
+        ctx->staging_cap[slot] = 0;
+        size_t cap = std::max<size_t>(n, 1 << 16);
+        void* p = nullptr;
+        HIP_TRY(hipHostMalloc(&p, cap * 4, hipHostMallocDefault));
+        ctx->staging[slot] = static_cast<int32_t*>(p);
+        ctx->staging_cap[slot] = cap;
+    }
+    *buf = ctx->staging[slot];
+    *slot_out = slot;
+    return SLW_OK;
+}
+
+int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+    const slw_model_cfg& c = ctx->cfg;
+    if (!bt) return fail(SLW_EINVAL, "null batch");
+    const int C = bt->C, B = bt->B, P = bt->prefix_len;
+    if (C < 0 || B < 0) return fail(SLW_EINVAL, "negative C or B");
+    if (C == 0 && B == 0) {
+        ctx->last_slots.clear();
+        return SLW_OK;
+    }
+    if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached (slw_kv_init)");
+    for (int l = 0; l < c.n_layers; ++l)
+        if (!ctx->have_w[l]) return fail(SLW_EINVAL, "weights of layer %d not set", l);
+    if (!x_in || !x_out || !ws) return fail(SLW_EINVAL, "null device buffer");
+    if (B > 0 && (!bt->decode_seqs || !bt->context_lens)) return fail(SLW_EINVAL, "null decode arrays");
+
+    // validation
+    std::vector<std::pair<int64_t, int32_t>> req;
+    req.reserve(B + 1);
+    if (C > 0) {
+        if (P < 0) return fail(SLW_EINVAL, "negative prefix_len");
+        if (static_cast<int64_t>(P) + C > c.max_pos) return fail(SLW_ERANGE, "prefix_len + C exceeds max_pos");
+        if (!ctx->kv.exists(bt->prefill_seq)) return fail(SLW_EINVAL, "prefill sequence %lld unknown", (long long)bt->prefill_seq);
+        if (ctx->kv.reserved(bt->prefill_seq) < P)
+            return fail(SLW_EINVAL, "prefill sequence holds %d positions, prefix_len is %d",
+                        ctx->kv.reserved(bt->prefill_seq), P);
+        req.emplace_back(bt->prefill_seq, P + C);
+    }
+    {
+        std::unordered_set<int64_t> seen;
+        seen.reserve(2 * B + 2);
+        for (int b = 0; b < B; ++b) {
+            const int64_t id = bt->decode_seqs[b];
+            const int32_t L = bt->context_lens[b];
+            if (!ctx->kv.exists(id)) return fail(SLW_EINVAL, "decode sequence %lld unknown", (long long)id);
+            if ((C > 0 && id == bt->prefill_seq) || !seen.insert(id).second)
+                return fail(SLW_EINVAL, "sequence %lld appears twice in the batch", (long long)id);
+            if (L < 0 || L + 1 > c.max_pos) return fail(SLW_ERANGE, "context_len %d out of range", L);
+            if (ctx->kv.reserved(id) < L)
+                return fail(SLW_EINVAL, "decode sequence %lld holds %d positions, context_len is %d",
+                            (long long)id, ctx->kv.reserved(id), L);
+            req.emplace_back(id, L + 1);
+        }
+    }
+    const Layout L = layout(c, C, B);
+    const size_t gpart = gemm_partial_bytes(c, C + B);
+    if (ws_bytes < L.end_fixed + gpart)
+        return fail(SLW_ENOMEM, "workspace holds %zu bytes, this iteration needs %zu", ws_bytes,
+                    L.end_fixed + gpart);
+
+    int rc = ctx->kv.reserve_all(req);
+    if (rc) return rc;
+    rc = ensure_hip(ctx);
+    if (rc) return rc;
+
+    // ---- metadata (host) ----
+    const int M = C + B;
+    const int W_cap = decode_work_cap(c, B);
+    int64_t total_keys = 0;
+    for (int b = 0; b < B; ++b) total_keys += bt->context_lens[b] + 1;
+    const int split = B > 0 ? decode_split_tokens(c, total_keys) : 64;
+
+    std::vector<int32_t>& m = ctx->meta;
+    m.clear();
+    m.reserve(meta_ints(c, C, B));
+    // slot[M], pos[M]
+    ctx->last_slots.resize(M);
+    for (int j = 0; j < C; ++j) ctx->last_slots[j] = ctx->kv.slot(bt->prefill_seq, P + j);
+    for (int b = 0; b < B; ++b) ctx->last_slots[C + b] = ctx->kv.slot(bt->decode_seqs[b], bt->context_lens[b]);
+    m.insert(m.end(), ctx->last_slots.begin(), ctx->last_slots.end());
+    for (int j = 0; j < C; ++j) m.push_back(P + j);
+    for (int b = 0; b < B; ++b) m.push_back(bt->context_lens[b]);
+    const size_t o_kvlen = m.size();
+    for (int b = 0; b < B; ++b) m.push_back(bt->context_lens[b] + 1);
+    const size_t o_btoff = m.size();
+    m.resize(m.size() + B + 1);
+    const size_t o_bt = m.size();
+    for (int b = 0; b < B; ++b) {
+        m[o_btoff + b] = static_cast<int32_t>(m.size() - o_bt);
+        const auto& t = ctx->kv.table(bt->decode_seqs[b]);
+        const int nb = static_cast<int>(ceil_div(bt->context_lens[b] + 1, 16));
+        m.insert(m.end(), t.begin(), t.begin() + nb);
+    }
+    m[o_btoff + B] = static_cast<int32_t>(m.size() - o_bt);
+    const size_t o_pre = m.size();
+    if (C > 0) {
+        const auto& t = ctx->kv.table(bt->prefill_seq);
+        const int nb = static_cast<int>(ceil_div(P + C, 16));
+        m.insert(m.end(), t.begin(), t.begin() + nb);
+    }
+    const size_t o_workb = m.size();
+    int n_work = 0;
+    for (int b = 0; b < B; ++b) n_work += static_cast<int>(ceil_div(bt->context_lens[b] + 1, split));
+    if (n_work > W_cap) return fail(SLW_EINVAL, "internal: decode work %d above cap %d", n_work, W_cap);
+    m.resize(m.size() + 2 * static_cast<size_t>(n_work) + B + 1);
+    {
+        int w = 0;
+        const size_t o_works = o_workb + n_work, o_workoff = o_workb + 2 * n_work;
+        for (int b = 0; b < B; ++b) {
+            m[o_workoff + b] = w;
+            const int ns = static_cast<int>(ceil_div(bt->context_lens[b] + 1, split));
+            for (int s = 0; s < ns; ++s, ++w) {
+                m[o_workb + w] = b;
+                m[o_works + w] = s;
+            }
+        }
+        m[o_workoff + B] = w;
+    }
+
+    // ---- upload ----
+    int32_t* stage = nullptr;
+    int slot = 0;
+    rc = next_staging(ctx, m.size(), &stage, &slot);
+    if (rc) return rc;
+    std::memcpy(stage, m.data(), m.size() * 4);
+    char* wsb = static_cast<char*>(ws);
+    int32_t* dmeta = reinterpret_cast<int32_t*>(wsb + L.meta);
+    HIP_TRY(hipMemcpyAsync(dmeta, stage, m.size() * 4, hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipEventRecord(ctx->staged[slot], stream));
+
+    const int32_t* d_slot = dmeta;
+    const int32_t* d_pos = dmeta + M;
+    void* xn = wsb + L.xn;
+    void* qkv = wsb + L.qkv;
+    void* attn = wsb + L.attn;
+    void* hbuf = wsb + L.h;
+    void* act = wsb + L.act;
+    void* gpartp = wsb + L.gemm_part;
+
+    const int d = c.d_model, hq = c.n_q_heads, hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
+    const int qw = qkv_width(c);
+    const GemmPlan p_qkv = plan_gemm(M, qw, d);
+    const GemmPlan p_o = plan_gemm(M, d, hq * hd);
+    const GemmPlan p_gu = plan_gemm(M, 2 * F, d);
+    const GemmPlan p_d = plan_gemm(M, d, F);
+    const size_t layer_pool = static_cast<size_t>(ctx->kv.num_blocks()) * hkv * hd * 16 * 2;
+
+    for (int l = 0; l < c.n_layers; ++l) {
+        const slw_layer_weights& wl = ctx->w[l];
+        const void* cur = l == 0 ? x_in : x_out;
+        void* kp = static_cast<char*>(ctx->k_pool) + l * layer_pool;
+        void* vp = static_cast<char*>(ctx->v_pool) + l * layer_pool;
+
+        launch_rmsnorm(cur, wl.g1, xn, M, d, c.rms_eps, stream);
+        launch_gemm(GemmArgs{xn, wl.wqkv, qkv, nullptr, M, qw, d, d, qw, EPI_STORE}, p_qkv, gpartp, stream);
+        launch_rope_append(RopeAppendArgs{qkv, d_pos, d_slot, kp, vp, M, hq, hkv, hd,
+                                          static_cast<double>(c.rope_theta)},
+                           stream);
+        if (C > 0)
+            launch_chunk_attention(ChunkAttnArgs{qkv, attn, kp, vp, dmeta + o_pre, C, P, hq, hkv, hd, qw},
+                                   stream);
+        if (B > 0) {
+            DecodeAttnArgs da{};
+            da.q = static_cast<const char*>(qkv) + static_cast<size_t>(C) * qw * 2;
+            da.out = static_cast<char*>(attn) + static_cast<size_t>(C) * hq * hd * 2;
+            da.k_pool = kp;
+            da.v_pool = vp;
+            da.kv_len = dmeta + o_kvlen;
+            da.bt_off = dmeta + o_btoff;
+            da.bt = dmeta + o_bt;
+            da.work_b = dmeta + o_workb;
+            da.work_s = dmeta + o_workb + n_work;
+            da.work_off = dmeta + o_workb + 2 * n_work;
+            da.part_o = reinterpret_cast<float*>(wsb + L.part_o);
+            da.part_ml = reinterpret_cast<float*>(wsb + L.part_ml);
+            da.b = B;
+            da.n_work = n_work;
+            da.split_tokens = split;
+            da.hq = hq;
+            da.hkv = hkv;
+            da.hd = hd;
+            da.ld_q = qw;
+            launch_decode_attention(da, stream);
+        }
+        launch_gemm(GemmArgs{attn, wl.wo, hbuf, cur, M, d, hq * hd, hq * hd, d, EPI_RESID}, p_o, gpartp, stream);
+        launch_rmsnorm(hbuf, wl.g2, xn, M, d, c.rms_eps, stream);
+        launch_gemm(GemmArgs{xn, wl.wgu, act, nullptr, M, 2 * F, d, d, F, EPI_SWIGLU}, p_gu, gpartp, stream);
+        launch_gemm(GemmArgs{act, wl.wd, x_out, hbuf, M, d, F, F, d, EPI_RESID}, p_d, gpartp, stream);
+    }
+    HIP_TRY(hipGetLastError());
+    return SLW_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" int slw_create(const slw_model_cfg* cfg, slw_ctx** out) {
+    return guarded([&] {
+        if (!cfg || !out) return fail(SLW_EINVAL, "null argument");
+        *out = nullptr;
+        int rc = check_cfg(*cfg);
+        if (rc) return rc;
+        auto ctx = std::make_unique<slw_ctx>();
+        ctx->cfg = *cfg;
+        ctx->w.assign(cfg->n_layers, slw_layer_weights{});
+        ctx->have_w.assign(cfg->n_layers, 0);
+        *out = ctx.release();
+        return SLW_OK;
+    });
+}
+
+extern "C" int slw_destroy(slw_ctx* ctx) {
+    delete ctx;
+    return SLW_OK;
+}
+
+extern "C" int slw_set_layer_weights(slw_ctx* ctx, int32_t layer, const slw_layer_weights* w) {
+    if (!ctx || !w) return fail(SLW_EINVAL, "null argument");
+    if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(SLW_ERANGE, "layer %d out of range", layer);
+    if (!w->wqkv || !w->wo || !w->wgu || !w->wd || !w->g1 || !w->g2)
+        return fail(SLW_EINVAL, "null weight pointer");
+    const void* ptrs[6] = {w->wqkv, w->wo, w->wgu, w->wd, w->g1, w->g2};
+    for (const void* p : ptrs)
+        if (reinterpret_cast<uintptr_t>(p) % 16) return fail(SLW_EINVAL, "weights must be 16-byte aligned");
+    ctx->w[layer] = *w;
+    ctx->have_w[layer] = 1;
+    return SLW_OK;
+}
+
+extern "C" int slw_kv_init(slw_ctx* ctx, void* k_pool, void* v_pool, int32_t num_blocks) {
+    return guarded([&] {
+        if (!ctx || !k_pool || !v_pool) return fail(SLW_EINVAL, "null argument");
+        if (num_blocks < 1) return fail(SLW_EINVAL, "num_blocks must be >= 1");
+        if (reinterpret_cast<uintptr_t>(k_pool) % 16 || reinterpret_cast<uintptr_t>(v_pool) % 16)
+            return fail(SLW_EINVAL, "pools must be 16-byte aligned");
+        ctx->k_pool = k_pool;
+        ctx->v_pool = v_pool;
+        ctx->kv.reset(num_blocks, 16);
+        ctx->kv_ready = true;
+        return SLW_OK;
+    });
+}
+
+extern "C" int slw_kv_free_blocks(slw_ctx* ctx, int32_t* n_free) {
+    if (!ctx || !n_free) return fail(SLW_EINVAL, "null argument");
+    if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+    *n_free = ctx->kv.free_count();
+    return SLW_OK;
+}
+
+extern "C" int slw_seq_create(slw_ctx* ctx, int64_t id) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+        return ctx->kv.create(id);
+    });
+}
+
+extern "C" int slw_seq_free(slw_ctx* ctx, int64_t id) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+        return ctx->kv.release(id);
+    });
+}
+
+extern "C" int slw_seq_reserve(slw_ctx* ctx, int64_t id, int32_t new_len) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+        if (new_len > ctx->cfg.max_pos) return fail(SLW_ERANGE, "length %d above max_pos", new_len);
+        return ctx->kv.reserve_all({{id, new_len}});
+    });
+}
+
+extern "C" int slw_seq_block_table(slw_ctx* ctx, int64_t id, int32_t* out, int32_t cap, int32_t* n) {
+    return guarded([&] {
+        if (!ctx || !n) return fail(SLW_EINVAL, "null argument");
+        if (!ctx->kv_ready || !ctx->kv.exists(id)) return fail(SLW_EINVAL, "sequence %lld unknown", (long long)id);
+        const auto& t = ctx->kv.table(id);
+        *n = static_cast<int32_t>(t.size());
+        if (out) {
+            if (cap < *n) return fail(SLW_ERANGE, "table has %d entries, cap %d", *n, cap);
+            std::copy(t.begin(), t.end(), out);
+        }
+        return SLW_OK;
+    });
+}
+
+extern "C" int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes) {
+    return guarded([&] {
+        if (!ctx || !bytes) return fail(SLW_EINVAL, "null argument");
+        if (max_C < 0 || max_B < 0) return fail(SLW_EINVAL, "negative size");
+        size_t gp = 0;
+        for (int m = 1; m <= max_C + max_B; ++m) gp = std::max(gp, gemm_partial_bytes(ctx->cfg, m));
+        *bytes = layout(ctx->cfg, max_C, max_B).end_fixed + gp;
+        return SLW_OK;
+    });
+}
+
+extern "C" int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_t B, size_t* offset,
+                                  size_t* bytes) {
+    if (!ctx || !offset || !bytes) return fail(SLW_EINVAL, "null argument");
+    if (C < 0 || B < 0) return fail(SLW_EINVAL, "negative size");
+    const slw_model_cfg& c = ctx->cfg;
+    const Layout L = layout(c, C, B);
+    const size_t M = static_cast<size_t>(C) + B;
+    switch (which) {
+        case SLW_VIEW_QKV: *offset = L.qkv; *bytes = M * qkv_width(c) * 2; break;
+        case SLW_VIEW_ATTN: *offset = L.attn; *bytes = M * c.n_q_heads * c.head_dim * 2; break;
+        case SLW_VIEW_H: *offset = L.h; *bytes = M * c.d_model * 2; break;
+        case SLW_VIEW_ACT: *offset = L.act; *bytes = M * c.ffn_dim * 2; break;
+        default: return fail(SLW_EINVAL, "unknown view %d", which);
+    }
+    return SLW_OK;
+}
+
+extern "C" int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const void* x_in, void* x_out,
+                                   void* ws, size_t ws_bytes, void* stream) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        return mixed_iteration_impl(ctx, batch, x_in, x_out, ws, ws_bytes, static_cast<hipStream_t>(stream));
+    });
+}
+
+extern "C" int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n) {
+    if (!ctx || !n) return fail(SLW_EINVAL, "null argument");
+    *n = static_cast<int32_t>(ctx->last_slots.size());
+    if (out) {
+        if (cap < *n) return fail(SLW_ERANGE, "%d slots, cap %d", *n, cap);
+        std::copy(ctx->last_slots.begin(), ctx->last_slots.end(), out);
+    }
+    return SLW_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Profiler (Sec. 5.1): time the mixed iteration over a (decode batch, chunk)
+// grid, keep every sample, then P50/P99 and a running maximum along chunks.
+// ---------------------------------------------------------------------------
+
+extern "C" int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                    int32_t nb, const slw_profile_opts* o, slw_cost_table** out) {
+    return guarded([&]() -> int {
+        if (!ctx || !o || !out || !c_grid || !b_grid) return fail(SLW_EINVAL, "null argument");
+        *out = nullptr;
+        if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+        if (nc < 1 || nb < 1) return fail(SLW_EINVAL, "empty grid");
+        if (o->repeats < 1 || o->warmup < 0) return fail(SLW_EINVAL, "repeats must be >= 1, warmup >= 0");
+        if (o->prefix_len < 0 || o->ctx_lo < 0 || o->ctx_hi < o->ctx_lo)
+            return fail(SLW_EINVAL, "bad prefix or context range");
+        auto t = std::make_unique<slw_cost_table>();
+        t->c_grid.assign(c_grid, c_grid + nc);
+        t->b_grid.assign(b_grid, b_grid + nb);
+        t->repeats = o->repeats;
+        // validate grids before reserving anything (finish_table repeats the check)
+        t->samples.assign(static_cast<size_t>(nb) * nc * o->repeats, 0);
+        int rc = finish_table(t.get());
+        if (rc) return rc;
+        const int c_last = c_grid[nc - 1], b_last = b_grid[nb - 1];
+
+        const int64_t base = INT64_MIN + 1;  // profiler-reserved ids
+        const int64_t pre_id = base;
+        std::vector<int64_t> dec(b_last);
+        std::vector<int32_t> ctxl(b_last);
+        std::mt19937_64 rng(o->seed);
+        std::uniform_int_distribution<int32_t> dist(o->ctx_lo, o->ctx_hi);
+        for (int i = 0; i < b_last; ++i) {
+            dec[i] = base + 1 + i;
+            ctxl[i] = dist(rng);
+        }
+        std::vector<int64_t> made;
+        auto cleanup = [&] {
+            for (int64_t id : made) (void)ctx->kv.release(id);
+        };
+        rc = ctx->kv.create(pre_id);
+        if (rc) return rc;
+        made.push_back(pre_id);
+        for (int i = 0; i < b_last; ++i) {
+            rc = ctx->kv.create(dec[i]);
+            if (rc) { cleanup(); return rc; }
+            made.push_back(dec[i]);
+        }
+        std::vector<std::pair<int64_t, int32_t>> req;
+        req.emplace_back(pre_id, o->prefix_len + c_last);
+        for (int i = 0; i < b_last; ++i) req.emplace_back(dec[i], ctxl[i] + 1);
+        rc = ctx->kv.reserve_all(req);
+        if (rc) { cleanup(); return rc; }
+
+        hipStream_t s = static_cast<hipStream_t>(o->stream);
+        auto run = [&](int b, int cc) {
+            slw_batch batch{cc, pre_id, o->prefix_len, b, dec.data(), ctxl.data()};
+            return mixed_iteration_impl(ctx, &batch, o->x_in, o->x_out, o->ws, o->ws_bytes, s);
+        };
+        auto sync = [&]() -> int {
+            hipError_t e = hipStreamSynchronize(s);
+            if (e != hipSuccess) return fail(SLW_EHIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
+            return SLW_OK;
+        };
+        for (int i = 0; i < nb && !rc; ++i)
+            for (int j = 0; j < nc && !rc; ++j) {
+                for (int r = 0; r < o->warmup && !rc; ++r) rc = run(b_grid[i], c_grid[j]);
+                if (!rc) rc = sync();
+                for (int r = 0; r < o->repeats && !rc; ++r) {
+                    if (o->flush_buf && o->flush_bytes) {
+                        launch_fill(o->flush_buf, o->flush_bytes, static_cast<uint32_t>(r), s);
+                        rc = sync();
+                        if (rc) break;
+                    }
+                    auto t0 = std::chrono::steady_clock::now();
+                    rc = run(b_grid[i], c_grid[j]);
+                    if (!rc) rc = sync();
+                    auto t1 = std::chrono::steady_clock::now();
+                    t->samples[(static_cast<size_t>(i) * nc + j) * o->repeats + r] =
+                        std::chrono::duration_cast<std::chrono::nanoseconds>(t1 - t0).count();
+                }
+            }
+        cleanup();
+        if (rc) return rc;
+        rc = finish_table(t.get());
+        if (rc) return rc;
+        *out = t.release();
+        return SLW_OK;
+    });
+}

@@ -1,0 +1,191 @@
+"""The C ABI on the CPU: exports, controller, cost table and block manager.
+
+No GPU is touched: these entry points are host code.  The controller, the
+table statistics and the block manager must agree bit-exactly with the
+oracle twins (oracle/schedule.py, oracle/paging.py).
+"""
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle import paging, schedule as S
+from paper_2609_07883_amd import api, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    with open(os.path.join(ROOT, "include", "sloweave.h")) as f:
+        declared = set(re.findall(r"^\s*(?:int|void|const char\*)\s+(slw_\w+)\s*\(", f.read(), re.M))
+    L = api.lib()
+    assert declared == set(api.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def _analytic_table(c_grid, b_grid):
+    vals = [[S.analytic_cost_ns(b, c) for c in c_grid] for b in b_grid]
+    return api.CostTable.from_samples(c_grid, b_grid, np.array(vals)[:, :, None]), \
+        S.CostTable.from_values(c_grid, b_grid, vals)
+
+
+def test_select_chunk_on_full_resolution_analytic_table_matches_worked_examples():
+    c_grid = list(range(0, 4097))
+    b_grid = [0, 1, 8, 32, 128, 256]
+    tab, _ = _analytic_table(c_grid, b_grid)
+    now = 10**9
+    for n, budget, want in [(32, 25_000_000, 3598), (32, 10_000_000, 1098), (1, 25_000_000, 3882),
+                            (8, 10_000_000, 1318), (128, 10_000_000, 218), (256, 10_000_000, 0)]:
+        c, flags, lookups = api.select_chunk(tab, [now + budget] * n, now, 100_000, 4096)
+        assert c == want
+        assert lookups <= math.ceil(math.log2(4097)) + 1
+        assert bool(flags & api.FLAG_DECODE_INFEASIBLE) == (want == 0)
+
+
+@settings(max_examples=200, deadline=None)
+@given(seed=st.integers(0, 2**31), n=st.integers(0, 300), budget=st.integers(-2_000_000, 40_000_000),
+       c_max=st.integers(-5, 6000), rem=st.integers(-2, 7000), margin=st.integers(0, 3_000_000))
+def test_select_chunk_bit_exact_vs_oracle(seed, n, budget, c_max, rem, margin):
+    rng = np.random.default_rng(seed)
+    nc, nb, reps = int(rng.integers(1, 8)), int(rng.integers(1, 6)), int(rng.integers(1, 5))
+    c_grid = [0] + sorted(rng.choice(np.arange(1, 5000), size=nc - 1, replace=False).tolist())
+    b_grid = sorted(rng.choice(np.arange(0, 300), size=nb, replace=False).tolist())
+    samples = rng.integers(500_000, 30_000_000, size=(nb, nc, reps))
+    ct = api.CostTable.from_samples(c_grid, b_grid, samples)
+    ot = S.CostTable(c_grid, b_grid, samples.tolist())
+    now = int(rng.integers(0, 10**12))
+    deadlines = (now + budget + rng.integers(0, 5_000_000, size=n)).tolist()
+    want_err = rem > 0 and n > 0 and n > b_grid[-1]
+    if want_err:
+        with pytest.raises(api.SloweaveError) as e:
+            api.select_chunk(ct, deadlines, now, rem, c_max, margin)
+        assert e.value.code == api.ERANGE
+        with pytest.raises(IndexError):
+            S.select_chunk_table(ot, deadlines, now, rem, c_max, margin)
+        return
+    got = api.select_chunk(ct, deadlines, now, rem, c_max, margin)
+    want = S.select_chunk_table(ot, deadlines, now, rem, c_max, margin)
+    assert got == want
+
+
+def test_cost_table_statistics_and_lookup_bit_exact():
+    rng = np.random.default_rng(5)
+    c_grid = [0, 32, 64, 128, 256, 512, 1024, 2048]
+    b_grid = [0, 1, 4, 16, 64, 256]
+    samples = rng.integers(1_000_000, 20_000_000, size=(len(b_grid), len(c_grid), 100))
+    ct = api.CostTable.from_samples(c_grid, b_grid, samples)
+    ot = S.CostTable(c_grid, b_grid, samples.tolist())
+    assert (ct.values(api.TABLE_SAMPLES) == samples).all()
+    assert ct.values(api.TABLE_P50).tolist() == ot.p50
+    assert ct.values(api.TABLE_P99).tolist() == ot.p99
+    assert ct.values(api.TABLE_THAT).tolist() == ot.t_hat
+    for n in range(0, 257, 7):
+        for c in list(range(0, 2049, 37)) + c_grid:
+            assert ct.lookup(n, c) == ot.lookup(n, c)
+    assert ct.monotone() == ot.monotone_violations()
+    with pytest.raises(api.SloweaveError):
+        ct.lookup(257, 0)
+    with pytest.raises(api.SloweaveError):
+        ct.lookup(0, 2049)
+
+
+def test_cost_table_save_load_roundtrip(tmp_path):
+    rng = np.random.default_rng(6)
+    samples = rng.integers(0, 10**9, size=(3, 4, 7))
+    ct = api.CostTable.from_samples([0, 5, 9, 100], [0, 2, 8], samples)
+    p = str(tmp_path / "t.txt")
+    ct.save(p)
+    back = api.CostTable.load(p)
+    for w in (api.TABLE_SAMPLES, api.TABLE_P50, api.TABLE_P99, api.TABLE_THAT):
+        assert (back.values(w) == ct.values(w)).all()
+    assert [g.tolist() for g in back.grids()] == [[0, 5, 9, 100], [0, 2, 8]]
+
+
+@pytest.mark.parametrize("c_grid,b_grid", [([1, 2], [0]), ([0, 5, 5], [0]), ([0], [3, 1]), ([0], [-1])])
+def test_cost_table_rejects_bad_grids(c_grid, b_grid):
+    with pytest.raises(api.SloweaveError) as e:
+        api.CostTable.from_samples(c_grid, b_grid, np.ones((len(b_grid), len(c_grid), 1)))
+    assert e.value.code == api.EINVAL
+
+
+def _host_ctx(num_blocks):
+    ctx = api.Context.from_shape(synth.TINY)
+    ctx.kv_init(0x10000, 0x20000, num_blocks)   # addresses are only stored, never touched here
+    return ctx
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.lists(st.tuples(st.sampled_from(["create", "reserve", "free"]), st.integers(0, 6),
+                          st.integers(0, 200)), max_size=80))
+def test_block_manager_bit_exact_vs_oracle(ops):
+    ctx = _host_ctx(30)
+    ref = paging.BlockManager(30, 16)
+    live = set()
+    for op, sid, n in ops:
+        if op == "create":
+            if sid in live:
+                with pytest.raises(api.SloweaveError):
+                    ctx.seq_create(sid)
+                continue
+            ctx.seq_create(sid)
+            ref.create(sid)
+            live.add(sid)
+        elif op == "reserve" and sid in live:
+            try:
+                ref.reserve(sid, n)
+                ctx.seq_reserve(sid, n)
+            except paging.OutOfBlocks:
+                with pytest.raises(api.SloweaveError) as e:
+                    ctx.seq_reserve(sid, n)
+                assert e.value.code == api.ENOMEM
+        elif op == "free" and sid in live:
+            ctx.seq_free(sid)
+            ref.free(sid)
+            live.discard(sid)
+        for s in live:
+            assert ctx.block_table(s) == ref.block_table(s)
+        assert ctx.free_blocks() == ref.free_count()
+
+
+def test_block_manager_hand_worked_scenario_through_abi():
+    ctx = _host_ctx(8)
+    ctx.seq_create(1)
+    ctx.seq_create(2)
+    ctx.seq_reserve(1, 20)
+    ctx.seq_reserve(2, 16)
+    ctx.seq_reserve(1, 33)
+    ctx.seq_reserve(2, 17)
+    assert ctx.block_table(1) == [0, 1, 3] and ctx.block_table(2) == [2, 4]
+    ctx.seq_free(1)
+    ctx.seq_create(3)
+    ctx.seq_reserve(3, 40)
+    assert ctx.block_table(3) == [0, 1, 3]
+    with pytest.raises(api.SloweaveError) as e:
+        ctx.seq_reserve(2, 100)
+    assert e.value.code == api.ENOMEM and ctx.block_table(2) == [2, 4]
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, api.EUNSUPPORTED), ("n_kv_heads", 3, api.EINVAL), ("block_size", 32, api.EUNSUPPORTED),
+    ("d_model", 200, api.EUNSUPPORTED), ("n_layers", 0, api.EINVAL)])
+def test_create_rejects_unsupported_shapes(field, value, code):
+    kw = dict(n_layers=1, d_model=256, n_q_heads=4, n_kv_heads=4, head_dim=64, ffn_dim=704,
+              rms_eps=1e-5, rope_theta=1e4, max_pos=4096, block_size=16)
+    kw[field] = value
+    with pytest.raises(api.SloweaveError) as e:
+        api.Context(**kw)
+    assert e.value.code == code
+
+
+def test_workspace_size_grows_with_batch():
+    ctx = api.Context.from_shape(synth.LLAMA8B_LAYER)
+    a = ctx.workspace_size(64, 32)
+    b = ctx.workspace_size(2048, 32)
+    c = ctx.workspace_size(2048, 256)
+    assert 0 < a < b < c
+    off, nb = ctx.workspace_view(api.VIEW_ATTN, 100, 7)
+    assert nb == 107 * 32 * 128 * 2 and off % 256 == 0
