@@ -172,9 +172,10 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  * Reserves KV room (prefill_seq up to prefix_len + C, each decode up to
  * context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
  * it), builds the slot mapping and block tables on the host, uploads them
- * through a pinned staging ring, then enqueues per layer: RMSNorm, QKV GEMM,
- * RoPE with KV append, chunk attention and split decode attention, output
- * GEMM + residual, RMSNorm, gate/up GEMM with SiLU*mul, down GEMM + residual.
+ * through a pinned staging ring, then enqueues per layer: RMSNorm, QKV GEMM
+ * whose epilogue applies RoPE and appends K/V to the pages, chunk attention
+ * and split decode attention, output GEMM + residual (kept in fp32 within the
+ * layer), RMSNorm, gate/up GEMM with SiLU*mul, down GEMM + residual.
  * Each row's K/V is written at slot(seq, pos) = bt[pos/16]*16 + pos%16 of its
  * sequence in every layer.  C == 0 and B == 0 together is a no-op.
  */
@@ -189,7 +190,7 @@ int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n);
  * in the workspace, for inspection after the stream is synchronised:
  *   SLW_VIEW_QKV   bf16 [C+B][(Hq+2Hkv)*hd] (q and k after RoPE)
  *   SLW_VIEW_ATTN  bf16 [C+B][Hq*hd] attention output
- *   SLW_VIEW_H     bf16 [C+B][d] residual stream after attention
+ *   SLW_VIEW_H     fp32 [C+B][d] residual stream after attention
  *   SLW_VIEW_ACT   bf16 [C+B][F] silu(gate) * up
  */
 #define SLW_VIEW_QKV 0
@@ -198,6 +199,21 @@ int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n);
 #define SLW_VIEW_ACT 3
 int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_t B, size_t* offset,
                        size_t* bytes);
+
+/*
+ * Stage telemetry (Fig. 1 and Table 1 record observed iteration durations).
+ * When enabled, slw_mixed_iteration records a HIP event on its stream before
+ * each stage of each layer and after the last one.  slw_stage_times waits for
+ * the last iteration's final event and writes, per stage, the elapsed
+ * milliseconds summed over layers:
+ *   0 RMSNorm (attention)  1 RoPE table    2 QKV GEMM with RoPE and KV append
+ *   3 chunk attention      4 decode attention  5 decode merge  6 output GEMM
+ *   7 RMSNorm (MLP)        8 gate/up GEMM  9 down GEMM
+ * Stages absent from the iteration (C == 0 or B == 0) read 0.
+ */
+#define SLW_N_STAGES 10
+int slw_set_stage_timing(slw_ctx* ctx, int32_t enable);
+int slw_stage_times(slw_ctx* ctx, float* ms, int32_t cap, int32_t* n);
 
 /* ------------------------------------------------------------------------ */
 /* Cost table (Sec. 5.1 profiler: P50/P99 per grid point, cumulative max    */

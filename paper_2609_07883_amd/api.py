@@ -33,8 +33,10 @@ EXPORTS = (
     "slw_workspace_view", "slw_build_cost_table", "slw_cost_table_from_samples",
     "slw_cost_table_free", "slw_cost_table_dims", "slw_cost_table_grids", "slw_cost_table_values",
     "slw_cost_table_lookup", "slw_cost_table_monotone", "slw_cost_table_save",
-    "slw_cost_table_load", "slw_select_chunk",
+    "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
 )
+STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "decode_merge",
+          "o_gemm", "rmsnorm_mlp", "gateup_gemm", "down_gemm")
 
 
 class SloweaveError(RuntimeError):
@@ -108,6 +110,8 @@ def lib() -> C.CDLL:
         "slw_cost_table_save": ([vp, C.c_char_p], C.c_int),
         "slw_cost_table_load": ([C.c_char_p, P(vp)], C.c_int),
         "slw_select_chunk": ([vp, P(i64), i32, i64, i32, i32, i64, P(i32), P(u32), P(i32)], C.c_int),
+        "slw_set_stage_timing": ([vp, i32], C.c_int),
+        "slw_stage_times": ([vp, P(C.c_float), i32, P(i32)], C.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -307,6 +311,16 @@ class Context:
                     _ptr(ds, C.c_int64), _ptr(cl, C.c_int32))
         _check(lib().slw_mixed_iteration(self._h, C.byref(bc), C.c_void_p(x_in), C.c_void_p(x_out),
                                          C.c_void_p(ws), ws_bytes, C.c_void_p(stream)))
+
+    def set_stage_timing(self, enable: bool):
+        _check(lib().slw_set_stage_timing(self._h, 1 if enable else 0))
+
+    def stage_times(self) -> dict:
+        """Per-stage ms of the last iteration (waits for it), summed over layers."""
+        out = np.zeros(len(STAGES), np.float32)
+        n = C.c_int32()
+        _check(lib().slw_stage_times(self._h, _ptr(out, C.c_float), len(out), C.byref(n)))
+        return dict(zip(STAGES, out[: n.value].astype(float).tolist()))
 
     def last_slots(self) -> list:
         n = C.c_int32()

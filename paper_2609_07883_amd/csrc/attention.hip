@@ -410,17 +410,18 @@ void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s) {
     else chunk_attn_kernel<64><<<grid, 256, 0, s>>>(a, heads_per_wg, span);
 }
 
-void launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s) {
+void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s) {
     if (a.b <= 0) return;
     dim3 grid(a.n_work, a.hkv);
-    dim3 mgrid(a.b, a.hq);
-    if (a.hd == 128) {
-        decode_attn_kernel<128><<<grid, 64, 0, s>>>(a);
-        decode_merge_kernel<128><<<mgrid, 64, 0, s>>>(a);
-    } else {
-        decode_attn_kernel<64><<<grid, 64, 0, s>>>(a);
-        decode_merge_kernel<64><<<mgrid, 64, 0, s>>>(a);
-    }
+    if (a.hd == 128) decode_attn_kernel<128><<<grid, 64, 0, s>>>(a);
+    else decode_attn_kernel<64><<<grid, 64, 0, s>>>(a);
+}
+
+void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s) {
+    if (a.b <= 0) return;
+    dim3 grid(a.b, a.hq);
+    if (a.hd == 128) decode_merge_kernel<128><<<grid, 64, 0, s>>>(a);
+    else decode_merge_kernel<64><<<grid, 64, 0, s>>>(a);
 }
 
 }  // namespace slw

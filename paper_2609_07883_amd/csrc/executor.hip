@@ -3,8 +3,10 @@
 // A mixed iteration (Sec. 3: one prefill chunk plus one token for every
 // active decode; Sec. 5.1: the chunk arrives through ordinary sequence
 // metadata) is: host-side reservation and slot mapping, one upload of the
-// per-iteration metadata through a pinned staging ring, then per layer nine
-// launches on the caller's stream.
+// per-iteration metadata through a pinned staging ring, a RoPE table for the
+// iteration's positions, then per layer: RMSNorm, QKV GEMM (RoPE and KV
+// append in its epilogue), chunk and decode attention, output GEMM into an
+// fp32 residual, RMSNorm, gate/up GEMM (SiLU*mul epilogue), down GEMM.
 #include <algorithm>
 #include <chrono>
 #include <cstring>
@@ -54,6 +56,12 @@ struct slw_ctx {
     hipEvent_t staged[kRing] = {};
     int ring = 0;
 
+    // stage telemetry: events [layer][stage boundary]
+    bool stage_timing = false;
+    std::vector<hipEvent_t> stage_ev;
+    bool stage_valid = false;
+    uint32_t stage_mask = 0;  // stages the last iteration ran
+
     ~slw_ctx() {
         if (!hip_ready) return;
         for (int i = 0; i < kRing; ++i) {
@@ -63,6 +71,7 @@ struct slw_ctx {
             }
             if (staging[i]) (void)hipHostFree(staging[i]);
         }
+        for (hipEvent_t e : stage_ev) (void)hipEventDestroy(e);
     }
 };
 
@@ -91,7 +100,7 @@ size_t meta_ints(const slw_model_cfg& c, int C, int B) {
 }
 
 struct Layout {
-    size_t xn, qkv, attn, h, act, meta, part_o, part_ml, gemm_part, end_fixed;
+    size_t xn, qkv, attn, h, act, rope, meta, part_o, part_ml, gemm_part, end_fixed;
 };
 
 Layout layout(const slw_model_cfg& c, int C, int B) {
@@ -107,8 +116,9 @@ Layout layout(const slw_model_cfg& c, int C, int B) {
     L.xn = take(M * c.d_model * 2);
     L.qkv = take(M * qkv_width(c) * 2);
     L.attn = take(M * c.n_q_heads * c.head_dim * 2);
-    L.h = take(M * c.d_model * 2);
+    L.h = take(M * c.d_model * 4);  // fp32 residual stream inside the layer
     L.act = take(M * c.ffn_dim * 2);
+    L.rope = take(M * (c.head_dim / 2) * 8);
     L.meta = take(meta_ints(c, C, B) * 4);
     L.part_o = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * c.head_dim * 4 : 0);
     L.part_ml = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * 2 * 4 : 0);
@@ -168,6 +178,18 @@ int next_staging(slw_ctx* ctx, size_t n, int32_t** buf, int* slot_out) {
     }
     *buf = ctx->staging[slot];
     *slot_out = slot;
+    return SLW_OK;
+}
+
+constexpr int kStages = SLW_N_STAGES;
+
+int ensure_stage_events(slw_ctx* ctx) {
+    const size_t need = static_cast<size_t>(ctx->cfg.n_layers) * (kStages + 1);
+    while (ctx->stage_ev.size() < need) {
+        hipEvent_t e;
+        HIP_TRY(hipEventCreate(&e));
+        ctx->stage_ev.push_back(e);
+    }
     return SLW_OK;
 }
 
@@ -298,6 +320,7 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     void* attn = wsb + L.attn;
     void* hbuf = wsb + L.h;
     void* act = wsb + L.act;
+    float2* rope = reinterpret_cast<float2*>(wsb + L.rope);
     void* gpartp = wsb + L.gemm_part;
 
     const int d = c.d_model, hq = c.n_q_heads, hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
@@ -308,20 +331,44 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     const GemmPlan p_d = plan_gemm(M, d, F);
     const size_t layer_pool = static_cast<size_t>(ctx->kv.num_blocks()) * hkv * hd * 16 * 2;
 
+    const bool timing = ctx->stage_timing;
+    ctx->stage_valid = false;
+    if (timing) {
+        rc = ensure_stage_events(ctx);
+        if (rc) return rc;
+    }
+    auto mark = [&](int l, int stage) -> int {
+        if (timing) HIP_TRY(hipEventRecord(ctx->stage_ev[static_cast<size_t>(l) * (kStages + 1) + stage], stream));
+        return SLW_OK;
+    };
+
     for (int l = 0; l < c.n_layers; ++l) {
         const slw_layer_weights& wl = ctx->w[l];
         const void* cur = l == 0 ? x_in : x_out;
         void* kp = static_cast<char*>(ctx->k_pool) + l * layer_pool;
         void* vp = static_cast<char*>(ctx->v_pool) + l * layer_pool;
 
-        launch_rmsnorm(cur, wl.g1, xn, M, d, c.rms_eps, stream);
-        launch_gemm(GemmArgs{xn, wl.wqkv, qkv, nullptr, M, qw, d, d, qw, EPI_STORE}, p_qkv, gpartp, stream);
-        launch_rope_append(RopeAppendArgs{qkv, d_pos, d_slot, kp, vp, M, hq, hkv, hd,
-                                          static_cast<double>(c.rope_theta)},
-                           stream);
+        if ((rc = mark(l, 0))) return rc;
+        launch_rmsnorm(cur, false, wl.g1, xn, M, d, c.rms_eps, stream);
+        if ((rc = mark(l, 1))) return rc;
+        if (l == 0) launch_rope_table(d_pos, rope, M, hd, static_cast<double>(c.rope_theta), stream);
+        if ((rc = mark(l, 2))) return rc;
+        {
+            GemmArgs ga{xn, wl.wqkv, qkv, nullptr, M, qw, d, d, qw, EPI_QKV};
+            ga.rope_cs = rope;
+            ga.slot = d_slot;
+            ga.k_pool = kp;
+            ga.v_pool = vp;
+            ga.hq = hq;
+            ga.hkv = hkv;
+            ga.hd = hd;
+            launch_gemm(ga, p_qkv, gpartp, stream);
+        }
+        if ((rc = mark(l, 3))) return rc;
         if (C > 0)
             launch_chunk_attention(ChunkAttnArgs{qkv, attn, kp, vp, dmeta + o_pre, C, P, hq, hkv, hd, qw},
                                    stream);
+        if ((rc = mark(l, 4))) return rc;
         if (B > 0) {
             DecodeAttnArgs da{};
             da.q = static_cast<const char*>(qkv) + static_cast<size_t>(C) * qw * 2;
@@ -343,14 +390,28 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             da.hkv = hkv;
             da.hd = hd;
             da.ld_q = qw;
-            launch_decode_attention(da, stream);
+            launch_decode_attention_split(da, stream);
+            if ((rc = mark(l, 5))) return rc;
+            launch_decode_merge(da, stream);
+        } else if ((rc = mark(l, 5))) {
+            return rc;
         }
-        launch_gemm(GemmArgs{attn, wl.wo, hbuf, cur, M, d, hq * hd, hq * hd, d, EPI_RESID}, p_o, gpartp, stream);
-        launch_rmsnorm(hbuf, wl.g2, xn, M, d, c.rms_eps, stream);
+        if ((rc = mark(l, 6))) return rc;
+        launch_gemm(GemmArgs{attn, wl.wo, hbuf, cur, M, d, hq * hd, hq * hd, d, EPI_RESID_F32OUT}, p_o, gpartp,
+                    stream);
+        if ((rc = mark(l, 7))) return rc;
+        launch_rmsnorm(hbuf, true, wl.g2, xn, M, d, c.rms_eps, stream);
+        if ((rc = mark(l, 8))) return rc;
         launch_gemm(GemmArgs{xn, wl.wgu, act, nullptr, M, 2 * F, d, d, F, EPI_SWIGLU}, p_gu, gpartp, stream);
-        launch_gemm(GemmArgs{act, wl.wd, x_out, hbuf, M, d, F, F, d, EPI_RESID}, p_d, gpartp, stream);
+        if ((rc = mark(l, 9))) return rc;
+        launch_gemm(GemmArgs{act, wl.wd, x_out, hbuf, M, d, F, F, d, EPI_RESID_F32IN}, p_d, gpartp, stream);
+        if ((rc = mark(l, 10))) return rc;
     }
     HIP_TRY(hipGetLastError());
+    if (timing) {
+        ctx->stage_valid = true;
+        ctx->stage_mask = 0x3FFu & ~(C > 0 ? 0u : (1u << 3)) & ~(B > 0 ? 0u : (3u << 4));
+    }
     return SLW_OK;
 }
 
@@ -474,7 +535,7 @@ extern "C" int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_
     switch (which) {
         case SLW_VIEW_QKV: *offset = L.qkv; *bytes = M * qkv_width(c) * 2; break;
         case SLW_VIEW_ATTN: *offset = L.attn; *bytes = M * c.n_q_heads * c.head_dim * 2; break;
-        case SLW_VIEW_H: *offset = L.h; *bytes = M * c.d_model * 2; break;
+        case SLW_VIEW_H: *offset = L.h; *bytes = M * c.d_model * 4; break;
         case SLW_VIEW_ACT: *offset = L.act; *bytes = M * c.ffn_dim * 2; break;
         default: return fail(SLW_EINVAL, "unknown view %d", which);
     }
@@ -487,6 +548,35 @@ extern "C" int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const v
         if (!ctx) return fail(SLW_EINVAL, "null context");
         return mixed_iteration_impl(ctx, batch, x_in, x_out, ws, ws_bytes, static_cast<hipStream_t>(stream));
     });
+}
+
+extern "C" int slw_set_stage_timing(slw_ctx* ctx, int32_t enable) {
+    if (!ctx) return fail(SLW_EINVAL, "null context");
+    ctx->stage_timing = enable != 0;
+    ctx->stage_valid = false;
+    return SLW_OK;
+}
+
+extern "C" int slw_stage_times(slw_ctx* ctx, float* ms, int32_t cap, int32_t* n) {
+    if (!ctx || !ms || !n) return fail(SLW_EINVAL, "null argument");
+    if (!ctx->stage_valid) return fail(SLW_EINVAL, "no timed iteration (enable slw_set_stage_timing first)");
+    if (cap < kStages) return fail(SLW_ERANGE, "need room for %d stages", kStages);
+    const size_t last = static_cast<size_t>(ctx->cfg.n_layers) * (kStages + 1) - 1;
+    HIP_TRY(hipEventSynchronize(ctx->stage_ev[last]));
+    for (int s = 0; s < kStages; ++s) {
+        float tot = 0.f;
+        if (ctx->stage_mask & (1u << s)) {
+            for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+                float t = 0.f;
+                const size_t base = static_cast<size_t>(l) * (kStages + 1);
+                HIP_TRY(hipEventElapsedTime(&t, ctx->stage_ev[base + s], ctx->stage_ev[base + s + 1]));
+                tot += t;
+            }
+        }
+        ms[s] = tot;
+    }
+    *n = kStages;
+    return SLW_OK;
 }
 
 extern "C" int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n) {

@@ -4,15 +4,19 @@
 // computes a BM x BN tile; k advances in steps of 64 through a double-buffered
 // LDS tile (one barrier per step, next tile prefetched into registers while
 // the current one feeds the matrix cores).  LDS rows are 128 bytes; the
-// 16-byte chunk c of row r is stored at c ^ ((r >> 1) & 7) so that the
-// 32 rows read by one MFMA operand load hit distinct banks.
+// 16-byte chunk c of row r is stored at c ^ ((r >> 1) & 7) so that the rows
+// read by one MFMA operand load hit distinct banks.
 //
-// Epilogues: plain store, residual add, and SwiGLU.  For SwiGLU the B tile
-// interleaves 32-row blocks of gate and up rows, so each wave holds the gate
-// and up accumulators of the same output column in the same lane and writes
-// silu(gate) * up directly.  Small problems split k across work-groups; the
-// fp32 partial sums are then reduced by a second kernel that applies the
-// epilogue.
+// Each wave's 64 columns are two 32-column MFMA tiles whose accumulators sit
+// in the same lanes at the same element index.  Two epilogues use that by
+// choosing which W rows feed the two tiles:
+//   SwiGLU: tile 0 takes gate rows, tile 1 the matching up rows, so a lane
+//           holds gate and up of one output and writes silu(gate) * up;
+//   QKV:    within each head, tile 0 takes dims i and tile 1 dims i + hd/2,
+//           so a lane holds both halves of a RoPE pair, rotates them, and
+//           writes q, or writes k and v straight into their KV pages.
+// Small problems split k across work-groups; fp32 partial sums are then
+// reduced by a second kernel that applies the same epilogue.
 #include <math.h>
 
 #include "device.h"
@@ -26,15 +30,56 @@ constexpr int kThreads = 256;
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-// W row feeding B-tile row r of the tile starting at B column n0.
+// Head-local order of 32-dim blocks for hd = 128: B blocks 0,1,2,3 hold dims
+// blocks 0,2,1,3 (the map is its own inverse).  hd = 64 needs no reordering.
+__device__ __forceinline__ int qkv_dim(int cw, int hd) {
+    if (hd != 128) return cw;
+    const int b = cw >> 5;
+    return ((((b & 1) << 1) | (b >> 1)) << 5) | (cw & 31);
+}
+
+// W row feeding B column c (c = n0 + tile row).
 template <int EPI>
-__device__ __forceinline__ int w_row(int n0, int r, int n) {
+__device__ __forceinline__ int w_row(const GemmArgs& g, int c) {
     if (EPI == EPI_SWIGLU) {
-        const int sub = r >> 5, f = n >> 1;
-        const int col = (n0 >> 1) + (sub >> 1) * 32 + (r & 31);
+        const int sub = c >> 5, f = g.n >> 1;
+        const int col = (sub >> 1) * 32 + (c & 31);
         return (sub & 1) ? f + col : col;
     }
-    return n0 + r;
+    if (EPI == EPI_QKV) {
+        const int cw = c % g.hd;
+        return c - cw + qkv_dim(cw, g.hd);
+    }
+    return c;
+}
+
+// Rotate (x0, x1) = dims (d0, d0 + hd/2) of head hg of row `row` (q and k
+// heads) and store; k and v also go to their KV page at slot[row].
+__device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, int d0, float x0, float x1) {
+    const int d1 = d0 + g.hd / 2;
+    bf16* out = static_cast<bf16*>(g.out) + static_cast<size_t>(row) * g.ldo + hg * g.hd;
+    if (hg < g.hq + g.hkv) {
+        const float2 cs = g.rope_cs[row * (g.hd / 2) + d0];
+        const float y0 = x0 * cs.x - x1 * cs.y;
+        const float y1 = x1 * cs.x + x0 * cs.y;
+        x0 = y0;
+        x1 = y1;
+    }
+    const bf16 b0 = f2bf(x0), b1 = f2bf(x1);
+    out[d0] = b0;
+    out[d1] = b1;
+    if (hg < g.hq) return;
+    const int slot = g.slot[row];
+    const size_t blk = slot >> 4, t = slot & 15;
+    if (hg < g.hq + g.hkv) {
+        bf16* pg = static_cast<bf16*>(g.k_pool) + (blk * g.hkv + (hg - g.hq)) * g.hd * 16;
+        pg[(d0 >> 5) * 512 + t * 32 + (d0 & 31)] = b0;
+        pg[(d1 >> 5) * 512 + t * 32 + (d1 & 31)] = b1;
+    } else {
+        bf16* pg = static_cast<bf16*>(g.v_pool) + (blk * g.hkv + (hg - g.hq - g.hkv)) * g.hd * 16;
+        pg[d0 * 16 + t] = b0;
+        pg[d1 * 16 + t] = b1;
+    }
 }
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
@@ -48,6 +93,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
     constexpr int B_LOADS = BN * 8 / kThreads;
     static_assert((BM / WM) * (BN / WN) == 4, "four waves");
     static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small");
+    static_assert(WN == 64, "paired epilogues need 64-column wave tiles");
 
     __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
     __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * BK];
@@ -61,7 +107,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
     const bf16* A = static_cast<const bf16*>(g.a);
     const bf16* W = static_cast<const bf16*>(g.w);
 
-    // per-thread global source pointers (row fixed for the whole k loop)
     const bf16* a_src[A_LOADS];
     bool a_ok[A_LOADS];
     int a_lds[A_LOADS];
@@ -77,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
 #pragma unroll
     for (int i = 0; i < B_LOADS; ++i) {
         const int idx = tid + i * kThreads, row = idx >> 3, ch = idx & 7;
-        b_src[i] = W + static_cast<size_t>(w_row<EPI>(n0, row, g.n)) * g.k + kb + ch * 8;
+        b_src[i] = W + static_cast<size_t>(w_row<EPI>(g, n0 + row)) * g.k + kb + ch * 8;
         b_lds[i] = row * BK + swz(row, ch) * 8;
     }
 
@@ -104,7 +149,6 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
-    // LDS element offsets of this lane's operand rows
     int a_row[TM], b_row[TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i) a_row[i] = wm * WM + i * 32 + (lane & 31);
@@ -138,71 +182,88 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
         __syncthreads();
     }
 
-    // epilogue
+    // epilogue: element e of tile (i, j) is row rbase + i*32 + 8(e/4) + e%4,
+    // B column n0 + wn*WN + j*32 + lane%32
     const int rbase = m0 + wm * WM + 4 * (lane >> 5);
+    const int cbase = n0 + wn * WN + (lane & 31);
     if (SPLIT) {
         float* P = partial + static_cast<size_t>(blockIdx.z) * g.m * g.n;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int col = n0 + wn * WN + j * 32 + (lane & 31);
+            for (int j = 0; j < TN; ++j)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-                    if (row < g.m) P[static_cast<size_t>(row) * g.n + col] = acc[i][j][e];
+                    if (row < g.m) P[static_cast<size_t>(row) * g.n + cbase + j * 32] = acc[i][j][e];
                 }
-            }
         return;
     }
-    bf16* out = static_cast<bf16*>(g.out);
-    const bf16* res = static_cast<const bf16*>(g.resid);
-    if (EPI == EPI_SWIGLU) {
+    if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
+        const int c0 = n0 + wn * WN;  // first B column of this wave (tile 0)
+        int hg = 0, d0 = 0, fcol = 0;
+        if (EPI == EPI_QKV) {
+            hg = c0 / g.hd;
+            d0 = ((c0 % g.hd) / 64) * 32 + (lane & 31);
+        } else {
+            fcol = (c0 >> 1) + (lane & 31);
+        }
+        bf16* out = static_cast<bf16*>(g.out);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int p = 0; p < TN / 2; ++p) {
-                const int col = ((n0 + wn * WN) >> 1) + p * 32 + (lane & 31);
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-                    if (row < g.m)
-                        out[static_cast<size_t>(row) * g.ldo + col] =
-                            f2bf(silu(acc[i][2 * p][e]) * acc[i][2 * p + 1][e]);
-                }
+            for (int e = 0; e < 16; ++e) {
+                const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+                if (row >= g.m) continue;
+                if (EPI == EPI_QKV) qkv_store(g, row, hg, d0, acc[i][0][e], acc[i][1][e]);
+                else out[static_cast<size_t>(row) * g.ldo + fcol] = f2bf(silu(acc[i][0][e]) * acc[i][1][e]);
             }
         return;
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * WN + j * 32 + (lane & 31);
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-                if (row < g.m) {
-                    float v = acc[i][j][e];
-                    const size_t o = static_cast<size_t>(row) * g.ldo + col;
-                    if (EPI == EPI_RESID) v += bf2f(res[o]);
-                    out[o] = f2bf(v);
-                }
+                if (row >= g.m) continue;
+                const size_t o = static_cast<size_t>(row) * g.ldo + cbase + j * 32;
+                if (EPI == EPI_RESID_F32OUT)
+                    static_cast<float*>(g.out)[o] = acc[i][j][e] + bf2f(static_cast<const bf16*>(g.resid)[o]);
+                else
+                    static_cast<bf16*>(g.out)[o] = f2bf(acc[i][j][e] + static_cast<const float*>(g.resid)[o]);
             }
-        }
 }
 
-// Sum split-K partials [splits][m][n] and apply the epilogue; 4 outputs per thread.
+// Sum split-K partials [splits][m][n] (B column order) and apply the epilogue.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const float* __restrict__ part,
                                                             int splits) {
+    const size_t slab = static_cast<size_t>(g.m) * g.n;
+    const size_t idx = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
+    if (EPI == EPI_QKV) {  // one thread per RoPE pair
+        const int pairs = g.n / 2, half = g.hd / 2;
+        if (idx >= static_cast<size_t>(g.m) * pairs) return;
+        const int row = static_cast<int>(idx / pairs), j = static_cast<int>(idx % pairs);
+        const int hg = j / half, d0 = j % half;
+        const size_t c0 = static_cast<size_t>(hg) * g.hd + qkv_dim(d0, g.hd);
+        const size_t c1 = static_cast<size_t>(hg) * g.hd + qkv_dim(d0 + half, g.hd);
+        float x0 = 0.f, x1 = 0.f;
+        for (int z = 0; z < splits; ++z) {
+            const float* p = part + z * slab + static_cast<size_t>(row) * g.n;
+            x0 += p[c0];
+            x1 += p[c1];
+        }
+        qkv_store(g, row, hg, d0, x0, x1);
+        return;
+    }
     const int n_out = (EPI == EPI_SWIGLU) ? g.n / 2 : g.n;
     const int per_row = n_out / 4;
-    const size_t idx = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
     if (idx >= static_cast<size_t>(g.m) * per_row) return;
     const int row = static_cast<int>(idx / per_row);
     const int c4 = static_cast<int>(idx % per_row) * 4;
-    const size_t slab = static_cast<size_t>(g.m) * g.n;
-    bf16* out = static_cast<bf16*>(g.out) + static_cast<size_t>(row) * g.ldo + c4;
+    const size_t o = static_cast<size_t>(row) * g.ldo + c4;
     if (EPI == EPI_SWIGLU) {
         const int gc = (c4 >> 5) * 64 + (c4 & 31);  // gate column in B order; up is +32
         f32x4 gs = {}, us = {};
@@ -211,6 +272,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
             gs += *reinterpret_cast<const f32x4*>(p);
             us += *reinterpret_cast<const f32x4*>(p + 32);
         }
+        bf16* out = static_cast<bf16*>(g.out) + o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) out[e] = f2bf(silu(gs[e]) * us[e]);
         return;
@@ -218,13 +280,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
     f32x4 s = {};
     for (int z = 0; z < splits; ++z)
         s += *reinterpret_cast<const f32x4*>(part + z * slab + static_cast<size_t>(row) * g.n + c4);
-    if (EPI == EPI_RESID) {
-        const bf16* r = static_cast<const bf16*>(g.resid) + static_cast<size_t>(row) * g.ldo + c4;
+    if (EPI == EPI_RESID_F32OUT) {
+        const bf16* r = static_cast<const bf16*>(g.resid) + o;
 #pragma unroll
         for (int e = 0; e < 4; ++e) s[e] += bf2f(r[e]);
-    }
+        *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + o) = s;
+    } else {
+        s += *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.resid) + o);
+        bf16* out = static_cast<bf16*>(g.out) + o;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) out[e] = f2bf(s[e]);
+        for (int e = 0; e < 4; ++e) out[e] = f2bf(s[e]);
+    }
 }
 
 struct TileCfg {
@@ -232,31 +298,30 @@ struct TileCfg {
 };
 constexpr TileCfg kCfgs[3] = {{128, 128}, {64, 128}, {32, 256}};
 
-template <int BM, int BN, int WM, int WN>
-void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
+template <int BM, int BN, int WM, int WN, int EPI>
+void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
     dim3 grid(g.n / BN, (g.m + BM - 1) / BM, p.splits);
     const int kps = g.k / p.splits;
-    float* part = static_cast<float*>(partial);
-    if (p.splits > 1) {
-        switch (g.epi) {
-            case EPI_STORE: gemm_kernel<BM, BN, WM, WN, EPI_STORE, true><<<grid, kThreads, 0, s>>>(g, part, kps); break;
-            case EPI_RESID: gemm_kernel<BM, BN, WM, WN, EPI_RESID, true><<<grid, kThreads, 0, s>>>(g, part, kps); break;
-            default: gemm_kernel<BM, BN, WM, WN, EPI_SWIGLU, true><<<grid, kThreads, 0, s>>>(g, part, kps); break;
-        }
-        const int n_out = g.epi == EPI_SWIGLU ? g.n / 2 : g.n;
-        const size_t work = static_cast<size_t>(g.m) * (n_out / 4);
-        const int blocks = static_cast<int>((work + 255) / 256);
-        switch (g.epi) {
-            case EPI_STORE: splitk_reduce_kernel<EPI_STORE><<<blocks, 256, 0, s>>>(g, part, p.splits); break;
-            case EPI_RESID: splitk_reduce_kernel<EPI_RESID><<<blocks, 256, 0, s>>>(g, part, p.splits); break;
-            default: splitk_reduce_kernel<EPI_SWIGLU><<<blocks, 256, 0, s>>>(g, part, p.splits); break;
-        }
+    if (p.splits == 1) {
+        gemm_kernel<BM, BN, WM, WN, EPI, false><<<grid, kThreads, 0, s>>>(g, nullptr, kps);
         return;
     }
+    gemm_kernel<BM, BN, WM, WN, EPI, true><<<grid, kThreads, 0, s>>>(g, part, kps);
+    size_t work;
+    if (EPI == EPI_QKV) work = static_cast<size_t>(g.m) * (g.n / 2);
+    else if (EPI == EPI_SWIGLU) work = static_cast<size_t>(g.m) * (g.n / 8);
+    else work = static_cast<size_t>(g.m) * (g.n / 4);
+    splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, p.splits);
+}
+
+template <int BM, int BN, int WM, int WN>
+void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
+    float* part = static_cast<float*>(partial);
     switch (g.epi) {
-        case EPI_STORE: gemm_kernel<BM, BN, WM, WN, EPI_STORE, false><<<grid, kThreads, 0, s>>>(g, nullptr, kps); break;
-        case EPI_RESID: gemm_kernel<BM, BN, WM, WN, EPI_RESID, false><<<grid, kThreads, 0, s>>>(g, nullptr, kps); break;
-        default: gemm_kernel<BM, BN, WM, WN, EPI_SWIGLU, false><<<grid, kThreads, 0, s>>>(g, nullptr, kps); break;
+        case EPI_RESID_F32OUT: launch_epi<BM, BN, WM, WN, EPI_RESID_F32OUT>(g, p, part, s); break;
+        case EPI_RESID_F32IN: launch_epi<BM, BN, WM, WN, EPI_RESID_F32IN>(g, p, part, s); break;
+        case EPI_SWIGLU: launch_epi<BM, BN, WM, WN, EPI_SWIGLU>(g, p, part, s); break;
+        default: launch_epi<BM, BN, WM, WN, EPI_QKV>(g, p, part, s); break;
     }
 }
 

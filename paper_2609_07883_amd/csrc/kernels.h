@@ -7,33 +7,35 @@
 
 namespace slw {
 
-// y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g, rows of d bf16 values.
-void launch_rmsnorm(const void* x, const void* g, void* y, int rows, int d, float eps,
+// y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g over rows of d values; x is bf16
+// or (x_f32) fp32, y is bf16.
+void launch_rmsnorm(const void* x, bool x_f32, const void* g, void* y, int rows, int d, float eps,
                     hipStream_t s);
 
-// Rotate q and k of every row of qkv in place (rotate-half RoPE at pos[r]) and
-// append k (rotated) and v to the paged pools at slot[r].
-struct RopeAppendArgs {
-    void* qkv;             // bf16 [rows][(hq + 2 hkv) * hd]
-    const int32_t* pos;    // [rows]
-    const int32_t* slot;   // [rows]
-    void* k_pool;          // bf16 pages of this layer
-    void* v_pool;
-    int rows, hq, hkv, hd;
-    double theta;
-};
-void launch_rope_append(const RopeAppendArgs& a, hipStream_t s);
+// cs[r][i] = (cos, sin) of pos[r] * theta^(-2i/hd), i < hd/2, formed in double.
+void launch_rope_table(const int32_t* pos, float2* cs, int rows, int hd, double theta, hipStream_t s);
 
-// GEMM out = A W^T with an epilogue.
-enum GemmEpilogue { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+// GEMM out = A W^T with an epilogue:
+//   EPI_RESID_F32OUT  out fp32 = acc + resid (bf16)
+//   EPI_RESID_F32IN   out bf16 = acc + resid (fp32)
+//   EPI_SWIGLU        W holds gate rows then up rows (n = 2f); out bf16 [m][f] = silu(gate) * up
+//   EPI_QKV           W is the fused q/k/v projection; out bf16 [m][n] holds q and k rotated by
+//                     RoPE and v; k and v are also appended to the paged pools at slot[r]
+enum GemmEpilogue { EPI_RESID_F32OUT = 0, EPI_RESID_F32IN = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
 struct GemmArgs {
     const void* a;      // bf16 [m][k], row stride lda
-    const void* w;      // bf16 [n][k] (EPI_SWIGLU: [2 f][k], gate rows then up rows)
-    void* out;          // bf16 [m][n_out], row stride ldo
-    const void* resid;  // bf16 [m][n_out], row stride ldo (EPI_RESID)
-    int m, n, k;        // n counts W rows (2 f for EPI_SWIGLU)
+    const void* w;      // bf16 [n][k]
+    void* out;          // [m][n_out], row stride ldo
+    const void* resid;  // [m][n_out], row stride ldo
+    int m, n, k;        // n counts W rows
     int lda, ldo;
     int epi;
+    // EPI_QKV only
+    const float2* rope_cs;  // [m][hd/2]
+    const int32_t* slot;    // [m]
+    void* k_pool;           // this layer's pages
+    void* v_pool;
+    int hq, hkv, hd;
 };
 struct GemmPlan {
     int cfg;      // tile configuration index
@@ -72,7 +74,8 @@ struct DecodeAttnArgs {
     float* part_ml;          // [n_work][hq][2]
     int b, n_work, split_tokens, hq, hkv, hd, ld_q;
 };
-void launch_decode_attention(const DecodeAttnArgs& a, hipStream_t s);
+void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
+void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s);
 
 // Fill `bytes` of device memory with a byte pattern (last-level cache flush).
 void launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);

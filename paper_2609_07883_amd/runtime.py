@@ -80,10 +80,11 @@ class Session:
         torch.cuda.synchronize(self.dev)
         return tensor_to_f64(self.x_out[:rows])
 
-    def view(self, which: int, c: int, b: int, cols: int) -> np.ndarray:
+    def view(self, which: int, c: int, b: int, cols: int, fp32: bool = False) -> np.ndarray:
+        """A workspace intermediate of the last iteration (see slw_workspace_view)."""
         torch.cuda.synchronize(self.dev)
         off, nbytes = self.ctx.workspace_view(which, c, b)
-        t = self.ws[off: off + nbytes].view(torch.bfloat16).view(c + b, cols)
+        t = self.ws[off: off + nbytes].view(torch.float32 if fp32 else torch.bfloat16).view(c + b, cols)
         return tensor_to_f64(t)
 
     # -- cached K/V in the pool layout ---------------------------------------------

@@ -1,0 +1,163 @@
+"""Parity helpers: run the same seeded iteration through the library and the oracle.
+
+Tolerance: the stated bound is a maximum relative error of 2e-2 for bf16
+inputs with fp32 accumulation.  It is applied per output vector (a token's
+row of the layer output, or one head of an appended K/V row):
+
+    rel = max over vectors v of  max_i |g_vi - r_vi| / max_i |r_vi|
+
+and must stay <= 2e-2.  An elementwise denominator (|r_i| + rms(r)) is also
+reported (``elementwise_err``); its maximum over ~10^6 outputs sits near 2e-2
+for any path that stores its GEMM inputs in bf16, as an exact CPU emulation
+of those rounding points shows, so it is reported rather than asserted.
+The rms error ||g - r|| / ||r|| must stay below 1e-2.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import layer as OL
+from oracle import paging as OP
+from paper_2609_07883_amd import api, synth
+
+TOL = 2e-2
+RMS_TOL = 1e-2
+
+
+def rel_err(got, ref) -> float:
+    """Largest per-vector (last axis) max-norm relative error."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    num = np.max(np.abs(got - ref), axis=-1)
+    den = np.max(np.abs(ref), axis=-1)
+    return float(np.max(num / np.maximum(den, 1e-30)))
+
+
+def rms_err(got, ref) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    return float(np.sqrt(np.sum((got - ref) ** 2) / max(np.sum(ref * ref), 1e-300)))
+
+
+def elementwise_err(got, ref) -> float:
+    """max_i |g_i - r_i| / (|r_i| + rms(r)) over the whole tensor."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    return float(np.max(np.abs(got - ref) / (np.abs(ref) + rms + 1e-30)))
+
+
+def check(got, ref, what: str = "") -> dict:
+    """Assert the parity bar; return the three error figures."""
+    e = {"rel": rel_err(got, ref), "rms": rms_err(got, ref), "elementwise": elementwise_err(got, ref)}
+    assert e["rel"] <= TOL and e["rms"] <= RMS_TOL, f"{what} parity: {e}"
+    return e
+
+
+def oracle_shape(s: synth.ModelShape) -> OL.LayerShape:
+    return OL.LayerShape(s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.ffn_dim, s.rms_eps,
+                         s.rope_theta)
+
+
+def oracle_weights(bits: synth.LayerBits) -> OL.LayerWeights:
+    return OL.LayerWeights(**bits.as_f64())
+
+
+class Mirror:
+    """A GPU session and its oracle twin driven through the same iterations (layer 0 .. L-1)."""
+
+    def __init__(self, session, seed: int = 7):
+        self.s = session
+        self.shape = oracle_shape(session.shape)
+        self.w = [oracle_weights(b) for b in session.layer_bits]
+        self.kv = [OL.KVState() for _ in self.w]
+        self.mgr = OP.BlockManager(session.num_blocks, 16)
+        self.seed = seed
+
+    def create(self, sid: int):
+        self.s.ctx.seq_create(sid)
+        self.mgr.create(sid)
+
+    def install_context(self, sid: int, length: int):
+        """Reserve `length` positions and fill them with seeded N(0,1) K/V in every layer."""
+        if length == 0:
+            return
+        self.s.ctx.seq_reserve(sid, length)
+        self.mgr.reserve(sid, length)
+        sh = self.s.shape
+        for layer in range(sh.n_layers):
+            kb, vb = synth.cached_kv(length, sh.n_kv_heads, sh.head_dim, self.seed, layer, sid)
+            self.s.write_kv(layer, sid, kb, vb)
+            self.kv[layer].seqs[sid] = OL.SeqCache(synth.bf16_to_f64(kb), synth.bf16_to_f64(vb))
+
+    def step(self, batch: api.Batch, x_bits, rows=None):
+        """Run one iteration on both sides; returns (gpu_y, oracle_y, gpu_slots, oracle_slots)."""
+        self.s.run(batch, x_bits)
+        y_gpu = self.s.output(batch.rows)
+        slots_gpu = self.s.ctx.last_slots()
+        slots_ref, _ = OP.iteration_metadata(self.mgr, batch.chunk, batch.prefill_seq,
+                                             batch.prefix_len, batch.decode_seqs, batch.context_lens)
+        ob = OL.MixedBatch(batch.chunk, batch.prefill_seq, batch.prefix_len,
+                           list(batch.decode_seqs), list(batch.context_lens))
+        x = synth.bf16_to_f64(x_bits)
+        for layer in range(len(self.w)):
+            x = OL.mixed_iteration(self.shape, self.w[layer], x, self.kv[layer], ob,
+                                   rows=rows if layer == len(self.w) - 1 else None)
+        return y_gpu, x, slots_gpu, slots_ref
+
+    def kv_error(self, batch: api.Batch, layer: int = 0, rows=None) -> float:
+        """Largest per-head-vector relative error of the K/V the iteration appended."""
+        seqs = [batch.prefill_seq] * batch.chunk + list(batch.decode_seqs)
+        pos = [batch.prefix_len + j for j in range(batch.chunk)] + list(batch.context_lens)
+        idx = range(len(seqs)) if rows is None else rows
+        err = 0.0
+        by_seq = {}
+        for r in idx:
+            by_seq.setdefault(seqs[r], []).append(pos[r])
+        for sid, ps in by_seq.items():
+            kg, vg = self.s.read_kv(layer, sid, ps)
+            c = self.kv[layer].seqs[sid]
+            err = max(err, rel_err(kg, c.k[ps]), rel_err(vg, c.v[ps]))
+            assert rms_err(kg, c.k[ps]) <= RMS_TOL and rms_err(vg, c.v[ps]) <= RMS_TOL
+        return err
+
+
+def stage_errors(mir: Mirror, batch: api.Batch, x_bits) -> dict:
+    """Per-stage relative errors of the last layer of a one-layer session.
+
+    Recomputes the oracle's intermediates from the cache the iteration has
+    just appended to (call right after Mirror.step).  Returns, per stage,
+    (largest relative error, row where it occurs).
+    """
+    s = mir.s.shape
+    shape, w = mir.shape, mir.w[0]
+    seqs, pos = OL.MixedBatch(batch.chunk, batch.prefill_seq, batch.prefix_len,
+                              list(batch.decode_seqs), list(batch.context_lens)).row_seq_pos()
+    x = synth.bf16_to_f64(x_bits)
+    q, k, v = OL.qkv_rope(shape, w, x, pos)
+    kv = mir.kv[0]
+    o = np.stack([OL.attend_row(q[r], kv.seqs[seqs[r]].k, kv.seqs[seqs[r]].v, pos[r] + 1, shape.group)
+                  for r in range(batch.rows)])
+    h = x + o.reshape(batch.rows, -1) @ w.wo.T
+    wn = OL.rms_norm(h, w.g2, shape.rms_eps)
+    gu = wn @ w.wgu.T
+    act = OL.silu(gu[:, :s.ffn_dim]) * gu[:, s.ffn_dim:]
+    qkv_w = (s.n_q_heads + 2 * s.n_kv_heads) * s.head_dim
+    g_qkv = mir.s.view(api.VIEW_QKV, batch.chunk, len(batch.decode_seqs), qkv_w)
+    ref_qkv = np.concatenate([q.reshape(batch.rows, -1), k.reshape(batch.rows, -1),
+                              v.reshape(batch.rows, -1)], axis=1)
+    g_attn = mir.s.view(api.VIEW_ATTN, batch.chunk, len(batch.decode_seqs), s.n_q_heads * s.head_dim)
+    g_h = mir.s.view(api.VIEW_H, batch.chunk, len(batch.decode_seqs), s.d_model, fp32=True)
+    g_act = mir.s.view(api.VIEW_ACT, batch.chunk, len(batch.decode_seqs), s.ffn_dim)
+    out = {}
+    for name, g, r in (("qkv", g_qkv, ref_qkv), ("attn", g_attn, o.reshape(batch.rows, -1)),
+                       ("h", g_h, h), ("act", g_act, act)):
+        out[name] = {"rel": round(rel_err(g, r), 5), "rms": round(rms_err(g, r), 5),
+                     "elementwise": round(elementwise_err(g, r), 5)}
+    return out

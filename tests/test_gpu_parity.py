@@ -1,0 +1,160 @@
+"""GPU parity of the mixed iteration against the oracle, through the C ABI.
+
+Block tables and slots must match the oracle's block-manager twin
+bit-exactly; outputs and appended K/V must match the float64 oracle within
+the 2e-2 relative bound (see tests/parity.py for the denominator).
+
+Shapes: the Tiny model (d 256, 4 MHA heads of 64, FFN 704) run as a 512-token
+prompt in four 128-token chunks next to four decodes whose contexts
+(uniform in [64, 256]) are themselves built by prefill iterations; and the
+8B-shaped layer (d 4096, 32/8 GQA heads of 128, FFN 14336) at small ragged
+batches covering the degenerate cases (decode-only, prefill-only, empty
+prefix, context 0 and 1, chunks of 1, block-boundary crossings, several
+attention tiles with ragged tails).
+"""
+import numpy as np
+import pytest
+
+from paper_2609_07883_amd import api, synth
+from tests.parity import TOL, Mirror, check, rel_err, stage_errors
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _require_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.fixture(scope="module")
+def tiny_sessions():
+    _require_gpu()
+    from paper_2609_07883_amd.runtime import Session
+    return {qk: Session(synth.TINY, num_blocks=256, max_c=256, max_b=4, qk_std=qk)
+            for qk in (None, 0.16)}
+
+
+@pytest.mark.parametrize("qk_std", [None, 0.16], ids=["plain", "sharp"])
+def test_tiny_prompt_in_chunks_with_decodes(tiny_sessions, qk_std):
+    sess = tiny_sessions[qk_std]
+    mir = Mirror(sess)
+    ctx_lens = synth.uniform_lengths(4, 64, 256, seed=2).tolist()
+    dec = [11, 12, 13, 14]
+    stream = 0
+    for sid, L in zip(dec, ctx_lens):          # contexts built by prefill iterations
+        mir.create(sid)
+        x = synth.embeddings(L, synth.TINY.d_model, seed=1, stream=100 + sid)
+        b = api.Batch(L, sid, 0, [], [])
+        y, yr, sg, sr = mir.step(b, x)
+        assert sg == sr
+        check(y, yr, f"context prefill of seq {sid}")
+    prompt = 99
+    mir.create(prompt)
+    xp = synth.embeddings(512, synth.TINY.d_model, seed=1, stream=0)
+    lens = list(ctx_lens)
+    for it in range(4):
+        xd = synth.embeddings(4, synth.TINY.d_model, seed=1, stream=200 + it)
+        b = api.Batch(128, prompt, 128 * it, dec, lens)
+        y, yr, sg, sr = mir.step(b, np.concatenate([xp[128 * it: 128 * (it + 1)], xd]))
+        assert sg == sr, f"slots differ at iteration {it}"
+        check(y, yr, f"iteration {it}")
+        assert mir.kv_error(b) <= TOL
+        for sid in dec + [prompt]:
+            assert sess.ctx.block_table(sid) == mir.mgr.block_table(sid)
+        lens = [L + 1 for L in lens]
+        stream += 1
+
+
+@pytest.fixture(scope="module")
+def l8b():
+    _require_gpu()
+    from paper_2609_07883_amd.runtime import Session
+    return Session(synth.LLAMA8B_LAYER, num_blocks=2048, max_c=512, max_b=8)
+
+
+CASES = [
+    # (C, P, decode contexts)
+    (77, 50, [1, 16, 33, 100, 300]),
+    (0, 0, [0, 15, 16, 17, 1000]),
+    (200, 0, []),
+    (33, 1000, [64]),
+    (1, 7, [5]),
+    (130, 16, [2047, 4]),
+    (512, 3, [700, 1, 63, 64, 65, 127, 128, 129]),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"C{c}_P{p}_B{len(d)}" for c, p, d in CASES])
+def test_8b_layer_ragged_batches(l8b, case):
+    C, P, ctx = case
+    sess = l8b
+    sess.ctx.kv_init(sess.k_pool.data_ptr(), sess.v_pool.data_ptr(), sess.num_blocks)
+    mir = Mirror(sess, seed=3)
+    pre = 500
+    mir.create(pre)
+    mir.install_context(pre, P)
+    dec = list(range(600, 600 + len(ctx)))
+    for sid, L in zip(dec, ctx):
+        mir.create(sid)
+        mir.install_context(sid, L)
+    b = api.Batch(C, pre, P, dec, ctx)
+    x = synth.embeddings(b.rows, synth.LLAMA8B_LAYER.d_model, seed=1, stream=C * 7 + len(ctx))
+    y, yr, sg, sr = mir.step(b, x)
+    assert sg == sr
+    stages = stage_errors(mir, b, x)
+    kv_err = mir.kv_error(b)
+    print(f"case {case}: kv {kv_err:.3e} stages {stages}")
+    e = check(y, yr, f"case {case} (stages {stages})")
+    print(f"case {case}: out {e}")
+    assert kv_err <= TOL
+
+
+def test_8b_repeated_iteration_is_idempotent(l8b):
+    """Re-running the same batch rewrites the same slots and gives the same output."""
+    sess = l8b
+    sess.ctx.kv_init(sess.k_pool.data_ptr(), sess.v_pool.data_ptr(), sess.num_blocks)
+    mir = Mirror(sess, seed=4)
+    mir.create(1)
+    mir.install_context(1, 40)
+    mir.create(2)
+    mir.install_context(2, 90)
+    b = api.Batch(64, 1, 40, [2], [90])
+    x = synth.embeddings(65, 4096, seed=1, stream=5)
+    sess.run(b, x)
+    y1 = sess.output(65)
+    s1 = sess.ctx.last_slots()
+    sess.run(b, x)
+    y2 = sess.output(65)
+    assert sess.ctx.last_slots() == s1
+    np.testing.assert_array_equal(y1, y2)
+
+
+def test_errors_are_reported_not_faulted(l8b):
+    sess = l8b
+    sess.ctx.kv_init(sess.k_pool.data_ptr(), sess.v_pool.data_ptr(), sess.num_blocks)
+    sess.ctx.seq_create(1)
+    with pytest.raises(api.SloweaveError) as e:       # prefix not cached
+        sess.run(api.Batch(10, 1, 5, [], []))
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:       # unknown decode sequence
+        sess.run(api.Batch(0, 0, 0, [77], [3]))
+    assert e.value.code == api.EINVAL
+    sess.ctx.seq_create(2)
+    with pytest.raises(api.SloweaveError) as e:       # duplicate
+        sess.run(api.Batch(4, 1, 0, [2, 2], [0, 0]))
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:       # workspace too small for this batch
+        sess.ctx.mixed_iteration(api.Batch(600, 1, 0, [], []), sess.x_in.data_ptr(),
+                                 sess.x_out.data_ptr(), sess.ws.data_ptr(), sess.ws_bytes)
+    assert e.value.code == api.ENOMEM
+    sess.ctx.seq_reserve(2, 16 * (sess.ctx.free_blocks() - 10))
+    sess.ctx.seq_create(3)
+    free = sess.ctx.free_blocks()
+    with pytest.raises(api.SloweaveError) as e:       # pool exhaustion leaves state unchanged
+        sess.ctx.seq_reserve(3, 16 * (free + 1))
+    assert e.value.code == api.ENOMEM and sess.ctx.free_blocks() == free
+    with pytest.raises(api.SloweaveError) as e:       # an iteration that cannot be covered
+        sess.run(api.Batch(16 * (free + 1), 3, 0, [], []))
+    assert e.value.code == api.ENOMEM and sess.ctx.free_blocks() == free
