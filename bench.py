@@ -1,0 +1,279 @@
+"""Mixed-iteration benchmark on one MI355X.
+
+Workload (the 8B-shaped layer sweep): one decoder layer with d 4096, 32 query /
+8 KV heads of 128, SwiGLU FFN 14336, bf16, seeded random weights; a paged KV
+cache with 16-token blocks; a decode batch of B = 32 requests whose contexts
+are uniform in [512, 2048]; one prefill chunk C in {64, 128, 256, 512, 1024,
+2048} at prefix lengths P in {0, 2048, 8192}.  One step runs the 18 (C, P)
+mixed iterations once each; tokens/s counts the C + B rows of every iteration.
+
+Printed (one JSON line on stdout): throughput, per-point iteration ms and
+tokens/s, per-stage time with its roofline fraction (HIP events recorded by
+the library on the iteration's stream over the timed region), the roofline
+entry of the dominant kernel, the oracle timed on the host cores on a bounded
+sample, the cost table profiled over (B, C) with its monotonicity, and the
+controller's per-decision time.
+
+    python bench.py [--steps K] [--warmup W] [--no-cpu] [--no-table]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mixed-batch iteration ms vs chunk size; tokens/s; % HBM/MFMA roofline"
+PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
+PEAK_BF16 = 2.5e15         # FLOP/s, dense bf16 MFMA
+C_SWEEP = (64, 128, 256, 512, 1024, 2048)
+P_SWEEP = (0, 2048, 8192)
+B_DEC = 32
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_work(shape, C, P, B, ctx_sum):
+    """Algorithmic (flops, bytes) of each stage of one layer for one iteration."""
+    d, hq, hkv, hd, F = shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn_dim
+    M = C + B
+    qw = (hq + 2 * hkv) * hd
+    kvb = hkv * hd * 2 * 2                      # K and V bytes per token
+    w = {}
+    w["rmsnorm_attn"] = (0, M * d * 2 * 2)
+    w["rope_table"] = (0, M * hd // 2 * 8)
+    w["qkv_gemm"] = (2 * M * qw * d, qw * d * 2 + M * d * 2 + M * qw * 2 + M * kvb // 2 * 2)
+    w["chunk_attn"] = (4 * hq * hd * (C * P + C * (C + 1) // 2),
+                       (P + C) * kvb + C * hq * hd * 2 * 2)
+    w["decode_attn"] = (4 * hq * hd * ctx_sum, ctx_sum * kvb + B * hq * hd * 2)
+    w["decode_merge"] = (0, 0)
+    w["o_gemm"] = (2 * M * d * hq * hd, d * hq * hd * 2 + M * hq * hd * 2 + M * d * (2 + 4))
+    w["rmsnorm_mlp"] = (0, M * d * (4 + 2))
+    w["gateup_gemm"] = (2 * M * 2 * F * d, 2 * F * d * 2 + M * d * 2 + M * F * 2)
+    w["down_gemm"] = (2 * M * d * F, d * F * 2 + M * F * 2 + M * d * (4 + 2))
+    return w
+
+
+def roof_time(flops, nbytes):
+    return max(flops / PEAK_BF16, nbytes / PEAK_HBM)
+
+
+def cpu_baseline(shape, ctx_lens, budget_s=30.0):
+    """The oracle on the host cores over the P = 0 column of the sweep (bounded)."""
+    from oracle import layer as OL
+    from paper_2609_07883_amd import synth
+    from tests.parity import oracle_shape, oracle_weights
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    sh = oracle_shape(shape)
+    w = oracle_weights(synth.layer_weights(shape, weight_seed=0))
+    kv = OL.KVState()
+    for i, L in enumerate(ctx_lens):
+        kb, vb = synth.cached_kv(int(L), shape.n_kv_heads, shape.head_dim, 3, 0, 100 + i)
+        kv.seqs[100 + i] = OL.SeqCache(synth.bf16_to_f64(kb), synth.bf16_to_f64(vb))
+    rows, secs, done = 0, 0.0, []
+    for C in C_SWEEP:
+        if secs > budget_s:
+            break
+        k2 = kv.copy()
+        k2.seqs[1] = OL.SeqCache(np.zeros((0, shape.n_kv_heads, shape.head_dim)),
+                                 np.zeros((0, shape.n_kv_heads, shape.head_dim)))
+        b = OL.MixedBatch(C, 1, 0, list(range(100, 100 + len(ctx_lens))), [int(x) for x in ctx_lens])
+        x = synth.bf16_to_f64(synth.embeddings(C + len(ctx_lens), shape.d_model, seed=1, stream=C))
+        t0 = time.perf_counter()
+        OL.mixed_iteration(sh, w, x, k2, b)
+        secs += time.perf_counter() - t0
+        rows += C + len(ctx_lens)
+        done.append(C)
+    return {"value": rows / secs, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"float64 oracle, one mixed iteration at each C in {done} with P=0 and the same "
+                      f"B={len(ctx_lens)} decodes ({rows} rows, {secs:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-table", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the path has no multi-GPU mode",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_07883_amd import api, synth
+    from paper_2609_07883_amd.runtime import Session
+
+    torch.cuda.set_device(0)
+    shape = synth.LLAMA8B_LAYER
+    ctx_lens = synth.uniform_lengths(B_DEC, 512, 2048, seed=2)
+    max_c = max(C_SWEEP)
+    pre_len = max(P_SWEEP) + max_c
+    blocks = pre_len // 16 + int(sum((ctx_lens + 16) // 16)) + 1
+    prof_blocks = (2048 + max_c) // 16 + B_DEC * (2048 + 16) // 16 + 16
+    t0 = time.time()
+    sess = Session(shape, num_blocks=blocks + prof_blocks, max_c=max_c, max_b=B_DEC)
+    ctx = sess.ctx
+    # pre-existing contexts: seeded N(0,1) bf16 K/V
+    pre = 1
+    ctx.seq_create(pre)
+    ctx.seq_reserve(pre, pre_len)
+    kb, vb = synth.cached_kv(pre_len, shape.n_kv_heads, shape.head_dim, 3, 0, pre)
+    sess.write_kv(0, pre, kb, vb)
+    dec = list(range(100, 100 + B_DEC))
+    for sid, L in zip(dec, ctx_lens):
+        ctx.seq_create(sid)
+        ctx.seq_reserve(sid, int(L) + 1)
+        kb, vb = synth.cached_kv(int(L), shape.n_kv_heads, shape.head_dim, 3, 0, sid)
+        sess.write_kv(0, sid, kb, vb)
+    x = synth.embeddings(max_c + B_DEC, shape.d_model, seed=1, stream=0)
+    sess.x_in.copy_(torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16))
+    torch.cuda.synchronize()
+    log(f"setup {time.time() - t0:.1f}s: {blocks + prof_blocks} KV blocks, workspace {sess.ws_bytes / 2**20:.0f} MiB")
+
+    points = [(C, P) for P in P_SWEEP for C in C_SWEEP]
+    batches = [api.Batch(C, pre, P, dec, [int(v) for v in ctx_lens]) for C, P in points]
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        for b in batches:
+            ctx.mixed_iteration(b, sess.x_in.data_ptr(), sess.x_out.data_ptr(), sess.ws.data_ptr(),
+                                sess.ws_bytes, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: per-stage HIP events recorded on the iteration stream
+    n_iter = args.steps * len(points)
+    ctx.set_stage_timing(n_iter)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    stage_ms = [ctx.stage_times(ago) for ago in range(n_iter)][::-1]  # oldest first
+    ctx.set_stage_timing(0)
+
+    rows_per_step = sum(C + B_DEC for C, _ in points)
+    tokens_s = rows_per_step * args.steps / elapsed
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    # per-point iteration ms (sum of stage events) and per-stage totals
+    ctx_sum = int(np.sum(ctx_lens + 1))
+    per_point = []
+    stage_tot = {s: 0.0 for s in api.STAGES}
+    stage_roof = {s: 0.0 for s in api.STAGES}
+    stage_flops = {s: 0.0 for s in api.STAGES}
+    stage_bytes = {s: 0.0 for s in api.STAGES}
+    for i, st in enumerate(stage_ms):
+        C, P = points[i % len(points)]
+        work = stage_work(shape, C, P, B_DEC, ctx_sum)
+        for s in api.STAGES:
+            stage_tot[s] += st[s]
+            f, b = work[s]
+            stage_flops[s] += f
+            stage_bytes[s] += b
+            stage_roof[s] += roof_time(f, b) * 1e3
+    for j, (C, P) in enumerate(points):
+        its = [stage_ms[k] for k in range(j, n_iter, len(points))]
+        ms = float(np.median([sum(st.values()) for st in its]))
+        work = stage_work(shape, C, P, B_DEC, ctx_sum)
+        roof = sum(roof_time(*work[s]) for s in api.STAGES) * 1e3
+        per_point.append({"C": C, "P": P, "B": B_DEC, "ms": round(ms, 4),
+                          "tokens_s": round((C + B_DEC) / ms * 1e3, 1),
+                          "roofline_frac": round(roof / ms, 3)})
+    kernels = {}
+    for s in api.STAGES:
+        t = stage_tot[s] / 1e3
+        if t <= 0:
+            continue
+        kernels[s] = {"ms_total": round(stage_tot[s], 4),
+                      "tflops": round(stage_flops[s] / t / 1e12, 2),
+                      "gbps": round(stage_bytes[s] / t / 1e9, 1),
+                      "roofline_frac": round(stage_roof[s] / stage_tot[s], 3)}
+    dom = max(kernels, key=lambda s: kernels[s]["ms_total"])
+    t_dom = stage_tot[dom] / 1e3
+    mfma_time = stage_flops[dom] / PEAK_BF16
+    hbm_time = stage_bytes[dom] / PEAK_HBM
+    if mfma_time >= hbm_time:
+        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(stage_flops[dom] / t_dom / 1e12, 2),
+                    "peak": 2500.0, "unit": "TFLOP/s"}
+    else:
+        roofline = {"kernel": dom, "bound": "hbm", "achieved": round(stage_bytes[dom] / t_dom / 1e9, 1),
+                    "peak": 8000.0, "unit": "GB/s"}
+    roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
+    roofline["traffic"] = None
+    roofline["launches"] = n_iter
+    roofline["avg_launch_us"] = round(t_dom / n_iter * 1e6, 2)
+    log(f"timed {args.steps} steps x {len(points)} iterations: {elapsed * 1e3:.1f} ms, {tokens_s:.0f} tokens/s")
+
+    # cost table over (B, C), monotonicity, controller decision time
+    table = None
+    if not args.no_table:
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        t1 = time.time()
+        c_grid = [0] + list(C_SWEEP)
+        b_grid = [0, 8, 16, 32]
+        ct = ctx.build_cost_table(c_grid, b_grid, prefix_len=2048, ctx_lo=512, ctx_hi=2048, seed=2,
+                                  warmup=3, repeats=20, x_in=sess.x_in.data_ptr(),
+                                  x_out=sess.x_out.data_ptr(), ws=sess.ws.data_ptr(),
+                                  ws_bytes=sess.ws_bytes, flush_buf=flush.data_ptr(),
+                                  flush_bytes=flush.numel(), stream=stream)
+        viol, worst = ct.monotone()
+        t_hat = ct.values(api.TABLE_THAT)
+        p50 = ct.values(api.TABLE_P50)
+        now = 10**12
+        dl = [now + 25_000_000 + 1000 * i for i in range(32)]
+        n_dec = 20000
+        t2 = time.perf_counter()
+        for _ in range(n_dec):
+            api.select_chunk(ct, dl, now, 100_000, 4096)
+        dec_ns = (time.perf_counter() - t2) / n_dec * 1e9
+        c25, _, _ = api.select_chunk(ct, dl, now, 100_000, 4096)
+        table = {"c_grid": c_grid, "b_grid": b_grid, "repeats": 20, "flush_bytes": flush.numel(),
+                 "p50_ms": (p50 / 1e6).round(4).tolist(), "p99_cummax_ms": (t_hat / 1e6).round(4).tolist(),
+                 "raw_p99_decreases_along_c": viol, "largest_decrease_ns": worst,
+                 "monotone_after_cummax": bool(np.all(np.diff(t_hat, axis=1) >= 0)),
+                 "select_chunk_ns_per_decision_incl_ctypes": round(dec_ns, 1),
+                 "chunk_at_25ms_budget_b32": c25, "seconds": round(time.time() - t1, 1)}
+        del flush
+        log(f"cost table {table['seconds']}s, {viol} raw decreases")
+
+    cpu = None
+    if not args.no_cpu:
+        t1 = time.time()
+        cpu = cpu_baseline(shape, ctx_lens)
+        log(f"cpu baseline {time.time() - t1:.1f}s: {cpu['value']:.1f} tokens/s on {cpu['cores']} threads")
+
+    out = {"metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": "8B-shaped single decoder layer (d 4096, 32/8 heads x 128, FFN 14336), "
+                                  "B=32 decodes with contexts U[512,2048], chunk C in "
+                                  "{64,128,256,512,1024,2048} x prefix P in {0,2048,8192}; one step = the 18 "
+                                  "mixed iterations",
+                      "block_size": 16, "seeds": {"weights": 0, "embeddings": 1, "contexts": 2, "kv": 3}},
+           "roofline": roofline, "cpu_baseline": cpu, "sweep": per_point, "kernels": kernels,
+           "cost_table": table}
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

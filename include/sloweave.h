@@ -202,18 +202,21 @@ int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_t B, size_t
 
 /*
  * Stage telemetry (Fig. 1 and Table 1 record observed iteration durations).
- * When enabled, slw_mixed_iteration records a HIP event on its stream before
- * each stage of each layer and after the last one.  slw_stage_times waits for
- * the last iteration's final event and writes, per stage, the elapsed
- * milliseconds summed over layers:
+ * slw_set_stage_timing(ctx, depth) with depth > 0 makes every following
+ * slw_mixed_iteration record HIP events on its stream before each stage of
+ * each layer and after the last one, keeping the events of the last `depth`
+ * iterations (depth 0 turns recording off; at most 4096).
+ * slw_stage_times(ctx, ago, ms, cap, n) waits for the iteration `ago` steps
+ * before the most recent one (0 = most recent) and writes, per stage, its
+ * elapsed milliseconds summed over layers:
  *   0 RMSNorm (attention)  1 RoPE table    2 QKV GEMM with RoPE and KV append
  *   3 chunk attention      4 decode attention  5 decode merge  6 output GEMM
  *   7 RMSNorm (MLP)        8 gate/up GEMM  9 down GEMM
- * Stages absent from the iteration (C == 0 or B == 0) read 0.
+ * Stages absent from that iteration (C == 0 or B == 0) read 0.
  */
 #define SLW_N_STAGES 10
-int slw_set_stage_timing(slw_ctx* ctx, int32_t enable);
-int slw_stage_times(slw_ctx* ctx, float* ms, int32_t cap, int32_t* n);
+int slw_set_stage_timing(slw_ctx* ctx, int32_t depth);
+int slw_stage_times(slw_ctx* ctx, int32_t ago, float* ms, int32_t cap, int32_t* n);
 
 /* ------------------------------------------------------------------------ */
 /* Cost table (Sec. 5.1 profiler: P50/P99 per grid point, cumulative max    */

@@ -111,7 +111,7 @@ def lib() -> C.CDLL:
         "slw_cost_table_load": ([C.c_char_p, P(vp)], C.c_int),
         "slw_select_chunk": ([vp, P(i64), i32, i64, i32, i32, i64, P(i32), P(u32), P(i32)], C.c_int),
         "slw_set_stage_timing": ([vp, i32], C.c_int),
-        "slw_stage_times": ([vp, P(C.c_float), i32, P(i32)], C.c_int),
+        "slw_stage_times": ([vp, i32, P(C.c_float), i32, P(i32)], C.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -312,14 +312,15 @@ class Context:
         _check(lib().slw_mixed_iteration(self._h, C.byref(bc), C.c_void_p(x_in), C.c_void_p(x_out),
                                          C.c_void_p(ws), ws_bytes, C.c_void_p(stream)))
 
-    def set_stage_timing(self, enable: bool):
-        _check(lib().slw_set_stage_timing(self._h, 1 if enable else 0))
+    def set_stage_timing(self, depth: int):
+        """Record per-stage HIP events for the last `depth` iterations (0: off)."""
+        _check(lib().slw_set_stage_timing(self._h, int(depth)))
 
-    def stage_times(self) -> dict:
-        """Per-stage ms of the last iteration (waits for it), summed over layers."""
+    def stage_times(self, ago: int = 0) -> dict:
+        """Per-stage ms of the iteration `ago` before the last (waits for it), summed over layers."""
         out = np.zeros(len(STAGES), np.float32)
         n = C.c_int32()
-        _check(lib().slw_stage_times(self._h, _ptr(out, C.c_float), len(out), C.byref(n)))
+        _check(lib().slw_stage_times(self._h, int(ago), _ptr(out, C.c_float), len(out), C.byref(n)))
         return dict(zip(STAGES, out[: n.value].astype(float).tolist()))
 
     def last_slots(self) -> list:

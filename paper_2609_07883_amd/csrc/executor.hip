@@ -56,11 +56,11 @@ struct slw_ctx {
     hipEvent_t staged[kRing] = {};
     int ring = 0;
 
-    // stage telemetry: events [layer][stage boundary]
-    bool stage_timing = false;
+    // stage telemetry: a ring of `stage_depth` event sets, each [layer][stage boundary]
+    int stage_depth = 0;
     std::vector<hipEvent_t> stage_ev;
-    bool stage_valid = false;
-    uint32_t stage_mask = 0;  // stages the last iteration ran
+    std::vector<uint32_t> stage_mask;  // per set: stages that iteration ran (0: none recorded)
+    int64_t stage_iter = 0;            // iterations recorded so far
 
     ~slw_ctx() {
         if (!hip_ready) return;
@@ -184,7 +184,7 @@ int next_staging(slw_ctx* ctx, size_t n, int32_t** buf, int* slot_out) {
 constexpr int kStages = SLW_N_STAGES;
 
 int ensure_stage_events(slw_ctx* ctx) {
-    const size_t need = static_cast<size_t>(ctx->cfg.n_layers) * (kStages + 1);
+    const size_t need = static_cast<size_t>(ctx->stage_depth) * ctx->cfg.n_layers * (kStages + 1);
     while (ctx->stage_ev.size() < need) {
         hipEvent_t e;
         HIP_TRY(hipEventCreate(&e));
@@ -331,14 +331,19 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     const GemmPlan p_d = plan_gemm(M, d, F);
     const size_t layer_pool = static_cast<size_t>(ctx->kv.num_blocks()) * hkv * hd * 16 * 2;
 
-    const bool timing = ctx->stage_timing;
-    ctx->stage_valid = false;
+    const bool timing = ctx->stage_depth > 0;
+    size_t set_base = 0;
+    int set = 0;
     if (timing) {
         rc = ensure_stage_events(ctx);
         if (rc) return rc;
+        set = static_cast<int>(ctx->stage_iter % ctx->stage_depth);
+        set_base = static_cast<size_t>(set) * c.n_layers * (kStages + 1);
+        ctx->stage_mask[set] = 0;
     }
     auto mark = [&](int l, int stage) -> int {
-        if (timing) HIP_TRY(hipEventRecord(ctx->stage_ev[static_cast<size_t>(l) * (kStages + 1) + stage], stream));
+        if (timing)
+            HIP_TRY(hipEventRecord(ctx->stage_ev[set_base + static_cast<size_t>(l) * (kStages + 1) + stage], stream));
         return SLW_OK;
     };
 
@@ -409,8 +414,8 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     }
     HIP_TRY(hipGetLastError());
     if (timing) {
-        ctx->stage_valid = true;
-        ctx->stage_mask = 0x3FFu & ~(C > 0 ? 0u : (1u << 3)) & ~(B > 0 ? 0u : (3u << 4));
+        ctx->stage_mask[set] = 0x3FFu & ~(C > 0 ? 0u : (1u << 3)) & ~(B > 0 ? 0u : (3u << 4));
+        ++ctx->stage_iter;
     }
     return SLW_OK;
 }
@@ -550,25 +555,33 @@ extern "C" int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const v
     });
 }
 
-extern "C" int slw_set_stage_timing(slw_ctx* ctx, int32_t enable) {
-    if (!ctx) return fail(SLW_EINVAL, "null context");
-    ctx->stage_timing = enable != 0;
-    ctx->stage_valid = false;
-    return SLW_OK;
+extern "C" int slw_set_stage_timing(slw_ctx* ctx, int32_t depth) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        if (depth < 0 || depth > 4096) return fail(SLW_ERANGE, "depth must be in [0, 4096]");
+        ctx->stage_depth = depth;
+        ctx->stage_mask.assign(depth, 0u);
+        ctx->stage_iter = 0;
+        return SLW_OK;
+    });
 }
 
-extern "C" int slw_stage_times(slw_ctx* ctx, float* ms, int32_t cap, int32_t* n) {
+extern "C" int slw_stage_times(slw_ctx* ctx, int32_t ago, float* ms, int32_t cap, int32_t* n) {
     if (!ctx || !ms || !n) return fail(SLW_EINVAL, "null argument");
-    if (!ctx->stage_valid) return fail(SLW_EINVAL, "no timed iteration (enable slw_set_stage_timing first)");
+    if (ctx->stage_depth <= 0) return fail(SLW_EINVAL, "stage timing is off");
+    if (ago < 0 || ago >= ctx->stage_depth || ago >= ctx->stage_iter)
+        return fail(SLW_ERANGE, "iteration %d ago is not recorded", ago);
     if (cap < kStages) return fail(SLW_ERANGE, "need room for %d stages", kStages);
-    const size_t last = static_cast<size_t>(ctx->cfg.n_layers) * (kStages + 1) - 1;
-    HIP_TRY(hipEventSynchronize(ctx->stage_ev[last]));
+    const int set = static_cast<int>((ctx->stage_iter - 1 - ago) % ctx->stage_depth);
+    const uint32_t mask = ctx->stage_mask[set];
+    const size_t base0 = static_cast<size_t>(set) * ctx->cfg.n_layers * (kStages + 1);
+    if (mask) HIP_TRY(hipEventSynchronize(ctx->stage_ev[base0 + static_cast<size_t>(ctx->cfg.n_layers) * (kStages + 1) - 1]));
     for (int s = 0; s < kStages; ++s) {
         float tot = 0.f;
-        if (ctx->stage_mask & (1u << s)) {
+        if (mask & (1u << s)) {
             for (int l = 0; l < ctx->cfg.n_layers; ++l) {
                 float t = 0.f;
-                const size_t base = static_cast<size_t>(l) * (kStages + 1);
+                const size_t base = base0 + static_cast<size_t>(l) * (kStages + 1);
                 HIP_TRY(hipEventElapsedTime(&t, ctx->stage_ev[base + s], ctx->stage_ev[base + s + 1]));
                 tot += t;
             }
