@@ -39,6 +39,14 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // ---------------------------------------------------------------------------
 // Chunk attention: C queries at positions P..P+C-1 of one sequence attend to
 // its keys 0..P+C-1 under the causal mask.
+//
+// A work-group owns one kv head and 256 rows = (position, q head) pairs of
+// that head's group; each wave owns 64 rows, the four 16-column Q^T tiles of
+// its MFMAs, so one K or V fragment read from LDS feeds four MFMAs.  Keys
+// advance 64 at a time (four pages) through a double-buffered LDS tile shared
+// by the four waves.  A work item covers one key range of one query tile; in
+// split mode it writes fp32 partials (running max, sum, unnormalised output)
+// that chunk_merge_kernel combines.
 // ---------------------------------------------------------------------------
 
 // LDS swizzles: K rows (64 B = four 16-byte chunks) and V rows (32 B = four
@@ -46,42 +54,43 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 __device__ __forceinline__ int kswz(int t, int sub) { return sub ^ ((t >> 1) & 3); }
 __device__ __forceinline__ int vswz(int d, int grp) { return grp ^ ((d >> 2) & 3); }
 
-template <int HD>
-__global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a, int heads_per_wg,
-                                                         int span) {
+template <int HD, int GROUP>
+__global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
-    constexpr int CHUNKS = 4 * PAGE / 8;                 // 16-byte chunks per K (or V) tile
+    constexpr int CHUNKS = 4 * PAGE / 8;  // 16-byte chunks per K (or V) tile of 64 keys
     constexpr int PER_THREAD = 2 * CHUNKS / 256;
+    constexpr int PW = 64 / GROUP;        // positions per wave
+    constexpr int PWG = 4 * PW;           // positions per work-group
     __shared__ __attribute__((aligned(16))) bf16 Ks[2][4 * PAGE];
     __shared__ __attribute__((aligned(16))) bf16 Vs[2][4 * PAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
-    const int group = a.hq / a.hkv;
-    const int head = blockIdx.y * heads_per_wg + (wave % heads_per_wg);
-    const int kvh = head / group;
-    const int q0 = blockIdx.x * span + (wave / heads_per_wg) * 32;
-    const int key_end = min(a.prefix + a.c, a.prefix + (int)blockIdx.x * span + span);
-    const int n_tiles = (key_end + 63) / 64;
+    const int item = blockIdx.x, kvh = blockIdx.y;
+    const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
+    const int key_lim = a.prefix + a.c;  // slots at or past this are unwritten
+    const int p0 = qt * PWG + wave * PW; // first chunk position of this wave
+    const int n_tiles = (ke - kb + 63) / 64;
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
+    const int wave_qpos_lo = a.prefix + p0, wave_qpos_hi = a.prefix + p0 + PW - 1;
+    const bool wave_live = p0 < a.c;
 
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
 
-    // Q^T operand: query col of sub-tile qt, dims kk*32 + grp*8 .. +8
-    bf16x8 qf[2][KK];
+    // Q^T operand: row r = ct*16 + col is position p0 + r / GROUP, head kvh*GROUP + r % GROUP
+    bf16x8 qf[4][KK];
     const bf16* qkv = static_cast<const bf16*>(a.qkv);
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-        const int qi = q0 + qt * 16 + col;
+    for (int ct = 0; ct < 4; ++ct) {
+        const int r = ct * 16 + col, qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
-            qf[qt][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
-                                        qkv + static_cast<size_t>(qi) * a.ld_qkv + head * HD + kk * 32 + grp * 8)
+            qf[ct][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
+                                        qkv + static_cast<size_t>(qi) * a.ld_qkv + h * HD + kk * 32 + grp * 8)
                                   : bf16x8{};
     }
 
-    // staging: thread handles PER_THREAD 16-byte chunks of the K and V tiles
     bf16x8 stage[PER_THREAD];
     auto load_tile = [&](int t) {
 #pragma unroll
@@ -90,17 +99,16 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a, int he
             const bool is_v = c >= CHUNKS;
             const int cc = is_v ? c - CHUNKS : c;
             const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
-            const int pg = 4 * t + p;
+            const int pg = (kb >> 4) + 4 * t + p;
             bf16x8 v = {};
-            if (pg * 16 < key_end) {
+            if (pg * 16 < ke) {
                 const size_t blk = a.bt[pg];
-                const bf16* src = (is_v ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + q * 8;
-                v = *reinterpret_cast<const bf16x8*>(src);
-                if (is_v) {  // zero tokens at or past key_end (unwritten slots)
+                v = *reinterpret_cast<const bf16x8*>((is_v ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + q * 8);
+                if (is_v) {  // zero unwritten slots so that masked keys contribute exactly 0
                     const int tok0 = pg * 16 + (q & 1) * 8;
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        if (tok0 + e >= key_end) v[e] = bf16(0.0f);
+                        if (tok0 + e >= key_lim) v[e] = bf16(0.0f);
                 }
             }
             stage[j] = v;
@@ -127,12 +135,21 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a, int he
         }
     };
 
-    f32x4 o[2][NT];
+    f32x4 o[4][NT];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) o[qt][nt] = f32x4{};
-    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+        for (int nt = 0; nt < NT; ++nt) o[ct][nt] = f32x4{};
+    float m_run[4], l_run[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+        m_run[ct] = -INFINITY;
+        l_run[ct] = 0.f;
+    }
+    // query position of row ct*16 + col (column owner) and of output row ct*16 + 4*grp + e
+    int qpos_col[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
 
     load_tile(0);
     store_tile(0);
@@ -140,106 +157,145 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a, int he
     for (int t = 0; t < n_tiles; ++t) {
         const int buf = t & 1;
         if (t + 1 < n_tiles) load_tile(t + 1);
-
-        f32x4 s[4][2];
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) s[p][qt] = f32x4{};
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-                    &Ks[buf][p * PAGE + kk * 512 + col * 32 + kswz(col, grp) * 8]);
-#pragma unroll
-                for (int qt = 0; qt < 2; ++qt) s[p][qt] = mfma16(kf, qf[qt][kk], s[p][qt]);
-            }
-
-        const int key0 = t * 64;
-        const bool need_mask = key0 + 63 > a.prefix + q0 || key0 + 63 >= key_end;
-        f32x4 pr[4][2];
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt) {
-            const int qpos = a.prefix + q0 + qt * 16 + col;
-            float mx = -INFINITY;
+        const int key0 = kb + t * 64;
+        if (wave_live && key0 <= wave_qpos_hi) {
+            f32x4 sc[4][4];  // [page][ct]
 #pragma unroll
             for (int p = 0; p < 4; ++p)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float x = s[p][qt][e] * sl2;
-                    if (need_mask) {
-                        const int kpos = key0 + p * 16 + grp * 4 + e;
-                        x = (kpos <= qpos && kpos < key_end) ? x : -INFINITY;
+                for (int ct = 0; ct < 4; ++ct) sc[p][ct] = f32x4{};
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk) {
+                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+                        &Ks[buf][p * PAGE + kk * 512 + col * 32 + kswz(col, grp) * 8]);
+#pragma unroll
+                    for (int ct = 0; ct < 4; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
+                }
+            const bool need_mask = key0 + 63 > wave_qpos_lo || key0 + 63 >= ke;
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float x = sc[p][ct][e];
+                        if (need_mask) {
+                            const int kpos = key0 + p * 16 + grp * 4 + e;
+                            x = (kpos <= qpos_col[ct] && kpos < ke) ? x : -INFINITY;
+                            sc[p][ct][e] = x;
+                        }
+                        mx = fmaxf(mx, x);
                     }
-                    s[p][qt][e] = x;
-                    mx = fmaxf(mx, x);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float m_new = fmaxf(m_run[qt], mx);
-            const float m_use = m_new == -INFINITY ? 0.f : m_new;
-            const float alpha = exp2f(m_run[qt] - m_use);
-            float ls = 0.f;
+                mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+                mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                const float m_new = fmaxf(m_run[ct], mx * sl2);
+                const float m_use = m_new == -INFINITY ? 0.f : m_new;
+                const float alpha = exp2f(m_run[ct] - m_use);
+                float ls = 0.f;
 #pragma unroll
-            for (int p = 0; p < 4; ++p)
+                for (int p = 0; p < 4; ++p)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float v = exp2f(fmaf(sc[p][ct][e], sl2, -m_use));
+                        sc[p][ct][e] = v;
+                        ls += v;
+                    }
+                l_run[ct] = l_run[ct] * alpha + ls;
+                m_run[ct] = m_new;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float v = exp2f(s[p][qt][e] - m_use);
-                    pr[p][qt][e] = v;
-                    ls += v;
+                    const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
                 }
-            l_run[qt] = l_run[qt] * alpha + ls;
-            m_run[qt] = m_new;
-            // rescale the output rows (query grp*4 + e) by their alpha
+            }
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float ae = __shfl(alpha, grp * 4 + e, 64);
+            for (int j = 0; j < 2; ++j) {
+                bf16x8 pf[4];
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) o[qt][nt][e] *= ae;
+                for (int ct = 0; ct < 4; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    const int d = nt * 16 + col;
+                    const int off = d * 16 + vswz(d, grp) * 4;
+                    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
+                    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
+                    const bf16x8 vf = cat44(lo, hi);
+#pragma unroll
+                    for (int ct = 0; ct < 4; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
+                }
             }
         }
-
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            bf16x8 pf[2];
-#pragma unroll
-            for (int qt = 0; qt < 2; ++qt) pf[qt] = to_bf16x8(pr[2 * j][qt], pr[2 * j + 1][qt]);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                const int d = nt * 16 + col;
-                const int off = d * 16 + vswz(d, grp) * 4;
-                const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
-                const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
-                const bf16x8 vf = cat44(lo, hi);
-#pragma unroll
-                for (int qt = 0; qt < 2; ++qt) o[qt][nt] = mfma16(pf[qt], vf, o[qt][nt]);
-            }
-        }
-
         if (t + 1 < n_tiles) store_tile(buf ^ 1);
         __syncthreads();
     }
+    if (!wave_live) return;
 
-    bf16* out = static_cast<bf16*>(a.out);
-    const int ldo = a.hq * HD;
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-        float l = l_run[qt];
+    for (int ct = 0; ct < 4; ++ct) {
+        float l = l_run[ct];
         l += __shfl_xor(l, 16, 64);
         l += __shfl_xor(l, 32, 64);
+        if (a.split) {
+            const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 64 + ct * 16;
+            if (grp == 0) {
+                a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
+                a.part_ml[(rbase + col) * 2 + 1] = l;
+            }
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float le = __shfl(l, grp * 4 + e, 64);
-            const int qi = q0 + qt * 16 + grp * 4 + e;
-            if (qi < a.c) {
-                const float inv = 1.0f / le;
+            for (int e = 0; e < 4; ++e)
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt)
-                    out[static_cast<size_t>(qi) * ldo + head * HD + nt * 16 + col] = f2bf(o[qt][nt][e] * inv);
+                    a.part_o[(rbase + grp * 4 + e) * HD + nt * 16 + col] = o[ct][nt][e];
+        } else {
+            bf16* out = static_cast<bf16*>(a.out);
+            const int ldo = a.hq * HD;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = ct * 16 + grp * 4 + e;
+                const int qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
+                const float inv = 1.0f / __shfl(l, grp * 4 + e, 64);
+                if (qi < a.c) {
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+                        out[static_cast<size_t>(qi) * ldo + h * HD + nt * 16 + col] = f2bf(o[ct][nt][e] * inv);
+                }
             }
         }
     }
+}
+
+// Combine the key-range partials of one (chunk position, q head).
+template <int HD, int GROUP>
+__global__ __launch_bounds__(64) void chunk_merge_kernel(ChunkAttnArgs a) {
+    constexpr int PWG = 256 / GROUP;
+    const int pos = blockIdx.x, h = blockIdx.y;
+    const int kvh = h / GROUP;
+    const int qt = pos / PWG;
+    const int row = (pos % PWG) * GROUP + h % GROUP;
+    const int w0 = a.qt_off[qt], w1 = a.qt_off[qt + 1];
+    float mmax = -INFINITY;
+    for (int w = w0; w < w1; ++w)
+        mmax = fmaxf(mmax, a.part_ml[((static_cast<size_t>(w) * a.hkv + kvh) * 256 + row) * 2]);
+    constexpr int PER = HD / 64;
+    float acc[PER] = {};
+    float lsum = 0.f;
+    for (int w = w0; w < w1; ++w) {
+        const size_t r = (static_cast<size_t>(w) * a.hkv + kvh) * 256 + row;
+        const float mw = a.part_ml[r * 2];
+        if (mw == -INFINITY) continue;  // every key of this range was masked for the row
+        const float sc = exp2f(mw - mmax);
+        lsum += sc * a.part_ml[r * 2 + 1];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) acc[j] += sc * a.part_o[r * HD + threadIdx.x + 64 * j];
+    }
+    bf16* out = static_cast<bf16*>(a.out) + static_cast<size_t>(pos) * a.hq * HD + h * HD;
+    const float inv = 1.0f / lsum;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
 }
 
 // ---------------------------------------------------------------------------
@@ -398,16 +454,29 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
     for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
 }
 
+template <int HD, int GROUP>
+void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
+    chunk_attn_kernel<HD, GROUP><<<dim3(a.n_items, a.hkv), 256, 0, s>>>(a);
+    if (a.split) chunk_merge_kernel<HD, GROUP><<<dim3(a.c, a.hq), 64, 0, s>>>(a);
+}
+
+template <int HD>
+void launch_chunk_hd(const ChunkAttnArgs& a, hipStream_t s) {
+    switch (a.hq / a.hkv) {
+        case 1: launch_chunk_g<HD, 1>(a, s); break;
+        case 2: launch_chunk_g<HD, 2>(a, s); break;
+        case 4: launch_chunk_g<HD, 4>(a, s); break;
+        case 8: launch_chunk_g<HD, 8>(a, s); break;
+        default: launch_chunk_g<HD, 16>(a, s); break;
+    }
+}
+
 }  // namespace
 
 void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s) {
-    if (a.c <= 0) return;
-    const int group = a.hq / a.hkv;
-    const int heads_per_wg = group >= 4 ? 4 : group;
-    const int span = 32 * (4 / heads_per_wg);
-    dim3 grid((a.c + span - 1) / span, a.hq / heads_per_wg);
-    if (a.hd == 128) chunk_attn_kernel<128><<<grid, 256, 0, s>>>(a, heads_per_wg, span);
-    else chunk_attn_kernel<64><<<grid, 256, 0, s>>>(a, heads_per_wg, span);
+    if (a.c <= 0 || a.n_items <= 0) return;
+    if (a.hd == 128) launch_chunk_hd<128>(a, s);
+    else launch_chunk_hd<64>(a, s);
 }
 
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s) {

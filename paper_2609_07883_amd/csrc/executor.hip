@@ -26,6 +26,7 @@ namespace {
 
 constexpr int kRing = 4;                 // pinned staging buffers in flight
 constexpr int kDecodeTargetWaves = 2048; // decode work-groups aimed for per iteration
+constexpr int kChunkTargetWgs = 512;     // chunk-attention work-groups aimed for per iteration
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -48,6 +49,7 @@ struct slw_ctx {
     bool kv_ready = false;
     std::vector<int32_t> last_slots;
     std::vector<int32_t> meta;  // host build area
+    std::vector<int32_t> items; // chunk-attention work items (host build area)
 
     // HIP resources, created on first device use
     bool hip_ready = false;
@@ -92,15 +94,23 @@ int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
     return static_cast<int>(s);
 }
 
+int chunk_tiles(const slw_model_cfg& c, int C) {
+    return static_cast<int>(ceil_div(C, chunk_tile_positions(c.n_q_heads / c.n_kv_heads)));
+}
+int chunk_item_cap(const slw_model_cfg& c, int C) {
+    return C > 0 ? chunk_tiles(c, C) + static_cast<int>(ceil_div(kChunkTargetWgs, c.n_kv_heads)) + 1 : 0;
+}
+
 size_t meta_ints(const slw_model_cfg& c, int C, int B) {
     const int M = C + B;
     const size_t mb = static_cast<size_t>(max_blocks(c));
     return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + mb +
-           2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1);
+           2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + 3 * static_cast<size_t>(chunk_item_cap(c, C)) +
+           chunk_tiles(c, C) + 1;
 }
 
 struct Layout {
-    size_t xn, qkv, attn, h, act, rope, meta, part_o, part_ml, gemm_part, end_fixed;
+    size_t xn, qkv, attn, h, act, rope, meta, part_o, part_ml, cpart_o, cpart_ml, gemm_part, end_fixed;
 };
 
 Layout layout(const slw_model_cfg& c, int C, int B) {
@@ -122,6 +132,9 @@ Layout layout(const slw_model_cfg& c, int C, int B) {
     L.meta = take(meta_ints(c, C, B) * 4);
     L.part_o = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * c.head_dim * 4 : 0);
     L.part_ml = take(B > 0 ? static_cast<size_t>(W) * c.n_q_heads * 2 * 4 : 0);
+    const size_t crows = static_cast<size_t>(chunk_item_cap(c, C)) * c.n_kv_heads * 256;
+    L.cpart_o = take(crows * c.head_dim * 4);
+    L.cpart_ml = take(crows * 2 * 4);
     L.gemm_part = off;  // split-K partials take the rest of the workspace
     L.end_fixed = off;
     return L;
@@ -301,6 +314,41 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
         }
         m[o_workoff + B] = w;
     }
+    // chunk attention work items: (query tile, key range); split the key axis
+    // when the query tiles alone give too few work-groups
+    const int n_qt = C > 0 ? chunk_tiles(c, C) : 0;
+    const int pwg = chunk_tile_positions(c.n_q_heads / c.n_kv_heads);
+    int64_t ckeys = 0;
+    for (int q = 0; q < n_qt; ++q) ckeys += P + std::min(C, (q + 1) * pwg);
+    int64_t span = INT64_MAX;
+    if (static_cast<int64_t>(n_qt) * c.n_kv_heads < kChunkTargetWgs && n_qt > 0) {
+        span = ceil_div(ckeys * c.n_kv_heads, kChunkTargetWgs);
+        span = std::max<int64_t>(256, ceil_div(span, 64) * 64);
+    }
+    std::vector<int32_t>& it = ctx->items;
+    it.clear();
+    std::vector<int32_t> qt_off(n_qt + 1);
+    for (int q = 0; q < n_qt; ++q) {
+        qt_off[q] = static_cast<int32_t>(it.size() / 3);
+        const int64_t ke = P + std::min(C, (q + 1) * pwg);
+        for (int64_t kb = 0; kb < ke; kb += span) {
+            it.push_back(q);
+            it.push_back(static_cast<int32_t>(kb));
+            it.push_back(static_cast<int32_t>(std::min(ke, kb + span)));
+        }
+    }
+    qt_off[n_qt] = static_cast<int32_t>(it.size() / 3);
+    const int n_items = static_cast<int>(it.size() / 3);
+    if (n_items > chunk_item_cap(c, C)) return fail(SLW_EINVAL, "internal: chunk items %d above cap", n_items);
+    const size_t o_item = m.size();
+    m.resize(m.size() + 3 * static_cast<size_t>(n_items));
+    for (int i = 0; i < n_items; ++i) {
+        m[o_item + i] = it[3 * i];
+        m[o_item + n_items + i] = it[3 * i + 1];
+        m[o_item + 2 * n_items + i] = it[3 * i + 2];
+    }
+    const size_t o_qtoff = m.size();
+    m.insert(m.end(), qt_off.begin(), qt_off.end());
 
     // ---- upload ----
     int32_t* stage = nullptr;
@@ -370,9 +418,29 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             launch_gemm(ga, p_qkv, gpartp, stream);
         }
         if ((rc = mark(l, 3))) return rc;
-        if (C > 0)
-            launch_chunk_attention(ChunkAttnArgs{qkv, attn, kp, vp, dmeta + o_pre, C, P, hq, hkv, hd, qw},
-                                   stream);
+        if (C > 0) {
+            ChunkAttnArgs ca{};
+            ca.qkv = qkv;
+            ca.out = attn;
+            ca.k_pool = kp;
+            ca.v_pool = vp;
+            ca.bt = dmeta + o_pre;
+            ca.item_qt = dmeta + o_item;
+            ca.item_kb = dmeta + o_item + n_items;
+            ca.item_ke = dmeta + o_item + 2 * n_items;
+            ca.qt_off = dmeta + o_qtoff;
+            ca.part_o = reinterpret_cast<float*>(wsb + L.cpart_o);
+            ca.part_ml = reinterpret_cast<float*>(wsb + L.cpart_ml);
+            ca.c = C;
+            ca.prefix = P;
+            ca.hq = hq;
+            ca.hkv = hkv;
+            ca.hd = hd;
+            ca.ld_qkv = qw;
+            ca.n_items = n_items;
+            ca.split = n_items > n_qt ? 1 : 0;
+            launch_chunk_attention(ca, stream);
+        }
         if ((rc = mark(l, 4))) return rc;
         if (B > 0) {
             DecodeAttnArgs da{};

@@ -26,7 +26,6 @@ namespace slw {
 namespace {
 
 constexpr int BK = 64;
-constexpr int kThreads = 256;
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -84,57 +83,75 @@ __device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, in
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <int BM, int BN, int WM, int WN, int EPI, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __restrict__ partial,
-                                                        int k_per_split) {
-    constexpr int WAVES_N = BN / WN;
+// Tile (m, n) of linear block id `pid`.  Blocks are dispatched round-robin to
+// the 8 XCDs (pid % 8), each with its own L2; the remap gives every XCD a
+// contiguous range of the tile order, and the tile order walks GROUP_M tile
+// rows at a time so that blocks running together share A rows and B columns.
+__device__ __forceinline__ void tile_of(int pid, int nt_m, int nt_n, int& tm, int& tn) {
+    constexpr int kXcd = 8, GROUP_M = 8;
+    const int total = nt_m * nt_n;
+    const int q = total / kXcd, r = total % kXcd;
+    const int xcd = pid % kXcd, local = pid / kXcd;
+    const int v = xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+    const int per_group = GROUP_M * nt_n;
+    const int first_m = (v / per_group) * GROUP_M;
+    const int gsize = min(nt_m - first_m, GROUP_M);
+    const int in_group = v % per_group;
+    tm = first_m + in_group % gsize;
+    tn = in_group / gsize;
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool SPLIT>
+__global__ __launch_bounds__(WAVES_M * WAVES_N * 64) void gemm_kernel(GemmArgs g, float* __restrict__ partial,
+                                                                      int k_per_split) {
+    constexpr int THREADS = WAVES_M * WAVES_N * 64;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int A_LOADS = BM * 8 / kThreads;
-    constexpr int B_LOADS = BN * 8 / kThreads;
-    static_assert((BM / WM) * (BN / WN) == 4, "four waves");
+    constexpr int A_LOADS = BM * 8 / THREADS;
+    constexpr int B_LOADS = BN * 8 / THREADS;
     static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small");
-    static_assert(WN == 64, "paired epilogues need 64-column wave tiles");
+    static_assert(WN % 64 == 0, "paired epilogues need whole 64-column pairs per wave");
 
     __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
     __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * BK];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-    const int kb = blockIdx.z * k_per_split;
+    int tm, tn;
+    tile_of(blockIdx.x, (g.m + BM - 1) / BM, g.n / BN, tm, tn);
+    const int n0 = tn * BN, m0 = tm * BM;
+    const int kb = blockIdx.y * k_per_split;
     const int nk = k_per_split / BK;
 
-    const bf16* A = static_cast<const bf16*>(g.a);
-    const bf16* W = static_cast<const bf16*>(g.w);
-
-    const bf16* a_src[A_LOADS];
-    bool a_ok[A_LOADS];
-    int a_lds[A_LOADS];
+    // Wave-uniform bases plus 32-bit per-lane element offsets (operands are
+    // below 2^31 elements).  Rows past m read row m-1 instead: they only feed
+    // output rows that are never stored, and an unconditional load keeps the
+    // prefetch asynchronous.
+    const bf16* A = static_cast<const bf16*>(g.a) + kb;
+    const bf16* W = static_cast<const bf16*>(g.w) + kb;
+    int a_off[A_LOADS], a_lds[A_LOADS];
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-        const int idx = tid + i * kThreads, row = idx >> 3, ch = idx & 7;
-        a_ok[i] = (m0 + row) < g.m;
-        a_src[i] = A + static_cast<size_t>(a_ok[i] ? m0 + row : 0) * g.lda + kb + ch * 8;
+        const int idx = tid + i * THREADS, row = idx >> 3, ch = idx & 7;
+        a_off[i] = min(m0 + row, g.m - 1) * g.lda + ch * 8;
         a_lds[i] = row * BK + swz(row, ch) * 8;
     }
-    const bf16* b_src[B_LOADS];
-    int b_lds[B_LOADS];
+    int b_off[B_LOADS], b_lds[B_LOADS];
 #pragma unroll
     for (int i = 0; i < B_LOADS; ++i) {
-        const int idx = tid + i * kThreads, row = idx >> 3, ch = idx & 7;
-        b_src[i] = W + static_cast<size_t>(w_row<EPI>(g, n0 + row)) * g.k + kb + ch * 8;
+        const int idx = tid + i * THREADS, row = idx >> 3, ch = idx & 7;
+        b_off[i] = w_row<EPI>(g, n0 + row) * g.k + ch * 8;
         b_lds[i] = row * BK + swz(row, ch) * 8;
     }
 
     bf16x8 ra[A_LOADS], rb[B_LOADS];
-    const bf16x8 zero8 = {};
     auto load_tile = [&](int kt) {
-        const int off = kt * BK;
+        const bf16* Ak = A + kt * BK;
+        const bf16* Wk = W + kt * BK;
 #pragma unroll
-        for (int i = 0; i < A_LOADS; ++i)
-            ra[i] = a_ok[i] ? *reinterpret_cast<const bf16x8*>(a_src[i] + off) : zero8;
+        for (int i = 0; i < A_LOADS; ++i) ra[i] = *reinterpret_cast<const bf16x8*>(Ak + a_off[i]);
 #pragma unroll
-        for (int i = 0; i < B_LOADS; ++i) rb[i] = *reinterpret_cast<const bf16x8*>(b_src[i] + off);
+        for (int i = 0; i < B_LOADS; ++i) rb[i] = *reinterpret_cast<const bf16x8*>(Wk + b_off[i]);
     };
     auto store_tile = [&](int buf) {
 #pragma unroll
@@ -156,13 +173,10 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
     for (int j = 0; j < TN; ++j) b_row[j] = wn * WN + j * 32 + (lane & 31);
     const int kg = lane >> 5;
 
-    load_tile(0);
-    store_tile(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load_tile(kt + 1);
-#pragma unroll
+    auto compute = [&](int buf) {
+        // two k-steps per unrolled body: enough independent MFMAs to cover
+        // LDS latency without holding every step's fragments at once
+#pragma unroll 2
         for (int s = 0; s < BK / 16; ++s) {
             bf16x8 fa[TM], fb[TN];
 #pragma unroll
@@ -178,6 +192,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
 #pragma unroll
                 for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
         }
+    };
+
+    load_tile(0);
+    store_tile(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) load_tile(kt + 1);
+        compute(buf);
         if (kt + 1 < nk) store_tile(buf ^ 1);
         __syncthreads();
     }
@@ -187,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
     const int rbase = m0 + wm * WM + 4 * (lane >> 5);
     const int cbase = n0 + wn * WN + (lane & 31);
     if (SPLIT) {
-        float* P = partial + static_cast<size_t>(blockIdx.z) * g.m * g.n;
+        float* P = partial + static_cast<size_t>(blockIdx.y) * g.m * g.n;
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -200,24 +223,28 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g, float* __res
         return;
     }
     if (EPI == EPI_SWIGLU || EPI == EPI_QKV) {
-        const int c0 = n0 + wn * WN;  // first B column of this wave (tile 0)
-        int hg = 0, d0 = 0, fcol = 0;
-        if (EPI == EPI_QKV) {
-            hg = c0 / g.hd;
-            d0 = ((c0 % g.hd) / 64) * 32 + (lane & 31);
-        } else {
-            fcol = (c0 >> 1) + (lane & 31);
-        }
         bf16* out = static_cast<bf16*>(g.out);
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
-                if (row >= g.m) continue;
-                if (EPI == EPI_QKV) qkv_store(g, row, hg, d0, acc[i][0][e], acc[i][1][e]);
-                else out[static_cast<size_t>(row) * g.ldo + fcol] = f2bf(silu(acc[i][0][e]) * acc[i][1][e]);
+        for (int pr = 0; pr < TN / 2; ++pr) {
+            const int c0 = n0 + wn * WN + pr * 64;  // first B column of the pair (tile 2pr)
+            int hg = 0, d0 = 0, fcol = 0;
+            if (EPI == EPI_QKV) {
+                hg = c0 / g.hd;
+                d0 = ((c0 % g.hd) / 64) * 32 + (lane & 31);
+            } else {
+                fcol = (c0 >> 1) + (lane & 31);
             }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
+                    if (row >= g.m) continue;
+                    const float x0 = acc[i][2 * pr][e], x1 = acc[i][2 * pr + 1][e];
+                    if (EPI == EPI_QKV) qkv_store(g, row, hg, d0, x0, x1);
+                    else out[static_cast<size_t>(row) * g.ldo + fcol] = f2bf(silu(x0) * x1);
+                }
+        }
         return;
     }
 #pragma unroll
@@ -294,19 +321,26 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
 }
 
 struct TileCfg {
-    int bm, bn;
+    int bm, bn, waves_m, waves_n;
 };
-constexpr TileCfg kCfgs[3] = {{128, 128}, {64, 128}, {32, 256}};
+// 0: 128x128 / 4 waves (64x64 each)      1: 64x128 / 4 waves (32x64)
+// 2: 32x256 / 4 waves (32x64)            3: 256x256 / 8 waves (128x64)
+// 4: 256x256 / 4 waves (128x128)         5: 128x256 / 8 waves (64x64)
+constexpr TileCfg kCfgs[] = {{128, 128, 2, 2}, {64, 128, 2, 2}, {32, 256, 1, 4},
+                             {256, 256, 2, 4}, {256, 256, 2, 2}, {128, 256, 2, 4}};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
-    dim3 grid(g.n / BN, (g.m + BM - 1) / BM, p.splits);
+    constexpr int THREADS = WAVES_M * WAVES_N * 64;
+    const int tiles = ((g.m + BM - 1) / BM) * (g.n / BN);
+    dim3 grid(tiles, p.splits);
     const int kps = g.k / p.splits;
     if (p.splits == 1) {
-        gemm_kernel<BM, BN, WM, WN, EPI, false><<<grid, kThreads, 0, s>>>(g, nullptr, kps);
+        gemm_kernel<BM, BN, WAVES_M, WAVES_N, EPI, false><<<grid, THREADS, 0, s>>>(g, nullptr, kps);
         return;
     }
-    gemm_kernel<BM, BN, WM, WN, EPI, true><<<grid, kThreads, 0, s>>>(g, part, kps);
+    gemm_kernel<BM, BN, WAVES_M, WAVES_N, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
     size_t work;
     if (EPI == EPI_QKV) work = static_cast<size_t>(g.m) * (g.n / 2);
     else if (EPI == EPI_SWIGLU) work = static_cast<size_t>(g.m) * (g.n / 8);
@@ -314,27 +348,39 @@ void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s
     splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, p.splits);
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WAVES_M, int WAVES_N>
 void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     float* part = static_cast<float*>(partial);
     switch (g.epi) {
-        case EPI_RESID_F32OUT: launch_epi<BM, BN, WM, WN, EPI_RESID_F32OUT>(g, p, part, s); break;
-        case EPI_RESID_F32IN: launch_epi<BM, BN, WM, WN, EPI_RESID_F32IN>(g, p, part, s); break;
-        case EPI_SWIGLU: launch_epi<BM, BN, WM, WN, EPI_SWIGLU>(g, p, part, s); break;
-        default: launch_epi<BM, BN, WM, WN, EPI_QKV>(g, p, part, s); break;
+        case EPI_RESID_F32OUT: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_RESID_F32OUT>(g, p, part, s); break;
+        case EPI_RESID_F32IN: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_RESID_F32IN>(g, p, part, s); break;
+        case EPI_SWIGLU: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_SWIGLU>(g, p, part, s); break;
+        default: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_QKV>(g, p, part, s); break;
     }
 }
 
 }  // namespace
 
-// Tile and split choice.  n must be a multiple of 128 and k of 64.
+// Tile and split choice, from timings of every configuration on the
+// 8B-layer shapes (m = 96 .. 4104): 64-row tiles with split-K while weight
+// streaming dominates, 128x128 in the middle, 256x256 once there are enough
+// tiles to fill the chip.  n must be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
+    int cfg;
+    if (k >= 8192) cfg = m >= 1024 ? 3 : 1;               // deep k (down projection)
+    else if (n >= 16384) cfg = m <= 320 ? 1 : (m < 1600 ? 0 : 3);  // wide n (gate/up)
+    else if (m <= 320) cfg = 1;
+    else if (n >= 6144) cfg = 0;
+    else cfg = m > 3000 ? 3 : 1;
+    if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
+    return plan_with_cfg(cfg, m, n, k);
+}
+
+GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
     GemmPlan p{};
-    if (m <= 32 && n % 256 == 0) p.cfg = 2;
-    else if (m <= 64) p.cfg = 1;
-    else p.cfg = 0;
-    p.bm = kCfgs[p.cfg].bm;
-    p.bn = kCfgs[p.cfg].bn;
+    p.cfg = cfg;
+    p.bm = kCfgs[cfg].bm;
+    p.bn = kCfgs[cfg].bn;
     const long tiles = static_cast<long>(n / p.bn) * ((m + p.bm - 1) / p.bm);
     int splits = 1;
     // Too few tiles to fill 256 compute units: split k (each split >= 512 deep).
@@ -345,12 +391,19 @@ GemmPlan plan_gemm(int m, int n, int k) {
     return p;
 }
 
+bool gemm_shape_ok(const GemmPlan& p, int n, int k) {
+    return p.cfg >= 0 && p.cfg < kNumCfgs && n % p.bn == 0 && k % (p.splits * BK) == 0;
+}
+
 void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     if (g.m <= 0) return;
     switch (p.cfg) {
-        case 0: launch_cfg<128, 128, 64, 64>(g, p, partial, s); break;
-        case 1: launch_cfg<64, 128, 32, 64>(g, p, partial, s); break;
-        default: launch_cfg<32, 256, 32, 64>(g, p, partial, s); break;
+        case 0: launch_cfg<128, 128, 2, 2>(g, p, partial, s); break;
+        case 1: launch_cfg<64, 128, 2, 2>(g, p, partial, s); break;
+        case 2: launch_cfg<32, 256, 1, 4>(g, p, partial, s); break;
+        case 3: launch_cfg<256, 256, 2, 4>(g, p, partial, s); break;
+        case 4: launch_cfg<256, 256, 2, 2>(g, p, partial, s); break;
+        default: launch_cfg<128, 256, 2, 4>(g, p, partial, s); break;
     }
 }
 

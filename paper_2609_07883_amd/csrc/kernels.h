@@ -44,18 +44,35 @@ struct GemmPlan {
     size_t partial_bytes;
 };
 GemmPlan plan_gemm(int m, int n, int k);
+// The plan for a given tile configuration (split-K chosen by tile count).
+GemmPlan plan_with_cfg(int cfg, int m, int n, int k);
+// Whether the plan's tiles divide n and k.
+bool gemm_shape_ok(const GemmPlan& p, int n, int k);
 // Enqueue the GEMM; `partial` must hold plan.partial_bytes when plan.splits > 1.
 void launch_gemm(const GemmArgs& g, const GemmPlan& plan, void* partial, hipStream_t s);
 
 // Causal chunk-vs-prefix attention over the prefill sequence's pages.
+// A work-group covers 256 (position, head) rows of one kv head: 256 / group
+// consecutive chunk positions times the group's q heads.  Work item i covers
+// query tile item_qt[i] against keys [item_kb[i], item_ke[i]); when a tile's
+// keys are split over several items, partials are merged afterwards.
 struct ChunkAttnArgs {
     const void* qkv;       // bf16 rows 0..c-1 (q after RoPE), row stride ld_qkv
     void* out;             // bf16 [c][hq * hd]
     const void* k_pool;    // this layer
     const void* v_pool;
     const int32_t* bt;     // block table of the prefill sequence
+    const int32_t* item_qt;   // [n_items]
+    const int32_t* item_kb;   // [n_items] multiple of 64
+    const int32_t* item_ke;   // [n_items]
+    const int32_t* qt_off;    // [n_qt + 1] first item of each query tile
+    float* part_o;            // [n_items][hkv][256][hd]   (split mode)
+    float* part_ml;           // [n_items][hkv][256][2]
     int c, prefix, hq, hkv, hd, ld_qkv;
+    int n_items, split;       // split: partials + merge instead of direct stores
 };
+// Query positions per work-group for a group size (rows / group).
+inline int chunk_tile_positions(int group) { return 256 / group; }
 void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s);
 
 // Split-K paged decode attention plus merge.

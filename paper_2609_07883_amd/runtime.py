@@ -71,6 +71,9 @@ class Session:
     def run(self, batch: api.Batch, x_bits=None) -> None:
         """Enqueue one iteration on the current stream (x_bits: uint16 [rows][d] or None)."""
         m = batch.rows
+        if m > self.x_in.shape[0] or batch.chunk > self.max_c or len(batch.decode_seqs) > self.max_b:
+            raise ValueError(f"batch of C={batch.chunk}, B={len(batch.decode_seqs)} exceeds this session's "
+                             f"buffers (C<={self.max_c}, B<={self.max_b})")
         if x_bits is not None:
             self.x_in[:m].copy_(bits_to_tensor(x_bits, self.dev))
         self.ctx.mixed_iteration(batch, self.x_in.data_ptr(), self.x_out.data_ptr(),

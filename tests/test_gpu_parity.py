@@ -83,6 +83,9 @@ CASES = [
     (1, 7, [5]),
     (130, 16, [2047, 4]),
     (512, 3, [700, 1, 63, 64, 65, 127, 128, 129]),
+    (64, 8192, [1000, 3]),        # few query tiles: key axis split across work-groups
+    (100, 3000, []),              # split with a ragged final tile
+    (512, 0, [2]),                # 8 query tiles, split with a causal diagonal in every tile
 ]
 
 
@@ -145,10 +148,12 @@ def test_errors_are_reported_not_faulted(l8b):
     with pytest.raises(api.SloweaveError) as e:       # duplicate
         sess.run(api.Batch(4, 1, 0, [2, 2], [0, 0]))
     assert e.value.code == api.EINVAL
-    with pytest.raises(api.SloweaveError) as e:       # workspace too small for this batch
-        sess.ctx.mixed_iteration(api.Batch(600, 1, 0, [], []), sess.x_in.data_ptr(),
+    with pytest.raises(api.SloweaveError) as e:       # workspace far too small: refused before any launch
+        sess.ctx.mixed_iteration(api.Batch(30000, 1, 0, [], []), sess.x_in.data_ptr(),
                                  sess.x_out.data_ptr(), sess.ws.data_ptr(), sess.ws_bytes)
     assert e.value.code == api.ENOMEM
+    with pytest.raises(ValueError):                   # more rows than the session's buffers hold
+        sess.run(api.Batch(600, 1, 0, [], []))
     sess.ctx.seq_reserve(2, 16 * (sess.ctx.free_blocks() - 10))
     sess.ctx.seq_create(3)
     free = sess.ctx.free_blocks()
