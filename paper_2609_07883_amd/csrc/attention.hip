@@ -41,10 +41,11 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // its keys 0..P+C-1 under the causal mask.
 //
 // A work-group owns one kv head and 256 rows = (position, q head) pairs of
-// that head's group; each wave owns 64 rows, the four 16-column Q^T tiles of
-// its MFMAs, so one K or V fragment read from LDS feeds four MFMAs.  Keys
-// advance 64 at a time (four pages) through a double-buffered LDS tile shared
-// by the four waves.  A work item covers one key range of one query tile; in
+// that head's group; each of its eight waves owns 32 rows, the two 16-column
+// Q^T tiles of its MFMAs, so one K or V fragment read from LDS feeds two
+// MFMAs and two waves share each SIMD, overlapping one wave's softmax with
+// the other's matrix work.  Keys advance 64 at a time (four pages) through a
+// double-buffered LDS tile shared by the eight waves.  A work item covers one key range of one query tile; in
 // split mode it writes fp32 partials (running max, sum, unnormalised output)
 // that chunk_merge_kernel combines.
 // ---------------------------------------------------------------------------
@@ -55,12 +56,17 @@ __device__ __forceinline__ int kswz(int t, int sub) { return sub ^ ((t >> 1) & 3
 __device__ __forceinline__ int vswz(int d, int grp) { return grp ^ ((d >> 2) & 3); }
 
 template <int HD, int GROUP>
-__global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
+__global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
     constexpr int CHUNKS = 4 * PAGE / 8;  // 16-byte chunks per K (or V) tile of 64 keys
-    constexpr int PER_THREAD = 2 * CHUNKS / 256;
-    constexpr int PW = 64 / GROUP;        // positions per wave
-    constexpr int PWG = 4 * PW;           // positions per work-group
+    constexpr int PER_THREAD = 2 * CHUNKS / 512;
+    constexpr int CT = 2;                 // 16-row column tiles per wave (32 rows)
+    constexpr int PW = 32 / GROUP;        // positions per wave
+    constexpr int PWG = 8 * PW;           // positions per work-group (eight waves)
+    // Lazy rescaling: a row keeps its running max until a tile exceeds it by
+    // 2^kSlack, so probabilities stay <= 2^kSlack and most tiles skip the
+    // rescale of the output accumulators.
+    constexpr float kSlack = 8.0f;
     __shared__ __attribute__((aligned(16))) bf16 Ks[2][4 * PAGE];
     __shared__ __attribute__((aligned(16))) bf16 Vs[2][4 * PAGE];
 
@@ -79,10 +85,10 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
 
     // Q^T operand: row r = ct*16 + col is position p0 + r / GROUP, head kvh*GROUP + r % GROUP
-    bf16x8 qf[4][KK];
+    bf16x8 qf[CT][KK];
     const bf16* qkv = static_cast<const bf16*>(a.qkv);
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
         const int r = ct * 16 + col, qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
 #pragma unroll
         for (int kk = 0; kk < KK; ++kk)
@@ -95,7 +101,7 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
     auto load_tile = [&](int t) {
 #pragma unroll
         for (int j = 0; j < PER_THREAD; ++j) {
-            const int c = tid + j * 256;
+            const int c = tid + j * 512;
             const bool is_v = c >= CHUNKS;
             const int cc = is_v ? c - CHUNKS : c;
             const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
@@ -117,7 +123,7 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
     auto store_tile = [&](int buf) {
 #pragma unroll
         for (int j = 0; j < PER_THREAD; ++j) {
-            const int c = tid + j * 256;
+            const int c = tid + j * 512;
             const bool is_v = c >= CHUNKS;
             const int cc = is_v ? c - CHUNKS : c;
             const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
@@ -135,21 +141,19 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
         }
     };
 
-    f32x4 o[4][NT];
+    f32x4 o[CT][NT];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) o[ct][nt] = f32x4{};
-    float m_run[4], l_run[4];
+    float m_run[CT], l_run[CT];
+    int qpos_col[CT];  // query position of row ct*16 + col
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
         m_run[ct] = -INFINITY;
         l_run[ct] = 0.f;
+        qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
     }
-    // query position of row ct*16 + col (column owner) and of output row ct*16 + 4*grp + e
-    int qpos_col[4];
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct) qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
 
     load_tile(0);
     store_tile(0);
@@ -159,11 +163,11 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
         if (t + 1 < n_tiles) load_tile(t + 1);
         const int key0 = kb + t * 64;
         if (wave_live && key0 <= wave_qpos_hi) {
-            f32x4 sc[4][4];  // [page][ct]
+            f32x4 sc[4][CT];  // [page][ct]
 #pragma unroll
             for (int p = 0; p < 4; ++p)
 #pragma unroll
-                for (int ct = 0; ct < 4; ++ct) sc[p][ct] = f32x4{};
+                for (int ct = 0; ct < CT; ++ct) sc[p][ct] = f32x4{};
 #pragma unroll
             for (int p = 0; p < 4; ++p)
 #pragma unroll
@@ -171,12 +175,14 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
                     const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
                         &Ks[buf][p * PAGE + kk * 512 + col * 32 + kswz(col, grp) * 8]);
 #pragma unroll
-                    for (int ct = 0; ct < 4; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
+                    for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
                 }
             const bool need_mask = key0 + 63 > wave_qpos_lo || key0 + 63 >= ke;
+            float mx[CT];
+            bool grow = false;
 #pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
-                float mx = -INFINITY;
+            for (int ct = 0; ct < CT; ++ct) {
+                float m = -INFINITY;
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
 #pragma unroll
@@ -187,13 +193,31 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
                             x = (kpos <= qpos_col[ct] && kpos < ke) ? x : -INFINITY;
                             sc[p][ct][e] = x;
                         }
-                        mx = fmaxf(mx, x);
+                        m = fmaxf(m, x);
                     }
-                mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-                mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-                const float m_new = fmaxf(m_run[ct], mx * sl2);
-                const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                const float alpha = exp2f(m_run[ct] - m_use);
+                m = fmaxf(m, __shfl_xor(m, 16, 64));
+                m = fmaxf(m, __shfl_xor(m, 32, 64));
+                mx[ct] = m * sl2;
+                grow |= mx[ct] > m_run[ct] + kSlack;
+            }
+            if (__any(grow)) {  // wave-uniform: move every row's max up to its tile max
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+                    const float m_new = fmaxf(m_run[ct], mx[ct]);
+                    const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run[ct] - m_new);
+                    l_run[ct] *= alpha;
+                    m_run[ct] = m_new;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
+                    }
+                }
+            }
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const float m_use = m_run[ct] == -INFINITY ? 0.f : m_run[ct];
                 float ls = 0.f;
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
@@ -203,20 +227,13 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
                         sc[p][ct][e] = v;
                         ls += v;
                     }
-                l_run[ct] = l_run[ct] * alpha + ls;
-                m_run[ct] = m_new;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float ae = __shfl(alpha, grp * 4 + e, 64);
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
-                }
+                l_run[ct] += ls;
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                bf16x8 pf[4];
+                bf16x8 pf[CT];
 #pragma unroll
-                for (int ct = 0; ct < 4; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
+                for (int ct = 0; ct < CT; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
                     const int d = nt * 16 + col;
@@ -225,7 +242,7 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
                     const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
                     const bf16x8 vf = cat44(lo, hi);
 #pragma unroll
-                    for (int ct = 0; ct < 4; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
+                    for (int ct = 0; ct < CT; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
                 }
             }
         }
@@ -235,12 +252,12 @@ __global__ __launch_bounds__(256) void chunk_attn_kernel(ChunkAttnArgs a) {
     if (!wave_live) return;
 
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
+    for (int ct = 0; ct < CT; ++ct) {
         float l = l_run[ct];
         l += __shfl_xor(l, 16, 64);
         l += __shfl_xor(l, 32, 64);
         if (a.split) {
-            const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 64 + ct * 16;
+            const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 32 + ct * 16;
             if (grp == 0) {
                 a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
                 a.part_ml[(rbase + col) * 2 + 1] = l;
@@ -456,7 +473,7 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
 
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
-    chunk_attn_kernel<HD, GROUP><<<dim3(a.n_items, a.hkv), 256, 0, s>>>(a);
+    chunk_attn_kernel<HD, GROUP><<<dim3(a.n_items, a.hkv), 512, 0, s>>>(a);
     if (a.split) chunk_merge_kernel<HD, GROUP><<<dim3(a.c, a.hq), 64, 0, s>>>(a);
 }
 
