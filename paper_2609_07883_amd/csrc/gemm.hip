@@ -173,24 +173,26 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64) void gemm_kernel(GemmArgs g
     for (int j = 0; j < TN; ++j) b_row[j] = wn * WN + j * 32 + (lane & 31);
     const int kg = lane >> 5;
 
+    // Fragments of k-step s+1 are read from LDS while the MFMAs of step s run.
     auto compute = [&](int buf) {
-        // two k-steps per unrolled body: enough independent MFMAs to cover
-        // LDS latency without holding every step's fragments at once
-#pragma unroll 2
-        for (int s = 0; s < BK / 16; ++s) {
-            bf16x8 fa[TM], fb[TN];
+        bf16x8 fa[2][TM], fb[2][TN];
+        auto read_frags = [&](int s, bf16x8* a, bf16x8* b) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                fa[i] = *reinterpret_cast<const bf16x8*>(
-                    &As[buf][a_row[i] * BK + swz(a_row[i], 2 * s + kg) * 8]);
+                a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][a_row[i] * BK + swz(a_row[i], 2 * s + kg) * 8]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                fb[j] = *reinterpret_cast<const bf16x8*>(
-                    &Bs[buf][b_row[j] * BK + swz(b_row[j], 2 * s + kg) * 8]);
+                b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][b_row[j] * BK + swz(b_row[j], 2 * s + kg) * 8]);
+        };
+        read_frags(0, fa[0], fb[0]);
+#pragma unroll
+        for (int s = 0; s < BK / 16; ++s) {
+            const int c = s & 1;
+            if (s + 1 < BK / 16) read_frags(s + 1, fa[c ^ 1], fb[c ^ 1]);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
+                for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[c][i], fb[c][j], acc[i][j]);
         }
     };
 
