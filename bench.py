@@ -30,6 +30,17 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "mixed-batch iteration ms vs chunk size; tokens/s; % HBM/MFMA roofline"
+WORKLOADS = {
+    "sweep8b": "8B-shaped single decoder layer (d 4096, 32/8 heads x 128, FFN 14336), B=32 decodes with "
+               "contexts U[512,2048], chunk C in {64,128,256,512,1024,2048} x prefix P in {0,2048,8192}; "
+               "one step = the 18 mixed iterations",
+    "long": "8B-shaped layer, long context: prompt of 32768 tokens chunked with C in {512,1024,2048,4096} at "
+            "prefixes 0..28672 (step 4096, P+C <= 32768), B=8 decodes with contexts U[16384,32768]; one step = "
+            "the 32 mixed iterations",
+    "chat": "8B-shaped layer, chat/bursty: B in {64,128,256} decodes with log-normal contexts (median 700, "
+            "sigma 0.8, cap 8192), C in {32,64,128,256,512} at a seeded chunk boundary of a log-normal prompt "
+            "(median 1024, cap 8192); one step = the 15 mixed iterations",
+}
 PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
 PEAK_BF16 = 2.5e15         # FLOP/s, dense bf16 MFMA
 C_SWEEP = (64, 128, 256, 512, 1024, 2048)
@@ -108,6 +119,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-table", action="store_true")
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="sweep8b")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path has no multi-GPU mode",
@@ -120,13 +132,30 @@ def main():
 
     torch.cuda.set_device(0)
     shape = synth.LLAMA8B_LAYER
-    ctx_lens = synth.uniform_lengths(B_DEC, 512, 2048, seed=2)
-    max_c = max(C_SWEEP)
-    pre_len = max(P_SWEEP) + max_c
+    # (C, P, B) points of the workload; decode contexts per B
+    if args.workload == "sweep8b":
+        points = [(C, P, B_DEC) for P in P_SWEEP for C in C_SWEEP]
+        ctx_all = synth.uniform_lengths(B_DEC, 512, 2048, seed=2)
+    elif args.workload == "long":
+        points = [(C, P, 8) for C in (512, 1024, 2048, 4096) for P in range(0, 28673, 4096) if P + C <= 32768]
+        ctx_all = synth.uniform_lengths(8, 16384, 32768, seed=2)
+    else:
+        prompt = int(synth.lognormal_lengths(1, 1024, 0.8, 8192, seed=4)[0])
+        rng = np.random.default_rng(5)
+        points = []
+        for B in (64, 128, 256):
+            for C in (32, 64, 128, 256, 512):
+                k = int(rng.integers(0, max(1, -(-prompt // C))))
+                points.append((C, min(k * C, 8192 - C), B))
+        ctx_all = synth.lognormal_lengths(256, 700, 0.8, 8192, seed=2)
+    max_b = max(p[2] for p in points)
+    max_c = max(p[0] for p in points)
+    pre_len = max(p[0] + p[1] for p in points)
+    ctx_lens = ctx_all[:max_b]
     blocks = pre_len // 16 + int(sum((ctx_lens + 16) // 16)) + 1
-    prof_blocks = (2048 + max_c) // 16 + B_DEC * (2048 + 16) // 16 + 16
+    prof_blocks = (2048 + 2048) // 16 + B_DEC * (2048 + 16) // 16 + 16
     t0 = time.time()
-    sess = Session(shape, num_blocks=blocks + prof_blocks, max_c=max_c, max_b=B_DEC)
+    sess = Session(shape, num_blocks=blocks + prof_blocks, max_c=max(max_c, 2048), max_b=max(max_b, B_DEC))
     ctx = sess.ctx
     # pre-existing contexts: seeded N(0,1) bf16 K/V
     pre = 1
@@ -134,19 +163,18 @@ def main():
     ctx.seq_reserve(pre, pre_len)
     kb, vb = synth.cached_kv(pre_len, shape.n_kv_heads, shape.head_dim, 3, 0, pre)
     sess.write_kv(0, pre, kb, vb)
-    dec = list(range(100, 100 + B_DEC))
+    dec = list(range(100, 100 + max_b))
     for sid, L in zip(dec, ctx_lens):
         ctx.seq_create(sid)
         ctx.seq_reserve(sid, int(L) + 1)
         kb, vb = synth.cached_kv(int(L), shape.n_kv_heads, shape.head_dim, 3, 0, sid)
         sess.write_kv(0, sid, kb, vb)
-    x = synth.embeddings(max_c + B_DEC, shape.d_model, seed=1, stream=0)
+    x = synth.embeddings(sess.x_in.shape[0], shape.d_model, seed=1, stream=0)
     sess.x_in.copy_(torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16))
     torch.cuda.synchronize()
     log(f"setup {time.time() - t0:.1f}s: {blocks + prof_blocks} KV blocks, workspace {sess.ws_bytes / 2**20:.0f} MiB")
 
-    points = [(C, P) for P in P_SWEEP for C in C_SWEEP]
-    batches = [api.Batch(C, pre, P, dec, [int(v) for v in ctx_lens]) for C, P in points]
+    batches = [api.Batch(C, pre, P, dec[:B], [int(v) for v in ctx_lens[:B]]) for C, P, B in points]
     stream = torch.cuda.current_stream().cuda_stream
 
     def step():
@@ -170,33 +198,32 @@ def main():
     stage_ms = [ctx.stage_times(ago) for ago in range(n_iter)][::-1]  # oldest first
     ctx.set_stage_timing(0)
 
-    rows_per_step = sum(C + B_DEC for C, _ in points)
+    rows_per_step = sum(C + B for C, _, B in points)
     tokens_s = rows_per_step * args.steps / elapsed
     ms_per_step = elapsed * 1e3 / args.steps
 
     # per-point iteration ms (sum of stage events) and per-stage totals
-    ctx_sum = int(np.sum(ctx_lens + 1))
     per_point = []
     stage_tot = {s: 0.0 for s in api.STAGES}
     stage_roof = {s: 0.0 for s in api.STAGES}
     stage_flops = {s: 0.0 for s in api.STAGES}
     stage_bytes = {s: 0.0 for s in api.STAGES}
     for i, st in enumerate(stage_ms):
-        C, P = points[i % len(points)]
-        work = stage_work(shape, C, P, B_DEC, ctx_sum)
+        C, P, B = points[i % len(points)]
+        work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
         for s in api.STAGES:
             stage_tot[s] += st[s]
             f, b = work[s]
             stage_flops[s] += f
             stage_bytes[s] += b
             stage_roof[s] += roof_time(f, b) * 1e3
-    for j, (C, P) in enumerate(points):
+    for j, (C, P, B) in enumerate(points):
         its = [stage_ms[k] for k in range(j, n_iter, len(points))]
         ms = float(np.median([sum(st.values()) for st in its]))
-        work = stage_work(shape, C, P, B_DEC, ctx_sum)
+        work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
         roof = sum(roof_time(*work[s]) for s in api.STAGES) * 1e3
-        per_point.append({"C": C, "P": P, "B": B_DEC, "ms": round(ms, 4),
-                          "tokens_s": round((C + B_DEC) / ms * 1e3, 1),
+        per_point.append({"C": C, "P": P, "B": B, "ms": round(ms, 4),
+                          "tokens_s": round((C + B) / ms * 1e3, 1),
                           "roofline_frac": round(roof / ms, 3)})
     kernels = {}
     for s in api.STAGES:
@@ -221,11 +248,12 @@ def main():
     roofline["traffic"] = None
     roofline["launches"] = n_iter
     roofline["avg_launch_us"] = round(t_dom / n_iter * 1e6, 2)
-    log(f"timed {args.steps} steps x {len(points)} iterations: {elapsed * 1e3:.1f} ms, {tokens_s:.0f} tokens/s")
+    log(f"{args.workload}: timed {args.steps} steps x {len(points)} iterations: {elapsed * 1e3:.1f} ms, "
+        f"{tokens_s:.0f} tokens/s")
 
     # cost table over (B, C), monotonicity, controller decision time
     table = None
-    if not args.no_table:
+    if not args.no_table and args.workload == "sweep8b":
         flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         t1 = time.time()
         c_grid = [0] + list(C_SWEEP)
@@ -256,7 +284,7 @@ def main():
         log(f"cost table {table['seconds']}s, {viol} raw decreases")
 
     cpu = None
-    if not args.no_cpu:
+    if not args.no_cpu and args.workload == "sweep8b":
         t1 = time.time()
         cpu = cpu_baseline(shape, ctx_lens)
         log(f"cpu baseline {time.time() - t1:.1f}s: {cpu['value']:.1f} tokens/s on {cpu['cores']} threads")
@@ -265,11 +293,8 @@ def main():
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
-           "config": {"workload": "8B-shaped single decoder layer (d 4096, 32/8 heads x 128, FFN 14336), "
-                                  "B=32 decodes with contexts U[512,2048], chunk C in "
-                                  "{64,128,256,512,1024,2048} x prefix P in {0,2048,8192}; one step = the 18 "
-                                  "mixed iterations",
-                      "block_size": 16, "seeds": {"weights": 0, "embeddings": 1, "contexts": 2, "kv": 3}},
+           "config": {"workload": WORKLOADS[args.workload], "block_size": 16,
+                      "seeds": {"weights": 0, "embeddings": 1, "contexts": 2, "kv": 3}},
            "roofline": roofline, "cpu_baseline": cpu, "sweep": per_point, "kernels": kernels,
            "cost_table": table}
     print(json.dumps(out))

@@ -318,11 +318,47 @@ __global__ __launch_bounds__(64) void chunk_merge_kernel(ChunkAttnArgs a) {
 // ---------------------------------------------------------------------------
 // Decode attention, split over the key axis: one wave per (work item, kv
 // head); a work item is one split of `split_tokens` keys of one decode.  All
-// q heads of the kv head's group (<= 16) are the columns of Q^T.
+// q heads of the kv head's group (<= 16) are the columns of Q^T.  Keys are
+// taken 32 at a time (two pages) straight from the pages into MFMA operand
+// registers, with the next step's pages requested before the current step is
+// multiplied (two register sets), so every wave keeps 16 KB of loads in
+// flight while it computes.
 // ---------------------------------------------------------------------------
 template <int HD>
-__global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
+struct DecodeStep {
+    bf16x8 k[2][HD / 32];
+    bf16x4 v[2][HD / 16];
+};
+
+template <int HD>
+__device__ __forceinline__ void decode_load(DecodeStep<HD>& st, const bf16* kpool, const bf16* vpool,
+                                            const int* bt, int c0, int tok1, int hkv, int kvh, int col,
+                                            int grp) {
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const int pg = (c0 >> 4) + p;
+        if (pg * 16 < tok1) {
+            const size_t page = (static_cast<size_t>(bt[pg]) * hkv + kvh) * PAGE;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                st.k[p][kk] = *reinterpret_cast<const bf16x8*>(kpool + page + kk * 512 + col * 32 + grp * 8);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                st.v[p][nt] = *reinterpret_cast<const bf16x4*>(vpool + page + (nt * 16 + col) * 16 + grp * 4);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) st.k[p][kk] = bf16x8{};
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) st.v[p][nt] = bf16x4{};
+        }
+    }
+}
+
+template <int HD>
+__global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
+    constexpr int KK = HD / 32, NT = HD / 16;
+    constexpr float kSlack = 8.0f;  // lazy rescaling threshold (log2 units)
     const int lane = threadIdx.x, grp = lane >> 4, col = lane & 15;
     const int w = blockIdx.x, kvh = blockIdx.y;
     const int b = a.work_b[w], split = a.work_s[w];
@@ -351,83 +387,73 @@ __global__ __launch_bounds__(64) void decode_attn_kernel(DecodeAttnArgs a) {
     for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{};
     float m_run = -INFINITY, l_run = 0.f;
 
-    for (int c0 = tok0; c0 < tok1; c0 += 64) {
-        bf16x8 kf[4][KK];
-        bf16x4 vf[4][NT];
+    auto compute = [&](DecodeStep<HD>& st, int c0) {
+        const bool tail = c0 + 32 > tok1;
+        if (tail) {  // zero V of keys past the split (possibly unwritten slots)
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const int pg = (c0 >> 4) + p;
-            if (pg * 16 < tok1) {
-                const size_t page = (static_cast<size_t>(bt[pg]) * a.hkv + kvh) * PAGE;
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk)
-                    kf[p][kk] = *reinterpret_cast<const bf16x8*>(kpool + page + kk * 512 + col * 32 + grp * 8);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-                    vf[p][nt] = *reinterpret_cast<const bf16x4*>(vpool + page + (nt * 16 + col) * 16 + grp * 4);
-            } else {
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk) kf[p][kk] = bf16x8{};
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) vf[p][nt] = bf16x4{};
-            }
-        }
-        const bool tail = c0 + 64 > tok1;
-        if (tail) {  // zero V of tokens past the split (possibly unwritten slots)
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
+            for (int p = 0; p < 2; ++p)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (c0 + p * 16 + grp * 4 + e >= tok1)
 #pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) vf[p][nt][e] = bf16(0.0f);
+                        for (int nt = 0; nt < NT; ++nt) st.v[p][nt][e] = bf16(0.0f);
         }
-
-        f32x4 s[4];
+        f32x4 s[2];
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
+        for (int p = 0; p < 2; ++p) {
             s[p] = f32x4{};
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) s[p] = mfma16(kf[p][kk], qf[kk], s[p]);
+            for (int kk = 0; kk < KK; ++kk) s[p] = mfma16(st.k[p][kk], qf[kk], s[p]);
         }
         float mx = -INFINITY;
 #pragma unroll
-        for (int p = 0; p < 4; ++p)
+        for (int p = 0; p < 2; ++p)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                float x = s[p][e] * sl2;
+                float x = s[p][e];
                 if (tail && c0 + p * 16 + grp * 4 + e >= tok1) x = -INFINITY;
                 s[p][e] = x;
                 mx = fmaxf(mx, x);
             }
         mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run - m_use);
-        float ls = 0.f;
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
+        mx *= sl2;
+        if (__any(mx > m_run + kSlack)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+            l_run *= alpha;
+            m_run = m_new;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float v = exp2f(s[p][e] - m_use);
+                const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) o[nt][e] *= ae;
+            }
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        float ls = 0.f;
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float v = exp2f(fmaf(s[p][e], sl2, -m_use));
                 s[p][e] = v;
                 ls += v;
             }
-        l_run = l_run * alpha + ls;
-        m_run = m_new;
+        l_run += ls;
+        const bf16x8 pf = to_bf16x8(s[0], s[1]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float ae = __shfl(alpha, grp * 4 + e, 64);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) o[nt][e] *= ae;
-        }
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const bf16x8 pf = to_bf16x8(s[2 * j], s[2 * j + 1]);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, cat44(vf[2 * j][nt], vf[2 * j + 1][nt]), o[nt]);
-        }
+        for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, cat44(st.v[0][nt], st.v[1][nt]), o[nt]);
+    };
+
+    DecodeStep<HD> sa, sb;
+    decode_load<HD>(sa, kpool, vpool, bt, tok0, tok1, a.hkv, kvh, col, grp);
+    for (int c0 = tok0; c0 < tok1; c0 += 64) {
+        if (c0 + 32 < tok1) decode_load<HD>(sb, kpool, vpool, bt, c0 + 32, tok1, a.hkv, kvh, col, grp);
+        compute(sa, c0);
+        if (c0 + 32 >= tok1) break;
+        if (c0 + 64 < tok1) decode_load<HD>(sa, kpool, vpool, bt, c0 + 64, tok1, a.hkv, kvh, col, grp);
+        compute(sb, c0 + 32);
     }
 
     float l = l_run;

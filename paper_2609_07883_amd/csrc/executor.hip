@@ -25,7 +25,7 @@ using namespace slw;
 namespace {
 
 constexpr int kRing = 4;                 // pinned staging buffers in flight
-constexpr int kDecodeTargetWaves = 2048; // decode work-groups aimed for per iteration
+constexpr int kDecodeTargetWaves = 4096; // decode work-groups aimed for per iteration
 constexpr int kChunkTargetWgs = 512;     // chunk-attention work-groups aimed for per iteration
 constexpr size_t kAlign = 256;
 
@@ -86,11 +86,11 @@ int decode_work_cap(const slw_model_cfg& c, int B) {
 }
 
 // Keys per split: a multiple of 64 chosen so that about kDecodeTargetWaves
-// work-groups cover all decodes' keys.
+// work-groups cover all decodes' keys (at least 128 keys each).
 int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
     const int64_t per_head = std::max(1, kDecodeTargetWaves / c.n_kv_heads);
     int64_t s = ceil_div(total_keys, per_head);
-    s = ceil_div(std::max<int64_t>(s, 64), 64) * 64;
+    s = ceil_div(std::max<int64_t>(s, 128), 64) * 64;
     return static_cast<int>(s);
 }
 
