@@ -14,7 +14,7 @@ entry of the dominant kernel, the oracle timed on the host cores on a bounded
 sample, the cost table profiled over (B, C) with its monotonicity, and the
 controller's per-decision time.
 
-    python bench.py [--steps K] [--warmup W] [--no-cpu] [--no-table]
+    python bench.py [--steps K] [--warmup W] [--no-cpu] [--no-table] [--workload sweep8b|long|chat]
 """
 from __future__ import annotations
 
@@ -73,6 +73,36 @@ def stage_work(shape, C, P, B, ctx_sum):
     return w
 
 
+# Stage -> GEMM source whose kernels the stage runs (traffic is void once it changes).
+STAGE_SOURCE = {"qkv_gemm": "gemm.hip", "o_gemm": "gemm.hip", "gateup_gemm": "gemm.hip",
+                "down_gemm": "gemm.hip", "chunk_attn": "attention.hip", "decode_attn": "attention.hip"}
+
+
+def measured_traffic(stage, workload):
+    """HBM bytes per launch of `stage` from the committed counter summary, or None.
+
+    The summary (profiles/<stage>_<workload>_traffic.md) records FETCH_SIZE +
+    WRITE_SIZE per launch, scaled by the same counters on a plain copy of
+    known size, and the sha256 of the kernel source it was taken with; a
+    different source today makes the figure stale, so None is returned.
+    """
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{stage}_{workload}_traffic.md")
+    src = STAGE_SOURCE.get(stage)
+    if not src or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    with open(os.path.join(ROOT, "paper_2609_07883_amd", "csrc", src), "rb") as f:
+        digest = hashlib.sha256(f.read()).hexdigest()
+    if fields.get("source sha256") != digest or "bytes per launch" not in fields:
+        return None
+    return float(fields["bytes per launch"])
+
+
 def roof_time(flops, nbytes):
     return max(flops / PEAK_BF16, nbytes / PEAK_HBM)
 
@@ -120,7 +150,18 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-table", action="store_true")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="sweep8b")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": src.numel() * 4, "copies": 3}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path has no multi-GPU mode",
               file=sys.stderr)
@@ -245,7 +286,7 @@ def main():
         roofline = {"kernel": dom, "bound": "hbm", "achieved": round(stage_bytes[dom] / t_dom / 1e9, 1),
                     "peak": 8000.0, "unit": "GB/s"}
     roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
-    roofline["traffic"] = None
+    roofline["traffic"] = measured_traffic(dom, args.workload)
     roofline["launches"] = n_iter
     roofline["avg_launch_us"] = round(t_dom / n_iter * 1e6, 2)
     log(f"{args.workload}: timed {args.steps} steps x {len(points)} iterations: {elapsed * 1e3:.1f} ms, "

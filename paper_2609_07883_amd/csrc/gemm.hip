@@ -25,7 +25,7 @@
 namespace slw {
 namespace {
 
-constexpr int BK = 64;
+constexpr int BK_MAX = 64;  // k-steps per LDS stage are 32 or 64 wide
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
@@ -81,14 +81,25 @@ __device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, in
     }
 }
 
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+// LDS rows hold BK bf16 (BK/8 chunks of 16 bytes).  Chunk c of row r is
+// stored at c ^ ((r / (16 / CPR)) % CPR): the rows read by one MFMA operand
+// load land on distinct banks for both 128-byte (BK 64) and 64-byte (BK 32)
+// rows.
+template <int BK>
+__device__ __forceinline__ int swz(int row, int chunk) {
+    constexpr int CPR = BK / 8;
+    return chunk ^ ((row / (16 / CPR)) & (CPR - 1));
+}
 
 // Tile (m, n) of linear block id `pid`.  Blocks are dispatched round-robin to
 // the 8 XCDs (pid % 8), each with its own L2; the remap gives every XCD a
-// contiguous range of the tile order, and the tile order walks GROUP_M tile
+// contiguous range of the tile order, and the tile order walks group_m tile
 // rows at a time so that blocks running together share A rows and B columns.
+// With at most 16 tile rows a group spans them all: each weight panel is then
+// streamed into one XCD's L2 once for every row tile.
 __device__ __forceinline__ void tile_of(int pid, int nt_m, int nt_n, int& tm, int& tn) {
-    constexpr int kXcd = 8, GROUP_M = 8;
+    constexpr int kXcd = 8;
+    const int GROUP_M = nt_m <= 16 ? nt_m : 8;
     const int total = nt_m * nt_n;
     const int q = total / kXcd, r = total % kXcd;
     const int xcd = pid % kXcd, local = pid / kXcd;
@@ -101,14 +112,17 @@ __device__ __forceinline__ void tile_of(int pid, int nt_m, int nt_n, int& tm, in
     tn = in_group / gsize;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool SPLIT>
-__global__ __launch_bounds__(WAVES_M * WAVES_N * 64) void gemm_kernel(GemmArgs g, float* __restrict__ partial,
-                                                                      int k_per_split) {
+// The k-32 tiles ask for two waves per SIMD so that two work-groups fit on a CU.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int EPI, bool SPLIT>
+__global__ __launch_bounds__(WAVES_M * WAVES_N * 64, BK == 32 ? 2 : 1) void gemm_kernel(GemmArgs g,
+                                                                                        float* __restrict__ partial,
+                                                                                        int k_per_split) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int A_LOADS = BM * 8 / THREADS;
-    constexpr int B_LOADS = BN * 8 / THREADS;
+    constexpr int CPR = BK / 8;  // 16-byte chunks per LDS row
+    constexpr int A_LOADS = BM * CPR / THREADS;
+    constexpr int B_LOADS = BN * CPR / THREADS;
     static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small");
     static_assert(WN % 64 == 0, "paired epilogues need whole 64-column pairs per wave");
 
@@ -132,16 +146,16 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64) void gemm_kernel(GemmArgs g
     int a_off[A_LOADS], a_lds[A_LOADS];
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
-        const int idx = tid + i * THREADS, row = idx >> 3, ch = idx & 7;
+        const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
         a_off[i] = min(m0 + row, g.m - 1) * g.lda + ch * 8;
-        a_lds[i] = row * BK + swz(row, ch) * 8;
+        a_lds[i] = row * BK + swz<BK>(row, ch) * 8;
     }
     int b_off[B_LOADS], b_lds[B_LOADS];
 #pragma unroll
     for (int i = 0; i < B_LOADS; ++i) {
-        const int idx = tid + i * THREADS, row = idx >> 3, ch = idx & 7;
+        const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
         b_off[i] = w_row<EPI>(g, n0 + row) * g.k + ch * 8;
-        b_lds[i] = row * BK + swz(row, ch) * 8;
+        b_lds[i] = row * BK + swz<BK>(row, ch) * 8;
     }
 
     bf16x8 ra[A_LOADS], rb[B_LOADS];
@@ -179,10 +193,10 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64) void gemm_kernel(GemmArgs g
         auto read_frags = [&](int s, bf16x8* a, bf16x8* b) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
-                a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][a_row[i] * BK + swz(a_row[i], 2 * s + kg) * 8]);
+                a[i] = *reinterpret_cast<const bf16x8*>(&As[buf][a_row[i] * BK + swz<BK>(a_row[i], 2 * s + kg) * 8]);
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][b_row[j] * BK + swz(b_row[j], 2 * s + kg) * 8]);
+                b[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][b_row[j] * BK + swz<BK>(b_row[j], 2 * s + kg) * 8]);
         };
         read_frags(0, fa[0], fb[0]);
 #pragma unroll
@@ -323,26 +337,30 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
 }
 
 struct TileCfg {
-    int bm, bn, waves_m, waves_n;
+    int bm, bn, waves_m, waves_n, bk;
 };
 // 0: 128x128 / 4 waves (64x64 each)      1: 64x128 / 4 waves (32x64)
 // 2: 32x256 / 4 waves (32x64)            3: 256x256 / 8 waves (128x64)
 // 4: 256x256 / 4 waves (128x128)         5: 128x256 / 8 waves (64x64)
-constexpr TileCfg kCfgs[] = {{128, 128, 2, 2}, {64, 128, 2, 2}, {32, 256, 1, 4},
-                             {256, 256, 2, 4}, {256, 256, 2, 2}, {128, 256, 2, 4}};
+// 6: 256x128 / 4 waves (128x64), k 32    7: 128x256 / 4 waves (64x128), k 32
+// The k-32 tiles use 48 KB of LDS, so two work-groups share a CU and one's
+// loads overlap the other's matrix work.
+constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64}, {64, 128, 2, 2, 64}, {32, 256, 1, 4, 64},
+                             {256, 256, 2, 4, 64}, {256, 256, 2, 2, 64}, {128, 256, 2, 4, 64},
+                             {256, 128, 2, 2, 32}, {128, 256, 2, 2, 32}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int EPI>
 void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
     const int tiles = ((g.m + BM - 1) / BM) * (g.n / BN);
     dim3 grid(tiles, p.splits);
     const int kps = g.k / p.splits;
     if (p.splits == 1) {
-        gemm_kernel<BM, BN, WAVES_M, WAVES_N, EPI, false><<<grid, THREADS, 0, s>>>(g, nullptr, kps);
+        gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, EPI, false><<<grid, THREADS, 0, s>>>(g, nullptr, kps);
         return;
     }
-    gemm_kernel<BM, BN, WAVES_M, WAVES_N, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
+    gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
     size_t work;
     if (EPI == EPI_QKV) work = static_cast<size_t>(g.m) * (g.n / 2);
     else if (EPI == EPI_SWIGLU) work = static_cast<size_t>(g.m) * (g.n / 8);
@@ -350,14 +368,14 @@ void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s
     splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, p.splits);
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK>
 void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     float* part = static_cast<float*>(partial);
     switch (g.epi) {
-        case EPI_RESID_F32OUT: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_RESID_F32OUT>(g, p, part, s); break;
-        case EPI_RESID_F32IN: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_RESID_F32IN>(g, p, part, s); break;
-        case EPI_SWIGLU: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_SWIGLU>(g, p, part, s); break;
-        default: launch_epi<BM, BN, WAVES_M, WAVES_N, EPI_QKV>(g, p, part, s); break;
+        case EPI_RESID_F32OUT: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_RESID_F32OUT>(g, p, part, s); break;
+        case EPI_RESID_F32IN: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_RESID_F32IN>(g, p, part, s); break;
+        case EPI_SWIGLU: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_SWIGLU>(g, p, part, s); break;
+        default: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_QKV>(g, p, part, s); break;
     }
 }
 
@@ -386,7 +404,7 @@ GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
     const long tiles = static_cast<long>(n / p.bn) * ((m + p.bm - 1) / p.bm);
     int splits = 1;
     // Too few tiles to fill 256 compute units: split k (each split >= 512 deep).
-    while (splits < 8 && tiles * splits < 384 && k % (2 * splits * BK) == 0 && k / (2 * splits) >= 512)
+    while (splits < 8 && tiles * splits < 384 && k % (2 * splits * BK_MAX) == 0 && k / (2 * splits) >= 512)
         splits *= 2;
     p.splits = splits;
     p.partial_bytes = splits > 1 ? static_cast<size_t>(splits) * m * n * sizeof(float) : 0;
@@ -394,18 +412,20 @@ GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
 }
 
 bool gemm_shape_ok(const GemmPlan& p, int n, int k) {
-    return p.cfg >= 0 && p.cfg < kNumCfgs && n % p.bn == 0 && k % (p.splits * BK) == 0;
+    return p.cfg >= 0 && p.cfg < kNumCfgs && n % p.bn == 0 && k % (p.splits * BK_MAX) == 0;
 }
 
 void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     if (g.m <= 0) return;
     switch (p.cfg) {
-        case 0: launch_cfg<128, 128, 2, 2>(g, p, partial, s); break;
-        case 1: launch_cfg<64, 128, 2, 2>(g, p, partial, s); break;
-        case 2: launch_cfg<32, 256, 1, 4>(g, p, partial, s); break;
-        case 3: launch_cfg<256, 256, 2, 4>(g, p, partial, s); break;
-        case 4: launch_cfg<256, 256, 2, 2>(g, p, partial, s); break;
-        default: launch_cfg<128, 256, 2, 4>(g, p, partial, s); break;
+        case 0: launch_cfg<128, 128, 2, 2, 64>(g, p, partial, s); break;
+        case 1: launch_cfg<64, 128, 2, 2, 64>(g, p, partial, s); break;
+        case 2: launch_cfg<32, 256, 1, 4, 64>(g, p, partial, s); break;
+        case 3: launch_cfg<256, 256, 2, 4, 64>(g, p, partial, s); break;
+        case 4: launch_cfg<256, 256, 2, 2, 64>(g, p, partial, s); break;
+        case 5: launch_cfg<128, 256, 2, 4, 64>(g, p, partial, s); break;
+        case 6: launch_cfg<256, 128, 2, 2, 32>(g, p, partial, s); break;
+        default: launch_cfg<128, 256, 2, 2, 32>(g, p, partial, s); break;
     }
 }
 
