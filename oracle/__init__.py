@@ -24,6 +24,6 @@ Contents
 ``serving``  Request-level metrics of Sec. 4.3 (TTFT, within-request P99
              TPOT, goodput).
 
-Every function states the passage it follows.  Readings where the paper is
-silent or ambiguous are listed in the design doc and repeated at the function.
+Every function states the passage it follows, and each reading taken where
+the paper is silent or ambiguous is stated at the function that relies on it.
 """

@@ -4,7 +4,7 @@ Test infrastructure only (see ``oracle/__init__``).
 
 The paper keeps the runtime's paged KV layout unchanged and allocates
 blocks as each chunk is processed (Table 1).  It does not spell out an
-allocation order, so this follows the reading stated in the design doc:
+allocation order, so this takes the following reading:
 
 * blocks hold ``block_size`` (16) consecutive positions of one sequence;
 * a sequence grows by whole blocks, always taking the lowest-numbered free

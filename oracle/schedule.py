@@ -12,7 +12,7 @@ Test infrastructure only (see ``oracle/__init__``).
 
 Times are integer nanoseconds so that every comparison is exact.
 
-Readings (the paper is silent or ambiguous):
+Readings (the paper is silent or ambiguous here):
 * percentiles are nearest-rank, x_sorted[ceil(q k) - 1] of k samples;
 * the decode-batch size n rounds up to the next grid point; n above the
   last grid point is out of range;

@@ -383,15 +383,16 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 
 // Tile and split choice, from timings of every configuration on the
 // 8B-layer shapes (m = 96 .. 4104): 64-row tiles with split-K while weight
-// streaming dominates, 128x128 in the middle, 256x256 once there are enough
-// tiles to fill the chip.  n must be a multiple of 128 and k of 64.
+// streaming dominates, then whichever of the k-64 (one work-group per CU) and
+// k-32 (two per CU) tiles measured fastest in each band of m.  n must be a
+// multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     int cfg;
-    if (k >= 8192) cfg = m >= 1024 ? 3 : 1;               // deep k (down projection)
-    else if (n >= 16384) cfg = m <= 320 ? 1 : (m < 1600 ? 0 : 3);  // wide n (gate/up)
-    else if (m <= 320) cfg = 1;
-    else if (n >= 6144) cfg = 0;
-    else cfg = m > 3000 ? 3 : 1;
+    if (k >= 8192) cfg = m <= 160 ? 1 : 3;                                   // deep k (down)
+    else if (n >= 16384)                                                     // wide n (gate/up)
+        cfg = m <= 160 ? 1 : m <= 400 ? 6 : m < 800 ? 1 : m < 1600 ? 7 : 3;
+    else if (n >= 6144) cfg = m <= 400 ? 1 : (m >= 1600 && m < 3000) ? 6 : 0;   // qkv
+    else cfg = m <= 400 ? 0 : (m >= 1600 && m < 3000) ? 7 : 1;               // o
     if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
     return plan_with_cfg(cfg, m, n, k);
 }
