@@ -21,8 +21,10 @@ Contents
              table with a cumulative maximum along the chunk axis
              (Sec. 5.1) and its lookup between grid points (Sec. 6.4), and
              the simulator's analytic cost model (Sec. 4.1).
-``serving``  Request-level metrics of Sec. 4.3 (TTFT, within-request P99
-             TPOT, goodput).
+``serving``  The iteration-level serving loop of Sec. 4.1 under the deadline
+             model of Sec. 3.1 (SLOWeave or fixed chunks, oldest-first), and
+             the request-level metrics of Sec. 4.3 (TTFT, within-request P99
+             TPOT, SLO attainment, goodput).
 
 Every function states the passage it follows, and each reading taken where
 the paper is silent or ambiguous is stated at the function that relies on it.

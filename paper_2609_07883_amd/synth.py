@@ -13,7 +13,9 @@ Recipe (all numpy PCG64 ``default_rng``):
   * token embeddings (the iteration's input rows): N(0, 1), bf16;
   * pre-existing cached K/V (decode contexts, prefill prefixes): N(0, 1),
     bf16, one independent stream per (layer, sequence);
-  * context and prompt lengths: uniform or clipped log-normal integers.
+  * context and prompt lengths: uniform or clipped log-normal integers;
+  * request traces: Poisson arrivals with seeded bursts, mixed prompt
+    lengths and geometric output lengths (``request_trace``).
 """
 from __future__ import annotations
 
@@ -129,3 +131,62 @@ def lognormal_lengths(n: int, median: float, sigma: float, cap: int, seed: int =
     """n integers min(cap, max(floor, round(median * exp(sigma z))))."""
     z = np.random.default_rng(seed).standard_normal(n)
     return np.clip(np.rint(median * np.exp(sigma * z)), floor, cap).astype(np.int64)
+
+
+@dataclass(frozen=True)
+class RequestTrace:
+    """Arrays of one synthetic request trace, ordered by arrival."""
+    arrival_ns: np.ndarray   # int64, first arrival at 0
+    prompt: np.ndarray       # int64 >= 1
+    output: np.ndarray       # int64 >= 1
+
+    def __len__(self):
+        return len(self.arrival_ns)
+
+
+def request_trace(n: int, rate_per_s: float, seed: int = 3, burst_factor: float = 4.0,
+                  burst_s: float = 2.0, burst_every_s: float = 20.0, short_median: float = 512,
+                  short_sigma: float = 0.8, short_cap: int = 16384, long_lo: int = 4096,
+                  long_hi: int = 16384, output_mean: float = 256.0, output_cap: int = 4096) -> RequestTrace:
+    """n requests: Poisson arrivals at rate_per_s, raised burst_factor-fold for
+    burst_s seconds at burst starts that themselves form a Poisson process of
+    mean gap burst_every_s (0 disables bursts); half the prompts (a fair coin
+    per request) are min(short_cap, round(short_median * exp(short_sigma z))),
+    the others uniform in [long_lo, long_hi]; outputs are geometric on
+    {1, 2, ...} with mean output_mean, capped at output_cap.
+    """
+    rng = np.random.default_rng(seed)
+    bursts = []
+    if burst_every_s > 0 and burst_factor != 1.0:
+        t = 0.0
+        while len(bursts) < 100000:
+            t += rng.exponential(burst_every_s)
+            bursts.append(t)
+            if t > 10.0 * n / rate_per_s + burst_every_s:
+                break
+
+    def rate_at(t):
+        """(arrival rate at time t, next time the rate changes)."""
+        i = int(np.searchsorted(bursts, t, side="right")) - 1
+        if i >= 0 and t < bursts[i] + burst_s:
+            return rate_per_s * burst_factor, bursts[i] + burst_s
+        return rate_per_s, (bursts[i + 1] if i + 1 < len(bursts) else np.inf)
+
+    times = np.empty(n)
+    t = 0.0
+    for k in range(n):
+        while True:            # memoryless: restart the draw at every rate change
+            rate, edge = rate_at(t)
+            dt = rng.exponential(1.0 / rate)
+            if t + dt < edge:
+                t += dt
+                break
+            t = edge
+        times[k] = t
+    arrival = np.rint((times - times[0]) * 1e9).astype(np.int64)
+    coin = rng.random(n) < 0.5
+    short = np.clip(np.rint(short_median * np.exp(short_sigma * rng.standard_normal(n))), 1, short_cap)
+    long_ = rng.integers(long_lo, long_hi + 1, size=n)
+    prompt = np.where(coin, short, long_).astype(np.int64)
+    output = np.minimum(rng.geometric(1.0 / output_mean, size=n), output_cap).astype(np.int64)
+    return RequestTrace(arrival, prompt, output)

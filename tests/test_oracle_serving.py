@@ -1,0 +1,182 @@
+"""Pins for the serving oracle (Sec. 3.1 deadline model, Sec. 4.1 simulator, Sec. 4.3 metrics).
+
+The worked traces below were stepped through by hand with the Sec. 4.1 cost
+model T(n, c) = 0.35 + 1[n>0](0.90 + 0.055 n) + 1[c>0](0.40 + 0.006 c) ms;
+each expected time is written out as its sum of terms.  They pin the event
+logic: chunk sequencing, when the first token appears, when a new arrival
+becomes eligible, oldest-first order, decode iterations, finishing.
+"""
+import numpy as np
+import pytest
+
+from oracle import schedule as S
+from oracle import serving as V
+from paper_2609_07883_amd import synth
+
+MS = 1_000_000
+
+
+def R(rid, arrival, prompt, output):
+    return V.Request(rid, arrival, prompt, output)
+
+
+def test_single_request_fixed_chunks_by_hand():
+    tr = V.simulate([R(0, 0, 100, 3)], cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS,
+                    policy="fixed", fixed_chunk=64)
+    t1 = 350_000 + 400_000 + 6_000 * 64            # chunk of 64, nothing decoding
+    t2 = t1 + 350_000 + 400_000 + 6_000 * 36       # last 36 prompt tokens -> first token
+    t3 = t2 + 350_000 + 900_000 + 55_000           # one decode
+    t4 = t3 + 350_000 + 900_000 + 55_000
+    assert tr.token_ns[0] == [t2, t3, t4]
+    assert [(i.chunk, i.n_decode) for i in tr.iterations] == [(64, 0), (36, 0), (0, 1), (0, 1)]
+    m = V.request_metrics(R(0, 0, 100, 3), tr.token_ns[0], 10 * MS, 10 * MS)
+    assert (m.ttft_ns, m.tpot_p99_ns, m.meets) == (2_100_000, 1_305_000, True)
+
+
+def test_arrival_during_iteration_waits_for_its_end():
+    reqs = [R(0, 0, 10, 2), R(1, 500_000, 5, 1)]
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="fixed", fixed_chunk=64)
+    e1 = 350_000 + 400_000 + 6_000 * 10                                  # r0 prompt alone
+    e2 = e1 + 350_000 + (900_000 + 55_000) + (400_000 + 6_000 * 5)      # r0 decode + r1 prompt
+    assert tr.token_ns == {0: [e1, e2], 1: [e2]}
+    assert tr.iterations[1].prefill_rid == 1 and tr.iterations[1].n_decode == 1
+    s = V.summarize(reqs, tr.token_ns, ttft_slo_ns=2 * MS, tpot_slo_ns=2 * MS)
+    # r0: TTFT 0.81 ms, one gap of 1.735 ms -> meets; r1: TTFT 2.045 ms -> misses
+    assert (s["met"], s["goodput_den_ns"], s["makespan_ns"]) == (1, 500_000, e2)
+    assert s["p99_ttft_ns"] == e2 - 500_000
+
+
+def test_sloweave_decisions_by_hand():
+    """Alg. 1 on the analytic model: with one decode and a 5 ms objective the chunk
+    is floor((5 - T(1,0) - 0.40) / 0.006) = 549 tokens (the closed form of the
+    linear model); with nothing decoding it is the cap, 4096."""
+    reqs = [R(0, 0, 1, 3), R(1, 0, 10_000, 1)]
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=5 * MS, policy="sloweave", c_max=4096)
+    chunks = [i.chunk for i in tr.iterations]
+    assert chunks == [1, 549, 549, 4096, 4096, 710]
+    assert sum(chunks[1:]) == 10_000
+    e1 = 350_000 + 400_000 + 6_000
+    e2 = e1 + 350_000 + 955_000 + 400_000 + 6_000 * 549
+    e3 = e2 + 350_000 + 955_000 + 400_000 + 6_000 * 549
+    assert tr.token_ns[0] == [e1, e2, e3]
+    assert e2 - e1 == 4_999_000                    # one microsecond inside the 5 ms deadline
+    e6 = e3 + 2 * (350_000 + 400_000 + 6_000 * 4096) + 350_000 + 400_000 + 6_000 * 710
+    assert tr.token_ns[1] == [e6]
+    assert [i.budget_ns for i in tr.iterations[1:3]] == [5 * MS, 5 * MS]
+
+
+def test_oldest_first_and_one_token_outputs():
+    reqs = [R(5, 100, 20, 1), R(2, 100, 20, 1), R(9, 50, 20, 1)]
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="fixed", fixed_chunk=20)
+    assert [i.prefill_rid for i in tr.iterations] == [9, 2, 5]
+    assert all(len(v) == 1 for v in tr.token_ns.values())
+
+
+def test_idle_gap_jumps_to_next_arrival():
+    reqs = [R(0, 0, 10, 1), R(1, 50 * MS, 10, 1)]
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="fixed", fixed_chunk=64)
+    assert tr.iterations[1].start_ns == 50 * MS
+    assert tr.token_ns[1] == [50 * MS + 350_000 + 400_000 + 60_000]
+
+
+def test_decode_cap_holds_back_prefill():
+    reqs = [R(i, 0, 4, 5) for i in range(3)]
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="fixed", fixed_chunk=64,
+                    max_decode=2)
+    assert max(i.n_decode for i in tr.iterations) == 2
+    # the third prompt waits until a decode finishes
+    third = [k for k, i in enumerate(tr.iterations) if i.prefill_rid == 2][0]
+    assert tr.iterations[third].n_decode < 2
+
+
+def _small_trace(n, rate, seed):
+    t = synth.request_trace(n, rate, seed=seed, long_lo=512, long_hi=2048, short_median=128,
+                            output_mean=16)
+    return [R(i, int(a), int(p), int(o)) for i, (a, p, o) in enumerate(zip(t.arrival_ns, t.prompt, t.output))]
+
+
+@pytest.mark.parametrize("policy,chunk", [("sloweave", 0), ("fixed", 256), ("fixed", 2048)])
+def test_conservation(policy, chunk):
+    reqs = _small_trace(120, 40.0, seed=7)
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, policy=policy, fixed_chunk=chunk,
+                    max_decode=32)
+    by = {r.rid: r for r in reqs}
+    for rid, toks in tr.token_ns.items():
+        assert len(toks) == by[rid].output
+        assert all(b > a for a, b in zip(toks, toks[1:]))
+        assert toks[0] > by[rid].arrival_ns
+    per = {}
+    for it in tr.iterations:
+        if it.chunk:
+            per[it.prefill_rid] = per.get(it.prefill_rid, 0) + it.chunk
+    assert per == {r.rid: r.prompt for r in reqs}
+    for a, b in zip(tr.iterations, tr.iterations[1:]):
+        assert b.start_ns >= a.end_ns
+        if b.start_ns > a.end_ns:   # only an idle system waits, and only for an arrival
+            assert b.start_ns in {r.arrival_ns for r in reqs}
+    assert max(i.n_decode for i in tr.iterations) <= 32
+
+
+def test_prop1_exact_predictions_never_miss():
+    """Prop. 1: with exact predictions and a feasible decode-only iteration the
+    controller meets every next-token deadline; a large fixed chunk does not."""
+    reqs = _small_trace(150, 60.0, seed=11)
+    D = 10 * MS
+    assert S.analytic_cost_ns(64, 0) <= D
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=D, policy="sloweave", max_decode=64)
+    gaps = [b - a for t in tr.token_ns.values() for a, b in zip(t, t[1:])]
+    assert gaps and max(gaps) <= D
+    fx = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=D, policy="fixed", fixed_chunk=2048,
+                    max_decode=64)
+    gaps_fx = [b - a for t in fx.token_ns.values() for a, b in zip(t, t[1:])]
+    assert max(gaps_fx) > D
+
+
+def test_margin_is_kept_free_in_every_chunked_iteration():
+    """Sec. 3.3: a chunk runs beside decodes only if its predicted time plus the
+    margin fits the budget; decode-only iterations are the fallback."""
+    reqs = _small_trace(80, 60.0, seed=3)
+    delta = 2 * MS
+    tr = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, policy="sloweave", max_decode=64,
+                    margin_ns=delta)
+    mixed = [i for i in tr.iterations if i.n_decode and i.chunk]
+    assert mixed and all(i.end_ns - i.start_ns + delta <= i.budget_ns for i in mixed)
+    gaps = [b - a for t in tr.token_ns.values() for a, b in zip(t, t[1:])]
+    assert max(gaps) <= 10 * MS
+
+
+def test_table_predictor_matches_analytic_on_a_dense_grid():
+    """A table holding the analytic model at every decode count and at chunks 0, 1
+    and a coarse grid above reproduces it exactly (linear between grid points)."""
+    c_grid = [0, 1, 64, 512, 4096]
+    b_grid = list(range(0, 65))
+    tab = S.CostTable.from_values(c_grid, b_grid, [[S.analytic_cost_ns(b, c) for c in c_grid] for b in b_grid])
+    for n in (0, 1, 7, 64):
+        for c in (0, 1, 2, 63, 64, 65, 511, 3000, 4096):
+            assert tab.lookup(n, c) == S.analytic_cost_ns(n, c)
+    reqs = _small_trace(60, 60.0, seed=5)
+    a = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, max_decode=64)
+    b = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, max_decode=64, predict=tab.lookup,
+                   c_last=4096)
+    assert a.token_ns == b.token_ns
+
+
+def test_tpot_is_nearest_rank_p99_of_gaps():
+    toks = list(np.cumsum(np.arange(1, 201)))      # gaps 2, 3, ..., 200
+    m = V.request_metrics(R(0, 0, 1, 200), [int(t) for t in toks], 10**9, 10**9)
+    # 199 gaps; rank ceil(199 * 0.99) = 198 -> the 198th smallest gap = 199
+    assert m.tpot_p99_ns == 199
+    assert V.request_metrics(R(0, 0, 1, 1), [5], 10, 0).meets          # no gap: meets any TPOT
+    with pytest.raises(ValueError):
+        V.request_metrics(R(0, 0, 1, 2), [5], 10, 10)
+
+
+def test_trace_generator_shape():
+    t = synth.request_trace(4000, 4.0, seed=3)
+    assert t.arrival_ns[0] == 0 and np.all(np.diff(t.arrival_ns) >= 0)
+    assert t.prompt.min() >= 1 and t.prompt.max() <= 16384 and t.output.min() >= 1
+    assert abs(t.output.mean() - 256) < 15
+    assert 0.4 < np.mean(t.prompt >= 4096) < 0.75
+    no_burst = synth.request_trace(4000, 4.0, seed=3, burst_factor=1.0)
+    assert abs(no_burst.arrival_ns[-1] / 1e9 - 1000) < 60            # Poisson at 4/s
+    assert t.arrival_ns[-1] < no_burst.arrival_ns[-1]                 # bursts add arrivals
