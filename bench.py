@@ -15,6 +15,18 @@ sample, the cost table profiled over (B, C) with its monotonicity, and the
 controller's per-decision time.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu] [--no-table] [--workload sweep8b|long|chat]
+
+The serving workload (``--workload serve``) is a separate report, not the
+iteration benchmark: the full 32-layer 8B-shaped stack driven by the
+library's serving loop, with the controller over a cost table profiled on
+the GPU, against fixed chunks of 256, 512 and 2048 tokens at TPOT objectives
+of 25 and 10 ms (TTFT objective 1000 ms), on a seeded trace of Poisson
+arrivals with 4x bursts, half log-normal (median 512) and half uniform
+[4096, 16384] prompts and geometric outputs of mean 256.  It prints one JSON
+line with goodput, P99 TTFT/TPOT, SLO attainment and throughput per run, the
+same runs on the analytic simulator, and the controller's decision time.
+
+    python bench.py --workload serve [--requests N] [--rate R] [--repeats K]
 """
 from __future__ import annotations
 
@@ -40,6 +52,10 @@ WORKLOADS = {
     "chat": "8B-shaped layer, chat/bursty: B in {64,128,256} decodes with log-normal contexts (median 700, "
             "sigma 0.8, cap 8192), C in {32,64,128,256,512} at a seeded chunk boundary of a log-normal prompt "
             "(median 1024, cap 8192); one step = the 15 mixed iterations",
+    "serve": "full 32-layer 8B-shaped stack served by the library's loop: Poisson arrivals with 4x bursts of 2 s "
+             "(one every 20 s on average), prompts 50% min(16384, lognormal(512, 0.8)) and 50% U[4096,16384], "
+             "outputs geometric with mean 256; SLOWeave (C_max 4096) vs fixed chunks {256, 512, 2048} at "
+             "TPOT 25 and 10 ms, TTFT 1000 ms",
 }
 PEAK_HBM = 8.0e12          # B/s, MI355X HBM3E
 PEAK_BF16 = 2.5e15         # FLOP/s, dense bf16 MFMA
@@ -150,6 +166,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-table", action="store_true")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="sweep8b")
+    ap.add_argument("--requests", type=int, default=200, help="serve: requests per run")
+    ap.add_argument("--rate", type=float, default=4.0, help="serve: base arrival rate (requests/s)")
+    ap.add_argument("--repeats", type=int, default=10, help="serve: profiler repeats per grid point")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -166,6 +185,9 @@ def main():
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the path has no multi-GPU mode",
               file=sys.stderr)
         sys.exit(2)
+    if args.workload == "serve":
+        serve_main(args)
+        return
 
     import torch
     from paper_2609_07883_amd import api, synth
@@ -338,6 +360,99 @@ def main():
                       "seeds": {"weights": 0, "embeddings": 1, "contexts": 2, "kv": 3}},
            "roofline": roofline, "cpu_baseline": cpu, "sweep": per_point, "kernels": kernels,
            "cost_table": table}
+    print(json.dumps(out))
+
+
+SERVE_C_GRID = [0, 32, 64, 128, 256, 512, 1024, 2048, 4096]
+SERVE_B_GRID = [0, 1, 2, 4, 8, 16, 32, 64, 128, 256]
+SERVE_POLICIES = [("sloweave", 0), ("fixed", 256), ("fixed", 512), ("fixed", 2048)]
+
+
+def serve_main(args):
+    import torch
+    from paper_2609_07883_amd import api, serving, synth
+    from paper_2609_07883_amd.runtime import Session
+
+    torch.cuda.set_device(0)
+    shape = synth.with_layers(synth.LLAMA8B_LAYER, 32)
+    max_c, max_b = 4096, 256
+    t0 = time.time()
+    free, _ = torch.cuda.mem_get_info()
+    block_bytes = 2 * shape.n_layers * shape.n_kv_heads * 16 * shape.head_dim * 2
+    weight_bytes = shape.n_layers * 2 * (shape.d_model * (shape.n_q_heads + 2 * shape.n_kv_heads) * shape.head_dim
+                                         + shape.d_model * shape.n_q_heads * shape.head_dim
+                                         + 3 * shape.d_model * shape.ffn_dim)
+    num_blocks = int(min(120_000, (free - weight_bytes - (12 << 30)) * 0.85 // block_bytes))
+    sess = Session(shape, num_blocks=num_blocks, max_c=max_c, max_b=max_b, device_weights=True)
+    stream = sess.stream()
+    torch.cuda.synchronize()
+    log(f"serve: 32-layer stack, {num_blocks} KV blocks ({num_blocks * block_bytes / 2**30:.0f} GiB), "
+        f"workspace {sess.ws_bytes / 2**20:.0f} MiB, set-up {time.time() - t0:.1f}s")
+
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    t1 = time.time()
+    ct = sess.ctx.build_cost_table(SERVE_C_GRID, SERVE_B_GRID, prefix_len=4096, ctx_lo=1024, ctx_hi=8192, seed=2,
+                                   warmup=2, repeats=args.repeats, x_in=sess.x_in.data_ptr(),
+                                   x_out=sess.x_out.data_ptr(), ws=sess.ws.data_ptr(), ws_bytes=sess.ws_bytes,
+                                   flush_buf=flush.data_ptr(), flush_bytes=flush.numel(), stream=stream)
+    del flush
+    viol, worst = ct.monotone()
+    t_hat = ct.values(api.TABLE_THAT)
+    log(f"serve: cost table {time.time() - t1:.1f}s, {viol} raw decreases along C (largest {worst} ns)")
+
+    trace = synth.request_trace(args.requests, args.rate, seed=3)
+    sim_table = api.CostTable.analytic(SERVE_C_GRID, SERVE_B_GRID)
+    runs = []
+    for D in (25.0, 10.0):
+        for pol, fc in SERVE_POLICIES:
+            name = "SLOWeave" if pol == "sloweave" else f"Fixed-{fc}"
+            t2 = time.time()
+            res = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
+                              table=ct, session=sess)
+            wall = time.time() - t2
+            m = serving.metrics(trace, res.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
+            it = res.iterations
+            dur = (it["end_ns"] - it["start_ns"]).astype(np.float64)
+            pred = it["predicted_ns"].astype(np.float64)
+            ok = pred > 0
+            rel = (dur[ok] - pred[ok]) / pred[ok]
+            run = {"policy": name, "tpot_slo_ms": D, **{k: round(v, 4) if isinstance(v, float) else v
+                                                       for k, v in m.items()},
+                   "iterations": int(len(it)), "wall_s": round(wall, 1),
+                   "mean_chunk": round(float(it["chunk"][it["chunk"] > 0].mean()), 1),
+                   "decode_only_iterations": int(np.sum(it["chunk"] == 0)),
+                   "iteration_ms_p50": round(float(np.median(dur)) / 1e6, 3),
+                   "measured_over_predicted_p50": round(float(np.median(rel)), 4) if ok.any() else None,
+                   "measured_over_predicted_p99": round(float(np.quantile(rel, 0.99)), 4) if ok.any() else None,
+                   "decide_ns_p50": int(np.median(it["decide_ns"])), "decide_ns_p99": int(np.quantile(it["decide_ns"], 0.99))}
+            sim = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
+                              table=sim_table)
+            sm = serving.metrics(trace, sim.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
+            run["analytic_simulator"] = {k: round(sm[k], 4) for k in ("goodput_req_s", "slo_attainment",
+                                                                      "p99_ttft_ms", "p99_tpot_ms")}
+            runs.append(run)
+            log(f"serve: {name} D={D:g} ms: goodput {m['goodput_req_s']:.3f} req/s, SLO {m['slo_attainment']:.3f}, "
+                f"P99 TTFT {m['p99_ttft_ms']:.0f} ms, P99 TPOT {m['p99_tpot_ms']:.2f} ms, {len(it)} iterations, "
+                f"{wall:.1f}s")
+    best = {D: max((r for r in runs if r["tpot_slo_ms"] == D and r["policy"] != "SLOWeave"),
+                   key=lambda r: r["goodput_req_s"]) for D in (25.0, 10.0)}
+    slw = {D: next(r for r in runs if r["tpot_slo_ms"] == D and r["policy"] == "SLOWeave") for D in (25.0, 10.0)}
+    gain = {f"{D:g}ms": {"vs": best[D]["policy"],
+                         "ratio": round(slw[D]["goodput_req_s"] / best[D]["goodput_req_s"], 3)
+                         if best[D]["goodput_req_s"] > 0 else None} for D in (25.0, 10.0)}
+    out = {"metric": "goodput (requests meeting TTFT 1000 ms and TPOT SLOs per second of arrival span)",
+           "value": slw[25.0]["goodput_req_s"], "unit": "req/s", "n_gpus": 1, "higher_is_better": True,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": WORKLOADS["serve"], "requests": args.requests, "rate_per_s": args.rate,
+                      "seed": 3, "layers": 32, "kv_blocks": num_blocks, "max_decode": max_b},
+           "cost_table": {"c_grid": SERVE_C_GRID, "b_grid": SERVE_B_GRID, "repeats": args.repeats,
+                          "prefix_len": 4096, "decode_ctx": [1024, 8192],
+                          "raw_p99_decreases_along_c": viol, "largest_decrease_ns": worst,
+                          "monotone_after_cummax": bool(np.all(np.diff(t_hat, axis=1) >= 0)),
+                          "p99_cummax_ms": (t_hat / 1e6).round(3).tolist()},
+           "runs": runs, "sloweave_vs_best_fixed": gain,
+           "paper_context": "simulator (analytic cost model, no accelerator): +39% mixed / +38% long at 25 ms, "
+                            "3.3x / 2.4x at 10 ms; A100 8B runtime: +27% (mixed), +14% (bursty)"}
     print(json.dumps(out))
 
 

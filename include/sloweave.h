@@ -255,6 +255,14 @@ int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const 
 int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
                                 int32_t nb, const int64_t* samples, int32_t repeats,
                                 slw_cost_table** out);
+/*
+ * A table holding the simulator's analytic cost model (Sec. 4.1) at every
+ * grid point, one sample each:
+ *   T(n, c) = 0.35 + 1[n>0](0.90 + 0.055 n) + 1[c>0](0.40 + 0.006 c) ms.
+ * Grids as for slw_cost_table_from_samples.
+ */
+int slw_cost_table_analytic(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                            slw_cost_table** out);
 void slw_cost_table_free(slw_cost_table* t);
 int slw_cost_table_dims(const slw_cost_table* t, int32_t* nc, int32_t* nb, int32_t* repeats);
 int slw_cost_table_grids(const slw_cost_table* t, int32_t* c_grid, int32_t* b_grid);
@@ -303,6 +311,88 @@ int slw_cost_table_load(const char* path, slw_cost_table** out);
 int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
                      int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
                      int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
+
+/* ------------------------------------------------------------------------ */
+/* Serving loop (Sec. 3.1 deadline model; Sec. 4.1 iteration semantics;     */
+/* Sec. 4.3 oldest-first queueing shared by every policy)                    */
+/* ------------------------------------------------------------------------ */
+
+/* One request of a trace (host memory). */
+typedef struct slw_request {
+    int64_t id;          /* distinct; the request's KV sequence id while it lives     */
+    int64_t arrival_ns;  /* arrival time on the trace clock (>= 0)                    */
+    int32_t prompt_len;  /* prompt tokens, >= 1                                       */
+    int32_t output_len;  /* output tokens, >= 1; the first one comes from the prefill */
+} slw_request;
+
+#define SLW_POLICY_SLOWEAVE 0 /* Alg. 1 over opts->table with margin and cap       */
+#define SLW_POLICY_FIXED 1    /* chunks of opts->fixed_chunk tokens                */
+
+#define SLW_EXEC_GPU 0        /* run each iteration with slw_mixed_iteration        */
+#define SLW_EXEC_ANALYTIC 1   /* advance a virtual clock by the Sec. 4.1 cost model */
+
+/* flags of an iteration record besides those of slw_select_chunk */
+#define SLW_SERVE_KV_WAIT 0x100u      /* the oldest prompt waits for KV blocks      */
+#define SLW_SERVE_DECODE_CAP 0x200u   /* the oldest prompt waits: decode batch full */
+#define SLW_SERVE_UNPRICED 0x400u     /* decode batch above the table: decode-only  */
+
+typedef struct slw_serve_opts {
+    int32_t policy;          /* SLW_POLICY_*                                            */
+    int32_t fixed_chunk;     /* SLW_POLICY_FIXED: tokens per chunk (>= 1)               */
+    int32_t c_max;           /* SLW_POLICY_SLOWEAVE: chunk cap (>= 1)                   */
+    int32_t max_decode;      /* decode-batch cap (>= 1)                                 */
+    int64_t tpot_ns;         /* D: next-token deadline d_i = l_i + D                    */
+    int64_t margin_ns;       /* delta of Sec. 3.3 (>= 0)                                */
+    const slw_cost_table* table; /* SLOWeave's predictor T_hat (required for it)        */
+    int32_t executor;        /* SLW_EXEC_*                                              */
+    int32_t skip_idle;       /* GPU: 1 = jump the clock over idle gaps, 0 = wait        */
+    /* SLW_EXEC_GPU only (device memory, as for slw_mixed_iteration): */
+    const void* x_in;        /* bf16 [max_rows][d] input rows                           */
+    void* x_out;             /* bf16 [max_rows][d]                                      */
+    int32_t max_rows;        /* rows x_in/x_out hold: >= chunk cap + max_decode         */
+    void* ws;                /* workspace for (chunk cap, max_decode)                   */
+    size_t ws_bytes;
+    void* stream;
+} slw_serve_opts;
+
+/* One iteration of a serving run (host memory). */
+typedef struct slw_iteration_record {
+    int64_t start_ns;     /* trace clock before the chunk decision                      */
+    int64_t end_ns;       /* trace clock once the iteration's work has completed        */
+    int64_t budget_ns;    /* earliest next-token deadline minus start_ns (0: no decode) */
+    int64_t decide_ns;    /* host nanoseconds spent choosing the chunk                  */
+    int64_t predicted_ns; /* T_hat(n_decode, chunk) from opts->table, -1 without one    */
+    int64_t prefill_id;   /* request the chunk belongs to, -1 when chunk == 0           */
+    int32_t chunk;        /* prefill tokens run                                          */
+    int32_t n_decode;     /* decode tokens run                                           */
+    int32_t remaining;    /* prompt tokens of the oldest eligible prompt before the chunk
+                             (0 when none may run)                                       */
+    uint32_t flags;       /* SLW_FLAG_* of the decision | SLW_SERVE_*                    */
+} slw_iteration_record;
+
+/*
+ * Serve a trace to completion (synchronous).  Each iteration decodes one
+ * token for every active request (decode rows in ascending id order) and
+ * runs at most one prefill chunk of the oldest eligible prompt (by arrival,
+ * then id); requests that arrive during an iteration become eligible when
+ * it ends; the first output token is emitted by the iteration that finishes
+ * the prompt, which also sets l_i; a prompt may start only while fewer than
+ * max_decode requests decode and (GPU) while the pool can hold every
+ * admitted request to its last token.  With no eligible work the clock
+ * moves to the next arrival (SLW_EXEC_ANALYTIC, or skip_idle) or waits for
+ * it.  The GPU executor synchronises `stream` after every iteration, creates
+ * a KV sequence per request when its prompt starts and frees it when its
+ * last token is out; ctx may be NULL with SLW_EXEC_ANALYTIC.
+ *   reqs       host [n], any order, distinct ids
+ *   token_ns   host [sum of output_len]: request k's tokens at offset
+ *              sum_{j<k} output_len[j], each the trace-clock time it was emitted
+ *   iters      host [iter_cap] iteration records; *n_iters receives the count
+ * SLW_ERANGE if the run needs more than iter_cap iterations or token_cap is
+ * short; SLW_ENOMEM if one request alone can never fit the KV pool.
+ */
+int slw_serve(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve_opts* opts,
+              int64_t* token_ns, int64_t token_cap, slw_iteration_record* iters, int64_t iter_cap,
+              int64_t* n_iters);
 
 #ifdef __cplusplus
 }

@@ -34,6 +34,7 @@ EXPORTS = (
     "slw_cost_table_free", "slw_cost_table_dims", "slw_cost_table_grids", "slw_cost_table_values",
     "slw_cost_table_lookup", "slw_cost_table_monotone", "slw_cost_table_save",
     "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
+    "slw_serve", "slw_cost_table_analytic",
 )
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "decode_merge",
           "o_gemm", "rmsnorm_mlp", "gateup_gemm", "down_gemm")
@@ -71,6 +72,30 @@ class ProfileOpts(C.Structure):
                 ("stream", C.c_void_p)]
 
 
+class RequestC(C.Structure):
+    _fields_ = [("id", C.c_int64), ("arrival_ns", C.c_int64), ("prompt_len", C.c_int32),
+                ("output_len", C.c_int32)]
+
+
+class ServeOpts(C.Structure):
+    _fields_ = [("policy", C.c_int32), ("fixed_chunk", C.c_int32), ("c_max", C.c_int32),
+                ("max_decode", C.c_int32), ("tpot_ns", C.c_int64), ("margin_ns", C.c_int64),
+                ("table", C.c_void_p), ("executor", C.c_int32), ("skip_idle", C.c_int32),
+                ("x_in", C.c_void_p), ("x_out", C.c_void_p), ("max_rows", C.c_int32),
+                ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p)]
+
+
+class IterationRecord(C.Structure):
+    _fields_ = [("start_ns", C.c_int64), ("end_ns", C.c_int64), ("budget_ns", C.c_int64),
+                ("decide_ns", C.c_int64), ("predicted_ns", C.c_int64), ("prefill_id", C.c_int64),
+                ("chunk", C.c_int32), ("n_decode", C.c_int32), ("remaining", C.c_int32),
+                ("flags", C.c_uint32)]
+
+
+POLICY_SLOWEAVE, POLICY_FIXED = 0, 1
+EXEC_GPU, EXEC_ANALYTIC = 0, 1
+SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED = 0x100, 0x200, 0x400
+
 _lib = None
 
 
@@ -101,6 +126,7 @@ def lib() -> C.CDLL:
         "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
         "slw_cost_table_from_samples": ([P(i32), i32, P(i32), i32, P(i64), i32, P(vp)], C.c_int),
+        "slw_cost_table_analytic": ([P(i32), i32, P(i32), i32, P(vp)], C.c_int),
         "slw_cost_table_free": ([vp], None),
         "slw_cost_table_dims": ([vp, P(i32), P(i32), P(i32)], C.c_int),
         "slw_cost_table_grids": ([vp, P(i32), P(i32)], C.c_int),
@@ -112,6 +138,8 @@ def lib() -> C.CDLL:
         "slw_select_chunk": ([vp, P(i64), i32, i64, i32, i32, i64, P(i32), P(u32), P(i32)], C.c_int),
         "slw_set_stage_timing": ([vp, i32], C.c_int),
         "slw_stage_times": ([vp, i32, P(C.c_float), i32, P(i32)], C.c_int),
+        "slw_serve": ([vp, P(RequestC), i32, P(ServeOpts), P(i64), i64, P(IterationRecord), i64, P(i64)],
+                      C.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -170,6 +198,15 @@ class CostTable:
         return cls(h.value)
 
     @classmethod
+    def analytic(cls, c_grid, b_grid) -> "CostTable":
+        """The simulator's analytic cost model (Sec. 4.1) at every grid point."""
+        cg, bg = _i32(c_grid), _i32(b_grid)
+        h = C.c_void_p()
+        _check(lib().slw_cost_table_analytic(_ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32), len(bg),
+                                             C.byref(h)))
+        return cls(h.value)
+
+    @classmethod
     def load(cls, path: str) -> "CostTable":
         h = C.c_void_p()
         _check(lib().slw_cost_table_load(path.encode(), C.byref(h)))
@@ -216,6 +253,46 @@ def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_
     _check(lib().slw_select_chunk(table.handle, _ptr(d, C.c_int64), len(d), int(now_ns), int(remaining),
                                   int(c_max), int(margin_ns), C.byref(ch), C.byref(fl), C.byref(nl)))
     return ch.value, fl.value, nl.value
+
+
+# ---------------------------------------------------------------------------
+# Serving loop
+# ---------------------------------------------------------------------------
+
+ITERATION_DTYPE = np.dtype([("start_ns", np.int64), ("end_ns", np.int64), ("budget_ns", np.int64),
+                            ("decide_ns", np.int64), ("predicted_ns", np.int64), ("prefill_id", np.int64),
+                            ("chunk", np.int32), ("n_decode", np.int32), ("remaining", np.int32),
+                            ("flags", np.uint32)])
+assert ITERATION_DTYPE.itemsize == C.sizeof(IterationRecord)
+
+
+def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_decode: int,
+          fixed_chunk: int = 0, c_max: int = 4096, margin_ns: int = 0, table: CostTable | None = None,
+          executor: int = EXEC_ANALYTIC, ctx: "Context | None" = None, skip_idle: bool = True,
+          x_in: int = 0, x_out: int = 0, max_rows: int = 0, ws: int = 0, ws_bytes: int = 0,
+          stream: int = 0, iter_cap: int | None = None):
+    """slw_serve over a trace given as arrays.
+
+    Returns (token_ns, iterations): token_ns is a list of int64 arrays, one per
+    request in the given order; iterations is a structured array of
+    ITERATION_DTYPE records.
+    """
+    n = len(ids)
+    reqs = (RequestC * max(n, 1))()
+    for k in range(n):
+        reqs[k] = RequestC(int(ids[k]), int(arrival_ns[k]), int(prompt[k]), int(output[k]))
+    out = np.asarray(output, dtype=np.int64)
+    tok = np.zeros(max(int(out.sum()), 1), np.int64)
+    cap = int(iter_cap if iter_cap is not None else 4 * (int(out.sum()) + int(np.sum(prompt))) + 16)
+    its = np.zeros(max(cap, 1), ITERATION_DTYPE)
+    o = ServeOpts(policy, fixed_chunk, c_max, max_decode, int(tpot_ns), int(margin_ns),
+                  table.handle if table is not None else None, executor, int(skip_idle),
+                  x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None)
+    nit = C.c_int64()
+    _check(lib().slw_serve(ctx._h if ctx is not None else None, reqs, n, C.byref(o), _ptr(tok, C.c_int64),
+                           len(tok), its.ctypes.data_as(C.POINTER(IterationRecord)), len(its), C.byref(nit)))
+    offs = np.concatenate([[0], np.cumsum(out)])
+    return [tok[offs[k]:offs[k + 1]].copy() for k in range(n)], its[: nit.value].copy()
 
 
 # ---------------------------------------------------------------------------

@@ -89,6 +89,28 @@ int finish_table(slw_cost_table* t) {
 
 using namespace slw;
 
+namespace slw {
+
+int64_t analytic_iteration_ns(int32_t n, int32_t c) {
+    int64_t t = 350000;
+    if (n > 0) t += 900000 + 55000 * static_cast<int64_t>(n);
+    if (c > 0) t += 400000 + 6000 * static_cast<int64_t>(c);
+    return t;
+}
+
+}  // namespace slw
+
+extern "C" int slw_cost_table_analytic(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                                       slw_cost_table** out) {
+    return guarded([&] {
+        if (!c_grid || !b_grid || !out || nc < 1 || nb < 1) return fail(SLW_EINVAL, "bad grids");
+        std::vector<int64_t> v(static_cast<size_t>(nc) * nb);
+        for (int32_t i = 0; i < nb; ++i)
+            for (int32_t j = 0; j < nc; ++j) v[static_cast<size_t>(i) * nc + j] = analytic_iteration_ns(b_grid[i], c_grid[j]);
+        return slw_cost_table_from_samples(c_grid, nc, b_grid, nb, v.data(), 1, out);
+    });
+}
+
 extern "C" int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
                                            int32_t nb, const int64_t* samples, int32_t repeats,
                                            slw_cost_table** out) {

@@ -22,4 +22,8 @@ namespace slw {
 // Validates grids, fills the percentiles and the running maximum.  SLW_* code.
 int finish_table(slw_cost_table* t);
 
+// The simulator's default cost model (Sec. 4.1), in ns:
+// T(n, c) = 0.35 + 1[n>0](0.90 + 0.055 n) + 1[c>0](0.40 + 0.006 c) ms.
+int64_t analytic_iteration_ns(int32_t n, int32_t c);
+
 }  // namespace slw

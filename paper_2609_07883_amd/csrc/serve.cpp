@@ -1,0 +1,282 @@
+// Serving loop: the iteration-level scheduler that drives the mixed iteration
+// (Sec. 3.1 deadline model, Sec. 3.2 / Alg. 1 chunk choice, Sec. 4.1 iteration
+// semantics, Sec. 4.3 oldest-first queueing).  It uses only the public calls
+// of this library: the KV manager, slw_select_chunk and slw_mixed_iteration.
+//
+// Two executors share every scheduling decision: the GPU one runs each
+// iteration on the device and reads the host clock once the stream drains;
+// the analytic one advances a virtual clock by the Sec. 4.1 cost model, which
+// makes the same loop an iteration-level simulator.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdint>
+#include <deque>
+#include <map>
+#include <thread>
+#include <vector>
+
+#include "common.h"
+#include "cost_table.h"
+#include "sloweave.h"
+
+namespace slw {
+namespace {
+
+int64_t host_ns() {
+    return std::chrono::duration_cast<std::chrono::nanoseconds>(
+               std::chrono::steady_clock::now().time_since_epoch())
+        .count();
+}
+
+struct Live {
+    int32_t req;          // index into the caller's array
+    int32_t prompt_done;  // prompt tokens processed
+    int32_t emitted;      // output tokens emitted
+    int64_t last_ns;      // l_i: time of the latest token
+    bool started;         // prompt begun (KV sequence exists)
+};
+
+int64_t kv_blocks_for(const slw_request& r) {
+    // positions 0 .. prompt + output - 2 are cached (the last token is never fed back)
+    return ceil_div(static_cast<int64_t>(r.prompt_len) + r.output_len - 1, 16);
+}
+
+int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve_opts* o) {
+    if (!o || (n > 0 && !reqs)) return fail(SLW_EINVAL, "null argument");
+    if (n < 0) return fail(SLW_EINVAL, "negative request count");
+    if (o->policy != SLW_POLICY_SLOWEAVE && o->policy != SLW_POLICY_FIXED)
+        return fail(SLW_EINVAL, "unknown policy %d", o->policy);
+    if (o->policy == SLW_POLICY_FIXED && o->fixed_chunk < 1) return fail(SLW_EINVAL, "fixed_chunk must be >= 1");
+    if (o->policy == SLW_POLICY_SLOWEAVE && (!o->table || o->c_max < 1))
+        return fail(SLW_EINVAL, "SLOWeave needs a cost table and c_max >= 1");
+    if (o->max_decode < 1) return fail(SLW_EINVAL, "max_decode must be >= 1");
+    if (o->tpot_ns <= 0 || o->margin_ns < 0) return fail(SLW_EINVAL, "bad TPOT objective or margin");
+    if (o->executor != SLW_EXEC_GPU && o->executor != SLW_EXEC_ANALYTIC)
+        return fail(SLW_EINVAL, "unknown executor %d", o->executor);
+    if (o->executor == SLW_EXEC_GPU) {
+        if (!ctx || !o->x_in || !o->x_out || !o->ws) return fail(SLW_EINVAL, "GPU executor needs ctx and buffers");
+        const int64_t cap = o->policy == SLW_POLICY_FIXED ? o->fixed_chunk : o->c_max;
+        if (cap + o->max_decode > o->max_rows)
+            return fail(SLW_ERANGE, "chunk cap %lld + max_decode %d exceeds max_rows %d",
+                        static_cast<long long>(cap), o->max_decode, o->max_rows);
+    }
+    std::map<int64_t, int> seen;
+    for (int32_t i = 0; i < n; ++i) {
+        const slw_request& r = reqs[i];
+        if (r.prompt_len < 1 || r.output_len < 1 || r.arrival_ns < 0)
+            return fail(SLW_EINVAL, "request %lld: bad lengths or arrival", static_cast<long long>(r.id));
+        if (seen[r.id]++) return fail(SLW_EINVAL, "duplicate request id %lld", static_cast<long long>(r.id));
+    }
+    return SLW_OK;
+}
+
+int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve_opts* o, int64_t* token_ns,
+               int64_t token_cap, slw_iteration_record* iters, int64_t iter_cap, int64_t* n_iters) {
+    int rc = check_opts(ctx, reqs, n, o);
+    if (rc) return rc;
+    if (!n_iters || (n > 0 && (!token_ns || !iters))) return fail(SLW_EINVAL, "null output");
+    *n_iters = 0;
+    std::vector<int64_t> tok_off(n + 1, 0);
+    for (int32_t i = 0; i < n; ++i) tok_off[i + 1] = tok_off[i] + reqs[i].output_len;
+    if (tok_off[n] > token_cap) return fail(SLW_ERANGE, "token_ns holds %lld, need %lld",
+                                           static_cast<long long>(token_cap), static_cast<long long>(tok_off[n]));
+    if (n == 0) return SLW_OK;
+
+    const bool gpu = o->executor == SLW_EXEC_GPU;
+    int64_t pool_blocks = 0;
+    if (gpu) {
+        int32_t free_blocks = 0;
+        rc = slw_kv_free_blocks(ctx, &free_blocks);
+        if (rc) return rc;
+        pool_blocks = free_blocks;
+        for (int32_t i = 0; i < n; ++i)
+            if (kv_blocks_for(reqs[i]) > pool_blocks)
+                return fail(SLW_ENOMEM, "request %lld needs %lld KV blocks, the pool has %lld free",
+                            static_cast<long long>(reqs[i].id), static_cast<long long>(kv_blocks_for(reqs[i])),
+                            static_cast<long long>(pool_blocks));
+    }
+
+    std::vector<int32_t> order(n);  // arrival order (arrival, id)
+    for (int32_t i = 0; i < n; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+        return reqs[a].arrival_ns != reqs[b].arrival_ns ? reqs[a].arrival_ns < reqs[b].arrival_ns
+                                                        : reqs[a].id < reqs[b].id;
+    });
+
+    std::deque<Live> pending;            // eligible, prompt not finished, oldest first
+    std::map<int64_t, Live> active;      // decoding, keyed (and batched) by id
+    int64_t committed_blocks = 0;        // KV blocks every started request may reach
+    int32_t next = 0, finished = 0;
+
+    // Trace clock.  Analytic: purely virtual.  GPU: host time since the start
+    // minus the idle gaps jumped over.
+    int64_t virt = reqs[order[0]].arrival_ns;
+    const int64_t t0_host = host_ns();
+    int64_t host_shift = virt;  // trace time = host_ns() - t0_host + host_shift
+    auto now = [&]() { return gpu ? host_ns() - t0_host + host_shift : virt; };
+
+    std::vector<int64_t> dec_ids, deadlines;
+    std::vector<int32_t> ctx_lens;
+    const hipStream_t stream = static_cast<hipStream_t>(o->stream);
+
+    while (finished < n) {
+        int64_t t = now();
+        while (next < n && reqs[order[next]].arrival_ns <= t) {
+            pending.push_back(Live{order[next], 0, 0, 0, false});
+            ++next;
+        }
+        if (pending.empty() && active.empty()) {
+            const int64_t arr = reqs[order[next]].arrival_ns;  // next < n: someone is still to come
+            if (!gpu) {
+                virt = arr;
+            } else if (o->skip_idle) {
+                host_shift += arr - t;
+            } else {
+                std::this_thread::sleep_for(std::chrono::nanoseconds(std::max<int64_t>(0, arr - t)));
+            }
+            continue;
+        }
+        if (*n_iters >= iter_cap) return fail(SLW_ERANGE, "more than %lld iterations", static_cast<long long>(iter_cap));
+        slw_iteration_record rec{};
+        rec.start_ns = t;
+        rec.prefill_id = -1;
+        rec.predicted_ns = -1;
+
+        const int64_t t_dec0 = host_ns();
+        dec_ids.clear();
+        deadlines.clear();
+        ctx_lens.clear();
+        for (const auto& kv : active) {
+            const Live& a = kv.second;
+            const slw_request& r = reqs[a.req];
+            dec_ids.push_back(r.id);
+            deadlines.push_back(a.last_ns + o->tpot_ns);
+            ctx_lens.push_back(r.prompt_len + a.emitted - 1);
+        }
+        const int32_t nd = static_cast<int32_t>(dec_ids.size());
+        if (nd > 0) rec.budget_ns = *std::min_element(deadlines.begin(), deadlines.end()) - t;
+
+        Live* head = nullptr;
+        if (!pending.empty()) {
+            Live& h = pending.front();
+            if (nd >= o->max_decode) {
+                rec.flags |= SLW_SERVE_DECODE_CAP;
+            } else if (gpu && !h.started && committed_blocks + kv_blocks_for(reqs[h.req]) > pool_blocks) {
+                rec.flags |= SLW_SERVE_KV_WAIT;
+            } else {
+                head = &h;
+            }
+        }
+        int32_t chunk = 0;
+        if (head) {
+            const int32_t remaining = reqs[head->req].prompt_len - head->prompt_done;
+            rec.remaining = remaining;
+            if (o->policy == SLW_POLICY_FIXED) {
+                chunk = std::min(o->fixed_chunk, remaining);
+            } else {
+                uint32_t fl = 0;
+                rc = slw_select_chunk(o->table, deadlines.data(), nd, t, remaining, o->c_max, o->margin_ns, &chunk,
+                                      &fl, nullptr);
+                if (rc == SLW_ERANGE) {  // more decodes than the table prices
+                    clear_error();
+                    chunk = 0;
+                    fl = SLW_SERVE_UNPRICED;
+                } else if (rc) {
+                    return rc;
+                }
+                rec.flags |= fl;
+            }
+        }
+        rec.decide_ns = host_ns() - t_dec0;
+        rec.chunk = chunk;
+        rec.n_decode = nd;
+        if (o->table) {
+            int64_t p = 0;
+            if (slw_cost_table_lookup(o->table, nd, chunk, &p) == SLW_OK) rec.predicted_ns = p;
+            else clear_error();
+        }
+
+        if (gpu) {
+            if (chunk > 0 && !head->started) {
+                rc = slw_seq_create(ctx, reqs[head->req].id);
+                if (rc) return rc;
+                head->started = true;
+                committed_blocks += kv_blocks_for(reqs[head->req]);
+            }
+            slw_batch b{};
+            b.C = chunk;
+            b.prefill_seq = chunk > 0 ? reqs[head->req].id : 0;
+            b.prefix_len = chunk > 0 ? head->prompt_done : 0;
+            b.B = nd;
+            b.decode_seqs = dec_ids.data();
+            b.context_lens = ctx_lens.data();
+            rc = slw_mixed_iteration(ctx, &b, o->x_in, o->x_out, o->ws, o->ws_bytes, o->stream);
+            if (rc) return rc;
+            if (hipStreamSynchronize(stream) != hipSuccess)
+                return fail(SLW_EHIP, "stream synchronisation failed after iteration %lld",
+                            static_cast<long long>(*n_iters));
+        } else {
+            virt = t + analytic_iteration_ns(nd, chunk);
+        }
+        const int64_t end = now();
+        rec.end_ns = end;
+        if (chunk > 0) rec.prefill_id = reqs[head->req].id;
+        iters[(*n_iters)++] = rec;
+
+        // decodes: one token each
+        for (auto it = active.begin(); it != active.end();) {
+            Live& a = it->second;
+            const slw_request& r = reqs[a.req];
+            token_ns[tok_off[a.req] + a.emitted] = end;
+            ++a.emitted;
+            a.last_ns = end;
+            if (a.emitted == r.output_len) {
+                if (gpu) {
+                    rc = slw_seq_free(ctx, r.id);
+                    if (rc) return rc;
+                    committed_blocks -= kv_blocks_for(r);
+                }
+                ++finished;
+                it = active.erase(it);
+            } else {
+                ++it;
+            }
+        }
+        // the chunk: the prompt's last chunk emits the first token
+        if (chunk > 0) {
+            Live h = *head;
+            h.prompt_done += chunk;
+            const slw_request& r = reqs[h.req];
+            if (h.prompt_done == r.prompt_len) {
+                pending.pop_front();
+                token_ns[tok_off[h.req]] = end;
+                h.emitted = 1;
+                h.last_ns = end;
+                if (r.output_len == 1) {
+                    if (gpu) {
+                        rc = slw_seq_free(ctx, r.id);
+                        if (rc) return rc;
+                        committed_blocks -= kv_blocks_for(r);
+                    }
+                    ++finished;
+                } else {
+                    active.emplace(r.id, h);
+                }
+            } else {
+                *head = h;
+            }
+        }
+    }
+    return SLW_OK;
+}
+
+}  // namespace
+}  // namespace slw
+
+extern "C" int slw_serve(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve_opts* opts,
+                         int64_t* token_ns, int64_t token_cap, slw_iteration_record* iters, int64_t iter_cap,
+                         int64_t* n_iters) {
+    return slw::guarded([&] { return slw::serve_impl(ctx, reqs, n, opts, token_ns, token_cap, iters, iter_cap, n_iters); });
+}

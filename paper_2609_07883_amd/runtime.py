@@ -35,7 +35,11 @@ class Session:
     """One context with its device buffers for iterations up to (max_c, max_b)."""
 
     def __init__(self, shape: synth.ModelShape, num_blocks: int, max_c: int, max_b: int,
-                 layers=None, weight_seed: int = 0, qk_std=None):
+                 layers=None, weight_seed: int = 0, qk_std=None, device_weights: bool = False):
+        """device_weights draws the weights on the GPU (torch's generator seeded
+        weight_seed + 1000 * layer; N(0, 0.02) matrices, 1 + N(0, 0.02) gains)
+        instead of the host recipe of ``synth.layer_weights``: for deep stacks
+        whose outputs are timed but never compared with the oracle."""
         self.shape = shape
         self.dev = _dev()
         self.ctx = api.Context.from_shape(shape)
@@ -49,11 +53,15 @@ class Session:
         self.weights = []
         self.layer_bits = []
         for layer in range(s.n_layers):
-            bits = layers[layer] if layers is not None else synth.layer_weights(
-                s, layer=layer, weight_seed=weight_seed, qk_std=qk_std)
-            self.layer_bits.append(bits)
-            w = {k: bits_to_tensor(getattr(bits, k), self.dev)
-                 for k in ("wqkv", "wo", "wgu", "wd", "g1", "g2")}
+            if device_weights:
+                w = self._device_layer(weight_seed + 1000 * layer)
+                self.layer_bits.append(None)
+            else:
+                bits = layers[layer] if layers is not None else synth.layer_weights(
+                    s, layer=layer, weight_seed=weight_seed, qk_std=qk_std)
+                self.layer_bits.append(bits)
+                w = {k: bits_to_tensor(getattr(bits, k), self.dev)
+                     for k in ("wqkv", "wo", "wgu", "wd", "g1", "g2")}
             self.weights.append(w)
             self.ctx.set_layer_weights(layer, *(w[k].data_ptr() for k in
                                                 ("wqkv", "wo", "wgu", "wd", "g1", "g2")))
@@ -63,6 +71,24 @@ class Session:
         self.x_out = torch.zeros_like(self.x_in)
         self.ws_bytes = self.ctx.workspace_size(max_c, max_b)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
+
+    def _device_layer(self, seed: int) -> dict:
+        s = self.shape
+        g = torch.Generator(device=self.dev)
+        g.manual_seed(seed)
+        nqkv = (s.n_q_heads + 2 * s.n_kv_heads) * s.head_dim
+        shapes = {"wqkv": (nqkv, s.d_model), "wo": (s.d_model, s.n_q_heads * s.head_dim),
+                  "wgu": (2 * s.ffn_dim, s.d_model), "wd": (s.d_model, s.ffn_dim)}
+        w = {}
+        for k, shp in shapes.items():
+            t = torch.empty(shp, dtype=torch.bfloat16, device=self.dev)
+            for r0 in range(0, shp[0], 2048):      # bounded float32 staging
+                r1 = min(shp[0], r0 + 2048)
+                t[r0:r1] = (torch.randn((r1 - r0, shp[1]), generator=g, device=self.dev) * 0.02).bfloat16()
+            w[k] = t
+        for k in ("g1", "g2"):
+            w[k] = (1.0 + 0.02 * torch.randn(s.d_model, generator=g, device=self.dev)).bfloat16()
+        return w
 
     # -- iteration ------------------------------------------------------------
     def stream(self) -> int:

@@ -1,0 +1,99 @@
+"""The serving loop on the GPU executor (through the C ABI), on a 2-layer Tiny stack.
+
+Each iteration really runs on the device and is timed on the host clock, so
+token times are not reproducible; what must hold exactly is checked instead:
+every SLOWeave decision replays bit-exactly through the oracle's Alg. 1 on
+the same measured table (the record holds the decision's inputs: start
+time, earliest deadline, decode count, remaining prompt); each request gets
+its output tokens in order after its arrival; chunks add up to the prompts;
+the decode batch respects its cap; the KV pool is whole again at the end;
+fixed-chunk runs cut prompts into min(chunk, remaining) pieces.
+"""
+import numpy as np
+import pytest
+
+from oracle import schedule as S
+from paper_2609_07883_amd import api, serving, synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+C_GRID = [0, 16, 32, 64, 128, 256]
+B_GRID = [0, 1, 2, 4, 8, 16]
+
+
+@pytest.fixture(scope="module")
+def setup():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_07883_amd.runtime import Session
+    sess = Session(synth.with_layers(synth.TINY, 2), num_blocks=1024, max_c=256, max_b=16)
+    ct = sess.ctx.build_cost_table(C_GRID, B_GRID, prefix_len=64, ctx_lo=16, ctx_hi=128, seed=3, warmup=1,
+                                   repeats=5, x_in=sess.x_in.data_ptr(), x_out=sess.x_out.data_ptr(),
+                                   ws=sess.ws.data_ptr(), ws_bytes=sess.ws_bytes,
+                                   stream=sess.stream())
+    tr = synth.request_trace(40, 400.0, seed=9, short_median=48, long_lo=128, long_hi=400, output_mean=6)
+    return sess, ct, tr
+
+
+def _check_run(sess, tr, res, max_decode):
+    n = len(tr)
+    for i in range(n):
+        t = res.token_ns[i]
+        assert len(t) == tr.output[i]
+        assert t[0] > tr.arrival_ns[i] and np.all(np.diff(t) > 0)
+    it = res.iterations
+    assert np.all(it["end_ns"] > it["start_ns"])
+    assert np.all(it["start_ns"][1:] >= it["end_ns"][:-1])
+    assert it["n_decode"].max() <= max_decode
+    per = np.zeros(n, np.int64)
+    np.add.at(per, it["prefill_id"][it["chunk"] > 0], it["chunk"][it["chunk"] > 0])
+    assert per.tolist() == tr.prompt.tolist()
+    assert sess.ctx.free_blocks() == sess.num_blocks
+
+
+@pytest.mark.parametrize("tpot_ms,margin_us", [(4.0, 0), (1.5, 200)])
+def test_sloweave_on_gpu(setup, tpot_ms, margin_us):
+    sess, ct, tr = setup
+    res = serving.run(tr, policy="sloweave", tpot_ms=tpot_ms, max_decode=16, c_max=256, table=ct,
+                      margin_ns=margin_us * 1000, session=sess)
+    torch.cuda.synchronize()
+    _check_run(sess, tr, res, 16)
+    ot = S.CostTable(C_GRID, B_GRID, ct.values(api.TABLE_SAMPLES).tolist())
+    decided = 0
+    for r in res.iterations:
+        if r["remaining"] <= 0:
+            continue
+        n = int(r["n_decode"])
+        dl = [int(r["start_ns"] + r["budget_ns"])] * n
+        exp = S.select_chunk_table(ot, dl, int(r["start_ns"]), int(r["remaining"]), 256, margin_us * 1000)
+        assert int(r["chunk"]) == exp[0], f"record {r}"
+        assert int(r["flags"]) & 0xFF == exp[1]
+        decided += 1
+    assert decided > 10
+    print(f"D={tpot_ms} ms: {len(res.iterations)} iterations, "
+          f"{serving.metrics(tr, res.token_ns, 1000, tpot_ms)}")
+
+
+def test_fixed_on_gpu(setup):
+    sess, _, tr = setup
+    res = serving.run(tr, policy="fixed", fixed_chunk=64, tpot_ms=4.0, max_decode=4, session=sess)
+    torch.cuda.synchronize()
+    _check_run(sess, tr, res, 4)
+    it = res.iterations
+    run = it[it["chunk"] > 0]
+    assert np.all(run["chunk"] == np.minimum(64, run["remaining"]))
+    assert np.all(it[(it["flags"] & api.SERVE_DECODE_CAP) != 0]["chunk"] == 0)
+
+
+def test_kv_wait_when_the_pool_is_small(setup):
+    """A pool that holds only a few requests at a time delays prompts instead of failing."""
+    from paper_2609_07883_amd.runtime import Session
+    _, _, tr = setup
+    need = max(int(-(-(p + o - 1) // 16)) for p, o in zip(tr.prompt, tr.output))
+    sess = Session(synth.with_layers(synth.TINY, 2), num_blocks=need + 8, max_c=256, max_b=16)
+    res = serving.run(tr, policy="fixed", fixed_chunk=128, tpot_ms=4.0, max_decode=16, session=sess)
+    torch.cuda.synchronize()
+    _check_run(sess, tr, res, 16)
+    assert np.any(res.iterations["flags"] & api.SERVE_KV_WAIT)

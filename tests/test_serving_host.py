@@ -1,0 +1,148 @@
+"""The library's serving loop against the serving oracle (CPU, analytic executor).
+
+slw_serve with the analytic executor is the Sec. 4.1 simulator; every token
+time and every iteration (start, end, chunk, decode count, prefill request,
+budget, remaining prompt) must equal the oracle's bit for bit, for both
+policies, with the controller reading a table that holds the cost model
+exactly (dense grid) or only approximately (a coarse grid: decode counts
+round up, chunks interpolate).  The request-level metrics computed by the
+product module must equal the oracle's.
+"""
+import numpy as np
+import pytest
+
+from oracle import schedule as S
+from oracle import serving as V
+from paper_2609_07883_amd import api, serving, synth
+
+MS = 1_000_000
+COARSE_C = [0, 32, 64, 128, 256, 512, 1024, 2048, 4096]
+COARSE_B = [0, 1, 2, 4, 8, 16, 32, 64, 128, 256]
+
+
+def _trace(n, rate, seed, **kw):
+    return synth.request_trace(n, rate, seed=seed, **kw)
+
+
+def _oracle_reqs(tr):
+    return [V.Request(i, int(a), int(p), int(o)) for i, (a, p, o) in
+            enumerate(zip(tr.arrival_ns, tr.prompt, tr.output))]
+
+
+def _oracle_table(c_grid, b_grid):
+    return S.CostTable.from_values(c_grid, b_grid, [[S.analytic_cost_ns(b, c) for c in c_grid] for b in b_grid])
+
+
+def _compare(tr, res, ref):
+    for i, toks in enumerate(res.token_ns):
+        assert toks.tolist() == ref.token_ns[i], f"request {i}"
+    it = res.iterations
+    assert len(it) == len(ref.iterations)
+    got = np.stack([it["start_ns"], it["end_ns"], it["chunk"], it["n_decode"], it["prefill_id"], it["budget_ns"]], 1)
+    exp = np.array([[r.start_ns, r.end_ns, r.chunk, r.n_decode, r.prefill_rid, r.budget_ns] for r in ref.iterations])
+    bad = np.nonzero((got != exp).any(1))[0]
+    assert len(bad) == 0, f"first differing iteration {bad[0]}: {got[bad[0]]} vs {exp[bad[0]]}"
+
+
+@pytest.mark.parametrize("grid", ["dense", "coarse"])
+@pytest.mark.parametrize("tpot_ms,margin_ms", [(25, 0), (10, 0), (10, 2)])
+def test_sloweave_matches_oracle(grid, tpot_ms, margin_ms):
+    tr = _trace(300, 6.0, seed=3)
+    if grid == "dense":
+        cg, bg = [0, 1, 64, 512, 4096], list(range(0, 257))
+    else:
+        cg, bg = COARSE_C, COARSE_B
+    tab = api.CostTable.analytic(cg, bg)
+    res = serving.run(tr, policy="sloweave", tpot_ms=tpot_ms, max_decode=256, table=tab, margin_ns=margin_ms * MS)
+    ot = _oracle_table(cg, bg)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=S.analytic_cost_ns, tpot_ns=tpot_ms * MS, policy="sloweave",
+                     predict=ot.lookup, c_last=cg[-1], c_max=4096, margin_ns=margin_ms * MS, max_decode=256)
+    _compare(tr, res, ref)
+
+
+@pytest.mark.parametrize("chunk", [256, 512, 2048])
+def test_fixed_matches_oracle(chunk):
+    tr = _trace(300, 6.0, seed=4)
+    res = serving.run(tr, policy="fixed", fixed_chunk=chunk, tpot_ms=25, max_decode=64)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="fixed",
+                     fixed_chunk=chunk, max_decode=64)
+    _compare(tr, res, ref)
+
+
+def test_decode_batch_above_table_is_decode_only():
+    tr = _trace(200, 40.0, seed=5, long_lo=256, long_hi=1024, short_median=64, output_mean=64)
+    cg, bg = COARSE_C, [0, 1, 2, 4, 8]
+    tab = api.CostTable.analytic(cg, bg)
+    res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=32, table=tab)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=S.analytic_cost_ns, tpot_ns=25 * MS, policy="sloweave",
+                     predict=_oracle_table(cg, bg).lookup, c_last=cg[-1], max_decode=32)
+    _compare(tr, res, ref)
+    it = res.iterations
+    over = it[(it["n_decode"] > 8) & (it["remaining"] > 0)]
+    assert len(over) > 0 and (over["chunk"] == 0).all()
+    assert (over["flags"] & api.SERVE_UNPRICED).all()
+
+
+def test_decode_cap_flags_and_predictions():
+    tr = _trace(200, 40.0, seed=6, long_lo=256, long_hi=1024, short_median=64, output_mean=64)
+    tab = api.CostTable.analytic(COARSE_C, COARSE_B)
+    res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=4, table=tab)
+    it = res.iterations
+    assert it["n_decode"].max() == 4
+    capped = it[(it["flags"] & api.SERVE_DECODE_CAP) != 0]
+    assert len(capped) > 0 and (capped["chunk"] == 0).all() and (capped["n_decode"] >= 4).all()
+    ot = _oracle_table(COARSE_C, COARSE_B)
+    assert all(r["predicted_ns"] == ot.lookup(int(r["n_decode"]), int(r["chunk"])) for r in it[:500])
+
+
+def test_metrics_match_oracle():
+    tr = _trace(400, 6.0, seed=7)
+    tab = api.CostTable.analytic(COARSE_C, COARSE_B)
+    for pol, fc, D in [("sloweave", 0, 10), ("fixed", 2048, 10), ("fixed", 256, 25)]:
+        res = serving.run(tr, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=256, table=tab)
+        got = serving.metrics(tr, res.token_ns, ttft_slo_ms=1000, tpot_slo_ms=D)
+        ref = V.summarize(_oracle_reqs(tr), {i: t.tolist() for i, t in enumerate(res.token_ns)},
+                          ttft_slo_ns=1000 * MS, tpot_slo_ns=D * MS)
+        assert got["met"] == ref["met"]
+        assert got["arrival_span_ns"] == ref["goodput_den_ns"]
+        assert got["makespan_ns"] == ref["makespan_ns"]
+        assert got["p99_ttft_ms"] * 1e6 == pytest.approx(ref["p99_ttft_ns"], abs=0.5)
+        assert got["p50_ttft_ms"] * 1e6 == pytest.approx(ref["p50_ttft_ns"], abs=0.5)
+        assert got["p99_tpot_ms"] * 1e6 == pytest.approx(ref["p99_tpot_ns"], abs=0.5)
+        assert got["goodput_req_s"] == pytest.approx(ref["goodput_num"] / ref["goodput_den_ns"] * 1e9)
+
+
+def test_sloweave_beats_fixed_at_tight_tpot_in_simulation():
+    """Trend of Sec. 4 (no numeric parity: the paper's workload parameters differ):
+    at a 10 ms TPOT objective the controller's goodput is at least that of every
+    fixed chunk on the config-4 trace under the analytic model."""
+    tr = _trace(600, 4.0, seed=3)
+    tab = api.CostTable.analytic(COARSE_C, COARSE_B)
+    good = {}
+    for pol, fc in [("sloweave", 0), ("fixed", 256), ("fixed", 512), ("fixed", 2048)]:
+        res = serving.run(tr, policy=pol, fixed_chunk=fc, tpot_ms=10, max_decode=256, table=tab)
+        good[(pol, fc)] = serving.metrics(tr, res.token_ns, 1000, 10)["goodput_req_s"]
+    assert good[("sloweave", 0)] >= max(v for k, v in good.items() if k[0] == "fixed")
+
+
+def test_errors():
+    tr = _trace(10, 4.0, seed=1)
+    with pytest.raises(api.SloweaveError) as e:
+        api.serve([1, 1], [0, 5], [4, 4], [1, 1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:      # SLOWeave without a table
+        serving.run(tr, policy="sloweave", tpot_ms=10, max_decode=4)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:      # GPU executor without a context
+        api.serve([0], [0], [4], [1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4,
+                  executor=api.EXEC_GPU)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:      # iteration cap
+        api.serve([0], [0], [400], [50], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4,
+                  iter_cap=10)
+    assert e.value.code == api.ERANGE
+    with pytest.raises(api.SloweaveError) as e:
+        api.serve([0], [0], [0], [1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4)
+    assert e.value.code == api.EINVAL
+    tok, its = api.serve([], [], [], [], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4)
+    assert tok == [] and len(its) == 0
