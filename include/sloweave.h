@@ -230,8 +230,9 @@ typedef struct slw_profile_opts {
     uint64_t seed;        /* seed of the context draw                                 */
     int32_t warmup;       /* untimed iterations per grid point (>= 0)                 */
     int32_t repeats;      /* timed iterations per grid point (>= 1)                   */
-    void* flush_buf;      /* device buffer overwritten before every timed iteration   */
-    size_t flush_bytes;   /* (flushes the last-level cache); 0 = no flush             */
+    void* flush_buf;      /* device buffer read in full before every timed iteration  */
+    size_t flush_bytes;   /* (evicts the last-level cache without dirtying it; its    */
+                          /* contents are left as they are); 0 = no flush            */
     const void* x_in;     /* device bf16 [max C + max B][d] input rows                */
     void* x_out;          /* device bf16 [max C + max B][d]                           */
     void* ws;             /* device workspace for (max C, max B)                      */

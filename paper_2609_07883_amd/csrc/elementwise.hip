@@ -82,10 +82,18 @@ __global__ void rope_table_kernel(const int32_t* __restrict__ pos, float2* __res
     cs[idx] = make_float2(static_cast<float>(c), static_cast<float>(s));
 }
 
-__global__ void fill_kernel(uint32_t* p, size_t n, uint32_t v) {
+// Reads the whole buffer so that it displaces whatever the caches hold, and
+// leaves no dirty lines behind (a write sweep would make the next kernel pay
+// for their write-back).  The store below keeps the loads alive; it fires
+// only in the unlikely case that a thread's xor equals `key`.
+__global__ void sweep_kernel(uint32_t* p, size_t n4, uint32_t key) {
     size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
     const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
-    for (; i < n; i += stride) p[i] = v + static_cast<uint32_t>(i);
+    const u32x4* q = reinterpret_cast<const u32x4*>(p);
+    u32x4 acc = {0u, 0u, 0u, 0u};
+    for (; i < n4; i += stride) acc ^= q[i];
+    const uint32_t x = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+    if (x == key) p[0] = x;
 }
 
 }  // namespace
@@ -109,10 +117,10 @@ void launch_rope_table(const int32_t* pos, float2* cs, int rows, int hd, double 
     rope_table_kernel<<<(n + 255) / 256, 256, 0, s>>>(pos, cs, rows, half, theta);
 }
 
-void launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s) {
-    const size_t n = bytes / 4;
-    if (n == 0) return;
-    fill_kernel<<<2048, 256, 0, s>>>(static_cast<uint32_t*>(p), n, pattern);
+void launch_cache_sweep(void* p, size_t bytes, uint32_t key, hipStream_t s) {
+    const size_t n4 = bytes / 16;
+    if (n4 == 0) return;
+    sweep_kernel<<<2048, 256, 0, s>>>(static_cast<uint32_t*>(p), n4, key);
 }
 
 }  // namespace slw

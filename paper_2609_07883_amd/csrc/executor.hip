@@ -739,7 +739,7 @@ extern "C" int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t
                 if (!rc) rc = sync();
                 for (int r = 0; r < o->repeats && !rc; ++r) {
                     if (o->flush_buf && o->flush_bytes) {
-                        launch_fill(o->flush_buf, o->flush_bytes, static_cast<uint32_t>(r), s);
+                        launch_cache_sweep(o->flush_buf, o->flush_bytes, 0x9e3779b9u + static_cast<uint32_t>(r), s);
                         rc = sync();
                         if (rc) break;
                     }

@@ -336,6 +336,141 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
     }
 }
 
+// Weight-streaming GEMM for small m (at most 32 T rows).  W is read once,
+// straight from memory into MFMA operand registers with no LDS staging, so
+// the bytes in flight per CU are bounded only by registers and occupancy.
+// A work-group has KS waves that split its k range; every wave computes the
+// same 64 B columns (two 32-column groups that pair like the tile kernel's
+// epilogue tiles) for all tokens over its k slice, and the slices are summed
+// through LDS before the epilogue.  Work-groups are small so that several
+// share a CU and the whole grid runs in one round.
+// In a 64-wide k step a lane reads 64 contiguous bytes of its row (lanes
+// 0-31 the first 32 k, lanes 32-63 the next 32); the step's four MFMAs take
+// its 16-byte quarters.  Both operands use this same order of k inside the
+// step, so every dot product is unchanged.  MFMA rows are W rows and columns
+// are tokens: element e of lane l is W row 8(e/4) + 4(l/32) + e%4 of its
+// column group, token 32 t + l%32.
+template <int T, int EPI, bool SPLIT>
+__global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restrict__ partial, int k_per_split,
+                                                     int ks_count) {
+    constexpr int NA = 2 * T;  // accumulator tiles: 2 column groups x T token groups
+    __shared__ float red[2][NA * 16][64];  // ks_count / 2 <= 2 slots
+
+    const int lane = threadIdx.x & 63, ks = threadIdx.x >> 6;
+    const int r = lane & 31, h = lane >> 5;
+    const int c0 = blockIdx.x * 64;
+    const int k_wave = k_per_split / ks_count;
+    const int kbeg = blockIdx.y * k_per_split + ks * k_wave + 32 * h;
+    const int nkb = k_wave / 64;
+
+    const bf16* W = static_cast<const bf16*>(g.w);
+    const bf16* A = static_cast<const bf16*>(g.a);
+    const bf16* wp[2];
+    wp[0] = W + static_cast<size_t>(w_row<EPI>(g, c0 + r)) * g.k + kbeg;
+    wp[1] = W + static_cast<size_t>(w_row<EPI>(g, c0 + 32 + r)) * g.k + kbeg;
+    const bf16* ap[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t)  // rows past m read row m-1; their results are never stored
+        ap[t] = A + static_cast<size_t>(min(t * 32 + r, g.m - 1)) * g.lda + kbeg;
+
+    bf16x8 wf[2][2][4], af[2][T][4];
+    auto load = [&](int kb, int b) {
+        const int off = kb * 64;
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) wf[b][c][j] = *reinterpret_cast<const bf16x8*>(wp[c] + off + 8 * j);
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) af[b][t][j] = *reinterpret_cast<const bf16x8*>(ap[t] + off + 8 * j);
+    };
+    f32x16 acc[2][T];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int t = 0; t < T; ++t) acc[c][t] = f32x16{};
+    auto compute = [&](int b) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int t = 0; t < T; ++t) acc[c][t] = mfma32(wf[b][c][j], af[b][t][j], acc[c][t]);
+    };
+
+    load(0, 0);
+    for (int kb = 0; kb < nkb; kb += 2) {
+        if (kb + 1 < nkb) load(kb + 1, 1);
+        compute(0);
+        if (kb + 1 >= nkb) break;
+        if (kb + 2 < nkb) load(kb + 2, 0);
+        compute(1);
+    }
+
+    // Sum the k slices: halve the active slices per round.
+    for (int half = ks_count / 2; half >= 1; half /= 2) {
+        if (ks >= half && ks < 2 * half) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int t = 0; t < T; ++t)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) red[ks - half][(c * T + t) * 16 + e][lane] = acc[c][t][e];
+        }
+        __syncthreads();
+        if (ks < half) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int t = 0; t < T; ++t)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[c][t][e] += red[ks][(c * T + t) * 16 + e][lane];
+        }
+        __syncthreads();
+    }
+    if (ks != 0) return;
+
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const int row = t * 32 + r;
+        if (row >= g.m) continue;
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+            const int i0 = 8 * e4 + 4 * h;  // W row of element 4 e4 within its column group
+            if (SPLIT) {
+                float* P = partial + (static_cast<size_t>(blockIdx.y) * g.m + row) * g.n + c0 + i0;
+#pragma unroll
+                for (int c = 0; c < 2; ++c)
+                    *reinterpret_cast<f32x4*>(P + 32 * c) =
+                        f32x4{acc[c][t][4 * e4], acc[c][t][4 * e4 + 1], acc[c][t][4 * e4 + 2], acc[c][t][4 * e4 + 3]};
+                continue;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int e = 4 * e4 + q;
+                const float x0 = acc[0][t][e], x1 = acc[1][t][e];
+                if (EPI == EPI_QKV) {
+                    qkv_store(g, row, c0 / g.hd, ((c0 % g.hd) / 64) * 32 + i0 + q, x0, x1);
+                } else if (EPI == EPI_SWIGLU) {
+                    static_cast<bf16*>(g.out)[static_cast<size_t>(row) * g.ldo + (c0 >> 1) + i0 + q] =
+                        f2bf(silu(x0) * x1);
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 2; ++c) {
+                        const size_t o = static_cast<size_t>(row) * g.ldo + c0 + 32 * c + i0 + q;
+                        const float v = c ? x1 : x0;
+                        if (EPI == EPI_RESID_F32OUT)
+                            static_cast<float*>(g.out)[o] = v + bf2f(static_cast<const bf16*>(g.resid)[o]);
+                        else
+                            static_cast<bf16*>(g.out)[o] = f2bf(v + static_cast<const float*>(g.resid)[o]);
+                    }
+                }
+            }
+        }
+    }
+}
+
 struct TileCfg {
     int bm, bn, waves_m, waves_n, bk;
 };
@@ -350,6 +485,15 @@ constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64}, {64, 128, 2, 2, 64}, {32, 256
                              {256, 128, 2, 2, 32}, {128, 256, 2, 2, 32}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
+template <int EPI>
+void launch_reduce(const GemmArgs& g, const float* part, int splits, hipStream_t s) {
+    size_t work;
+    if (EPI == EPI_QKV) work = static_cast<size_t>(g.m) * (g.n / 2);
+    else if (EPI == EPI_SWIGLU) work = static_cast<size_t>(g.m) * (g.n / 8);
+    else work = static_cast<size_t>(g.m) * (g.n / 4);
+    splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, splits);
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int EPI>
 void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
@@ -361,11 +505,31 @@ void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s
         return;
     }
     gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
-    size_t work;
-    if (EPI == EPI_QKV) work = static_cast<size_t>(g.m) * (g.n / 2);
-    else if (EPI == EPI_SWIGLU) work = static_cast<size_t>(g.m) * (g.n / 8);
-    else work = static_cast<size_t>(g.m) * (g.n / 4);
-    splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, p.splits);
+    launch_reduce<EPI>(g, part, p.splits, s);
+}
+
+template <int T, int EPI>
+void launch_skinny_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
+    dim3 grid(g.n / 64, p.splits);
+    const int threads = 64 * p.ks;
+    const int kps = g.k / p.splits;
+    if (p.splits == 1) {
+        skinny_kernel<T, EPI, false><<<grid, threads, 0, s>>>(g, nullptr, kps, p.ks);
+        return;
+    }
+    skinny_kernel<T, EPI, true><<<grid, threads, 0, s>>>(g, part, kps, p.ks);
+    launch_reduce<EPI>(g, part, p.splits, s);
+}
+
+template <int T>
+void launch_skinny(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
+    float* part = static_cast<float*>(partial);
+    switch (g.epi) {
+        case EPI_RESID_F32OUT: launch_skinny_epi<T, EPI_RESID_F32OUT>(g, p, part, s); break;
+        case EPI_RESID_F32IN: launch_skinny_epi<T, EPI_RESID_F32IN>(g, p, part, s); break;
+        case EPI_SWIGLU: launch_skinny_epi<T, EPI_SWIGLU>(g, p, part, s); break;
+        default: launch_skinny_epi<T, EPI_QKV>(g, p, part, s); break;
+    }
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int BK>
@@ -387,6 +551,10 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 // k-32 (two per CU) tiles measured fastest in each band of m.  n must be a
 // multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
+    // Up to 32 rows the weight-streaming kernel wins on the narrower
+    // projections (o, down: 12-16% at m <= 32, qkv even); on gate/up the
+    // 64 x 128 tiles keep up with it.
+    if (m <= 32 && n < 16384 && n % 64 == 0) return plan_with_cfg(kSkinnyCfg, m, n, k);
     int cfg;
     if (k >= 8192) cfg = m <= 160 ? 1 : 3;                                   // deep k (down)
     else if (n >= 16384)                                                     // wide n (gate/up)
@@ -400,6 +568,21 @@ GemmPlan plan_gemm(int m, int n, int k) {
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
     GemmPlan p{};
     p.cfg = cfg;
+    if (cfg == kSkinnyCfg) {
+        // Four waves slice k inside a work-group (fewer when k is short); k is
+        // also split across work-groups until there are 384 of them (three
+        // share a CU), keeping whole 64-wide steps per wave.
+        p.bn = 64;
+        p.bm = 32;
+        int ks = 4;
+        while (ks > 1 && k % (64 * ks)) ks /= 2;
+        p.ks = ks;
+        int splits = 1;
+        while (splits < 8 && (n / 64) * splits < 384 && k % (2 * 64 * ks * splits) == 0) splits *= 2;
+        p.splits = splits;
+        p.partial_bytes = splits > 1 ? static_cast<size_t>(splits) * m * n * sizeof(float) : 0;
+        return p;
+    }
     p.bm = kCfgs[cfg].bm;
     p.bn = kCfgs[cfg].bn;
     const long tiles = static_cast<long>(n / p.bn) * ((m + p.bm - 1) / p.bm);
@@ -413,11 +596,17 @@ GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
 }
 
 bool gemm_shape_ok(const GemmPlan& p, int n, int k) {
+    if (p.cfg == kSkinnyCfg)  // m <= 32 is the caller's part (plan_gemm)
+        return n % 64 == 0 && p.ks >= 1 && p.ks <= 4 && k % (64 * p.ks * p.splits) == 0;
     return p.cfg >= 0 && p.cfg < kNumCfgs && n % p.bn == 0 && k % (p.splits * BK_MAX) == 0;
 }
 
 void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     if (g.m <= 0) return;
+    if (p.cfg == kSkinnyCfg) {
+        launch_skinny<1>(g, p, partial, s);  // plans cover m <= 32
+        return;
+    }
     switch (p.cfg) {
         case 0: launch_cfg<128, 128, 2, 2, 64>(g, p, partial, s); break;
         case 1: launch_cfg<64, 128, 2, 2, 64>(g, p, partial, s); break;

@@ -38,11 +38,13 @@ struct GemmArgs {
     int hq, hkv, hd;
 };
 struct GemmPlan {
-    int cfg;      // tile configuration index
+    int cfg;      // tile configuration index (kSkinnyCfg: the weight-streaming kernel)
     int bm, bn;
-    int splits;   // split-K factor (1: fused epilogue)
+    int splits;   // split-K factor across work-groups (1: fused epilogue)
     size_t partial_bytes;
+    int ks;     // weight-streaming kernel (m <= 32): k slices per work-group
 };
+constexpr int kSkinnyCfg = 8;
 GemmPlan plan_gemm(int m, int n, int k);
 // The plan for a given tile configuration (split-K chosen by tile count).
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k);
@@ -94,7 +96,8 @@ struct DecodeAttnArgs {
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
 void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s);
 
-// Fill `bytes` of device memory with a byte pattern (last-level cache flush).
-void launch_fill(void* p, size_t bytes, uint32_t pattern, hipStream_t s);
+// Read `bytes` of device memory (last-level cache flush that leaves no dirty
+// lines); the buffer is written only if a thread's xor of its words equals key.
+void launch_cache_sweep(void* p, size_t bytes, uint32_t key, hipStream_t s);
 
 }  // namespace slw

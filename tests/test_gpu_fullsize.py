@@ -87,3 +87,20 @@ def test_chat_bursty_point():
     C = 32
     k = int(np.random.default_rng(5).integers(0, max(1, prompt // C)))
     _run(C, k * C, ctx, seed=14)
+
+
+def test_decode_only_batch():
+    """C = 0, B = 64: every GEMM runs the weight-streaming kernel on 64 rows."""
+    ctx = synth.lognormal_lengths(64, 700, 0.8, 8192, seed=2)
+    _run(0, 0, ctx, seed=15)
+
+
+def test_small_chunk_with_decodes():
+    """C = 32 at prefix 512 with B = 64 decodes (96 rows: two token waves)."""
+    ctx = synth.lognormal_lengths(64, 700, 0.8, 8192, seed=3)
+    _run(32, 512, ctx, seed=16)
+
+
+def test_single_decode():
+    """C = 0, B = 1: one row through every kernel."""
+    _run(0, 0, [1500], seed=17)
