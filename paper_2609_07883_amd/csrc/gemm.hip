@@ -112,11 +112,43 @@ __device__ __forceinline__ void tile_of(int pid, int nt_m, int nt_n, int& tm, in
     tn = in_group / gsize;
 }
 
-// The k-32 tiles ask for two waves per SIMD so that two work-groups fit on a CU.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int EPI, bool SPLIT>
-__global__ __launch_bounds__(WAVES_M * WAVES_N * 64, BK == 32 ? 2 : 1) void gemm_kernel(GemmArgs g,
-                                                                                        float* __restrict__ partial,
-                                                                                        int k_per_split) {
+// Wait until at most n vector-memory operations of this wave are
+// outstanding (gfx9 s_waitcnt encoding, other counters left alone).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// lds + 16 l (lds is wave-uniform).  Issued as assembly so that the compiler,
+// which cannot tell which LDS buffer such a load writes, does not make every
+// later LDS read wait for all of them; the main loop waits for them itself.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds) {
+    const uint32_t dst = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst) : "memory", "m0");
+}
+
+// Workgroup barrier with no memory fence: the asm statement's memory clobber
+// keeps the compiler from moving LDS or global accesses across it, and the
+// waits it needs are issued explicitly before it.
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
+// Main loops:
+//   STAGES == 2: registers prefetch the next k step while the current one
+//                feeds the matrix cores, then write it to the second LDS buffer
+//                (one barrier per step).  The k-32 tiles of this kind ask for
+//                two waves per SIMD so that two work-groups fit on a CU.
+//   STAGES >= 3: a ring of STAGES LDS buffers filled by direct global->LDS
+//                loads (16 bytes per lane) issued STAGES - 1 steps ahead; no
+//                staging registers.  Each lane loads the 16-byte chunk that
+//                belongs at its LDS slot, so the XOR layout is kept.  A counted
+//                wait for the wave's own loads of the step plus a bare barrier
+//                make every wave's loads visible; the same barrier proves that
+//                the buffer refilled next was finished by all waves.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int STAGES, int EPI, bool SPLIT>
+__global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ? 2 : 1) void gemm_kernel(
+    GemmArgs g, float* __restrict__ partial, int k_per_split) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
@@ -126,8 +158,8 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, BK == 32 ? 2 : 1) void gemm
     static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small");
     static_assert(WN % 64 == 0, "paired epilogues need whole 64-column pairs per wave");
 
-    __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
-    __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * BK];
+    __shared__ __attribute__((aligned(16))) bf16 As[STAGES][BM * BK];
+    __shared__ __attribute__((aligned(16))) bf16 Bs[STAGES][BN * BK];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -143,36 +175,6 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, BK == 32 ? 2 : 1) void gemm
     // prefetch asynchronous.
     const bf16* A = static_cast<const bf16*>(g.a) + kb;
     const bf16* W = static_cast<const bf16*>(g.w) + kb;
-    int a_off[A_LOADS], a_lds[A_LOADS];
-#pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-        const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
-        a_off[i] = min(m0 + row, g.m - 1) * g.lda + ch * 8;
-        a_lds[i] = row * BK + swz<BK>(row, ch) * 8;
-    }
-    int b_off[B_LOADS], b_lds[B_LOADS];
-#pragma unroll
-    for (int i = 0; i < B_LOADS; ++i) {
-        const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
-        b_off[i] = w_row<EPI>(g, n0 + row) * g.k + ch * 8;
-        b_lds[i] = row * BK + swz<BK>(row, ch) * 8;
-    }
-
-    bf16x8 ra[A_LOADS], rb[B_LOADS];
-    auto load_tile = [&](int kt) {
-        const bf16* Ak = A + kt * BK;
-        const bf16* Wk = W + kt * BK;
-#pragma unroll
-        for (int i = 0; i < A_LOADS; ++i) ra[i] = *reinterpret_cast<const bf16x8*>(Ak + a_off[i]);
-#pragma unroll
-        for (int i = 0; i < B_LOADS; ++i) rb[i] = *reinterpret_cast<const bf16x8*>(Wk + b_off[i]);
-    };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < A_LOADS; ++i) *reinterpret_cast<bf16x8*>(&As[buf][a_lds[i]]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_LOADS; ++i) *reinterpret_cast<bf16x8*>(&Bs[buf][b_lds[i]]) = rb[i];
-    };
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -210,15 +212,97 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, BK == 32 ? 2 : 1) void gemm
         }
     };
 
-    load_tile(0);
-    store_tile(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load_tile(kt + 1);
-        compute(buf);
-        if (kt + 1 < nk) store_tile(buf ^ 1);
+    if constexpr (STAGES == 2) {
+        int a_off[A_LOADS], a_lds[A_LOADS];
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) {
+            const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
+            a_off[i] = min(m0 + row, g.m - 1) * g.lda + ch * 8;
+            a_lds[i] = row * BK + swz<BK>(row, ch) * 8;
+        }
+        int b_off[B_LOADS], b_lds[B_LOADS];
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+            const int idx = tid + i * THREADS, row = idx / CPR, ch = idx % CPR;
+            b_off[i] = w_row<EPI>(g, n0 + row) * g.k + ch * 8;
+            b_lds[i] = row * BK + swz<BK>(row, ch) * 8;
+        }
+        bf16x8 ra[A_LOADS], rb[B_LOADS];
+        auto load_tile = [&](int kt) {
+            const bf16* Ak = A + kt * BK;
+            const bf16* Wk = W + kt * BK;
+#pragma unroll
+            for (int i = 0; i < A_LOADS; ++i) ra[i] = *reinterpret_cast<const bf16x8*>(Ak + a_off[i]);
+#pragma unroll
+            for (int i = 0; i < B_LOADS; ++i) rb[i] = *reinterpret_cast<const bf16x8*>(Wk + b_off[i]);
+        };
+        auto store_tile = [&](int buf) {
+#pragma unroll
+            for (int i = 0; i < A_LOADS; ++i) *reinterpret_cast<bf16x8*>(&As[buf][a_lds[i]]) = ra[i];
+#pragma unroll
+            for (int i = 0; i < B_LOADS; ++i) *reinterpret_cast<bf16x8*>(&Bs[buf][b_lds[i]]) = rb[i];
+        };
+        load_tile(0);
+        store_tile(0);
         __syncthreads();
+        for (int kt = 0; kt < nk; ++kt) {
+            const int buf = kt & 1;
+            if (kt + 1 < nk) load_tile(kt + 1);
+            compute(buf);
+            if (kt + 1 < nk) store_tile(buf ^ 1);
+            __syncthreads();
+        }
+    } else {
+        // One direct load fills 1 KB of LDS: RPI rows of BK values.  Wave w
+        // issues A loads w, w + NW, ... and B loads likewise.
+        constexpr int NW = WAVES_M * WAVES_N;
+        constexpr int RPI = 64 / CPR;
+        constexpr int A_INS = BM / RPI / NW, B_INS = BN / RPI / NW;
+        constexpr int PER_STEP = A_INS + B_INS;
+        static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "direct loads must split evenly");
+        static_assert(STAGES == 3 || STAGES == 4, "the counted waits cover three or four stages");
+        const int r_in = lane / CPR, stored = lane % CPR;
+        const bf16* a_src[A_INS];
+        int a_dst[A_INS];
+#pragma unroll
+        for (int i = 0; i < A_INS; ++i) {
+            const int row = (wave + i * NW) * RPI + r_in;
+            const int ch = stored ^ ((row / (16 / CPR)) & (CPR - 1));  // logical chunk stored at this slot
+            a_src[i] = A + static_cast<size_t>(min(m0 + row, g.m - 1)) * g.lda + ch * 8;
+            a_dst[i] = (wave + i * NW) * RPI * BK;
+        }
+        const bf16* b_src[B_INS];
+        int b_dst[B_INS];
+#pragma unroll
+        for (int i = 0; i < B_INS; ++i) {
+            const int row = (wave + i * NW) * RPI + r_in;
+            const int ch = stored ^ ((row / (16 / CPR)) & (CPR - 1));
+            b_src[i] = W + static_cast<size_t>(w_row<EPI>(g, n0 + row)) * g.k + ch * 8;
+            b_dst[i] = (wave + i * NW) * RPI * BK;
+        }
+        auto issue = [&](int kt) {
+            const int buf = kt % STAGES;
+#pragma unroll
+            for (int i = 0; i < A_INS; ++i)
+                load_lds16(a_src[i] + kt * BK, &As[buf][a_dst[i]]);
+#pragma unroll
+            for (int i = 0; i < B_INS; ++i)
+                load_lds16(b_src[i] + kt * BK, &Bs[buf][b_dst[i]]);
+        };
+#pragma unroll
+        for (int s = 0; s < STAGES - 1; ++s)
+            if (s < nk) issue(s);
+        for (int kt = 0; kt < nk; ++kt) {
+            // this wave's loads of step kt are done once at most the younger
+            // steps' loads (up to STAGES - 2 of them) are outstanding
+            const int younger = min(nk - 1 - kt, STAGES - 2);
+            if (younger >= STAGES - 2) wait_vmcnt<PER_STEP * (STAGES - 2)>();
+            else if (STAGES > 3 && younger == 1) wait_vmcnt<PER_STEP>();
+            else wait_vmcnt<0>();
+            barrier_only();
+            if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+            compute(kt % STAGES);
+        }
     }
 
     // epilogue: element e of tile (i, j) is row rbase + i*32 + 8(e/4) + e%4,
@@ -472,17 +556,21 @@ __global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restri
 }
 
 struct TileCfg {
-    int bm, bn, waves_m, waves_n, bk;
+    int bm, bn, waves_m, waves_n, bk, stages;
 };
 // 0: 128x128 / 4 waves (64x64 each)      1: 64x128 / 4 waves (32x64)
 // 2: 32x256 / 4 waves (32x64)            3: 256x256 / 8 waves (128x64)
 // 4: 256x256 / 4 waves (128x128)         5: 128x256 / 8 waves (64x64)
 // 6: 256x128 / 4 waves (128x64), k 32    7: 128x256 / 4 waves (64x128), k 32
-// The k-32 tiles use 48 KB of LDS, so two work-groups share a CU and one's
-// loads overlap the other's matrix work.
-constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64}, {64, 128, 2, 2, 64}, {32, 256, 1, 4, 64},
-                             {256, 256, 2, 4, 64}, {256, 256, 2, 2, 64}, {128, 256, 2, 4, 64},
-                             {256, 128, 2, 2, 32}, {128, 256, 2, 2, 32}};
+// 8: 256x256 / 8 waves, k 32, 4-stage direct-load ring (128 KB of LDS)
+// 9: 128x256 / 8 waves, k 32, 4-stage ring (96 KB)
+// 10: 128x128 / 4 waves, k 32, 4-stage ring (64 KB: two work-groups per CU)
+// The register-staged k-32 tiles (6, 7) use 48 KB of LDS, so two
+// work-groups share a CU and one's loads overlap the other's matrix work.
+constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 2}, {64, 128, 2, 2, 64, 2}, {32, 256, 1, 4, 64, 2},
+                             {256, 256, 2, 4, 64, 2}, {256, 256, 2, 2, 64, 2}, {128, 256, 2, 4, 64, 2},
+                             {256, 128, 2, 2, 32, 2}, {128, 256, 2, 2, 32, 2}, {256, 256, 2, 4, 32, 4},
+                             {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int EPI>
@@ -494,17 +582,17 @@ void launch_reduce(const GemmArgs& g, const float* part, int splits, hipStream_t
     splitk_reduce_kernel<EPI><<<static_cast<unsigned>((work + 255) / 256), 256, 0, s>>>(g, part, splits);
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int EPI>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int ST, int EPI>
 void launch_epi(const GemmArgs& g, const GemmPlan& p, float* part, hipStream_t s) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
     const int tiles = ((g.m + BM - 1) / BM) * (g.n / BN);
     dim3 grid(tiles, p.splits);
     const int kps = g.k / p.splits;
     if (p.splits == 1) {
-        gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, EPI, false><<<grid, THREADS, 0, s>>>(g, nullptr, kps);
+        gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI, false><<<grid, THREADS, 0, s>>>(g, nullptr, kps);
         return;
     }
-    gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
+    gemm_kernel<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI, true><<<grid, THREADS, 0, s>>>(g, part, kps);
     launch_reduce<EPI>(g, part, p.splits, s);
 }
 
@@ -532,35 +620,36 @@ void launch_skinny(const GemmArgs& g, const GemmPlan& p, void* partial, hipStrea
     }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int BK>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int ST>
 void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     float* part = static_cast<float*>(partial);
     switch (g.epi) {
-        case EPI_RESID_F32OUT: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_RESID_F32OUT>(g, p, part, s); break;
-        case EPI_RESID_F32IN: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_RESID_F32IN>(g, p, part, s); break;
-        case EPI_SWIGLU: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_SWIGLU>(g, p, part, s); break;
-        default: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, EPI_QKV>(g, p, part, s); break;
+        case EPI_RESID_F32OUT: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI_RESID_F32OUT>(g, p, part, s); break;
+        case EPI_RESID_F32IN: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI_RESID_F32IN>(g, p, part, s); break;
+        case EPI_SWIGLU: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI_SWIGLU>(g, p, part, s); break;
+        default: launch_epi<BM, BN, WAVES_M, WAVES_N, BK, ST, EPI_QKV>(g, p, part, s); break;
     }
 }
 
 }  // namespace
 
 // Tile and split choice, from timings of every configuration on the
-// 8B-layer shapes (m = 96 .. 4104): 64-row tiles with split-K while weight
-// streaming dominates, then whichever of the k-64 (one work-group per CU) and
-// k-32 (two per CU) tiles measured fastest in each band of m.  n must be a
-// multiple of 128 and k of 64.
+// 8B-layer shapes (m = 96 .. 4104, caches swept with reads between runs):
+// the weight-streaming kernel up to 32 rows on the narrower projections,
+// 64-row tiles with split-K while weight streaming dominates, then whichever
+// tile measured fastest in each band of m; from m = 1600 on the 256 x 256
+// tile fed by the four-stage direct-load ring.  n must be a multiple of 128
+// and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     // Up to 32 rows the weight-streaming kernel wins on the narrower
     // projections (o, down: 12-16% at m <= 32, qkv even); on gate/up the
     // 64 x 128 tiles keep up with it.
     if (m <= 32 && n < 16384 && n % 64 == 0) return plan_with_cfg(kSkinnyCfg, m, n, k);
     int cfg;
-    if (k >= 8192) cfg = m <= 160 ? 1 : 3;                                   // deep k (down)
-    else if (n >= 16384)                                                     // wide n (gate/up)
-        cfg = m <= 160 ? 1 : m <= 400 ? 6 : m < 800 ? 1 : m < 1600 ? 7 : 3;
-    else if (n >= 6144) cfg = m <= 400 ? 1 : (m >= 1600 && m < 3000) ? 6 : 0;   // qkv
-    else cfg = m <= 400 ? 0 : (m >= 1600 && m < 3000) ? 7 : 1;               // o
+    if (k >= 8192) cfg = m <= 160 ? 1 : m < 450 ? 8 : m < 800 ? 10 : 8;                  // deep k (down)
+    else if (n >= 16384) cfg = m <= 160 ? 1 : m <= 400 ? 10 : m < 800 ? 1 : m < 1600 ? 7 : 8;  // gate/up
+    else if (n >= 6144) cfg = m <= 400 ? 1 : m < 1600 ? 0 : 8;                           // qkv
+    else cfg = m <= 400 ? 0 : m < 800 ? 1 : m < 1600 ? 10 : 8;                          // o
     if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
     return plan_with_cfg(cfg, m, n, k);
 }
@@ -608,14 +697,17 @@ void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_
         return;
     }
     switch (p.cfg) {
-        case 0: launch_cfg<128, 128, 2, 2, 64>(g, p, partial, s); break;
-        case 1: launch_cfg<64, 128, 2, 2, 64>(g, p, partial, s); break;
-        case 2: launch_cfg<32, 256, 1, 4, 64>(g, p, partial, s); break;
-        case 3: launch_cfg<256, 256, 2, 4, 64>(g, p, partial, s); break;
-        case 4: launch_cfg<256, 256, 2, 2, 64>(g, p, partial, s); break;
-        case 5: launch_cfg<128, 256, 2, 4, 64>(g, p, partial, s); break;
-        case 6: launch_cfg<256, 128, 2, 2, 32>(g, p, partial, s); break;
-        default: launch_cfg<128, 256, 2, 2, 32>(g, p, partial, s); break;
+        case 0: launch_cfg<128, 128, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 1: launch_cfg<64, 128, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 2: launch_cfg<32, 256, 1, 4, 64, 2>(g, p, partial, s); break;
+        case 3: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 4: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 5: launch_cfg<128, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 6: launch_cfg<256, 128, 2, 2, 32, 2>(g, p, partial, s); break;
+        case 7: launch_cfg<128, 256, 2, 2, 32, 2>(g, p, partial, s); break;
+        case 8: launch_cfg<256, 256, 2, 4, 32, 4>(g, p, partial, s); break;
+        case 9: launch_cfg<128, 256, 2, 4, 32, 4>(g, p, partial, s); break;
+        default: launch_cfg<128, 128, 2, 2, 32, 4>(g, p, partial, s); break;
     }
 }
 

@@ -44,7 +44,7 @@ struct GemmPlan {
     size_t partial_bytes;
     int ks;     // weight-streaming kernel (m <= 32): k slices per work-group
 };
-constexpr int kSkinnyCfg = 8;
+constexpr int kSkinnyCfg = 99;
 GemmPlan plan_gemm(int m, int n, int k);
 // The plan for a given tile configuration (split-K chosen by tile count).
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k);
