@@ -299,17 +299,32 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
 # Context
 # ---------------------------------------------------------------------------
 
-@dataclass
+@dataclass(frozen=True)
 class Batch:
+    """One iteration's batch.  Immutable: its C struct is built on first use
+    and reused by every later call with the same batch."""
     chunk: int
     prefill_seq: int
     prefix_len: int
-    decode_seqs: list
-    context_lens: list
+    decode_seqs: tuple
+    context_lens: tuple
+
+    def __post_init__(self):
+        object.__setattr__(self, "decode_seqs", tuple(int(v) for v in self.decode_seqs))
+        object.__setattr__(self, "context_lens", tuple(int(v) for v in self.context_lens))
 
     @property
     def rows(self) -> int:
         return self.chunk + len(self.decode_seqs)
+
+    def c_struct(self):
+        c = self.__dict__.get("_c")
+        if c is None:
+            ds, cl = _i64(self.decode_seqs), _i32(self.context_lens)
+            c = (BatchC(self.chunk, self.prefill_seq, self.prefix_len, len(ds), _ptr(ds, C.c_int64),
+                        _ptr(cl, C.c_int32)), ds, cl)   # the arrays keep the pointers alive
+            object.__setattr__(self, "_c", c)
+        return c[0]
 
 
 class Context:
@@ -382,12 +397,8 @@ class Context:
 
     def mixed_iteration(self, batch: Batch, x_in: int, x_out: int, ws: int, ws_bytes: int,
                         stream: int = 0):
-        ds = _i64(batch.decode_seqs)
-        cl = _i32(batch.context_lens)
-        bc = BatchC(batch.chunk, batch.prefill_seq, batch.prefix_len, len(ds),
-                    _ptr(ds, C.c_int64), _ptr(cl, C.c_int32))
-        _check(lib().slw_mixed_iteration(self._h, C.byref(bc), C.c_void_p(x_in), C.c_void_p(x_out),
-                                         C.c_void_p(ws), ws_bytes, C.c_void_p(stream)))
+        _check(lib().slw_mixed_iteration(self._h, C.byref(batch.c_struct()), x_in, x_out, ws, ws_bytes,
+                                         stream or None))
 
     def set_stage_timing(self, depth: int):
         """Record per-stage HIP events for the last `depth` iterations (0: off)."""

@@ -21,6 +21,10 @@ namespace slw {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
+// LDS tiles in the chunk-attention ring: two (64 KB) let two work-groups
+// share a CU, which measured slightly ahead of three or four tiles (96 or
+// 128 KB, one work-group per CU) on the long-context and layer-sweep shapes.
+constexpr int kChunkStages = 2;
 
 __device__ __forceinline__ bf16x8 cat44(bf16x4 lo, bf16x4 hi) {
     return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -45,21 +49,47 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // Q^T tiles of its MFMAs, so one K or V fragment read from LDS feeds two
 // MFMAs and two waves share each SIMD, overlapping one wave's softmax with
 // the other's matrix work.  Keys advance 64 at a time (four pages) through a
-// double-buffered LDS tile shared by the eight waves.  A work item covers one key range of one query tile; in
+// ring of ST LDS tiles shared by the eight waves, filled by direct
+// global->LDS loads issued ST - 1 tiles ahead (each lane fetches the 16-byte
+// chunk that belongs at its swizzled LDS slot; every wave issues the same
+// number of loads per tile, so a counted wait for its own loads plus a bare
+// barrier publishes a tile).  A work item covers one key range of one query tile; in
 // split mode it writes fp32 partials (running max, sum, unnormalised output)
 // that chunk_merge_kernel combines.
 // ---------------------------------------------------------------------------
 
-// LDS swizzles: K rows (64 B = four 16-byte chunks) and V rows (32 B = four
-// 8-byte groups of four tokens).
+// LDS swizzles of 16-byte chunks: K rows (64 B = four chunks of 8 dims) and
+// V rows (32 B = two chunks of 8 tokens).
 __device__ __forceinline__ int kswz(int t, int sub) { return sub ^ ((t >> 1) & 3); }
-__device__ __forceinline__ int vswz(int d, int grp) { return grp ^ ((d >> 2) & 3); }
+__device__ __forceinline__ int vswz(int d, int h) { return h ^ ((d >> 2) & 1); }
 
-template <int HD, int GROUP>
+// Direct global->LDS load of 16 bytes per lane: lane l's bytes land at
+// lds + 16 l (lds is wave-uniform).  Issued as assembly so that the compiler,
+// which cannot tell which LDS buffer such a load writes, does not make every
+// later LDS read wait for all of them; the kernel waits for them itself.
+__device__ __forceinline__ void load_lds16(const void* src, void* lds) {
+    const uint32_t dst = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst) : "memory", "m0");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier with no memory fence (the memory clobber keeps the
+// compiler from moving LDS or global accesses across it).
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
+template <int HD, int GROUP, int ST>
 __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
-    constexpr int CHUNKS = 4 * PAGE / 8;  // 16-byte chunks per K (or V) tile of 64 keys
-    constexpr int PER_THREAD = 2 * CHUNKS / 512;
+    constexpr int SLABS = 2 * 4 * PAGE / 512;  // 1 KB direct loads per tile (K and V of four pages)
+    constexpr int PER_WAVE = SLABS / 8;        // loads each wave issues per tile
+    static_assert(SLABS % 8 == 0, "tile loads must split evenly over the waves");
+    static_assert(ST >= 2 && ST <= 4, "ring of two to four tiles");
     constexpr int CT = 2;                 // 16-row column tiles per wave (32 rows)
     constexpr int PW = 32 / GROUP;        // positions per wave
     constexpr int PWG = 8 * PW;           // positions per work-group (eight waves)
@@ -67,14 +97,13 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // 2^kSlack, so probabilities stay <= 2^kSlack and most tiles skip the
     // rescale of the output accumulators.
     constexpr float kSlack = 8.0f;
-    __shared__ __attribute__((aligned(16))) bf16 Ks[2][4 * PAGE];
-    __shared__ __attribute__((aligned(16))) bf16 Vs[2][4 * PAGE];
+    __shared__ __attribute__((aligned(16))) bf16 Ks[ST][4 * PAGE];
+    __shared__ __attribute__((aligned(16))) bf16 Vs[ST][4 * PAGE];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
     const int item = blockIdx.x, kvh = blockIdx.y;
     const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
-    const int key_lim = a.prefix + a.c;  // slots at or past this are unwritten
     const int p0 = qt * PWG + wave * PW; // first chunk position of this wave
     const int n_tiles = (ke - kb + 63) / 64;
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
@@ -97,47 +126,43 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
                                   : bf16x8{};
     }
 
-    bf16x8 stage[PER_THREAD];
-    auto load_tile = [&](int t) {
+    // Load j of a tile (j = wave + 8 i): 0 .. 4 KK - 1 are K slabs (page j / KK,
+    // dims 32 (j % KK) ..), the rest V slabs (page, 32 dims of 16 tokens).
+    // Pages past the key range load the range's last page instead (finite
+    // values whose scores are masked), so every wave issues PER_WAVE loads.
+    int l_page[PER_WAVE], l_elem[PER_WAVE], l_dst[PER_WAVE];
+    bool l_isv[PER_WAVE];
 #pragma unroll
-        for (int j = 0; j < PER_THREAD; ++j) {
-            const int c = tid + j * 512;
-            const bool is_v = c >= CHUNKS;
-            const int cc = is_v ? c - CHUNKS : c;
-            const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
-            const int pg = (kb >> 4) + 4 * t + p;
-            bf16x8 v = {};
-            if (pg * 16 < ke) {
-                const size_t blk = a.bt[pg];
-                v = *reinterpret_cast<const bf16x8*>((is_v ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + q * 8);
-                if (is_v) {  // zero unwritten slots so that masked keys contribute exactly 0
-                    const int tok0 = pg * 16 + (q & 1) * 8;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (tok0 + e >= key_lim) v[e] = bf16(0.0f);
-                }
-            }
-            stage[j] = v;
+    for (int i = 0; i < PER_WAVE; ++i) {
+        const int j = wave + 8 * i;
+        const bool is_v = j >= 4 * KK;
+        const int jj = is_v ? j - 4 * KK : j;
+        const int p = jj / KK, slab = jj % KK;
+        l_isv[i] = is_v;
+        l_page[i] = p;
+        if (!is_v) {  // lane: token t, stored chunk lane % 4 holds dims chunk kswz(t, .)
+            const int t = lane >> 2, sub = (lane & 3) ^ ((t >> 1) & 3);
+            l_elem[i] = slab * 512 + t * 32 + sub * 8;
+        } else {      // lane: dim d, stored chunk lane % 2 holds tokens 8 vswz(d, .)
+            const int d = slab * 32 + (lane >> 1), h = (lane & 1) ^ ((d >> 2) & 1);
+            l_elem[i] = d * 16 + h * 8;
         }
-    };
-    auto store_tile = [&](int buf) {
+        l_dst[i] = p * PAGE + slab * 512;
+    }
+    // Block-table entries are read through the scalar cache (a uniform index
+    // into constant memory): a vector load here would make the compiler wait
+    // for every direct load in flight before using its result.
+    typedef const int32_t __attribute__((address_space(4))) const_i32;
+    const const_i32* bt_s = (const const_i32*)a.bt;
+    const int last_page = (ke - 1) >> 4;
+    auto issue = [&](int t) {
+        const int buf = t % ST;
 #pragma unroll
-        for (int j = 0; j < PER_THREAD; ++j) {
-            const int c = tid + j * 512;
-            const bool is_v = c >= CHUNKS;
-            const int cc = is_v ? c - CHUNKS : c;
-            const int p = cc / (PAGE / 8), q = cc % (PAGE / 8);
-            if (!is_v) {
-                const int kk = q / 64, t = (q % 64) / 4, sub = q % 4;
-                *reinterpret_cast<bf16x8*>(&Ks[buf][p * PAGE + kk * 512 + t * 32 + kswz(t, sub) * 8]) = stage[j];
-            } else {
-                const int d = q / 2, h = q % 2;
-                bf16* row = &Vs[buf][p * PAGE + d * 16];
-                const bf16x4 lo = {stage[j][0], stage[j][1], stage[j][2], stage[j][3]};
-                const bf16x4 hi = {stage[j][4], stage[j][5], stage[j][6], stage[j][7]};
-                *reinterpret_cast<bf16x4*>(row + vswz(d, 2 * h) * 4) = lo;
-                *reinterpret_cast<bf16x4*>(row + vswz(d, 2 * h + 1) * 4) = hi;
-            }
+        for (int i = 0; i < PER_WAVE; ++i) {
+            const int pg = __builtin_amdgcn_readfirstlane(min((kb >> 4) + 4 * t + l_page[i], last_page));
+            const size_t blk = bt_s[pg];
+            const bf16* src = (l_isv[i] ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + l_elem[i];
+            load_lds16(src, l_isv[i] ? &Vs[buf][l_dst[i]] : &Ks[buf][l_dst[i]]);
         }
     };
 
@@ -155,12 +180,22 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
         qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
     }
 
-    load_tile(0);
-    store_tile(0);
-    __syncthreads();
+    // Q fragments land before the ring starts; the compiler then has no
+    // loads of its own pending inside the loop, so it adds no waits there.
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int t = 0; t < ST - 1; ++t)
+        if (t < n_tiles) issue(t);
     for (int t = 0; t < n_tiles; ++t) {
-        const int buf = t & 1;
-        if (t + 1 < n_tiles) load_tile(t + 1);
+        const int buf = t % ST;
+        // this wave's loads of tile t are done once at most the loads of the
+        // younger tiles in flight (up to ST - 2 of them) are outstanding
+        const int younger = min(n_tiles - 1 - t, ST - 2);
+        if (ST >= 4 && younger >= 2) wait_vmcnt<2 * PER_WAVE>();
+        else if (ST >= 3 && younger >= 1) wait_vmcnt<PER_WAVE>();
+        else wait_vmcnt<0>();
+        barrier_only();
+        if (t + ST - 1 < n_tiles) issue(t + ST - 1);
         const int key0 = kb + t * 64;
         if (wave_live && key0 <= wave_qpos_hi) {
             f32x4 sc[4][CT];  // [page][ct]
@@ -229,6 +264,11 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
                     }
                 l_run[ct] += ls;
             }
+            // keys at or past ke (the range end; unwritten slots lie past
+            // key_lim >= ke, stand-in pages past ke) have probability 0; their
+            // V values are zeroed too so that whatever the pool holds there
+            // cannot turn 0 into NaN
+            const bool v_mask = key0 + 63 >= ke;
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 bf16x8 pf[CT];
@@ -237,17 +277,23 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
                     const int d = nt * 16 + col;
-                    const int off = d * 16 + vswz(d, grp) * 4;
-                    const bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
-                    const bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
+                    const int off = d * 16 + vswz(d, grp >> 1) * 8 + (grp & 1) * 4;
+                    bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
+                    bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
+                    if (v_mask) {
+                        const int k_lo = key0 + 2 * j * 16 + grp * 4;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            if (k_lo + e >= ke) lo[e] = bf16(0.0f);
+                            if (k_lo + 16 + e >= ke) hi[e] = bf16(0.0f);
+                        }
+                    }
                     const bf16x8 vf = cat44(lo, hi);
 #pragma unroll
                     for (int ct = 0; ct < CT; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
                 }
             }
         }
-        if (t + 1 < n_tiles) store_tile(buf ^ 1);
-        __syncthreads();
     }
     if (!wave_live) return;
 
@@ -499,7 +545,7 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
 
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
-    chunk_attn_kernel<HD, GROUP><<<dim3(a.n_items, a.hkv), 512, 0, s>>>(a);
+    chunk_attn_kernel<HD, GROUP, kChunkStages><<<dim3(a.n_items, a.hkv), 512, 0, s>>>(a);
     if (a.split) chunk_merge_kernel<HD, GROUP><<<dim3(a.c, a.hq), 64, 0, s>>>(a);
 }
 
