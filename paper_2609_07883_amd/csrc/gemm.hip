@@ -135,19 +135,20 @@ __device__ __forceinline__ void load_lds16(const void* src, void* lds) {
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
 // Main loops:
-//   STAGES == 2: registers prefetch the next k step while the current one
-//                feeds the matrix cores, then write it to the second LDS buffer
-//                (one barrier per step).  The k-32 tiles of this kind ask for
-//                two waves per SIMD so that two work-groups fit on a CU.
-//   STAGES >= 3: a ring of STAGES LDS buffers filled by direct global->LDS
-//                loads (16 bytes per lane) issued STAGES - 1 steps ahead; no
+//   RING == 0:   registers prefetch the next k step while the current one
+//                feeds the matrix cores, then write it to the second of two
+//                LDS buffers (one barrier per step).  The k-32 tiles of this
+//                kind ask for two waves per SIMD so that two work-groups fit
+//                on a CU.
+//   RING = 2..4: a ring of RING LDS buffers filled by direct global->LDS
+//                loads (16 bytes per lane) issued RING - 1 steps ahead; no
 //                staging registers.  Each lane loads the 16-byte chunk that
 //                belongs at its LDS slot, so the XOR layout is kept.  A counted
 //                wait for the wave's own loads of the step plus a bare barrier
 //                make every wave's loads visible; the same barrier proves that
 //                the buffer refilled next was finished by all waves.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int STAGES, int EPI, bool SPLIT>
-__global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ? 2 : 1) void gemm_kernel(
+template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int RING, int EPI, bool SPLIT>
+__global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && RING == 0) ? 2 : 1) void gemm_kernel(
     GemmArgs g, float* __restrict__ partial, int k_per_split) {
     constexpr int THREADS = WAVES_M * WAVES_N * 64;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
@@ -158,8 +159,9 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ?
     static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small");
     static_assert(WN % 64 == 0, "paired epilogues need whole 64-column pairs per wave");
 
-    __shared__ __attribute__((aligned(16))) bf16 As[STAGES][BM * BK];
-    __shared__ __attribute__((aligned(16))) bf16 Bs[STAGES][BN * BK];
+    constexpr int NBUF = RING == 0 ? 2 : RING;
+    __shared__ __attribute__((aligned(16))) bf16 As[NBUF][BM * BK];
+    __shared__ __attribute__((aligned(16))) bf16 Bs[NBUF][BN * BK];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
@@ -212,7 +214,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ?
         }
     };
 
-    if constexpr (STAGES == 2) {
+    if constexpr (RING == 0) {
         int a_off[A_LOADS], a_lds[A_LOADS];
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) {
@@ -260,7 +262,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ?
         constexpr int A_INS = BM / RPI / NW, B_INS = BN / RPI / NW;
         constexpr int PER_STEP = A_INS + B_INS;
         static_assert(BM % (RPI * NW) == 0 && BN % (RPI * NW) == 0, "direct loads must split evenly");
-        static_assert(STAGES == 3 || STAGES == 4, "the counted waits cover three or four stages");
+        static_assert(RING >= 2 && RING <= 4, "the counted waits cover rings of two to four buffers");
         const int r_in = lane / CPR, stored = lane % CPR;
         const bf16* a_src[A_INS];
         int a_dst[A_INS];
@@ -281,7 +283,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ?
             b_dst[i] = (wave + i * NW) * RPI * BK;
         }
         auto issue = [&](int kt) {
-            const int buf = kt % STAGES;
+            const int buf = kt % RING;
 #pragma unroll
             for (int i = 0; i < A_INS; ++i)
                 load_lds16(a_src[i] + kt * BK, &As[buf][a_dst[i]]);
@@ -290,18 +292,18 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * 64, (BK == 32 && STAGES == 2) ?
                 load_lds16(b_src[i] + kt * BK, &Bs[buf][b_dst[i]]);
         };
 #pragma unroll
-        for (int s = 0; s < STAGES - 1; ++s)
+        for (int s = 0; s < RING - 1; ++s)
             if (s < nk) issue(s);
         for (int kt = 0; kt < nk; ++kt) {
             // this wave's loads of step kt are done once at most the younger
-            // steps' loads (up to STAGES - 2 of them) are outstanding
-            const int younger = min(nk - 1 - kt, STAGES - 2);
-            if (younger >= STAGES - 2) wait_vmcnt<PER_STEP * (STAGES - 2)>();
-            else if (STAGES > 3 && younger == 1) wait_vmcnt<PER_STEP>();
+            // steps' loads (up to RING - 2 of them) are outstanding
+            const int younger = min(nk - 1 - kt, RING - 2);
+            if (RING >= 4 && younger >= 2) wait_vmcnt<2 * PER_STEP>();
+            else if (RING >= 3 && younger >= 1) wait_vmcnt<PER_STEP>();
             else wait_vmcnt<0>();
             barrier_only();
-            if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
-            compute(kt % STAGES);
+            if (kt + RING - 1 < nk) issue(kt + RING - 1);
+            compute(kt % RING);
         }
     }
 
@@ -556,21 +558,25 @@ __global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restri
 }
 
 struct TileCfg {
-    int bm, bn, waves_m, waves_n, bk, stages;
+    int bm, bn, waves_m, waves_n, bk, ring;  // ring 0: register-staged double buffer
 };
 // 0: 128x128 / 4 waves (64x64 each)      1: 64x128 / 4 waves (32x64)
 // 2: 32x256 / 4 waves (32x64)            3: 256x256 / 8 waves (128x64)
 // 4: 256x256 / 4 waves (128x128)         5: 128x256 / 8 waves (64x64)
 // 6: 256x128 / 4 waves (128x64), k 32    7: 128x256 / 4 waves (64x128), k 32
-// 8: 256x256 / 8 waves, k 32, 4-stage direct-load ring (128 KB of LDS)
-// 9: 128x256 / 8 waves, k 32, 4-stage ring (96 KB)
-// 10: 128x128 / 4 waves, k 32, 4-stage ring (64 KB: two work-groups per CU)
+// 8: 256x256 / 8 waves, k 32, 4-buffer direct-load ring (128 KB of LDS)
+// 9: 128x256 / 8 waves, k 32, 4-buffer ring (96 KB)
+// 10: 128x128 / 4 waves, k 32, 4-buffer ring (64 KB: two work-groups per CU)
+// 11: 256x256 / 8 waves, k 64, 2-buffer ring (128 KB)
+// 12: 256x256 / 4 waves (128x128), k 32, 4-buffer ring (128 KB)
+// 13: 256x256 / 4 waves (128x128), k 64, 2-buffer ring (128 KB)
 // The register-staged k-32 tiles (6, 7) use 48 KB of LDS, so two
 // work-groups share a CU and one's loads overlap the other's matrix work.
-constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 2}, {64, 128, 2, 2, 64, 2}, {32, 256, 1, 4, 64, 2},
-                             {256, 256, 2, 4, 64, 2}, {256, 256, 2, 2, 64, 2}, {128, 256, 2, 4, 64, 2},
-                             {256, 128, 2, 2, 32, 2}, {128, 256, 2, 2, 32, 2}, {256, 256, 2, 4, 32, 4},
-                             {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}};
+constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 0}, {64, 128, 2, 2, 64, 0}, {32, 256, 1, 4, 64, 0},
+                             {256, 256, 2, 4, 64, 0}, {256, 256, 2, 2, 64, 0}, {128, 256, 2, 4, 64, 0},
+                             {256, 128, 2, 2, 32, 0}, {128, 256, 2, 2, 32, 0}, {256, 256, 2, 4, 32, 4},
+                             {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}, {256, 256, 2, 4, 64, 2},
+                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int EPI>
@@ -638,18 +644,18 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 // the weight-streaming kernel up to 32 rows on the narrower projections,
 // 64-row tiles with split-K while weight streaming dominates, then whichever
 // tile measured fastest in each band of m; from m = 1600 on the 256 x 256
-// tile fed by the four-stage direct-load ring.  n must be a multiple of 128
-// and k of 64.
+// tile fed by a two-buffer direct-load ring of k-64 steps.  n must be a
+// multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     // Up to 32 rows the weight-streaming kernel wins on the narrower
     // projections (o, down: 12-16% at m <= 32, qkv even); on gate/up the
     // 64 x 128 tiles keep up with it.
     if (m <= 32 && n < 16384 && n % 64 == 0) return plan_with_cfg(kSkinnyCfg, m, n, k);
     int cfg;
-    if (k >= 8192) cfg = m <= 160 ? 1 : m < 450 ? 8 : m < 800 ? 10 : 8;                  // deep k (down)
-    else if (n >= 16384) cfg = m <= 160 ? 1 : m <= 400 ? 10 : m < 800 ? 1 : m < 1600 ? 7 : 8;  // gate/up
-    else if (n >= 6144) cfg = m <= 400 ? 1 : m < 1600 ? 0 : 8;                           // qkv
-    else cfg = m <= 400 ? 0 : m < 800 ? 1 : m < 1600 ? 10 : 8;                          // o
+    if (k >= 8192) cfg = m <= 160 ? 1 : m < 450 ? 8 : m < 800 ? 10 : 11;                 // deep k (down)
+    else if (n >= 16384) cfg = m <= 160 ? 1 : m <= 400 ? 10 : m < 800 ? 1 : m < 1600 ? 7 : 11;  // gate/up
+    else if (n >= 6144) cfg = m <= 400 ? 1 : m < 1600 ? 0 : 11;                          // qkv
+    else cfg = m <= 400 ? 0 : m < 800 ? 1 : m < 1600 ? 10 : 11;                         // o
     if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
     return plan_with_cfg(cfg, m, n, k);
 }
@@ -697,17 +703,20 @@ void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_
         return;
     }
     switch (p.cfg) {
-        case 0: launch_cfg<128, 128, 2, 2, 64, 2>(g, p, partial, s); break;
-        case 1: launch_cfg<64, 128, 2, 2, 64, 2>(g, p, partial, s); break;
-        case 2: launch_cfg<32, 256, 1, 4, 64, 2>(g, p, partial, s); break;
-        case 3: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
-        case 4: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
-        case 5: launch_cfg<128, 256, 2, 4, 64, 2>(g, p, partial, s); break;
-        case 6: launch_cfg<256, 128, 2, 2, 32, 2>(g, p, partial, s); break;
-        case 7: launch_cfg<128, 256, 2, 2, 32, 2>(g, p, partial, s); break;
+        case 0: launch_cfg<128, 128, 2, 2, 64, 0>(g, p, partial, s); break;
+        case 1: launch_cfg<64, 128, 2, 2, 64, 0>(g, p, partial, s); break;
+        case 2: launch_cfg<32, 256, 1, 4, 64, 0>(g, p, partial, s); break;
+        case 3: launch_cfg<256, 256, 2, 4, 64, 0>(g, p, partial, s); break;
+        case 4: launch_cfg<256, 256, 2, 2, 64, 0>(g, p, partial, s); break;
+        case 5: launch_cfg<128, 256, 2, 4, 64, 0>(g, p, partial, s); break;
+        case 6: launch_cfg<256, 128, 2, 2, 32, 0>(g, p, partial, s); break;
+        case 7: launch_cfg<128, 256, 2, 2, 32, 0>(g, p, partial, s); break;
         case 8: launch_cfg<256, 256, 2, 4, 32, 4>(g, p, partial, s); break;
         case 9: launch_cfg<128, 256, 2, 4, 32, 4>(g, p, partial, s); break;
-        default: launch_cfg<128, 128, 2, 2, 32, 4>(g, p, partial, s); break;
+        case 10: launch_cfg<128, 128, 2, 2, 32, 4>(g, p, partial, s); break;
+        case 11: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 12: launch_cfg<256, 256, 2, 2, 32, 4>(g, p, partial, s); break;
+        default: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
     }
 }
 
