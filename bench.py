@@ -7,9 +7,11 @@ are uniform in [512, 2048]; one prefill chunk C in {64, 128, 256, 512, 1024,
 2048} at prefix lengths P in {0, 2048, 8192}.  One step runs the 18 (C, P)
 mixed iterations once each; tokens/s counts the C + B rows of every iteration.
 
-Printed (one JSON line on stdout): throughput, per-point iteration ms and
-tokens/s, per-stage time with its roofline fraction (HIP events recorded by
-the library on the iteration's stream over the timed region), the roofline
+Printed (one JSON line on stdout): throughput (wall clock over K steps of the
+iterations alone), per-point iteration ms and tokens/s, per-stage time with
+its roofline fraction (HIP events recorded by the library on the iteration's
+stream over a second timed pass of the same K steps, whose wall time is
+reported as instrumented_ms_per_step), the roofline
 entry of the dominant kernel, the oracle timed on the host cores on a bounded
 sample, the cost table profiled over (B, C) with its monotonicity, and the
 controller's per-decision time.
@@ -249,15 +251,24 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: per-stage HIP events recorded on the iteration stream
+    # timed region 1 (the reported throughput): the iterations alone
     n_iter = args.steps * len(points)
-    ctx.set_stage_timing(n_iter)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    # timed region 2: the same steps again with per-stage HIP events recorded
+    # by the library on the iteration stream (per-stage times, roofline); the
+    # events cost some throughput, so this pass is reported separately
+    ctx.set_stage_timing(n_iter)
+    torch.cuda.synchronize()
+    t_ev = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed_ev = time.perf_counter() - t_ev
     stage_ms = [ctx.stage_times(ago) for ago in range(n_iter)][::-1]  # oldest first
     ctx.set_stage_timing(0)
 
@@ -354,6 +365,8 @@ def main():
 
     out = {"metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+           "instrumented_ms_per_step": round(elapsed_ev * 1e3 / args.steps, 4),
+           "kernel_ms_per_step": round(sum(stage_tot.values()) / args.steps, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
            "config": {"workload": WORKLOADS[args.workload], "block_size": 16,
