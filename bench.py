@@ -378,7 +378,7 @@ def main():
 
 SERVE_C_GRID = [0, 32, 64, 128, 256, 512, 1024, 2048, 4096]
 SERVE_B_GRID = [0, 1, 2, 4, 8, 16, 32, 64, 128, 256]
-SERVE_POLICIES = [("sloweave", 0), ("fixed", 256), ("fixed", 512), ("fixed", 2048)]
+SERVE_POLICIES = [("sloweave", 0, 0), ("sloweave", 0, 64), ("fixed", 256, 0), ("fixed", 512, 0), ("fixed", 2048, 0)]
 
 
 def serve_main(args):
@@ -417,11 +417,11 @@ def serve_main(args):
     sim_table = api.CostTable.analytic(SERVE_C_GRID, SERVE_B_GRID)
     runs = []
     for D in (25.0, 10.0):
-        for pol, fc in SERVE_POLICIES:
-            name = "SLOWeave" if pol == "sloweave" else f"Fixed-{fc}"
+        for pol, fc, window in SERVE_POLICIES:
+            name = (("SLOWeave+telemetry" if window else "SLOWeave") if pol == "sloweave" else f"Fixed-{fc}")
             t2 = time.time()
             res = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
-                              table=ct, session=sess)
+                              table=ct, session=sess, residual_window=window)
             wall = time.time() - t2
             m = serving.metrics(trace, res.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
             it = res.iterations
@@ -437,9 +437,12 @@ def serve_main(args):
                    "iteration_ms_p50": round(float(np.median(dur)) / 1e6, 3),
                    "measured_over_predicted_p50": round(float(np.median(rel)), 4) if ok.any() else None,
                    "measured_over_predicted_p99": round(float(np.quantile(rel, 0.99)), 4) if ok.any() else None,
-                   "decide_ns_p50": int(np.median(it["decide_ns"])), "decide_ns_p99": int(np.quantile(it["decide_ns"], 0.99))}
+                   "decide_ns_p50": int(np.median(it["decide_ns"])), "decide_ns_p99": int(np.quantile(it["decide_ns"], 0.99)),
+                   "residual_window": window,
+                   "telemetry_margin_ppm_p50": int(np.median(it["rel_margin_ppm"][it["remaining"] > 0]))
+                   if np.any(it["remaining"] > 0) else 0}
             sim = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
-                              table=sim_table)
+                              table=sim_table, residual_window=window)
             sm = serving.metrics(trace, sim.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
             run["analytic_simulator"] = {k: round(sm[k], 4) for k in ("goodput_req_s", "slo_attainment",
                                                                       "p99_ttft_ms", "p99_tpot_ms")}
@@ -449,10 +452,15 @@ def serve_main(args):
                 f"{wall:.1f}s")
     best = {D: max((r for r in runs if r["tpot_slo_ms"] == D and r["policy"] != "SLOWeave"),
                    key=lambda r: r["goodput_req_s"]) for D in (25.0, 10.0)}
-    slw = {D: next(r for r in runs if r["tpot_slo_ms"] == D and r["policy"] == "SLOWeave") for D in (25.0, 10.0)}
-    gain = {f"{D:g}ms": {"vs": best[D]["policy"],
-                         "ratio": round(slw[D]["goodput_req_s"] / best[D]["goodput_req_s"], 3)
-                         if best[D]["goodput_req_s"] > 0 else None} for D in (25.0, 10.0)}
+    gain = {}
+    for name in ("SLOWeave", "SLOWeave+telemetry"):
+        for D in (25.0, 10.0):
+            mine = next(r for r in runs if r["tpot_slo_ms"] == D and r["policy"] == name)
+            gain[f"{name} {D:g}ms"] = {"vs": best[D]["policy"],
+                                       "ratio": round(mine["goodput_req_s"] / best[D]["goodput_req_s"], 3)
+                                       if best[D]["goodput_req_s"] > 0 else None}
+    slw = {D: next(r for r in runs if r["tpot_slo_ms"] == D and r["policy"] == "SLOWeave+telemetry")
+           for D in (25.0, 10.0)}
     out = {"metric": "goodput (requests meeting TTFT 1000 ms and TPOT SLOs per second of arrival span)",
            "value": slw[25.0]["goodput_req_s"], "unit": "req/s", "n_gpus": 1, "higher_is_better": True,
            "dtype": "bf16", "data": "synthetic",

@@ -331,6 +331,7 @@ typedef struct slw_request {
 
 #define SLW_EXEC_GPU 0        /* run each iteration with slw_mixed_iteration        */
 #define SLW_EXEC_ANALYTIC 1   /* advance a virtual clock by the Sec. 4.1 cost model */
+#define SLW_EXEC_TABLE 2      /* advance a virtual clock by opts->exec_table         */
 
 /* flags of an iteration record besides those of slw_select_chunk */
 #define SLW_SERVE_KV_WAIT 0x100u      /* the oldest prompt waits for KV blocks      */
@@ -354,6 +355,16 @@ typedef struct slw_serve_opts {
     void* ws;                /* workspace for (chunk cap, max_decode)                   */
     size_t ws_bytes;
     void* stream;
+    /* Telemetry margin (Sec. 3.3 proposes a margin taken from a high
+     * percentile of observed prediction errors; Sec. 5.1 feeds observed
+     * durations back to the controller).  After every
+     * iteration that ran a chunk priced by `table`, the relative residual
+     * floor((observed - predicted) * 1e6 / predicted) ppm enters a window of
+     * the last residual_window such values; each SLOWeave decision then adds
+     * ceil(q * T_hat(n, c) / 1e6) to the prediction, q = max(0, nearest-rank
+     * P99 of the window).  0 = off. */
+    int32_t residual_window;
+    const slw_cost_table* exec_table;  /* SLW_EXEC_TABLE: the iteration times */
 } slw_serve_opts;
 
 /* One iteration of a serving run (host memory). */
@@ -369,6 +380,7 @@ typedef struct slw_iteration_record {
     int32_t remaining;    /* prompt tokens of the oldest eligible prompt before the chunk
                              (0 when none may run)                                       */
     uint32_t flags;       /* SLW_FLAG_* of the decision | SLW_SERVE_*                    */
+    int64_t rel_margin_ppm; /* telemetry margin q used by the decision (0 when off)       */
 } slw_iteration_record;
 
 /*
@@ -381,7 +393,9 @@ typedef struct slw_iteration_record {
  * max_decode requests decode and (GPU) while the pool can hold every
  * admitted request to its last token.  With no eligible work the clock
  * moves to the next arrival (SLW_EXEC_ANALYTIC, or skip_idle) or waits for
- * it.  The GPU executor synchronises `stream` after every iteration, creates
+ * it.  The table executor advances the clock by exec_table's T_hat(n, c)
+ * (a stand-in for hardware whose cost differs from the controller's table).
+ * The GPU executor synchronises `stream` after every iteration, creates
  * a KV sequence per request when its prompt starts and frees it when its
  * last token is out; ctx may be NULL with SLW_EXEC_ANALYTIC.
  *   reqs       host [n], any order, distinct ids

@@ -30,7 +30,16 @@ Readings (the paper is silent or ambiguous here):
   while fewer than that many requests decode (the prefill in flight is the
   only way the decode set grows, so the cap holds at all times);
 * a decode set larger than the cost table's last decode-batch point cannot
-  be priced: the iteration is decode-only.
+  be priced: the iteration is decode-only;
+* the telemetry margin (Sec. 3.3 proposes a margin taken from a high
+  percentile of observed prediction errors; Sec. 5.1 feeds observed
+  durations back to the controller) is relative:
+  every iteration that ran a chunk leaves the residual
+  floor((observed - predicted) * 1e6 / predicted) in parts per million, the
+  last W of them form the window, and a decision adds
+  ceil(q * T_hat(n, c) / 1e6) to every prediction it tests, q being the
+  nearest-rank P99 of the window clamped to [0, 1e8] (0 while the window is
+  empty).
 """
 from __future__ import annotations
 
@@ -55,6 +64,7 @@ class Iteration:
     n_decode: int
     prefill_rid: int     # -1 when the iteration runs no chunk
     budget_ns: int       # earliest deadline minus start (0 with no active decode)
+    rel_margin_ppm: int = 0  # telemetry margin used by the decision
 
 
 @dataclass
@@ -65,7 +75,8 @@ class Trace:
 
 def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed_chunk: int = 0,
              predict=None, c_last: int | None = None, c_max: int = 4096, margin_ns: int = 0,
-             max_decode: int | None = None, max_iterations: int = 10_000_000) -> Trace:
+             max_decode: int | None = None, residual_window: int = 0,
+             max_iterations: int = 10_000_000) -> Trace:
     """Run the trace through the iteration-level loop of Sec. 4.1.
 
     cost_ns(n, c) -> ns is how long an iteration with n decodes and a chunk
@@ -73,6 +84,7 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
     what the SLOWeave controller believes (defaults to cost_ns) and c_last
     the largest chunk it can price.  policy is "sloweave" (Alg. 1 with margin
     margin_ns and cap c_max) or "fixed" (chunks of fixed_chunk tokens).
+    residual_window > 0 turns on the telemetry margin (module docstring).
     """
     if policy not in ("sloweave", "fixed"):
         raise ValueError(policy)
@@ -87,6 +99,7 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
     t = reqs[0].arrival_ns if reqs else 0
     nxt = 0
     finished = 0
+    residuals = []          # relative residuals (ppm) of chunked iterations, oldest first
     for _ in range(max_iterations):
         if finished == len(reqs):
             return out
@@ -103,17 +116,28 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
         head = pending[0] if pending and (max_decode is None or n < max_decode) else None
         remaining = head.prompt - done_prompt[head.rid] if head else 0
         budget = min(deadlines) - t if deadlines else 0
+        rel = 0
         if head is None:
             chunk = 0
         elif policy == "fixed":
             chunk = min(fixed_chunk, remaining)
         else:
+            if residual_window > 0 and residuals:
+                rel = min(max(nearest_rank(residuals[-residual_window:], 99, 100), 0), 10**8)
+
+            def with_margin(nn, cc, q=rel):
+                v = predict(nn, cc)
+                return v + -(-q * v // 10**6)   # T_hat + ceil(q T_hat / 1e6)
             try:
-                chunk = select_chunk(predict, deadlines, t, remaining, c_max, margin_ns, c_last=c_last)[0]
+                chunk = select_chunk(with_margin, deadlines, t, remaining, c_max, margin_ns, c_last=c_last)[0]
             except IndexError:                 # n above the priced decode batches
                 chunk = 0
         end = t + cost_ns(n, chunk)
-        out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget))
+        out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget, rel))
+        if residual_window > 0 and chunk > 0:
+            pred = predict(n, chunk)
+            if pred > 0:
+                residuals.append((end - t - pred) * 10**6 // pred)
         for rid in order:
             req, _ = active[rid]
             out.token_ns[rid].append(end)

@@ -82,18 +82,19 @@ class ServeOpts(C.Structure):
                 ("max_decode", C.c_int32), ("tpot_ns", C.c_int64), ("margin_ns", C.c_int64),
                 ("table", C.c_void_p), ("executor", C.c_int32), ("skip_idle", C.c_int32),
                 ("x_in", C.c_void_p), ("x_out", C.c_void_p), ("max_rows", C.c_int32),
-                ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p)]
+                ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p),
+                ("residual_window", C.c_int32), ("exec_table", C.c_void_p)]
 
 
 class IterationRecord(C.Structure):
     _fields_ = [("start_ns", C.c_int64), ("end_ns", C.c_int64), ("budget_ns", C.c_int64),
                 ("decide_ns", C.c_int64), ("predicted_ns", C.c_int64), ("prefill_id", C.c_int64),
                 ("chunk", C.c_int32), ("n_decode", C.c_int32), ("remaining", C.c_int32),
-                ("flags", C.c_uint32)]
+                ("flags", C.c_uint32), ("rel_margin_ppm", C.c_int64)]
 
 
 POLICY_SLOWEAVE, POLICY_FIXED = 0, 1
-EXEC_GPU, EXEC_ANALYTIC = 0, 1
+EXEC_GPU, EXEC_ANALYTIC, EXEC_TABLE = 0, 1, 2
 SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED = 0x100, 0x200, 0x400
 
 _lib = None
@@ -262,7 +263,7 @@ def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_
 ITERATION_DTYPE = np.dtype([("start_ns", np.int64), ("end_ns", np.int64), ("budget_ns", np.int64),
                             ("decide_ns", np.int64), ("predicted_ns", np.int64), ("prefill_id", np.int64),
                             ("chunk", np.int32), ("n_decode", np.int32), ("remaining", np.int32),
-                            ("flags", np.uint32)])
+                            ("flags", np.uint32), ("rel_margin_ppm", np.int64)])
 assert ITERATION_DTYPE.itemsize == C.sizeof(IterationRecord)
 
 
@@ -270,7 +271,8 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
           fixed_chunk: int = 0, c_max: int = 4096, margin_ns: int = 0, table: CostTable | None = None,
           executor: int = EXEC_ANALYTIC, ctx: "Context | None" = None, skip_idle: bool = True,
           x_in: int = 0, x_out: int = 0, max_rows: int = 0, ws: int = 0, ws_bytes: int = 0,
-          stream: int = 0, iter_cap: int | None = None):
+          stream: int = 0, iter_cap: int | None = None, residual_window: int = 0,
+          exec_table: CostTable | None = None):
     """slw_serve over a trace given as arrays.
 
     Returns (token_ns, iterations): token_ns is a list of int64 arrays, one per
@@ -287,7 +289,8 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
     its = np.zeros(max(cap, 1), ITERATION_DTYPE)
     o = ServeOpts(policy, fixed_chunk, c_max, max_decode, int(tpot_ns), int(margin_ns),
                   table.handle if table is not None else None, executor, int(skip_idle),
-                  x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None)
+                  x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None,
+                  residual_window, exec_table.handle if exec_table is not None else None)
     nit = C.c_int64()
     _check(lib().slw_serve(ctx._h if ctx is not None else None, reqs, n, C.byref(o), _ptr(tok, C.c_int64),
                            len(tok), its.ctypes.data_as(C.POINTER(IterationRecord)), len(its), C.byref(nit)))

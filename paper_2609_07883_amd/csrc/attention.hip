@@ -67,9 +67,12 @@ __device__ __forceinline__ int vswz(int d, int h) { return h ^ ((d >> 2) & 1); }
 // lds + 16 l (lds is wave-uniform).  Issued as assembly so that the compiler,
 // which cannot tell which LDS buffer such a load writes, does not make every
 // later LDS read wait for all of them; the kernel waits for them itself.
+// M0 is a reserved register that the compiler sets right before each
+// instruction that reads it; no compiler-generated code in these kernels
+// uses it, so the value left there is never relied on.
 __device__ __forceinline__ void load_lds16(const void* src, void* lds) {
     const uint32_t dst = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst) : "memory", "m0");
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(dst) : "memory");
 }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.

@@ -15,7 +15,6 @@
 #include "common.h"
 
 namespace slw {
-namespace {
 
 // Nearest-rank percentile num/den: sorted[ceil(k*num/den) - 1].
 int64_t nearest_rank(std::vector<int64_t>& xs, int64_t num, int64_t den) {
@@ -25,6 +24,8 @@ int64_t nearest_rank(std::vector<int64_t>& xs, int64_t num, int64_t den) {
     if (rank < 1) rank = 1;
     return xs[rank - 1];
 }
+
+namespace {
 
 int check_grids(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb) {
     if (!c_grid || !b_grid || nc < 1 || nb < 1) return fail(SLW_EINVAL, "empty grid");
@@ -238,14 +239,17 @@ extern "C" int slw_cost_table_load(const char* path, slw_cost_table** out) {
     });
 }
 
-extern "C" int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
-                                int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
-                                int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
+namespace slw {
+
+int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
+                      int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm, int32_t* chunk,
+                      uint32_t* flags, int32_t* n_lookups) {
     if (!t || !chunk || !flags) return fail(SLW_EINVAL, "null argument");
     *chunk = 0;
     *flags = 0;
     if (n_lookups) *n_lookups = 0;
     if (n_active < 0 || (n_active > 0 && !deadlines_ns)) return fail(SLW_EINVAL, "bad active set");
+    if (rel_margin_ppm < 0 || rel_margin_ppm > 100000000) return fail(SLW_ERANGE, "relative margin out of range");
     if (remaining <= 0) {  // no pending prefill
         *flags = SLW_FLAG_NO_PENDING;
         return SLW_OK;
@@ -268,19 +272,33 @@ extern "C" int slw_select_chunk(const slw_cost_table* t, const int64_t* deadline
     int64_t earliest = deadlines_ns[0];
     for (int32_t i = 1; i < n_active; ++i) earliest = std::min(earliest, deadlines_ns[i]);
     const int64_t budget = earliest - now_ns;
+    // predicted time plus the relative margin ceil(rel * T_hat / 1e6) (monotone in c like T_hat)
+    auto predict = [&](int32_t c) {
+        const int64_t v = lookup_row(t, row, c);
+        return v + (rel_margin_ppm * v + 999999) / 1000000;
+    };
     int32_t lo = 0, hi = cap, lookups = 0;
     while (lo < hi) {
         int32_t mid = lo + (hi - lo + 1) / 2;  // floor((lo + hi + 1) / 2) without overflow
         ++lookups;
-        if (lookup_row(t, row, mid) + margin_ns <= budget) lo = mid;
+        if (predict(mid) + margin_ns <= budget) lo = mid;
         else hi = mid - 1;
     }
     if (lo == 0) {
         ++lookups;
-        if (lookup_row(t, row, 0) + margin_ns > budget) fl |= SLW_FLAG_DECODE_INFEASIBLE;
+        if (predict(0) + margin_ns > budget) fl |= SLW_FLAG_DECODE_INFEASIBLE;
     }
     *chunk = lo;
     *flags = fl;
     if (n_lookups) *n_lookups = lookups;
     return SLW_OK;
+}
+
+}  // namespace slw
+
+extern "C" int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
+                                int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
+                                int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
+    return slw::select_chunk_core(t, deadlines_ns, n_active, now_ns, remaining, c_max, margin_ns, 0, chunk, flags,
+                                  n_lookups);
 }

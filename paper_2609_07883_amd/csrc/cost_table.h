@@ -22,6 +22,17 @@ namespace slw {
 // Validates grids, fills the percentiles and the running maximum.  SLW_* code.
 int finish_table(slw_cost_table* t);
 
+// Nearest-rank percentile num/den of xs (sorted in place): sorted[ceil(k num/den) - 1].
+int64_t nearest_rank(std::vector<int64_t>& xs, int64_t num, int64_t den);
+
+// Alg. 1 with the margin of Sec. 3.3 split into an absolute part (ns) and a
+// part relative to the prediction: a chunk c is admissible when
+// T_hat(n, c) + ceil(rel_margin_ppm * T_hat(n, c) / 1e6) + margin_ns <= budget.
+// slw_select_chunk is this with rel_margin_ppm = 0.
+int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
+                      int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm, int32_t* chunk,
+                      uint32_t* flags, int32_t* n_lookups);
+
 // The simulator's default cost model (Sec. 4.1), in ns:
 // T(n, c) = 0.35 + 1[n>0](0.90 + 0.055 n) + 1[c>0](0.40 + 0.006 c) ms.
 int64_t analytic_iteration_ns(int32_t n, int32_t c);

@@ -53,8 +53,11 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         return fail(SLW_EINVAL, "SLOWeave needs a cost table and c_max >= 1");
     if (o->max_decode < 1) return fail(SLW_EINVAL, "max_decode must be >= 1");
     if (o->tpot_ns <= 0 || o->margin_ns < 0) return fail(SLW_EINVAL, "bad TPOT objective or margin");
-    if (o->executor != SLW_EXEC_GPU && o->executor != SLW_EXEC_ANALYTIC)
+    if (o->executor != SLW_EXEC_GPU && o->executor != SLW_EXEC_ANALYTIC && o->executor != SLW_EXEC_TABLE)
         return fail(SLW_EINVAL, "unknown executor %d", o->executor);
+    if (o->executor == SLW_EXEC_TABLE && !o->exec_table) return fail(SLW_EINVAL, "table executor needs exec_table");
+    if (o->residual_window < 0 || o->residual_window > 65536)
+        return fail(SLW_ERANGE, "residual_window must be in [0, 65536]");
     if (o->executor == SLW_EXEC_GPU) {
         if (!ctx || !o->x_in || !o->x_out || !o->ws) return fail(SLW_EINVAL, "GPU executor needs ctx and buffers");
         const int64_t cap = o->policy == SLW_POLICY_FIXED ? o->fixed_chunk : o->c_max;
@@ -119,6 +122,10 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
 
     std::vector<int64_t> dec_ids, deadlines;
     std::vector<int32_t> ctx_lens;
+    // telemetry: relative residuals (ppm) of the last residual_window chunked iterations
+    const int32_t W = o->residual_window;
+    std::vector<int64_t> resid(std::max(W, 1)), scratch;
+    int64_t n_resid = 0;
     const hipStream_t stream = static_cast<hipStream_t>(o->stream);
 
     while (finished < n) {
@@ -176,9 +183,15 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             if (o->policy == SLW_POLICY_FIXED) {
                 chunk = std::min(o->fixed_chunk, remaining);
             } else {
+                int64_t rel = 0;
+                if (W > 0 && n_resid > 0) {
+                    scratch.assign(resid.begin(), resid.begin() + std::min<int64_t>(n_resid, W));
+                    rel = std::min<int64_t>(std::max<int64_t>(nearest_rank(scratch, 99, 100), 0), 100000000);
+                }
+                rec.rel_margin_ppm = rel;
                 uint32_t fl = 0;
-                rc = slw_select_chunk(o->table, deadlines.data(), nd, t, remaining, o->c_max, o->margin_ns, &chunk,
-                                      &fl, nullptr);
+                rc = select_chunk_core(o->table, deadlines.data(), nd, t, remaining, o->c_max, o->margin_ns, rel,
+                                       &chunk, &fl, nullptr);
                 if (rc == SLW_ERANGE) {  // more decodes than the table prices
                     clear_error();
                     chunk = 0;
@@ -217,13 +230,25 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             if (hipStreamSynchronize(stream) != hipSuccess)
                 return fail(SLW_EHIP, "stream synchronisation failed after iteration %lld",
                             static_cast<long long>(*n_iters));
-        } else {
+        } else if (o->executor == SLW_EXEC_ANALYTIC) {
             virt = t + analytic_iteration_ns(nd, chunk);
+        } else {
+            int64_t dt = 0;
+            rc = slw_cost_table_lookup(o->exec_table, nd, chunk, &dt);
+            if (rc) return rc;
+            virt = t + dt;
         }
         const int64_t end = now();
         rec.end_ns = end;
         if (chunk > 0) rec.prefill_id = reqs[head->req].id;
         iters[(*n_iters)++] = rec;
+        if (W > 0 && chunk > 0 && rec.predicted_ns > 0) {
+            const int64_t num = (end - t - rec.predicted_ns) * 1000000;
+            int64_t q = num / rec.predicted_ns;
+            if (num % rec.predicted_ns != 0 && num < 0) --q;  // floor
+            resid[n_resid % W] = q;
+            ++n_resid;
+        }
 
         // decodes: one token each
         for (auto it = active.begin(); it != active.end();) {

@@ -33,11 +33,13 @@ class RunResult:
 
 
 def run(trace, *, policy: str, tpot_ms: float, max_decode: int, fixed_chunk: int = 0, c_max: int = 4096,
-        margin_ns: int = 0, table: api.CostTable | None = None, session=None, skip_idle: bool = True) -> RunResult:
+        margin_ns: int = 0, table: api.CostTable | None = None, session=None, skip_idle: bool = True,
+        residual_window: int = 0, exec_table: api.CostTable | None = None) -> RunResult:
     """Serve `trace` (synth.RequestTrace; request ids are 0..n-1).
 
     session (runtime.Session) selects the GPU executor; without it the loop
-    runs on the analytic cost model.
+    runs on exec_table's iteration times if given, else on the analytic cost
+    model.  residual_window > 0 turns on the telemetry margin.
     """
     pol = {"sloweave": api.POLICY_SLOWEAVE, "fixed": api.POLICY_FIXED}[policy]
     kw = {}
@@ -46,10 +48,12 @@ def run(trace, *, policy: str, tpot_ms: float, max_decode: int, fixed_chunk: int
                   x_in=session.x_in.data_ptr(), x_out=session.x_out.data_ptr(),
                   max_rows=session.x_in.shape[0], ws=session.ws.data_ptr(), ws_bytes=session.ws_bytes,
                   stream=session.stream())
+    elif exec_table is not None:
+        kw = dict(executor=api.EXEC_TABLE, exec_table=exec_table)
     n = len(trace)
     tok, its = api.serve(np.arange(n), trace.arrival_ns, trace.prompt, trace.output, policy=pol,
                          tpot_ns=int(round(tpot_ms * 1e6)), max_decode=max_decode, fixed_chunk=fixed_chunk,
-                         c_max=c_max, margin_ns=margin_ns, table=table, **kw)
+                         c_max=c_max, margin_ns=margin_ns, table=table, residual_window=residual_window, **kw)
     return RunResult(tok, its)
 
 

@@ -97,3 +97,35 @@ def test_kv_wait_when_the_pool_is_small(setup):
     torch.cuda.synchronize()
     _check_run(sess, tr, res, 16)
     assert np.any(res.iterations["flags"] & api.SERVE_KV_WAIT)
+
+
+def test_telemetry_margin_on_gpu(setup):
+    """With the telemetry window on, every decision's margin is the nearest-rank
+    P99 of the relative residuals of the chunked iterations before it (recomputed
+    from the records), and the chunk is Alg. 1 on the widened predictions."""
+    sess, ct, tr = setup
+    W = 8
+    res = serving.run(tr, policy="sloweave", tpot_ms=3.0, max_decode=16, c_max=256, table=ct,
+                      residual_window=W, session=sess)
+    torch.cuda.synchronize()
+    _check_run(sess, tr, res, 16)
+    ot = S.CostTable(C_GRID, B_GRID, ct.values(api.TABLE_SAMPLES).tolist())
+    resid = []
+    checked = 0
+    for r in res.iterations:
+        if r["remaining"] > 0:
+            q = min(max(S.nearest_rank(resid[-W:], 99, 100), 0), 10**8) if resid else 0
+            assert int(r["rel_margin_ppm"]) == q
+            n = int(r["n_decode"])
+
+            def widened(nn, cc, q=q):
+                v = ot.lookup(nn, cc)
+                return v + -(-q * v // 10**6)
+            exp = S.select_chunk(widened, [int(r["start_ns"] + r["budget_ns"])] * n, int(r["start_ns"]),
+                                 int(r["remaining"]), 256, 0, c_last=C_GRID[-1])
+            assert int(r["chunk"]) == exp[0]
+            checked += 1
+        if r["chunk"] > 0 and r["predicted_ns"] > 0:
+            pred = int(r["predicted_ns"])
+            resid.append((int(r["end_ns"]) - int(r["start_ns"]) - pred) * 10**6 // pred)
+    assert checked > 10

@@ -180,3 +180,56 @@ def test_trace_generator_shape():
     no_burst = synth.request_trace(4000, 4.0, seed=3, burst_factor=1.0)
     assert abs(no_burst.arrival_ns[-1] / 1e9 - 1000) < 60            # Poisson at 4/s
     assert t.arrival_ns[-1] < no_burst.arrival_ns[-1]                 # bursts add arrivals
+
+
+def test_telemetry_margin_is_inert_with_exact_predictions():
+    """Residuals of an exact predictor are 0, so the margin stays 0 and the run is unchanged."""
+    reqs = _small_trace(80, 60.0, seed=21)
+    base = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, max_decode=64)
+    tele = V.simulate(reqs, cost_ns=S.analytic_cost_ns, tpot_ns=10 * MS, max_decode=64, residual_window=16)
+    assert base.token_ns == tele.token_ns
+    assert all(i.rel_margin_ppm == 0 for i in tele.iterations)
+
+
+def _slow_hw(n, c):
+    """Hardware 20% slower than the analytic table (every T is a multiple of 1000 ns)."""
+    return S.analytic_cost_ns(n, c) * 6 // 5
+
+
+def test_telemetry_margin_restores_deadlines_on_slow_hardware():
+    """Sec. 3.3: a margin bounding the one-sided prediction error keeps Prop. 1.
+    With iterations 20% slower than predicted, the plain controller overruns
+    the objective; with the telemetry window the first chunked iteration
+    leaves a residual of exactly 200000 ppm, every later decision adds 20% to
+    its predictions, and no token gap exceeds D."""
+    reqs = _small_trace(150, 60.0, seed=11)
+    D = 10 * MS
+    assert _slow_hw(64, 0) <= D
+    plain = V.simulate(reqs, cost_ns=_slow_hw, predict=S.analytic_cost_ns, tpot_ns=D, max_decode=64)
+    gaps = [b - a for t in plain.token_ns.values() for a, b in zip(t, t[1:])]
+    assert max(gaps) > D
+    tele = V.simulate(reqs, cost_ns=_slow_hw, predict=S.analytic_cost_ns, tpot_ns=D, max_decode=64,
+                      residual_window=16)
+    gaps = [b - a for t in tele.token_ns.values() for a, b in zip(t, t[1:])]
+    assert max(gaps) <= D
+    first = next(k for k, i in enumerate(tele.iterations) if i.chunk > 0)
+    assert tele.iterations[first].rel_margin_ppm == 0
+    later = [i.rel_margin_ppm for i in tele.iterations[first + 1:] if i.chunk > 0 or i.n_decode == 0]
+    assert later and all(q == 200_000 for q in later if q)
+
+
+def test_telemetry_window_uses_nearest_rank_p99():
+    """The margin is the nearest-rank P99 of the last W residuals: with W = 2
+    it is the larger of the last two."""
+    reqs = [R(0, 0, 300, 1)]
+    costs = iter([1_000_000, 2_000_000, 1_500_000])   # ns of the three chunked iterations
+    observed = {}
+
+    def hw(n, c):
+        return observed.setdefault((n, c, len(observed)), next(costs))
+
+    tr = V.simulate(reqs, cost_ns=lambda n, c: hw(n, c), predict=lambda n, c: 1_000_000, tpot_ns=MS,
+                    policy="sloweave", c_max=100, residual_window=2)
+    assert [i.chunk for i in tr.iterations] == [100, 100, 100]
+    # residuals: 0, 1e6 ppm, 0.5e6 ppm; margins seen by the 2nd and 3rd decisions
+    assert [i.rel_margin_ppm for i in tr.iterations] == [0, 0, 1_000_000]

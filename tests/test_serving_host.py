@@ -1,4 +1,4 @@
-"""The library's serving loop against the serving oracle (CPU, analytic executor).
+"""The library's serving loop against the serving oracle (CPU: analytic and table executors).
 
 slw_serve with the analytic executor is the Sec. 4.1 simulator; every token
 time and every iteration (start, end, chunk, decode count, prefill request,
@@ -38,8 +38,10 @@ def _compare(tr, res, ref):
         assert toks.tolist() == ref.token_ns[i], f"request {i}"
     it = res.iterations
     assert len(it) == len(ref.iterations)
-    got = np.stack([it["start_ns"], it["end_ns"], it["chunk"], it["n_decode"], it["prefill_id"], it["budget_ns"]], 1)
-    exp = np.array([[r.start_ns, r.end_ns, r.chunk, r.n_decode, r.prefill_rid, r.budget_ns] for r in ref.iterations])
+    got = np.stack([it["start_ns"], it["end_ns"], it["chunk"], it["n_decode"], it["prefill_id"], it["budget_ns"],
+                    it["rel_margin_ppm"]], 1)
+    exp = np.array([[r.start_ns, r.end_ns, r.chunk, r.n_decode, r.prefill_rid, r.budget_ns, r.rel_margin_ppm]
+                    for r in ref.iterations])
     bad = np.nonzero((got != exp).any(1))[0]
     assert len(bad) == 0, f"first differing iteration {bad[0]}: {got[bad[0]]} vs {exp[bad[0]]}"
 
@@ -125,6 +127,41 @@ def test_sloweave_beats_fixed_at_tight_tpot_in_simulation():
     assert good[("sloweave", 0)] >= max(v for k, v in good.items() if k[0] == "fixed")
 
 
+def _scaled_tables(cg, bg, num, den):
+    """Controller table (analytic) and a hardware stand-in num/den slower, both as the
+    library's tables and the oracle's."""
+    vals = [[S.analytic_cost_ns(b, c) * num // den for c in cg] for b in bg]
+    return (api.CostTable.analytic(cg, bg), api.CostTable.from_samples(cg, bg, np.array(vals, dtype=np.int64)),
+            _oracle_table(cg, bg), S.CostTable.from_values(cg, bg, vals))
+
+
+@pytest.mark.parametrize("window,num,den,margin_ms", [(16, 6, 5, 0), (1, 5, 4, 0), (64, 11, 10, 1), (8, 9, 10, 0)])
+def test_telemetry_margin_matches_oracle(window, num, den, margin_ms):
+    """The relative-residual window, its P99 and the widened predictions are
+    the oracle's bit for bit, on hardware faster or slower than the table."""
+    tr = _trace(250, 6.0, seed=8)
+    ctl, hw, octl, ohw = _scaled_tables(COARSE_C, COARSE_B, num, den)
+    res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=256, table=ctl, exec_table=hw,
+                      residual_window=window, margin_ns=margin_ms * MS)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=ohw.lookup, predict=octl.lookup, c_last=COARSE_C[-1],
+                     tpot_ns=25 * MS, max_decode=256, residual_window=window, margin_ns=margin_ms * MS)
+    _compare(tr, res, ref)
+    if num > den:
+        assert res.iterations["rel_margin_ppm"].max() > 0
+
+
+def test_telemetry_margin_cuts_deadline_misses():
+    tr = _trace(300, 6.0, seed=9)
+    ctl, hw, _, _ = _scaled_tables(COARSE_C, COARSE_B, 6, 5)
+    miss = {}
+    for w in (0, 32):
+        res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=256, table=ctl, exec_table=hw,
+                          residual_window=w)
+        gaps = np.concatenate([np.diff(t) for t in res.token_ns if len(t) > 1])
+        miss[w] = int(np.sum(gaps > 25 * MS))
+    assert miss[0] > 0 and miss[32] < miss[0]
+
+
 def test_errors():
     tr = _trace(10, 4.0, seed=1)
     with pytest.raises(api.SloweaveError) as e:
@@ -146,3 +183,11 @@ def test_errors():
     assert e.value.code == api.EINVAL
     tok, its = api.serve([], [], [], [], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4)
     assert tok == [] and len(its) == 0
+    with pytest.raises(api.SloweaveError) as e:      # table executor without its table
+        api.serve([0], [0], [4], [1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4,
+                  executor=api.EXEC_TABLE)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.SloweaveError) as e:
+        api.serve([0], [0], [4], [1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4,
+                  residual_window=-1)
+    assert e.value.code == api.ERANGE
