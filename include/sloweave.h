@@ -251,11 +251,26 @@ typedef struct slw_profile_opts {
  */
 int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
                          int32_t nb, const slw_profile_opts* opts, slw_cost_table** out);
+/*
+ * The same with a cached-context axis (Sec. 5.1 indexes the runtime's table
+ * by decode batch, cached context and chunk): one (b, c) plane per entry of
+ * p_grid (strictly increasing, >= 0), each profiled with the chunk's sequence
+ * holding that many cached tokens (opts->prefix_len is ignored; the decode
+ * contexts are drawn as above).  Lookups take the prefix of the chunk's
+ * sequence and use the plane of the first p_grid point >= it.
+ */
+int slw_build_cost_table_ctx(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                             int32_t nb, const int32_t* p_grid, int32_t np, const slw_profile_opts* opts,
+                             slw_cost_table** out);
 
 /* Build a table from raw samples, host int64 ns [nb][nc][repeats] (e.g. an analytic model). */
 int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
                                 int32_t nb, const int64_t* samples, int32_t repeats,
                                 slw_cost_table** out);
+/* The same with a context axis: samples [np][nb][nc][repeats], p_grid as for the _ctx profiler. */
+int slw_cost_table_from_samples_ctx(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                                    const int32_t* p_grid, int32_t np, const int64_t* samples, int32_t repeats,
+                                    slw_cost_table** out);
 /*
  * A table holding the simulator's analytic cost model (Sec. 4.1) at every
  * grid point, one sample each:
@@ -267,12 +282,15 @@ int slw_cost_table_analytic(const int32_t* c_grid, int32_t nc, const int32_t* b_
 void slw_cost_table_free(slw_cost_table* t);
 int slw_cost_table_dims(const slw_cost_table* t, int32_t* nc, int32_t* nb, int32_t* repeats);
 int slw_cost_table_grids(const slw_cost_table* t, int32_t* c_grid, int32_t* b_grid);
+/* Context points of the table into p_grid (cap entries; may be NULL); *np = 0 without a context axis. */
+int slw_cost_table_prefixes(const slw_cost_table* t, int32_t* p_grid, int32_t cap, int32_t* np);
 
 /*
  * Copy a table view to host int64:
  *   SLW_TABLE_SAMPLES [nb][nc][repeats] raw ns; SLW_TABLE_P50 / SLW_TABLE_P99 [nb][nc]
  *   nearest-rank percentiles sorted[ceil(k*q)-1]; SLW_TABLE_THAT [nb][nc] the P99 with
- *   a running maximum along c (the table the controller reads).
+ *   a running maximum along c (the table the controller reads).  Tables with a
+ *   context axis have a leading [np] dimension.
  */
 #define SLW_TABLE_SAMPLES 0
 #define SLW_TABLE_P50 1
@@ -287,6 +305,13 @@ int slw_cost_table_values(const slw_cost_table* t, int32_t which, int64_t* out, 
  * c above the last grid point is SLW_ERANGE.
  */
 int slw_cost_table_lookup(const slw_cost_table* t, int32_t n, int32_t c, int64_t* t_ns);
+/*
+ * The same at the cached context `prefix` (tokens of the chunk's sequence
+ * cached before the chunk): the plane of the first context point >= prefix
+ * (SLW_ERANGE above the last).  Tables without a context axis ignore prefix;
+ * slw_cost_table_lookup is this with prefix 0.
+ */
+int slw_cost_table_lookup_ctx(const slw_cost_table* t, int32_t prefix, int32_t n, int32_t c, int64_t* t_ns);
 /* Raw P99 decreases along c before the running maximum: count and largest drop (ns). */
 int slw_cost_table_monotone(const slw_cost_table* t, int32_t* violations, int64_t* worst_ns);
 /* Text save / load of grids and raw samples (percentiles are recomputed on load). */
@@ -312,6 +337,15 @@ int slw_cost_table_load(const char* path, slw_cost_table** out);
 int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
                      int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
                      int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
+/*
+ * Alg. 1 priced at the cached context of the chunk's sequence: as
+ * slw_select_chunk with every lookup made by slw_cost_table_lookup_ctx at
+ * `prefix` (a prefix above the context grid is SLW_ERANGE once a lookup is
+ * needed).  slw_select_chunk is this with prefix 0.
+ */
+int slw_select_chunk_ctx(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
+                         int64_t now_ns, int32_t prefix, int32_t remaining, int32_t c_max, int64_t margin_ns,
+                         int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
 
 /* ------------------------------------------------------------------------ */
 /* Serving loop (Sec. 3.1 deadline model; Sec. 4.1 iteration semantics;     */
@@ -395,6 +429,8 @@ typedef struct slw_iteration_record {
  * moves to the next arrival (SLW_EXEC_ANALYTIC, or skip_idle) or waits for
  * it.  The table executor advances the clock by exec_table's T_hat(n, c)
  * (a stand-in for hardware whose cost differs from the controller's table).
+ * With a context axis in the table, decisions and predictions are priced
+ * at the oldest eligible prompt's cached prefix (0 with none).
  * The GPU executor synchronises `stream` after every iteration, creates
  * a KV sequence per request when its prompt starts and frees it when its
  * last token is out; ctx may be NULL with SLW_EXEC_ANALYTIC.

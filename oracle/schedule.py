@@ -60,14 +60,19 @@ def cummax(row):
 
 @dataclass
 class CostTable:
-    """Measured iteration times on a (decode batch) x (chunk) grid.
+    """Measured iteration times on a (decode batch) x (chunk) grid, optionally
+    one such plane per cached-context point (Sec. 5.1 indexes the runtime's
+    table by decode batch, cached context and chunk).
 
-    samples[i][j] holds the raw times (ns) at b_grid[i], c_grid[j].
+    Without p_grid, samples[i][j] holds the raw times (ns) at b_grid[i],
+    c_grid[j]; with it, samples[k][i][j] at p_grid[k].  p50, p99 and t_hat
+    have the same leading shape.
     """
 
     c_grid: list
     b_grid: list
     samples: list
+    p_grid: list | None = None
 
     def __post_init__(self):
         c, b = list(map(int, self.c_grid)), list(map(int, self.b_grid))
@@ -76,14 +81,29 @@ class CostTable:
         if not b or b[0] < 0 or any(x >= y for x, y in zip(b, b[1:])):
             raise ValueError("b_grid must be non-negative and increase strictly")
         self.c_grid, self.b_grid = c, b
-        self.p50 = [[nearest_rank(s, 1, 2) for s in row] for row in self.samples]
-        self.p99 = [[nearest_rank(s, 99, 100) for s in row] for row in self.samples]
-        self.t_hat = [cummax(row) for row in self.p99]
+        planes = [self.samples] if self.p_grid is None else list(self.samples)
+        if self.p_grid is not None:
+            pg = list(map(int, self.p_grid))
+            if not pg or pg[0] < 0 or any(x >= y for x, y in zip(pg, pg[1:])):
+                raise ValueError("p_grid must be non-negative and increase strictly")
+            if len(planes) != len(pg):
+                raise ValueError("one plane of samples per context point")
+            self.p_grid = pg
+        p50 = [[[nearest_rank(s, 1, 2) for s in row] for row in pl] for pl in planes]
+        p99 = [[[nearest_rank(s, 99, 100) for s in row] for row in pl] for pl in planes]
+        t_hat = [[cummax(row) for row in pl] for pl in p99]
+        self._t_hat_planes = t_hat
+        if self.p_grid is None:
+            self.p50, self.p99, self.t_hat = p50[0], p99[0], t_hat[0]
+        else:
+            self.p50, self.p99, self.t_hat = p50, p99, t_hat
 
     @classmethod
-    def from_values(cls, c_grid, b_grid, values):
+    def from_values(cls, c_grid, b_grid, values, p_grid=None):
         """A table whose every grid point holds one value (e.g. an analytic model)."""
-        return cls(c_grid, b_grid, [[[int(v)] for v in row] for row in values])
+        if p_grid is None:
+            return cls(c_grid, b_grid, [[[int(v)] for v in row] for row in values])
+        return cls(c_grid, b_grid, [[[[int(v)] for v in row] for row in pl] for pl in values], p_grid)
 
     def row_for(self, n: int) -> int:
         for i, b in enumerate(self.b_grid):
@@ -91,9 +111,18 @@ class CostTable:
                 return i
         raise IndexError(f"n={n} above the decode-batch grid")
 
-    def lookup(self, n: int, c: int) -> int:
-        """Predicted time T_hat(n, c) in ns from the cummax P99 table."""
-        row = self.t_hat[self.row_for(n)]
+    def plane_for(self, prefix: int) -> int:
+        """The plane of the first context point >= prefix (the only plane without a context axis)."""
+        if self.p_grid is None:
+            return 0
+        for k, p in enumerate(self.p_grid):
+            if p >= prefix:
+                return k
+        raise IndexError(f"prefix={prefix} above the context grid")
+
+    def lookup(self, n: int, c: int, prefix: int = 0) -> int:
+        """Predicted time T_hat(prefix, n, c) in ns from the cummax P99 table."""
+        row = self._t_hat_planes[self.plane_for(prefix)][self.row_for(n)]
         cg = self.c_grid
         if c < 0 or c > cg[-1]:
             raise IndexError(f"c={c} outside [0, {cg[-1]}]")
@@ -114,7 +143,8 @@ class CostTable:
     def monotone_violations(self):
         """Raw P99 decreases along the chunk axis: (count, largest drop in ns)."""
         count, worst = 0, 0
-        for row in self.p99:
+        rows = self.p99 if self.p_grid is None else [r for pl in self.p99 for r in pl]
+        for row in rows:
             for a, b in zip(row, row[1:]):
                 if b < a:
                     count += 1
@@ -170,13 +200,16 @@ def select_chunk(predict, deadlines_ns, now_ns: int, remaining: int, c_max: int,
     return lo, flags, lookups
 
 
-def select_chunk_table(table: CostTable, deadlines_ns, now_ns, remaining, c_max, margin_ns=0):
-    """Alg. 1 over a measured table (the capped, interpolated lookup).
+def select_chunk_table(table: CostTable, deadlines_ns, now_ns, remaining, c_max, margin_ns=0, prefix=0):
+    """Alg. 1 over a measured table (the capped, interpolated lookup at the
+    chunk sequence's cached prefix).
 
     Alg. 1 returns before any cost query when nothing is pending or nothing
-    is active; only then can the decode count fall outside the table.
+    is active; only then can the decode count or the prefix fall outside the
+    table.
     """
     if remaining > 0 and len(deadlines_ns) > 0:
         table.row_for(len(deadlines_ns))          # raises for n above the grid
-    return select_chunk(table.lookup, deadlines_ns, now_ns, remaining, c_max, margin_ns,
-                        c_last=table.c_grid[-1])
+        table.plane_for(prefix)                   # raises for a prefix above the grid
+    return select_chunk(lambda n, c: table.lookup(n, c, prefix), deadlines_ns, now_ns, remaining, c_max,
+                        margin_ns, c_last=table.c_grid[-1])

@@ -75,7 +75,7 @@ class Trace:
 
 def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed_chunk: int = 0,
              predict=None, c_last: int | None = None, c_max: int = 4096, margin_ns: int = 0,
-             max_decode: int | None = None, residual_window: int = 0,
+             max_decode: int | None = None, residual_window: int = 0, prefix_aware: bool = False,
              max_iterations: int = 10_000_000) -> Trace:
     """Run the trace through the iteration-level loop of Sec. 4.1.
 
@@ -85,12 +85,18 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
     the largest chunk it can price.  policy is "sloweave" (Alg. 1 with margin
     margin_ns and cap c_max) or "fixed" (chunks of fixed_chunk tokens).
     residual_window > 0 turns on the telemetry margin (module docstring).
+    With prefix_aware, cost_ns and predict take a third argument, the cached
+    prefix the iteration is priced at: that of the oldest eligible prompt
+    (its tokens already processed), 0 with none.
     """
     if policy not in ("sloweave", "fixed"):
         raise ValueError(policy)
     if policy == "fixed" and fixed_chunk <= 0:
         raise ValueError("fixed_chunk must be positive")
     predict = predict or cost_ns
+
+    def at(f, n, c, p):
+        return f(n, c, p) if prefix_aware else f(n, c)
     reqs = sorted(requests, key=lambda r: (r.arrival_ns, r.rid))
     out = Trace(token_ns={r.rid: [] for r in reqs})
     pending = []            # eligible requests whose prompt is not finished, oldest first
@@ -116,6 +122,7 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
         head = pending[0] if pending and (max_decode is None or n < max_decode) else None
         remaining = head.prompt - done_prompt[head.rid] if head else 0
         budget = min(deadlines) - t if deadlines else 0
+        prefix = done_prompt[head.rid] if head else 0
         rel = 0
         if head is None:
             chunk = 0
@@ -125,17 +132,17 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
             if residual_window > 0 and residuals:
                 rel = min(max(nearest_rank(residuals[-residual_window:], 99, 100), 0), 10**8)
 
-            def with_margin(nn, cc, q=rel):
-                v = predict(nn, cc)
+            def with_margin(nn, cc, q=rel, p=prefix):
+                v = at(predict, nn, cc, p)
                 return v + -(-q * v // 10**6)   # T_hat + ceil(q T_hat / 1e6)
             try:
                 chunk = select_chunk(with_margin, deadlines, t, remaining, c_max, margin_ns, c_last=c_last)[0]
             except IndexError:                 # n above the priced decode batches
                 chunk = 0
-        end = t + cost_ns(n, chunk)
+        end = t + at(cost_ns, n, chunk, prefix)
         out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget, rel))
         if residual_window > 0 and chunk > 0:
-            pred = predict(n, chunk)
+            pred = at(predict, n, chunk, prefix)
             if pred > 0:
                 residuals.append((end - t - pred) * 10**6 // pred)
         for rid in order:

@@ -34,7 +34,8 @@ EXPORTS = (
     "slw_cost_table_free", "slw_cost_table_dims", "slw_cost_table_grids", "slw_cost_table_values",
     "slw_cost_table_lookup", "slw_cost_table_monotone", "slw_cost_table_save",
     "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
-    "slw_serve", "slw_cost_table_analytic",
+    "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
+    "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
 )
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "decode_merge",
           "o_gemm", "rmsnorm_mlp", "gateup_gemm", "down_gemm")
@@ -128,6 +129,11 @@ def lib() -> C.CDLL:
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
         "slw_cost_table_from_samples": ([P(i32), i32, P(i32), i32, P(i64), i32, P(vp)], C.c_int),
         "slw_cost_table_analytic": ([P(i32), i32, P(i32), i32, P(vp)], C.c_int),
+        "slw_build_cost_table_ctx": ([vp, P(i32), i32, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
+        "slw_cost_table_from_samples_ctx": ([P(i32), i32, P(i32), i32, P(i32), i32, P(i64), i32, P(vp)], C.c_int),
+        "slw_cost_table_prefixes": ([vp, P(i32), i32, P(i32)], C.c_int),
+        "slw_cost_table_lookup_ctx": ([vp, i32, i32, i32, P(i64)], C.c_int),
+        "slw_select_chunk_ctx": ([vp, P(i64), i32, i64, i32, i32, i32, i64, P(i32), P(u32), P(i32)], C.c_int),
         "slw_cost_table_free": ([vp], None),
         "slw_cost_table_dims": ([vp, P(i32), P(i32), P(i32)], C.c_int),
         "slw_cost_table_grids": ([vp, P(i32), P(i32)], C.c_int),
@@ -187,15 +193,27 @@ class CostTable:
         return self._h
 
     @classmethod
-    def from_samples(cls, c_grid, b_grid, samples) -> "CostTable":
+    def from_samples(cls, c_grid, b_grid, samples, p_grid=None) -> "CostTable":
+        """samples [nb][nc][repeats] (or [nb][nc]); with p_grid, [np][nb][nc][repeats] (or [np][nb][nc])."""
         cg, bg = _i32(c_grid), _i32(b_grid)
         s = _i64(samples)
-        if s.ndim == 2:
-            s = s[:, :, None]
-        assert s.shape[:2] == (len(bg), len(cg))
         h = C.c_void_p()
-        _check(lib().slw_cost_table_from_samples(_ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
-                                                 len(bg), _ptr(s, C.c_int64), s.shape[2], C.byref(h)))
+        if p_grid is None:
+            if s.ndim == 2:
+                s = s[:, :, None]
+            assert s.shape[:2] == (len(bg), len(cg))
+            _check(lib().slw_cost_table_from_samples(_ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
+                                                     len(bg), _ptr(np.ascontiguousarray(s), C.c_int64), s.shape[2],
+                                                     C.byref(h)))
+        else:
+            pg = _i32(p_grid)
+            if s.ndim == 3:
+                s = s[:, :, :, None]
+            assert s.shape[:3] == (len(pg), len(bg), len(cg))
+            _check(lib().slw_cost_table_from_samples_ctx(_ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32), len(bg),
+                                                         _ptr(pg, C.c_int32), len(pg),
+                                                         _ptr(np.ascontiguousarray(s), C.c_int64), s.shape[3],
+                                                         C.byref(h)))
         return cls(h.value)
 
     @classmethod
@@ -228,16 +246,30 @@ class CostTable:
         _check(lib().slw_cost_table_grids(self._h, _ptr(cg, C.c_int32), _ptr(bg, C.c_int32)))
         return cg, bg
 
+    def prefixes(self):
+        """Context points, or None for a table without a context axis."""
+        n = C.c_int32()
+        _check(lib().slw_cost_table_prefixes(self._h, None, 0, C.byref(n)))
+        if n.value == 0:
+            return None
+        pg = np.zeros(n.value, np.int32)
+        _check(lib().slw_cost_table_prefixes(self._h, _ptr(pg, C.c_int32), len(pg), C.byref(n)))
+        return pg
+
     def values(self, which: int) -> np.ndarray:
+        """A view as [nb][nc] ([nb][nc][repeats] for samples), with a leading [np] on context tables."""
         nc, nb, r = self.dims()
         shape = (nb, nc, r) if which == TABLE_SAMPLES else (nb, nc)
+        pg = self.prefixes()
+        if pg is not None:
+            shape = (len(pg),) + shape
         out = np.zeros(shape, np.int64)
         _check(lib().slw_cost_table_values(self._h, which, _ptr(out, C.c_int64), out.size))
         return out
 
-    def lookup(self, n: int, c: int) -> int:
+    def lookup(self, n: int, c: int, prefix: int = 0) -> int:
         t = C.c_int64()
-        _check(lib().slw_cost_table_lookup(self._h, n, c, C.byref(t)))
+        _check(lib().slw_cost_table_lookup_ctx(self._h, prefix, n, c, C.byref(t)))
         return t.value
 
     def monotone(self):
@@ -247,12 +279,17 @@ class CostTable:
 
 
 def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_max: int,
-                 margin_ns: int = 0):
-    """(chunk, flags, n_lookups) from slw_select_chunk (Alg. 1)."""
+                 margin_ns: int = 0, prefix: int | None = None):
+    """(chunk, flags, n_lookups) from slw_select_chunk (Alg. 1); with prefix, slw_select_chunk_ctx."""
     d = _i64(deadlines_ns)
     ch, fl, nl = C.c_int32(), C.c_uint32(), C.c_int32()
-    _check(lib().slw_select_chunk(table.handle, _ptr(d, C.c_int64), len(d), int(now_ns), int(remaining),
-                                  int(c_max), int(margin_ns), C.byref(ch), C.byref(fl), C.byref(nl)))
+    if prefix is None:
+        _check(lib().slw_select_chunk(table.handle, _ptr(d, C.c_int64), len(d), int(now_ns), int(remaining),
+                                      int(c_max), int(margin_ns), C.byref(ch), C.byref(fl), C.byref(nl)))
+    else:
+        _check(lib().slw_select_chunk_ctx(table.handle, _ptr(d, C.c_int64), len(d), int(now_ns), int(prefix),
+                                          int(remaining), int(c_max), int(margin_ns), C.byref(ch), C.byref(fl),
+                                          C.byref(nl)))
     return ch.value, fl.value, nl.value
 
 
@@ -424,11 +461,17 @@ class Context:
     def build_cost_table(self, c_grid, b_grid, *, prefix_len: int, ctx_lo: int, ctx_hi: int,
                          seed: int, warmup: int, repeats: int, x_in: int, x_out: int, ws: int,
                          ws_bytes: int, flush_buf: int = 0, flush_bytes: int = 0,
-                         stream: int = 0) -> CostTable:
+                         stream: int = 0, p_grid=None) -> CostTable:
+        """slw_build_cost_table; with p_grid (context points), slw_build_cost_table_ctx."""
         cg, bg = _i32(c_grid), _i32(b_grid)
         o = ProfileOpts(prefix_len, ctx_lo, ctx_hi, seed, warmup, repeats, flush_buf or None,
                         flush_bytes, x_in, x_out, ws, ws_bytes, stream or None)
         h = C.c_void_p()
-        _check(lib().slw_build_cost_table(self._h, _ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
-                                          len(bg), C.byref(o), C.byref(h)))
+        if p_grid is None:
+            _check(lib().slw_build_cost_table(self._h, _ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
+                                              len(bg), C.byref(o), C.byref(h)))
+        else:
+            pg = _i32(p_grid)
+            _check(lib().slw_build_cost_table_ctx(self._h, _ptr(cg, C.c_int32), len(cg), _ptr(bg, C.c_int32),
+                                                  len(bg), _ptr(pg, C.c_int32), len(pg), C.byref(o), C.byref(h)))
         return CostTable(h.value)

@@ -1,9 +1,10 @@
 // Cost table and chunk controller.
 //
 // Sec. 5.1: the profiler keeps P50 and P99 per (decode batch, chunk) grid
-// point and applies a running maximum along the chunk axis; Sec. 6.4:
-// interpolate between profiled points.  Eq. 1 is solved by the upper-mid
-// binary search of Alg. 1 with the margin test of Sec. 3.3.
+// point and applies a running maximum along the chunk axis, and the
+// runtime's table is indexed by decode batch, cached context and chunk;
+// Sec. 6.4: interpolate between profiled points.  Eq. 1 is solved by the
+// upper-mid binary search of Alg. 1 with the margin test of Sec. 3.3.
 #include "cost_table.h"
 
 #include <algorithm>
@@ -38,11 +39,28 @@ int check_grids(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_
     return SLW_OK;
 }
 
-// Row index of the first b_grid point >= n, or -1.
-int32_t row_for(const slw_cost_table* t, int32_t n) {
-    auto it = std::lower_bound(t->b_grid.begin(), t->b_grid.end(), n);
-    if (it == t->b_grid.end()) return -1;
-    return static_cast<int32_t>(it - t->b_grid.begin());
+int check_p_grid(const int32_t* p_grid, int32_t np) {
+    if (!p_grid || np < 1) return fail(SLW_EINVAL, "empty context grid");
+    if (p_grid[0] < 0) return fail(SLW_EINVAL, "p_grid values must be >= 0");
+    for (int32_t k = 1; k < np; ++k)
+        if (p_grid[k] <= p_grid[k - 1]) return fail(SLW_EINVAL, "p_grid must increase strictly");
+    return SLW_OK;
+}
+
+// Index of the first grid point >= v, or -1.
+int32_t first_at_least(const std::vector<int32_t>& g, int32_t v) {
+    auto it = std::lower_bound(g.begin(), g.end(), v);
+    if (it == g.end()) return -1;
+    return static_cast<int32_t>(it - g.begin());
+}
+
+// Table row (plane * nb + decode row) for (prefix, n), or -1 outside the grids.
+int32_t row_for(const slw_cost_table* t, int32_t prefix, int32_t n) {
+    const int32_t b = first_at_least(t->b_grid, n);
+    if (b < 0) return -1;
+    const int32_t p = t->has_ctx ? first_at_least(t->p_grid, prefix) : 0;
+    if (p < 0) return -1;
+    return p * t->nb() + b;
 }
 
 // T_hat on row `row` at chunk c (0 <= c <= last grid C).
@@ -58,13 +76,40 @@ int64_t lookup_row(const slw_cost_table* t, int32_t row, int32_t c) {
     return r[j - 1] + (num + den - 1) / den;  // num >= 0: r is a running maximum
 }
 
+int range_error(const slw_cost_table* t, int32_t prefix, int32_t n) {
+    if (first_at_least(t->b_grid, n) < 0)
+        return fail(SLW_ERANGE, "n=%d above the decode grid (last %d)", n, t->b_grid.back());
+    return fail(SLW_ERANGE, "prefix %d above the context grid (last %d)", prefix, t->p_grid.back());
+}
+
+std::unique_ptr<slw_cost_table> make_table(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                                           const int32_t* p_grid, int32_t np, const int64_t* samples,
+                                           int32_t repeats) {
+    auto t = std::make_unique<slw_cost_table>();
+    t->c_grid.assign(c_grid, c_grid + nc);
+    t->b_grid.assign(b_grid, b_grid + nb);
+    if (p_grid) {
+        t->p_grid.assign(p_grid, p_grid + np);
+        t->has_ctx = true;
+    } else {
+        t->p_grid.assign(1, 0);
+    }
+    t->repeats = repeats;
+    t->samples.assign(samples, samples + static_cast<size_t>(t->np()) * nb * nc * repeats);
+    return t;
+}
+
 }  // namespace
 
 int finish_table(slw_cost_table* t) {
     int rc = check_grids(t->c_grid.data(), t->nc(), t->b_grid.data(), t->nb());
     if (rc) return rc;
+    rc = check_p_grid(t->p_grid.data(), t->np());
+    if (rc) return rc;
+    if (!t->has_ctx && t->np() != 1) return fail(SLW_EINVAL, "a table without a context axis has one plane");
     if (t->repeats < 1) return fail(SLW_EINVAL, "repeats must be >= 1");
-    const size_t cells = static_cast<size_t>(t->nb()) * t->nc();
+    const size_t rows = static_cast<size_t>(t->np()) * t->nb();
+    const size_t cells = rows * t->nc();
     if (t->samples.size() != cells * t->repeats) return fail(SLW_EINVAL, "sample count mismatch");
     t->p50.assign(cells, 0);
     t->p99.assign(cells, 0);
@@ -75,10 +120,10 @@ int finish_table(slw_cost_table* t) {
         t->p50[cell] = nearest_rank(tmp, 1, 2);
         t->p99[cell] = nearest_rank(tmp, 99, 100);
     }
-    for (int32_t i = 0; i < t->nb(); ++i) {
+    for (size_t i = 0; i < rows; ++i) {
         int64_t best = INT64_MIN;
         for (int32_t j = 0; j < t->nc(); ++j) {
-            size_t cell = static_cast<size_t>(i) * t->nc() + j;
+            size_t cell = i * t->nc() + j;
             best = std::max(best, t->p99[cell]);
             t->t_hat[cell] = best;
         }
@@ -86,11 +131,15 @@ int finish_table(slw_cost_table* t) {
     return SLW_OK;
 }
 
-}  // namespace slw
-
-using namespace slw;
-
-namespace slw {
+int lookup_ctx(const slw_cost_table* t, int32_t prefix, int32_t n, int32_t c, int64_t* t_ns) {
+    if (!t || !t_ns) return fail(SLW_EINVAL, "null argument");
+    if (n < 0 || prefix < 0) return fail(SLW_EINVAL, "negative decode count or prefix");
+    const int32_t row = row_for(t, prefix, n);
+    if (row < 0) return range_error(t, prefix, n);
+    if (c < 0 || c > t->c_grid.back()) return fail(SLW_ERANGE, "c=%d outside [0, %d]", c, t->c_grid.back());
+    *t_ns = lookup_row(t, row, c);
+    return SLW_OK;
+}
 
 int64_t analytic_iteration_ns(int32_t n, int32_t c) {
     int64_t t = 350000;
@@ -99,156 +148,15 @@ int64_t analytic_iteration_ns(int32_t n, int32_t c) {
     return t;
 }
 
-}  // namespace slw
-
-extern "C" int slw_cost_table_analytic(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
-                                       slw_cost_table** out) {
-    return guarded([&] {
-        if (!c_grid || !b_grid || !out || nc < 1 || nb < 1) return fail(SLW_EINVAL, "bad grids");
-        std::vector<int64_t> v(static_cast<size_t>(nc) * nb);
-        for (int32_t i = 0; i < nb; ++i)
-            for (int32_t j = 0; j < nc; ++j) v[static_cast<size_t>(i) * nc + j] = analytic_iteration_ns(b_grid[i], c_grid[j]);
-        return slw_cost_table_from_samples(c_grid, nc, b_grid, nb, v.data(), 1, out);
-    });
-}
-
-extern "C" int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
-                                           int32_t nb, const int64_t* samples, int32_t repeats,
-                                           slw_cost_table** out) {
-    return guarded([&] {
-        if (!out || !samples) return fail(SLW_EINVAL, "null argument");
-        *out = nullptr;
-        int rc = check_grids(c_grid, nc, b_grid, nb);
-        if (rc) return rc;
-        if (repeats < 1) return fail(SLW_EINVAL, "repeats must be >= 1");
-        auto t = std::make_unique<slw_cost_table>();
-        t->c_grid.assign(c_grid, c_grid + nc);
-        t->b_grid.assign(b_grid, b_grid + nb);
-        t->repeats = repeats;
-        t->samples.assign(samples, samples + static_cast<size_t>(nb) * nc * repeats);
-        rc = finish_table(t.get());
-        if (rc) return rc;
-        *out = t.release();
-        return SLW_OK;
-    });
-}
-
-extern "C" void slw_cost_table_free(slw_cost_table* t) { delete t; }
-
-extern "C" int slw_cost_table_dims(const slw_cost_table* t, int32_t* nc, int32_t* nb, int32_t* repeats) {
-    if (!t) return fail(SLW_EINVAL, "null table");
-    if (nc) *nc = t->nc();
-    if (nb) *nb = t->nb();
-    if (repeats) *repeats = t->repeats;
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_grids(const slw_cost_table* t, int32_t* c_grid, int32_t* b_grid) {
-    if (!t) return fail(SLW_EINVAL, "null table");
-    if (c_grid) std::copy(t->c_grid.begin(), t->c_grid.end(), c_grid);
-    if (b_grid) std::copy(t->b_grid.begin(), t->b_grid.end(), b_grid);
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_values(const slw_cost_table* t, int32_t which, int64_t* out, size_t cap) {
-    if (!t || !out) return fail(SLW_EINVAL, "null argument");
-    const std::vector<int64_t>* v = nullptr;
-    switch (which) {
-        case SLW_TABLE_SAMPLES: v = &t->samples; break;
-        case SLW_TABLE_P50: v = &t->p50; break;
-        case SLW_TABLE_P99: v = &t->p99; break;
-        case SLW_TABLE_THAT: v = &t->t_hat; break;
-        default: return fail(SLW_EINVAL, "unknown table view %d", which);
-    }
-    if (cap < v->size()) return fail(SLW_ERANGE, "output holds %zu values, need %zu", cap, v->size());
-    std::copy(v->begin(), v->end(), out);
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_lookup(const slw_cost_table* t, int32_t n, int32_t c, int64_t* t_ns) {
-    if (!t || !t_ns) return fail(SLW_EINVAL, "null argument");
-    if (n < 0) return fail(SLW_EINVAL, "negative decode count");
-    int32_t row = row_for(t, n);
-    if (row < 0) return fail(SLW_ERANGE, "n=%d above the decode grid (last %d)", n, t->b_grid.back());
-    if (c < 0 || c > t->c_grid.back())
-        return fail(SLW_ERANGE, "c=%d outside [0, %d]", c, t->c_grid.back());
-    *t_ns = lookup_row(t, row, c);
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_monotone(const slw_cost_table* t, int32_t* violations, int64_t* worst_ns) {
-    if (!t) return fail(SLW_EINVAL, "null table");
-    int32_t count = 0;
-    int64_t worst = 0;
-    for (int32_t i = 0; i < t->nb(); ++i)
-        for (int32_t j = 1; j < t->nc(); ++j) {
-            int64_t a = t->p99[static_cast<size_t>(i) * t->nc() + j - 1];
-            int64_t b = t->p99[static_cast<size_t>(i) * t->nc() + j];
-            if (b < a) {
-                ++count;
-                worst = std::max(worst, a - b);
-            }
-        }
-    if (violations) *violations = count;
-    if (worst_ns) *worst_ns = worst;
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_save(const slw_cost_table* t, const char* path) {
-    if (!t || !path) return fail(SLW_EINVAL, "null argument");
-    FILE* f = fopen(path, "w");
-    if (!f) return fail(SLW_EINVAL, "cannot open %s for writing", path);
-    fprintf(f, "sloweave-cost-table 1\n%d %d %d\n", t->nc(), t->nb(), t->repeats);
-    for (int32_t c : t->c_grid) fprintf(f, "%d ", c);
-    fprintf(f, "\n");
-    for (int32_t b : t->b_grid) fprintf(f, "%d ", b);
-    fprintf(f, "\n");
-    for (size_t i = 0; i < t->samples.size(); ++i)
-        fprintf(f, "%" PRId64 "%c", t->samples[i], (i + 1) % t->repeats ? ' ' : '\n');
-    int bad = ferror(f);
-    if (fclose(f) != 0 || bad) return fail(SLW_EINVAL, "write to %s failed", path);
-    return SLW_OK;
-}
-
-extern "C" int slw_cost_table_load(const char* path, slw_cost_table** out) {
-    return guarded([&] {
-        if (!path || !out) return fail(SLW_EINVAL, "null argument");
-        *out = nullptr;
-        FILE* f = fopen(path, "r");
-        if (!f) return fail(SLW_EINVAL, "cannot open %s", path);
-        std::unique_ptr<FILE, int (*)(FILE*)> guard(f, fclose);
-        int version = 0, nc = 0, nb = 0, reps = 0;
-        if (fscanf(f, "sloweave-cost-table %d %d %d %d", &version, &nc, &nb, &reps) != 4 || version != 1 ||
-            nc < 1 || nb < 1 || reps < 1 || nc > (1 << 20) || nb > (1 << 20) || reps > (1 << 20))
-            return fail(SLW_EINVAL, "%s: bad header", path);
-        auto t = std::make_unique<slw_cost_table>();
-        t->c_grid.resize(nc);
-        t->b_grid.resize(nb);
-        t->repeats = reps;
-        for (auto& c : t->c_grid)
-            if (fscanf(f, "%d", &c) != 1) return fail(SLW_EINVAL, "%s: truncated c grid", path);
-        for (auto& b : t->b_grid)
-            if (fscanf(f, "%d", &b) != 1) return fail(SLW_EINVAL, "%s: truncated b grid", path);
-        t->samples.resize(static_cast<size_t>(nc) * nb * reps);
-        for (auto& s : t->samples)
-            if (fscanf(f, "%" SCNd64, &s) != 1) return fail(SLW_EINVAL, "%s: truncated samples", path);
-        int rc = finish_table(t.get());
-        if (rc) return rc;
-        *out = t.release();
-        return SLW_OK;
-    });
-}
-
-namespace slw {
-
 int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
-                      int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm, int32_t* chunk,
-                      uint32_t* flags, int32_t* n_lookups) {
+                      int32_t prefix, int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm,
+                      int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
     if (!t || !chunk || !flags) return fail(SLW_EINVAL, "null argument");
     *chunk = 0;
     *flags = 0;
     if (n_lookups) *n_lookups = 0;
     if (n_active < 0 || (n_active > 0 && !deadlines_ns)) return fail(SLW_EINVAL, "bad active set");
+    if (prefix < 0) return fail(SLW_EINVAL, "negative prefix");
     if (rel_margin_ppm < 0 || rel_margin_ppm > 100000000) return fail(SLW_ERANGE, "relative margin out of range");
     if (remaining <= 0) {  // no pending prefill
         *flags = SLW_FLAG_NO_PENDING;
@@ -266,9 +174,8 @@ int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int3
         *flags = fl | SLW_FLAG_NO_ACTIVE;
         return SLW_OK;
     }
-    int32_t row = row_for(t, n_active);
-    if (row < 0) return fail(SLW_ERANGE, "%d active decodes above the decode grid (last %d)", n_active,
-                             t->b_grid.back());
+    const int32_t row = row_for(t, prefix, n_active);
+    if (row < 0) return range_error(t, prefix, n_active);
     int64_t earliest = deadlines_ns[0];
     for (int32_t i = 1; i < n_active; ++i) earliest = std::min(earliest, deadlines_ns[i]);
     const int64_t budget = earliest - now_ns;
@@ -296,9 +203,194 @@ int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int3
 
 }  // namespace slw
 
+using namespace slw;
+
+extern "C" int slw_cost_table_analytic(const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                                       slw_cost_table** out) {
+    return guarded([&] {
+        if (!c_grid || !b_grid || !out || nc < 1 || nb < 1) return fail(SLW_EINVAL, "bad grids");
+        std::vector<int64_t> v(static_cast<size_t>(nc) * nb);
+        for (int32_t i = 0; i < nb; ++i)
+            for (int32_t j = 0; j < nc; ++j) v[static_cast<size_t>(i) * nc + j] = analytic_iteration_ns(b_grid[i], c_grid[j]);
+        return slw_cost_table_from_samples(c_grid, nc, b_grid, nb, v.data(), 1, out);
+    });
+}
+
+extern "C" int slw_cost_table_from_samples(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                           int32_t nb, const int64_t* samples, int32_t repeats,
+                                           slw_cost_table** out) {
+    return guarded([&] {
+        if (!out || !samples) return fail(SLW_EINVAL, "null argument");
+        *out = nullptr;
+        int rc = check_grids(c_grid, nc, b_grid, nb);
+        if (rc) return rc;
+        if (repeats < 1) return fail(SLW_EINVAL, "repeats must be >= 1");
+        auto t = make_table(c_grid, nc, b_grid, nb, nullptr, 1, samples, repeats);
+        rc = finish_table(t.get());
+        if (rc) return rc;
+        *out = t.release();
+        return SLW_OK;
+    });
+}
+
+extern "C" int slw_cost_table_from_samples_ctx(const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                               int32_t nb, const int32_t* p_grid, int32_t np,
+                                               const int64_t* samples, int32_t repeats, slw_cost_table** out) {
+    return guarded([&] {
+        if (!out || !samples) return fail(SLW_EINVAL, "null argument");
+        *out = nullptr;
+        int rc = check_grids(c_grid, nc, b_grid, nb);
+        if (rc) return rc;
+        rc = check_p_grid(p_grid, np);
+        if (rc) return rc;
+        if (repeats < 1) return fail(SLW_EINVAL, "repeats must be >= 1");
+        auto t = make_table(c_grid, nc, b_grid, nb, p_grid, np, samples, repeats);
+        rc = finish_table(t.get());
+        if (rc) return rc;
+        *out = t.release();
+        return SLW_OK;
+    });
+}
+
+extern "C" void slw_cost_table_free(slw_cost_table* t) { delete t; }
+
+extern "C" int slw_cost_table_dims(const slw_cost_table* t, int32_t* nc, int32_t* nb, int32_t* repeats) {
+    if (!t) return fail(SLW_EINVAL, "null table");
+    if (nc) *nc = t->nc();
+    if (nb) *nb = t->nb();
+    if (repeats) *repeats = t->repeats;
+    return SLW_OK;
+}
+
+extern "C" int slw_cost_table_grids(const slw_cost_table* t, int32_t* c_grid, int32_t* b_grid) {
+    if (!t) return fail(SLW_EINVAL, "null table");
+    if (c_grid) std::copy(t->c_grid.begin(), t->c_grid.end(), c_grid);
+    if (b_grid) std::copy(t->b_grid.begin(), t->b_grid.end(), b_grid);
+    return SLW_OK;
+}
+
+extern "C" int slw_cost_table_prefixes(const slw_cost_table* t, int32_t* p_grid, int32_t cap, int32_t* np) {
+    if (!t || !np) return fail(SLW_EINVAL, "null argument");
+    *np = t->has_ctx ? t->np() : 0;
+    if (p_grid && t->has_ctx) {
+        if (cap < t->np()) return fail(SLW_ERANGE, "%d context points, cap %d", t->np(), cap);
+        std::copy(t->p_grid.begin(), t->p_grid.end(), p_grid);
+    }
+    return SLW_OK;
+}
+
+extern "C" int slw_cost_table_values(const slw_cost_table* t, int32_t which, int64_t* out, size_t cap) {
+    if (!t || !out) return fail(SLW_EINVAL, "null argument");
+    const std::vector<int64_t>* v = nullptr;
+    switch (which) {
+        case SLW_TABLE_SAMPLES: v = &t->samples; break;
+        case SLW_TABLE_P50: v = &t->p50; break;
+        case SLW_TABLE_P99: v = &t->p99; break;
+        case SLW_TABLE_THAT: v = &t->t_hat; break;
+        default: return fail(SLW_EINVAL, "unknown table view %d", which);
+    }
+    if (cap < v->size()) return fail(SLW_ERANGE, "output holds %zu values, need %zu", cap, v->size());
+    std::copy(v->begin(), v->end(), out);
+    return SLW_OK;
+}
+
+extern "C" int slw_cost_table_lookup(const slw_cost_table* t, int32_t n, int32_t c, int64_t* t_ns) {
+    return lookup_ctx(t, 0, n, c, t_ns);
+}
+
+extern "C" int slw_cost_table_lookup_ctx(const slw_cost_table* t, int32_t prefix, int32_t n, int32_t c,
+                                         int64_t* t_ns) {
+    return lookup_ctx(t, prefix, n, c, t_ns);
+}
+
+extern "C" int slw_cost_table_monotone(const slw_cost_table* t, int32_t* violations, int64_t* worst_ns) {
+    if (!t) return fail(SLW_EINVAL, "null table");
+    int32_t count = 0;
+    int64_t worst = 0;
+    const size_t rows = static_cast<size_t>(t->np()) * t->nb();
+    for (size_t i = 0; i < rows; ++i)
+        for (int32_t j = 1; j < t->nc(); ++j) {
+            int64_t a = t->p99[i * t->nc() + j - 1];
+            int64_t b = t->p99[i * t->nc() + j];
+            if (b < a) {
+                ++count;
+                worst = std::max(worst, a - b);
+            }
+        }
+    if (violations) *violations = count;
+    if (worst_ns) *worst_ns = worst;
+    return SLW_OK;
+}
+
+// Text format: version 1 (no context axis) or 2 (a line of context points after the b grid).
+extern "C" int slw_cost_table_save(const slw_cost_table* t, const char* path) {
+    if (!t || !path) return fail(SLW_EINVAL, "null argument");
+    FILE* f = fopen(path, "w");
+    if (!f) return fail(SLW_EINVAL, "cannot open %s for writing", path);
+    if (t->has_ctx) fprintf(f, "sloweave-cost-table 2\n%d %d %d %d\n", t->nc(), t->nb(), t->np(), t->repeats);
+    else fprintf(f, "sloweave-cost-table 1\n%d %d %d\n", t->nc(), t->nb(), t->repeats);
+    for (int32_t c : t->c_grid) fprintf(f, "%d ", c);
+    fprintf(f, "\n");
+    for (int32_t b : t->b_grid) fprintf(f, "%d ", b);
+    fprintf(f, "\n");
+    if (t->has_ctx) {
+        for (int32_t p : t->p_grid) fprintf(f, "%d ", p);
+        fprintf(f, "\n");
+    }
+    for (size_t i = 0; i < t->samples.size(); ++i)
+        fprintf(f, "%" PRId64 "%c", t->samples[i], (i + 1) % t->repeats ? ' ' : '\n');
+    int bad = ferror(f);
+    if (fclose(f) != 0 || bad) return fail(SLW_EINVAL, "write to %s failed", path);
+    return SLW_OK;
+}
+
+extern "C" int slw_cost_table_load(const char* path, slw_cost_table** out) {
+    return guarded([&] {
+        if (!path || !out) return fail(SLW_EINVAL, "null argument");
+        *out = nullptr;
+        FILE* f = fopen(path, "r");
+        if (!f) return fail(SLW_EINVAL, "cannot open %s", path);
+        std::unique_ptr<FILE, int (*)(FILE*)> guard(f, fclose);
+        int version = 0, nc = 0, nb = 0, np = 1, reps = 0;
+        if (fscanf(f, "sloweave-cost-table %d", &version) != 1 || (version != 1 && version != 2))
+            return fail(SLW_EINVAL, "%s: bad header", path);
+        const int got = version == 1 ? fscanf(f, "%d %d %d", &nc, &nb, &reps) : fscanf(f, "%d %d %d %d", &nc, &nb, &np, &reps);
+        if (got != (version == 1 ? 3 : 4) || nc < 1 || nb < 1 || np < 1 || reps < 1 || nc > (1 << 20) ||
+            nb > (1 << 20) || np > (1 << 20) || reps > (1 << 20))
+            return fail(SLW_EINVAL, "%s: bad header", path);
+        auto t = std::make_unique<slw_cost_table>();
+        t->c_grid.resize(nc);
+        t->b_grid.resize(nb);
+        t->p_grid.assign(np, 0);
+        t->has_ctx = version == 2;
+        t->repeats = reps;
+        for (auto& c : t->c_grid)
+            if (fscanf(f, "%d", &c) != 1) return fail(SLW_EINVAL, "%s: truncated c grid", path);
+        for (auto& b : t->b_grid)
+            if (fscanf(f, "%d", &b) != 1) return fail(SLW_EINVAL, "%s: truncated b grid", path);
+        if (t->has_ctx)
+            for (auto& p : t->p_grid)
+                if (fscanf(f, "%d", &p) != 1) return fail(SLW_EINVAL, "%s: truncated context grid", path);
+        t->samples.resize(static_cast<size_t>(np) * nc * nb * reps);
+        for (auto& s : t->samples)
+            if (fscanf(f, "%" SCNd64, &s) != 1) return fail(SLW_EINVAL, "%s: truncated samples", path);
+        int rc = finish_table(t.get());
+        if (rc) return rc;
+        *out = t.release();
+        return SLW_OK;
+    });
+}
+
 extern "C" int slw_select_chunk(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
                                 int64_t now_ns, int32_t remaining, int32_t c_max, int64_t margin_ns,
                                 int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
-    return slw::select_chunk_core(t, deadlines_ns, n_active, now_ns, remaining, c_max, margin_ns, 0, chunk, flags,
-                                  n_lookups);
+    return select_chunk_core(t, deadlines_ns, n_active, now_ns, 0, remaining, c_max, margin_ns, 0, chunk, flags,
+                             n_lookups);
+}
+
+extern "C" int slw_select_chunk_ctx(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active,
+                                    int64_t now_ns, int32_t prefix, int32_t remaining, int32_t c_max,
+                                    int64_t margin_ns, int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
+    return select_chunk_core(t, deadlines_ns, n_active, now_ns, prefix, remaining, c_max, margin_ns, 0, chunk,
+                             flags, n_lookups);
 }

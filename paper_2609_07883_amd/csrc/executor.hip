@@ -675,67 +675,80 @@ extern "C" int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* 
 // grid, keep every sample, then P50/P99 and a running maximum along chunks.
 // ---------------------------------------------------------------------------
 
-extern "C" int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
-                                    int32_t nb, const slw_profile_opts* o, slw_cost_table** out) {
-    return guarded([&]() -> int {
-        if (!ctx || !o || !out || !c_grid || !b_grid) return fail(SLW_EINVAL, "null argument");
-        *out = nullptr;
-        if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
-        if (nc < 1 || nb < 1) return fail(SLW_EINVAL, "empty grid");
-        if (o->repeats < 1 || o->warmup < 0) return fail(SLW_EINVAL, "repeats must be >= 1, warmup >= 0");
-        if (o->prefix_len < 0 || o->ctx_lo < 0 || o->ctx_hi < o->ctx_lo)
-            return fail(SLW_EINVAL, "bad prefix or context range");
-        auto t = std::make_unique<slw_cost_table>();
-        t->c_grid.assign(c_grid, c_grid + nc);
-        t->b_grid.assign(b_grid, b_grid + nb);
-        t->repeats = o->repeats;
-        // validate grids before reserving anything (finish_table repeats the check)
-        t->samples.assign(static_cast<size_t>(nb) * nc * o->repeats, 0);
-        int rc = finish_table(t.get());
-        if (rc) return rc;
-        const int c_last = c_grid[nc - 1], b_last = b_grid[nb - 1];
+namespace {
 
-        const int64_t base = INT64_MIN + 1;  // profiler-reserved ids
-        const int64_t pre_id = base;
-        std::vector<int64_t> dec(b_last);
-        std::vector<int32_t> ctxl(b_last);
-        std::mt19937_64 rng(o->seed);
-        std::uniform_int_distribution<int32_t> dist(o->ctx_lo, o->ctx_hi);
-        for (int i = 0; i < b_last; ++i) {
-            dec[i] = base + 1 + i;
-            ctxl[i] = dist(rng);
-        }
-        std::vector<int64_t> made;
-        auto cleanup = [&] {
-            for (int64_t id : made) (void)ctx->kv.release(id);
-        };
-        rc = ctx->kv.create(pre_id);
-        if (rc) return rc;
-        made.push_back(pre_id);
-        for (int i = 0; i < b_last; ++i) {
-            rc = ctx->kv.create(dec[i]);
-            if (rc) { cleanup(); return rc; }
-            made.push_back(dec[i]);
-        }
-        std::vector<std::pair<int64_t, int32_t>> req;
-        req.emplace_back(pre_id, o->prefix_len + c_last);
-        for (int i = 0; i < b_last; ++i) req.emplace_back(dec[i], ctxl[i] + 1);
-        rc = ctx->kv.reserve_all(req);
+// Profile planes of the table: for each prefix in p_grid (or the single
+// prefix opts->prefix_len when p_grid is null) time the iteration over every
+// (b, c) of b_grid x c_grid.
+int build_table_core(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid, int32_t nb,
+                     const int32_t* p_grid, int32_t np, const slw_profile_opts* o, slw_cost_table** out) {
+    if (!ctx || !o || !out || !c_grid || !b_grid) return fail(SLW_EINVAL, "null argument");
+    *out = nullptr;
+    if (!ctx->kv_ready) return fail(SLW_EINVAL, "KV pools not attached");
+    if (nc < 1 || nb < 1 || (p_grid && np < 1)) return fail(SLW_EINVAL, "empty grid");
+    if (o->repeats < 1 || o->warmup < 0) return fail(SLW_EINVAL, "repeats must be >= 1, warmup >= 0");
+    if (o->prefix_len < 0 || o->ctx_lo < 0 || o->ctx_hi < o->ctx_lo)
+        return fail(SLW_EINVAL, "bad prefix or context range");
+    auto t = std::make_unique<slw_cost_table>();
+    t->c_grid.assign(c_grid, c_grid + nc);
+    t->b_grid.assign(b_grid, b_grid + nb);
+    if (p_grid) {
+        t->p_grid.assign(p_grid, p_grid + np);
+        t->has_ctx = true;
+    } else {
+        t->p_grid.assign(1, o->prefix_len);
+    }
+    t->repeats = o->repeats;
+    // validate grids before reserving anything (finish_table repeats the check)
+    t->samples.assign(static_cast<size_t>(t->np()) * nb * nc * o->repeats, 0);
+    int rc = finish_table(t.get());
+    if (rc) return rc;
+    const int c_last = c_grid[nc - 1], b_last = b_grid[nb - 1];
+    const int p_last = t->p_grid.back();
+
+    const int64_t base = INT64_MIN + 1;  // profiler-reserved ids
+    const int64_t pre_id = base;
+    std::vector<int64_t> dec(b_last);
+    std::vector<int32_t> ctxl(b_last);
+    std::mt19937_64 rng(o->seed);
+    std::uniform_int_distribution<int32_t> dist(o->ctx_lo, o->ctx_hi);
+    for (int i = 0; i < b_last; ++i) {
+        dec[i] = base + 1 + i;
+        ctxl[i] = dist(rng);
+    }
+    std::vector<int64_t> made;
+    auto cleanup = [&] {
+        for (int64_t id : made) (void)ctx->kv.release(id);
+    };
+    rc = ctx->kv.create(pre_id);
+    if (rc) return rc;
+    made.push_back(pre_id);
+    for (int i = 0; i < b_last; ++i) {
+        rc = ctx->kv.create(dec[i]);
         if (rc) { cleanup(); return rc; }
+        made.push_back(dec[i]);
+    }
+    std::vector<std::pair<int64_t, int32_t>> req;
+    req.emplace_back(pre_id, p_last + c_last);
+    for (int i = 0; i < b_last; ++i) req.emplace_back(dec[i], ctxl[i] + 1);
+    rc = ctx->kv.reserve_all(req);
+    if (rc) { cleanup(); return rc; }
 
-        hipStream_t s = static_cast<hipStream_t>(o->stream);
-        auto run = [&](int b, int cc) {
-            slw_batch batch{cc, pre_id, o->prefix_len, b, dec.data(), ctxl.data()};
-            return mixed_iteration_impl(ctx, &batch, o->x_in, o->x_out, o->ws, o->ws_bytes, s);
-        };
-        auto sync = [&]() -> int {
-            hipError_t e = hipStreamSynchronize(s);
-            if (e != hipSuccess) return fail(SLW_EHIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
-            return SLW_OK;
-        };
+    hipStream_t s = static_cast<hipStream_t>(o->stream);
+    auto run = [&](int prefix, int b, int cc) {
+        slw_batch batch{cc, pre_id, prefix, b, dec.data(), ctxl.data()};
+        return mixed_iteration_impl(ctx, &batch, o->x_in, o->x_out, o->ws, o->ws_bytes, s);
+    };
+    auto sync = [&]() -> int {
+        hipError_t e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return fail(SLW_EHIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
+        return SLW_OK;
+    };
+    for (int k = 0; k < t->np() && !rc; ++k)
         for (int i = 0; i < nb && !rc; ++i)
             for (int j = 0; j < nc && !rc; ++j) {
-                for (int r = 0; r < o->warmup && !rc; ++r) rc = run(b_grid[i], c_grid[j]);
+                const int prefix = t->p_grid[k];
+                for (int r = 0; r < o->warmup && !rc; ++r) rc = run(prefix, b_grid[i], c_grid[j]);
                 if (!rc) rc = sync();
                 for (int r = 0; r < o->repeats && !rc; ++r) {
                     if (o->flush_buf && o->flush_bytes) {
@@ -744,18 +757,34 @@ extern "C" int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t
                         if (rc) break;
                     }
                     auto t0 = std::chrono::steady_clock::now();
-                    rc = run(b_grid[i], c_grid[j]);
+                    rc = run(prefix, b_grid[i], c_grid[j]);
                     if (!rc) rc = sync();
                     auto t1 = std::chrono::steady_clock::now();
-                    t->samples[(static_cast<size_t>(i) * nc + j) * o->repeats + r] =
+                    t->samples[((static_cast<size_t>(k) * nb + i) * nc + j) * o->repeats + r] =
                         std::chrono::duration_cast<std::chrono::nanoseconds>(t1 - t0).count();
                 }
             }
-        cleanup();
-        if (rc) return rc;
-        rc = finish_table(t.get());
-        if (rc) return rc;
-        *out = t.release();
-        return SLW_OK;
+    cleanup();
+    if (rc) return rc;
+    if (!p_grid) t->p_grid.assign(1, 0);  // one plane serves every prefix
+    rc = finish_table(t.get());
+    if (rc) return rc;
+    *out = t.release();
+    return SLW_OK;
+}
+
+}  // namespace
+
+extern "C" int slw_build_cost_table(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                    int32_t nb, const slw_profile_opts* o, slw_cost_table** out) {
+    return guarded([&]() -> int { return build_table_core(ctx, c_grid, nc, b_grid, nb, nullptr, 0, o, out); });
+}
+
+extern "C" int slw_build_cost_table_ctx(slw_ctx* ctx, const int32_t* c_grid, int32_t nc, const int32_t* b_grid,
+                                        int32_t nb, const int32_t* p_grid, int32_t np, const slw_profile_opts* o,
+                                        slw_cost_table** out) {
+    return guarded([&]() -> int {
+        if (!p_grid) return fail(SLW_EINVAL, "null context grid");
+        return build_table_core(ctx, c_grid, nc, b_grid, nb, p_grid, np, o, out);
     });
 }

@@ -190,8 +190,8 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
                 }
                 rec.rel_margin_ppm = rel;
                 uint32_t fl = 0;
-                rc = select_chunk_core(o->table, deadlines.data(), nd, t, remaining, o->c_max, o->margin_ns, rel,
-                                       &chunk, &fl, nullptr);
+                rc = select_chunk_core(o->table, deadlines.data(), nd, t, head->prompt_done, remaining, o->c_max,
+                                       o->margin_ns, rel, &chunk, &fl, nullptr);
                 if (rc == SLW_ERANGE) {  // more decodes than the table prices
                     clear_error();
                     chunk = 0;
@@ -205,9 +205,10 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         rec.decide_ns = host_ns() - t_dec0;
         rec.chunk = chunk;
         rec.n_decode = nd;
+        const int32_t prefix = head ? head->prompt_done : 0;  // context the iteration is priced at
         if (o->table) {
             int64_t p = 0;
-            if (slw_cost_table_lookup(o->table, nd, chunk, &p) == SLW_OK) rec.predicted_ns = p;
+            if (lookup_ctx(o->table, prefix, nd, chunk, &p) == SLW_OK) rec.predicted_ns = p;
             else clear_error();
         }
 
@@ -234,7 +235,7 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             virt = t + analytic_iteration_ns(nd, chunk);
         } else {
             int64_t dt = 0;
-            rc = slw_cost_table_lookup(o->exec_table, nd, chunk, &dt);
+            rc = lookup_ctx(o->exec_table, prefix, nd, chunk, &dt);
             if (rc) return rc;
             virt = t + dt;
         }

@@ -83,3 +83,30 @@ def test_iterations_still_correct_after_profiling(measured):
     y, yr, sg, sr = mir.step(b, synth.embeddings(41, 256, seed=1, stream=77))
     assert sg == sr
     check(y, yr, "after profiling")
+
+
+def test_context_table_on_gpu():
+    """slw_build_cost_table_ctx: one plane per cached-context point, its
+    statistics and lookups bit-exact against the oracle on the exported
+    samples, monotone along C in every plane, temporary sequences released."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_07883_amd.runtime import Session
+    sess = Session(synth.TINY, num_blocks=256, max_c=128, max_b=4)
+    free0 = sess.ctx.free_blocks()
+    c_grid, b_grid, p_grid = [0, 32, 128], [0, 2, 4], [0, 256, 1024]
+    ct = sess.ctx.build_cost_table(c_grid, b_grid, prefix_len=0, ctx_lo=16, ctx_hi=64, seed=5, warmup=1,
+                                   repeats=5, x_in=sess.x_in.data_ptr(), x_out=sess.x_out.data_ptr(),
+                                   ws=sess.ws.data_ptr(), ws_bytes=sess.ws_bytes,
+                                   stream=torch.cuda.current_stream().cuda_stream, p_grid=p_grid)
+    assert ct.prefixes().tolist() == p_grid
+    samples = ct.values(api.TABLE_SAMPLES)
+    assert samples.shape == (3, 3, 3, 5) and (samples > 0).all()
+    ot = S.CostTable(c_grid, b_grid, samples.tolist(), p_grid)
+    assert ct.values(api.TABLE_THAT).tolist() == ot.t_hat
+    assert (np.diff(ct.values(api.TABLE_THAT), axis=2) >= 0).all()
+    for p in (0, 1, 256, 257, 1024):
+        for n in range(0, 5):
+            for c in range(0, 129, 16):
+                assert ct.lookup(n, c, p) == ot.lookup(n, c, p)
+    assert sess.ctx.free_blocks() == free0

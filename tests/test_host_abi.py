@@ -189,3 +189,46 @@ def test_workspace_size_grows_with_batch():
     assert 0 < a < b < c
     off, nb = ctx.workspace_view(api.VIEW_ATTN, 100, 7)
     assert nb == 107 * 32 * 128 * 2 and off % 256 == 0
+
+
+def _ctx_tables(seed=0):
+    rng = np.random.default_rng(seed)
+    c_grid, b_grid, p_grid = [0, 32, 64, 256, 1024], [0, 1, 4, 16], [0, 2048, 8192, 16384]
+    samples = rng.integers(1_000_000, 60_000_000, size=(len(p_grid), len(b_grid), len(c_grid), 5))
+    return (api.CostTable.from_samples(c_grid, b_grid, samples, p_grid=p_grid),
+            S.CostTable(c_grid, b_grid, samples.tolist(), p_grid), c_grid, b_grid, p_grid)
+
+
+def test_context_table_statistics_and_lookup_bit_exact(tmp_path):
+    ct, ot, c_grid, b_grid, p_grid = _ctx_tables(1)
+    assert ct.prefixes().tolist() == p_grid
+    assert ct.values(api.TABLE_P99).tolist() == ot.p99
+    assert ct.values(api.TABLE_THAT).tolist() == ot.t_hat
+    assert ct.monotone() == ot.monotone_violations()
+    rng = np.random.default_rng(2)
+    for _ in range(400):
+        n, c, p = int(rng.integers(0, 17)), int(rng.integers(0, 1025)), int(rng.integers(0, 16385))
+        assert ct.lookup(n, c, p) == ot.lookup(n, c, p)
+    with pytest.raises(api.SloweaveError) as e:
+        ct.lookup(1, 32, 16385)
+    assert e.value.code == api.ERANGE
+    path = str(tmp_path / "ctx.txt")
+    ct.save(path)
+    back = api.CostTable.load(path)
+    assert back.prefixes().tolist() == p_grid
+    assert back.values(api.TABLE_SAMPLES).tolist() == ct.values(api.TABLE_SAMPLES).tolist()
+    flat = api.CostTable.from_samples(c_grid, b_grid, np.ones((4, 5), np.int64))
+    assert flat.prefixes() is None
+
+
+def test_select_chunk_ctx_bit_exact_vs_oracle():
+    ct, ot, *_ = _ctx_tables(3)
+    rng = np.random.default_rng(4)
+    for _ in range(500):
+        n = int(rng.integers(0, 17))
+        now = int(rng.integers(0, 10**9))
+        dl = (now + rng.integers(0, 80_000_000, size=n)).tolist()
+        rem, cmax, margin = int(rng.integers(-1, 1500)), int(rng.integers(0, 1500)), int(rng.integers(0, 10**6))
+        prefix = int(rng.integers(0, 16385))
+        assert api.select_chunk(ct, dl, now, rem, cmax, margin, prefix=prefix)[:2] == \
+            S.select_chunk_table(ot, dl, now, rem, cmax, margin, prefix=prefix)[:2]

@@ -231,3 +231,27 @@ def test_iteration_metadata_all_or_nothing():
     assert m.block_table(1) == [] and m.free_count() == 2
     slots, tables = paging.iteration_metadata(m, 10, 1, 0, [2], [15])
     assert tables[1] == [2] and slots == [32 + j for j in range(10)] + [0 * 16 + 15]
+
+
+def test_context_planes_round_prefix_up():
+    """A table with a cached-context axis keeps one (B, C) plane per context
+    point; a lookup uses the first point at or above the prefix (the cost of a
+    chunk grows with its prefix, so rounding up never under-predicts), and a
+    prefix above the last point cannot be priced."""
+    c_grid, b_grid, p_grid = [0, 64, 128], [0, 4], [0, 1000, 4000]
+    planes = [[[10 * (k + 1) + j + 100 * i for j in range(3)] for i in range(2)] for k in range(3)]
+    t = S.CostTable.from_values(c_grid, b_grid, planes, p_grid)
+    assert t.lookup(3, 64, 0) == planes[0][1][1]
+    assert t.lookup(3, 64, 1000) == planes[1][1][1]
+    assert t.lookup(3, 64, 1001) == planes[2][1][1]
+    assert t.lookup(0, 96, 2500) == planes[2][0][1] + (-(-(planes[2][0][2] - planes[2][0][1]) * 32 // 64))
+    with pytest.raises(IndexError):
+        t.lookup(1, 64, 4001)
+    flat = S.CostTable.from_values(c_grid, b_grid, planes[0])
+    assert flat.lookup(3, 64, 10**6) == flat.lookup(3, 64, 0)     # no context axis: prefix ignored
+    # Alg. 1 at a prefix reads that prefix's plane
+    pick = lambda pre: S.select_chunk_table(t, [10**9 + 120], 10**9, 500, 128, prefix=pre)[0]
+    assert pick(0) == 128 and pick(4000) == 0
+    with pytest.raises(IndexError):
+        S.select_chunk_table(t, [10**9 + 150], 10**9, 500, 128, prefix=5000)
+    assert S.select_chunk_table(t, [], 10**9, 500, 128, prefix=5000)[0] == 128   # nothing to price

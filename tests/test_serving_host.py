@@ -191,3 +191,48 @@ def test_errors():
         api.serve([0], [0], [4], [1], policy=api.POLICY_FIXED, fixed_chunk=8, tpot_ns=MS, max_decode=4,
                   residual_window=-1)
     assert e.value.code == api.ERANGE
+
+
+CTX_P = [0, 2048, 4096, 8192, 16384]
+
+
+def _ctx_tables(kappa_ctl, kappa_hw):
+    """Tables with a cached-context axis: the analytic model plus kappa ns per
+    chunk token per 1024 prefix tokens (the chunk's attention over its prefix)."""
+    def vals(kappa):
+        return [[[S.analytic_cost_ns(b, c) + kappa * c * p // 1024 for c in COARSE_C] for b in COARSE_B]
+                for p in CTX_P]
+    v_ctl, v_hw = vals(kappa_ctl), vals(kappa_hw)
+    lib_t = lambda v: api.CostTable.from_samples(COARSE_C, COARSE_B, np.array(v, dtype=np.int64), p_grid=CTX_P)
+    ora_t = lambda v: S.CostTable.from_values(COARSE_C, COARSE_B, v, CTX_P)
+    return lib_t(v_ctl), lib_t(v_hw), ora_t(v_ctl), ora_t(v_hw)
+
+
+@pytest.mark.parametrize("kappa_ctl,kappa_hw,window", [(400, 400, 0), (0, 600, 0), (300, 600, 16)])
+def test_context_tables_match_oracle(kappa_ctl, kappa_hw, window):
+    """Decisions and iteration times priced at the oldest prompt's cached
+    prefix, bit for bit against the oracle (with and without telemetry)."""
+    tr = _trace(250, 6.0, seed=12)
+    ctl, hw, octl, ohw = _ctx_tables(kappa_ctl, kappa_hw)
+    res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=256, table=ctl, exec_table=hw,
+                      residual_window=window)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=ohw.lookup, predict=octl.lookup, c_last=COARSE_C[-1],
+                     tpot_ns=25 * MS, max_decode=256, residual_window=window, prefix_aware=True)
+    _compare(tr, res, ref)
+    it = res.iterations
+    assert np.all(it["predicted_ns"][it["chunk"] > 0] > 0)
+
+
+def test_context_axis_removes_long_prefix_misses():
+    """On hardware whose chunk cost grows with the prefix, a controller that
+    prices at the profiled prefix 0 overruns deadlines; pricing at the
+    chunk's own prefix does not."""
+    tr = _trace(300, 6.0, seed=13)
+    ctl_ctx, hw, _, _ = _ctx_tables(600, 600)
+    flat = api.CostTable.analytic(COARSE_C, COARSE_B)
+    miss = {}
+    for name, tab in (("flat", flat), ("ctx", ctl_ctx)):
+        res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=256, table=tab, exec_table=hw)
+        gaps = np.concatenate([np.diff(t) for t in res.token_ns if len(t) > 1])
+        miss[name] = int(np.sum(gaps > 25 * MS))
+    assert miss["flat"] > 0 and miss["ctx"] == 0
