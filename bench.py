@@ -379,7 +379,8 @@ def main():
 SERVE_C_GRID = [0, 32, 64, 128, 256, 512, 1024, 2048, 4096]
 SERVE_B_GRID = [0, 1, 2, 4, 8, 16, 32, 64, 128, 256]
 SERVE_P_GRID = [0, 2048, 4096, 8192, 12288, 16384]
-SERVE_POLICIES = [("sloweave", 0, 0), ("sloweave", 0, 64), ("fixed", 256, 0), ("fixed", 512, 0), ("fixed", 2048, 0)]
+SERVE_POLICIES = [("sloweave", 0, 0), ("sloweave", 0, 256), ("fixed", 256, 0), ("fixed", 512, 0), ("fixed", 2048, 0)]
+SERVE_DECODE_CTX = (1024, 10240)   # profiled decode contexts: the trace's mean decode context (about 5.6 K)
 
 
 def serve_main(args):
@@ -405,7 +406,8 @@ def serve_main(args):
 
     flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     t1 = time.time()
-    ct = sess.ctx.build_cost_table(SERVE_C_GRID, SERVE_B_GRID, prefix_len=0, ctx_lo=1024, ctx_hi=8192, seed=2,
+    ct = sess.ctx.build_cost_table(SERVE_C_GRID, SERVE_B_GRID, prefix_len=0, ctx_lo=SERVE_DECODE_CTX[0],
+                                   ctx_hi=SERVE_DECODE_CTX[1], seed=2,
                                    warmup=2, repeats=args.repeats, x_in=sess.x_in.data_ptr(),
                                    x_out=sess.x_out.data_ptr(), ws=sess.ws.data_ptr(), ws_bytes=sess.ws_bytes,
                                    flush_buf=flush.data_ptr(), flush_bytes=flush.numel(), stream=stream,
@@ -469,7 +471,7 @@ def serve_main(args):
            "config": {"workload": WORKLOADS["serve"], "requests": args.requests, "rate_per_s": args.rate,
                       "seed": 3, "layers": 32, "kv_blocks": num_blocks, "max_decode": max_b},
            "cost_table": {"c_grid": SERVE_C_GRID, "b_grid": SERVE_B_GRID, "repeats": args.repeats,
-                          "p_grid": SERVE_P_GRID, "decode_ctx": [1024, 8192],
+                          "p_grid": SERVE_P_GRID, "decode_ctx": list(SERVE_DECODE_CTX),
                           "raw_p99_decreases_along_c": viol, "largest_decrease_ns": worst,
                           "monotone_after_cummax": bool(np.all(np.diff(t_hat, axis=-1) >= 0)),
                           "p99_cummax_ms": (t_hat / 1e6).round(3).tolist()},
