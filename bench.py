@@ -171,6 +171,8 @@ def main():
     ap.add_argument("--requests", type=int, default=200, help="serve: requests per run")
     ap.add_argument("--rate", type=float, default=4.0, help="serve: base arrival rate (requests/s)")
     ap.add_argument("--repeats", type=int, default=8, help="serve: profiler repeats per grid point")
+    ap.add_argument("--dump", default=None,
+                    help="serve: directory for per-run iteration records and token times (.npz)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -379,7 +381,7 @@ def main():
 SERVE_C_GRID = [0, 32, 64, 128, 256, 512, 1024, 2048, 4096]
 SERVE_B_GRID = [0, 1, 2, 4, 8, 16, 32, 64, 128, 256]
 SERVE_P_GRID = [0, 2048, 4096, 8192, 12288, 16384]
-SERVE_POLICIES = [("sloweave", 0, 0), ("sloweave", 0, 256), ("fixed", 256, 0), ("fixed", 512, 0), ("fixed", 2048, 0)]
+SERVE_POLICIES = [("sloweave", 0, 0), ("sloweave", 0, 64), ("fixed", 256, 0), ("fixed", 512, 0), ("fixed", 2048, 0)]
 SERVE_DECODE_CTX = (1024, 10240)   # profiled decode contexts: the trace's mean decode context (about 5.6 K)
 
 
@@ -445,6 +447,13 @@ def serve_main(args):
                    "residual_window": window,
                    "telemetry_margin_ppm_p50": int(np.median(it["rel_margin_ppm"][it["remaining"] > 0]))
                    if np.any(it["remaining"] > 0) else 0}
+            if args.dump:
+                os.makedirs(args.dump, exist_ok=True)
+                tok = res.token_ns
+                np.savez(os.path.join(args.dump, f"serve_{name}_{D:g}ms.npz"), iterations=it,
+                         token_ns=np.concatenate(tok), token_off=np.cumsum([0] + [len(t) for t in tok]),
+                         arrival_ns=np.asarray(trace.arrival_ns), prompt=np.asarray(trace.prompt),
+                         output=np.asarray(trace.output), table_values=t_hat)
             sim = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
                               table=sim_table, residual_window=window)
             sm = serving.metrics(trace, sim.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
@@ -452,7 +461,8 @@ def serve_main(args):
                                                                       "p99_ttft_ms", "p99_tpot_ms")}
             runs.append(run)
             log(f"serve: {name} D={D:g} ms: goodput {m['goodput_req_s']:.3f} req/s, SLO {m['slo_attainment']:.3f}, "
-                f"P99 TTFT {m['p99_ttft_ms']:.0f} ms, P99 TPOT {m['p99_tpot_ms']:.2f} ms, {len(it)} iterations, "
+                f"P99 TTFT {m['p99_ttft_ms']:.0f} ms, P99 TPOT {m['p99_tpot_ms']:.2f} ms, missed TTFT {m['ttft_missed']} / "
+                f"TPOT {m['tpot_missed']}, {len(it)} iterations, "
                 f"{wall:.1f}s")
     best = {D: max((r for r in runs if r["tpot_slo_ms"] == D and r["policy"] != "SLOWeave"),
                    key=lambda r: r["goodput_req_s"]) for D in (25.0, 10.0)}

@@ -73,6 +73,8 @@ def metrics(trace, token_ns, ttft_slo_ms: float, tpot_slo_ms: float) -> dict:
     return {
         "requests": n,
         "met": int(meets.sum()),
+        "ttft_missed": int(np.sum(ttft > ttft_slo)),
+        "tpot_missed": int(np.sum(tpot > tpot_slo)),
         "slo_attainment": float(meets.mean()),
         "goodput_req_s": float(meets.sum()) / span * 1e9 if span > 0 else float("nan"),
         "throughput_req_s": n / makespan * 1e9,

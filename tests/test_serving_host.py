@@ -112,6 +112,9 @@ def test_metrics_match_oracle():
         assert got["p50_ttft_ms"] * 1e6 == pytest.approx(ref["p50_ttft_ns"], abs=0.5)
         assert got["p99_tpot_ms"] * 1e6 == pytest.approx(ref["p99_tpot_ns"], abs=0.5)
         assert got["goodput_req_s"] == pytest.approx(ref["goodput_num"] / ref["goodput_den_ns"] * 1e9)
+        per = [V.request_metrics(r, res.token_ns[r.rid].tolist(), 1000 * MS, D * MS) for r in _oracle_reqs(tr)]
+        assert got["ttft_missed"] == sum(m.ttft_ns > 1000 * MS for m in per)
+        assert got["tpot_missed"] == sum(m.tpot_p99_ns > D * MS for m in per)
 
 
 def test_sloweave_beats_fixed_at_tight_tpot_in_simulation():
