@@ -171,8 +171,9 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  *   ws     device workspace of ws_bytes >= slw_workspace_size(ctx, C, B)
  * Reserves KV room (prefill_seq up to prefix_len + C, each decode up to
  * context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
- * it), builds the slot mapping and block tables on the host, uploads them
- * through a pinned staging ring, then enqueues per layer: RMSNorm, QKV GEMM
+ * it), builds the slot mapping and block tables on the host, writes them to
+ * a coherent pinned staging ring that a first kernel copies into the
+ * workspace, then enqueues per layer: RMSNorm, QKV GEMM
  * whose epilogue applies RoPE and appends K/V to the pages, chunk attention
  * and split decode attention, output GEMM + residual (kept in fp32 within the
  * layer), RMSNorm, gate/up GEMM with SiLU*mul, down GEMM + residual.

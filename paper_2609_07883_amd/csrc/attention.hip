@@ -21,10 +21,33 @@ namespace slw {
 namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
-// LDS tiles in the chunk-attention ring: two (64 KB) let two work-groups
-// share a CU, which measured slightly ahead of three or four tiles (96 or
-// 128 KB, one work-group per CU) on the long-context and layer-sweep shapes.
+// LDS tiles in the chunk-attention ring: two (64 KB) measured slightly ahead
+// of three or four (96 or 128 KB) on the long-context and layer-sweep shapes.
+// The kernel's registers (about 200 per lane) allow one work-group per CU.
 constexpr int kChunkStages = 2;
+
+// 2^x straight on the transcendental unit (v_exp_f32).  Results below
+// 2^-126 may flush to zero, which softmax weights taken relative to a running
+// maximum can afford; the library exp2f adds range scaling around the same
+// instruction, five more VALU operations per call.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Max and sum over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the four 16-lane rows
+// of a wave), with the gfx950 row-swap instructions instead of LDS permutes:
+// a swap of a register with itself leaves, in every lane, its own value in
+// one result and its partner's in the other.
+__device__ __forceinline__ float rows4_max(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 __device__ __forceinline__ bf16x8 cat44(bf16x4 lo, bf16x4 hi) {
     return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
@@ -53,14 +76,27 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // global->LDS loads issued ST - 1 tiles ahead (each lane fetches the 16-byte
 // chunk that belongs at its swizzled LDS slot; every wave issues the same
 // number of loads per tile, so a counted wait for its own loads plus a bare
-// barrier publishes a tile).  A work item covers one key range of one query tile; in
-// split mode it writes fp32 partials (running max, sum, unnormalised output)
-// that chunk_merge_kernel combines.
+// barrier publishes a tile).  A work item covers one key range of one query
+// tile, and a work-group runs the items of its slot one after the other (the
+// host cuts the keys of all query tiles into equal runs, one per work-group).
+// A query tile covered by one item is normalised and stored directly; the
+// items of a query tile split over several write fp32 partials (running max,
+// sum, unnormalised output) that chunk_merge_kernel combines.
 // ---------------------------------------------------------------------------
 
+// Keys of the two score tiles of a pair of pages (32 keys): row r of tile
+// tau holds key 16 (r / 8) + 8 ((r / 4) % 2) + 4 tau + r % 4, so that lane
+// group g (rows 4 g .. 4 g + 3 of both tiles) ends up with keys 8 g .. 8 g + 7:
+// the eight consecutive tokens of one page that the P V product's k slice g
+// covers, and one 16-byte chunk of a dim-major V page.
+__device__ __forceinline__ int pair_key(int r, int tau) { return 16 * (r >> 3) + 8 * ((r >> 2) & 1) + 4 * tau + (r & 3); }
+
 // LDS swizzles of 16-byte chunks: K rows (64 B = four chunks of 8 dims) and
-// V rows (32 B = two chunks of 8 tokens).
-__device__ __forceinline__ int kswz(int t, int sub) { return sub ^ ((t >> 1) & 3); }
+// V rows (32 B = two chunks of 8 tokens).  An operand read serves eight lanes
+// per pass: for K the rows of tokens {0..3, 8..11} or {4..7, 12..15} of a
+// page, for V eight consecutive dims; both swizzles put those on distinct
+// banks.
+__device__ __forceinline__ int kswz(int t, int sub) { return sub ^ (((t >> 1) & 1) | (((t >> 3) & 1) << 1)); }
 __device__ __forceinline__ int vswz(int d, int h) { return h ^ ((d >> 2) & 1); }
 
 // Direct global->LDS load of 16 bytes per lane: lane l's bytes land at
@@ -105,29 +141,10 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
-    const int item = blockIdx.x, kvh = blockIdx.y;
-    const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
-    const int p0 = qt * PWG + wave * PW; // first chunk position of this wave
-    const int n_tiles = (ke - kb + 63) / 64;
+    const int kvh = blockIdx.y;
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
-    const int wave_qpos_lo = a.prefix + p0, wave_qpos_hi = a.prefix + p0 + PW - 1;
-    const bool wave_live = p0 < a.c;
-
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
-
-    // Q^T operand: row r = ct*16 + col is position p0 + r / GROUP, head kvh*GROUP + r % GROUP
-    bf16x8 qf[CT][KK];
-    const bf16* qkv = static_cast<const bf16*>(a.qkv);
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-        const int r = ct * 16 + col, qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-            qf[ct][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
-                                        qkv + static_cast<size_t>(qi) * a.ld_qkv + h * HD + kk * 32 + grp * 8)
-                                  : bf16x8{};
-    }
 
     // Load j of a tile (j = wave + 8 i): 0 .. 4 KK - 1 are K slabs (page j / KK,
     // dims 32 (j % KK) ..), the rest V slabs (page, 32 dims of 16 tokens).
@@ -144,7 +161,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
         l_isv[i] = is_v;
         l_page[i] = p;
         if (!is_v) {  // lane: token t, stored chunk lane % 4 holds dims chunk kswz(t, .)
-            const int t = lane >> 2, sub = (lane & 3) ^ ((t >> 1) & 3);
+            const int t = lane >> 2, sub = kswz(t, lane & 3);
             l_elem[i] = slab * 512 + t * 32 + sub * 8;
         } else {      // lane: dim d, stored chunk lane % 2 holds tokens 8 vswz(d, .)
             const int d = slab * 32 + (lane >> 1), h = (lane & 1) ^ ((d >> 2) & 1);
@@ -157,181 +174,204 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // for every direct load in flight before using its result.
     typedef const int32_t __attribute__((address_space(4))) const_i32;
     const const_i32* bt_s = (const const_i32*)a.bt;
-    const int last_page = (ke - 1) >> 4;
-    auto issue = [&](int t) {
-        const int buf = t % ST;
+    const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
+    for (int item = i0; item < i1; ++item) {
+        const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
+        const int p0 = qt * PWG + wave * PW; // first chunk position of this wave
+        const int n_tiles = (ke - kb + 63) / 64;
+        const int wave_qpos_lo = a.prefix + p0, wave_qpos_hi = a.prefix + p0 + PW - 1;
+        const bool wave_live = p0 < a.c;
+        // a query tile covered by one item is written here, else as a partial
+        const bool whole = a.qt_off[qt + 1] - a.qt_off[qt] == 1;
+
+        // Q^T operand: row r = ct*16 + col is position p0 + r / GROUP, head kvh*GROUP + r % GROUP
+        bf16x8 qf[CT][KK];
+        const bf16* qkv = static_cast<const bf16*>(a.qkv);
 #pragma unroll
-        for (int i = 0; i < PER_WAVE; ++i) {
-            const int pg = __builtin_amdgcn_readfirstlane(min((kb >> 4) + 4 * t + l_page[i], last_page));
-            const size_t blk = bt_s[pg];
-            const bf16* src = (l_isv[i] ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + l_elem[i];
-            load_lds16(src, l_isv[i] ? &Vs[buf][l_dst[i]] : &Ks[buf][l_dst[i]]);
+        for (int ct = 0; ct < CT; ++ct) {
+            const int r = ct * 16 + col, qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk)
+                qf[ct][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
+                                            qkv + static_cast<size_t>(qi) * a.ld_qkv + h * HD + kk * 32 + grp * 8)
+                                      : bf16x8{};
         }
-    };
 
-    f32x4 o[CT][NT];
+        const int last_page = (ke - 1) >> 4;
+        auto issue = [&](int t) {
+            const int buf = t % ST;
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) o[ct][nt] = f32x4{};
-    float m_run[CT], l_run[CT];
-    int qpos_col[CT];  // query position of row ct*16 + col
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-        m_run[ct] = -INFINITY;
-        l_run[ct] = 0.f;
-        qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
-    }
+            for (int i = 0; i < PER_WAVE; ++i) {
+                const int pg = __builtin_amdgcn_readfirstlane(min((kb >> 4) + 4 * t + l_page[i], last_page));
+                const size_t blk = bt_s[pg];
+                const bf16* src = (l_isv[i] ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + l_elem[i];
+                load_lds16(src, l_isv[i] ? &Vs[buf][l_dst[i]] : &Ks[buf][l_dst[i]]);
+            }
+        };
 
-    // Q fragments land before the ring starts; the compiler then has no
-    // loads of its own pending inside the loop, so it adds no waits there.
-    wait_vmcnt<0>();
+        f32x4 o[CT][NT];
 #pragma unroll
-    for (int t = 0; t < ST - 1; ++t)
-        if (t < n_tiles) issue(t);
-    for (int t = 0; t < n_tiles; ++t) {
-        const int buf = t % ST;
-        // this wave's loads of tile t are done once at most the loads of the
-        // younger tiles in flight (up to ST - 2 of them) are outstanding
-        const int younger = min(n_tiles - 1 - t, ST - 2);
-        if (ST >= 4 && younger >= 2) wait_vmcnt<2 * PER_WAVE>();
-        else if (ST >= 3 && younger >= 1) wait_vmcnt<PER_WAVE>();
-        else wait_vmcnt<0>();
-        barrier_only();
-        if (t + ST - 1 < n_tiles) issue(t + ST - 1);
-        const int key0 = kb + t * 64;
-        if (wave_live && key0 <= wave_qpos_hi) {
-            f32x4 sc[4][CT];  // [page][ct]
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-            for (int p = 0; p < 4; ++p)
+            for (int nt = 0; nt < NT; ++nt) o[ct][nt] = f32x4{};
+        float m_run[CT], l_run[CT];
+        int qpos_col[CT];  // query position of row ct*16 + col
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct) sc[p][ct] = f32x4{};
+        for (int ct = 0; ct < CT; ++ct) {
+            m_run[ct] = -INFINITY;
+            l_run[ct] = 0.f;
+            qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
+        }
+
+        // Q fragments land before the ring starts; the compiler then has no
+        // loads of its own pending inside the loop, so it adds no waits there.
+        wait_vmcnt<0>();
+        // every wave is past the previous item's last tile before its buffers refill
+        if (item != i0) barrier_only();
 #pragma unroll
-            for (int p = 0; p < 4; ++p)
-#pragma unroll
-                for (int kk = 0; kk < KK; ++kk) {
-                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-                        &Ks[buf][p * PAGE + kk * 512 + col * 32 + kswz(col, grp) * 8]);
-#pragma unroll
-                    for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
-                }
-            const bool need_mask = key0 + 63 > wave_qpos_lo || key0 + 63 >= ke;
-            float mx[CT];
-            bool grow = false;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                float m = -INFINITY;
+        for (int t = 0; t < ST - 1; ++t)
+            if (t < n_tiles) issue(t);
+        for (int t = 0; t < n_tiles; ++t) {
+            const int buf = t % ST;
+            // this wave's loads of tile t are done once at most the loads of the
+            // younger tiles in flight (up to ST - 2 of them) are outstanding
+            const int younger = min(n_tiles - 1 - t, ST - 2);
+            if (ST >= 4 && younger >= 2) wait_vmcnt<2 * PER_WAVE>();
+            else if (ST >= 3 && younger >= 1) wait_vmcnt<PER_WAVE>();
+            else wait_vmcnt<0>();
+            barrier_only();
+            if (t + ST - 1 < n_tiles) issue(t + ST - 1);
+            const int key0 = kb + t * 64;
+            if (wave_live && key0 <= wave_qpos_hi) {
+                f32x4 sc[4][CT];  // [2 pair + tile][ct]
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float x = sc[p][ct][e];
-                        if (need_mask) {
-                            const int kpos = key0 + p * 16 + grp * 4 + e;
-                            x = (kpos <= qpos_col[ct] && kpos < ke) ? x : -INFINITY;
-                            sc[p][ct][e] = x;
-                        }
-                        m = fmaxf(m, x);
+                    for (int ct = 0; ct < CT; ++ct) sc[p][ct] = f32x4{};
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    const int key = pair_key(col, p & 1), tok = key & 15;
+                    const int base = (2 * (p >> 1) + (key >> 4)) * PAGE + tok * 32 + kswz(tok, grp) * 8;
+#pragma unroll
+                    for (int kk = 0; kk < KK; ++kk) {
+                        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[buf][base + kk * 512]);
+#pragma unroll
+                        for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
                     }
-                m = fmaxf(m, __shfl_xor(m, 16, 64));
-                m = fmaxf(m, __shfl_xor(m, 32, 64));
-                mx[ct] = m * sl2;
-                grow |= mx[ct] > m_run[ct] + kSlack;
-            }
-            if (__any(grow)) {  // wave-uniform: move every row's max up to its tile max
+                }
+                const bool need_mask = key0 + 63 > wave_qpos_lo || key0 + 63 >= ke;
+                float mx[CT];
+                bool grow = false;
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct) {
-                    const float m_new = fmaxf(m_run[ct], mx[ct]);
-                    const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run[ct] - m_new);
-                    l_run[ct] *= alpha;
-                    m_run[ct] = m_new;
+                    float m = -INFINITY;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float ae = __shfl(alpha, grp * 4 + e, 64);
-#pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
-                    }
-                }
-            }
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                const float m_use = m_run[ct] == -INFINITY ? 0.f : m_run[ct];
-                float ls = 0.f;
-#pragma unroll
-                for (int p = 0; p < 4; ++p)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float v = exp2f(fmaf(sc[p][ct][e], sl2, -m_use));
-                        sc[p][ct][e] = v;
-                        ls += v;
-                    }
-                l_run[ct] += ls;
-            }
-            // keys at or past ke (the range end; unwritten slots lie past
-            // key_lim >= ke, stand-in pages past ke) have probability 0; their
-            // V values are zeroed too so that whatever the pool holds there
-            // cannot turn 0 into NaN
-            const bool v_mask = key0 + 63 >= ke;
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                bf16x8 pf[CT];
-#pragma unroll
-                for (int ct = 0; ct < CT; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    const int d = nt * 16 + col;
-                    const int off = d * 16 + vswz(d, grp >> 1) * 8 + (grp & 1) * 4;
-                    bf16x4 lo = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j) * PAGE + off]);
-                    bf16x4 hi = *reinterpret_cast<const bf16x4*>(&Vs[buf][(2 * j + 1) * PAGE + off]);
-                    if (v_mask) {
-                        const int k_lo = key0 + 2 * j * 16 + grp * 4;
+                    for (int p = 0; p < 4; ++p)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            if (k_lo + e >= ke) lo[e] = bf16(0.0f);
-                            if (k_lo + 16 + e >= ke) hi[e] = bf16(0.0f);
+                            float x = sc[p][ct][e];
+                            if (need_mask) {
+                                const int kpos = key0 + 32 * (p >> 1) + pair_key(4 * grp + e, p & 1);
+                                x = (kpos <= qpos_col[ct] && kpos < ke) ? x : -INFINITY;
+                                sc[p][ct][e] = x;
+                            }
+                            m = fmaxf(m, x);
+                        }
+                    m = rows4_max(m);
+                    mx[ct] = m * sl2;
+                    grow |= mx[ct] > m_run[ct] + kSlack;
+                }
+                if (__any(grow)) {  // wave-uniform: move every row's max up to its tile max
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) {
+                        const float m_new = fmaxf(m_run[ct], mx[ct]);
+                        const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[ct] - m_new);
+                        l_run[ct] *= alpha;
+                        m_run[ct] = m_new;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                            for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
                         }
                     }
-                    const bf16x8 vf = cat44(lo, hi);
+                }
 #pragma unroll
-                    for (int ct = 0; ct < CT; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
+                for (int ct = 0; ct < CT; ++ct) {
+                    const float m_use = m_run[ct] == -INFINITY ? 0.f : m_run[ct];
+                    float ls = 0.f;
+#pragma unroll
+                    for (int p = 0; p < 4; ++p)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float v = fast_exp2(fmaf(sc[p][ct][e], sl2, -m_use));
+                            sc[p][ct][e] = v;
+                            ls += v;
+                        }
+                    l_run[ct] += ls;
+                }
+                // keys at or past ke (the range end; unwritten slots lie past
+                // key_lim >= ke, stand-in pages past ke) have probability 0; their
+                // V values are zeroed too so that whatever the pool holds there
+                // cannot turn 0 into NaN
+                const bool v_mask = key0 + 63 >= ke;
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    bf16x8 pf[CT];
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
+                    // k slice grp = tokens 8 (grp % 2) .. + 7 of page 2 j + grp / 2
+                    const int v_base = (2 * j + (grp >> 1)) * PAGE;
+                    const int k_lo = key0 + 32 * j + 8 * grp;
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const int d = nt * 16 + col;
+                        bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vs[buf][v_base + d * 16 + vswz(d, grp & 1) * 8]);
+                        if (v_mask) {
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                if (k_lo + e >= ke) vf[e] = bf16(0.0f);
+                        }
+#pragma unroll
+                        for (int ct = 0; ct < CT; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
+                    }
                 }
             }
         }
-    }
-    if (!wave_live) return;
+        if (!wave_live) continue;
 
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-        float l = l_run[ct];
-        l += __shfl_xor(l, 16, 64);
-        l += __shfl_xor(l, 32, 64);
-        if (a.split) {
-            const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 32 + ct * 16;
-            if (grp == 0) {
-                a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
-                a.part_ml[(rbase + col) * 2 + 1] = l;
-            }
+        for (int ct = 0; ct < CT; ++ct) {
+            float l = l_run[ct];
+            l = rows4_sum(l);
+            if (!whole) {
+                const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 32 + ct * 16;
+                if (grp == 0) {
+                    a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
+                    a.part_ml[(rbase + col) * 2 + 1] = l;
+                }
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-                    a.part_o[(rbase + grp * 4 + e) * HD + nt * 16 + col] = o[ct][nt][e];
-        } else {
-            bf16* out = static_cast<bf16*>(a.out);
-            const int ldo = a.hq * HD;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = ct * 16 + grp * 4 + e;
-                const int qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
-                const float inv = 1.0f / __shfl(l, grp * 4 + e, 64);
-                if (qi < a.c) {
+                for (int e = 0; e < 4; ++e)
 #pragma unroll
                     for (int nt = 0; nt < NT; ++nt)
-                        out[static_cast<size_t>(qi) * ldo + h * HD + nt * 16 + col] = f2bf(o[ct][nt][e] * inv);
+                        a.part_o[(rbase + grp * 4 + e) * HD + nt * 16 + col] = o[ct][nt][e];
+            } else {
+                bf16* out = static_cast<bf16*>(a.out);
+                const int ldo = a.hq * HD;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = ct * 16 + grp * 4 + e;
+                    const int qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
+                    const float inv = 1.0f / __shfl(l, grp * 4 + e, 64);
+                    if (qi < a.c) {
+#pragma unroll
+                        for (int nt = 0; nt < NT; ++nt)
+                            out[static_cast<size_t>(qi) * ldo + h * HD + nt * 16 + col] = f2bf(o[ct][nt][e] * inv);
+                    }
                 }
             }
         }
-    }
+    }  // items of this work-group
 }
 
 // Combine the key-range partials of one (chunk position, q head).
@@ -343,6 +383,7 @@ __global__ __launch_bounds__(64) void chunk_merge_kernel(ChunkAttnArgs a) {
     const int qt = pos / PWG;
     const int row = (pos % PWG) * GROUP + h % GROUP;
     const int w0 = a.qt_off[qt], w1 = a.qt_off[qt + 1];
+    if (w1 - w0 == 1) return;  // written by the attention kernel
     float mmax = -INFINITY;
     for (int w = w0; w < w1; ++w)
         mmax = fmaxf(mmax, a.part_ml[((static_cast<size_t>(w) * a.hkv + kvh) * 256 + row) * 2]);
@@ -464,12 +505,11 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
                 s[p][e] = x;
                 mx = fmaxf(mx, x);
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        mx = rows4_max(mx);
         mx *= sl2;
         if (__any(mx > m_run + kSlack)) {
             const float m_new = fmaxf(m_run, mx);
-            const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+            const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
             l_run *= alpha;
             m_run = m_new;
 #pragma unroll
@@ -485,7 +525,7 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
         for (int p = 0; p < 2; ++p)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float v = exp2f(fmaf(s[p][e], sl2, -m_use));
+                const float v = fast_exp2(fmaf(s[p][e], sl2, -m_use));
                 s[p][e] = v;
                 ls += v;
             }
@@ -506,8 +546,7 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
     }
 
     float l = l_run;
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    l = rows4_sum(l);
     const size_t hbase = static_cast<size_t>(w) * a.hq + kvh * group;
     if (grp == 0 && col < group) {
         a.part_ml[(hbase + col) * 2 + 0] = m_run;
@@ -548,7 +587,7 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
 
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
-    chunk_attn_kernel<HD, GROUP, kChunkStages><<<dim3(a.n_items, a.hkv), 512, 0, s>>>(a);
+    chunk_attn_kernel<HD, GROUP, kChunkStages><<<dim3(a.n_slots, a.hkv), 512, 0, s>>>(a);
     if (a.split) chunk_merge_kernel<HD, GROUP><<<dim3(a.c, a.hq), 64, 0, s>>>(a);
 }
 

@@ -96,7 +96,30 @@ __global__ void sweep_kernel(uint32_t* p, size_t n4, uint32_t key) {
     if (x == key) p[0] = x;
 }
 
+// Copy n words from coherent host memory mapped into the device's address
+// space: one 16-byte read per thread over the bus, then a tail of single
+// words.  Done by a kernel rather than the copy engine so that the copy is
+// ordered with the kernels around it on the stream without a hand-off
+// between engines.
+__global__ void copy_from_host_kernel(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src, size_t n) {
+    const size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
+    const size_t n4 = n / 4;
+    if (i < n4) {
+        reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+    } else if (i < n4 + (n & 3)) {
+        const size_t w = 4 * n4 + (i - n4);
+        dst[w] = src[w];
+    }
+}
+
 }  // namespace
+
+void launch_copy_from_host(void* dst, const void* src, size_t words, hipStream_t s) {
+    if (words == 0) return;
+    const size_t threads = words / 4 + (words & 3);
+    copy_from_host_kernel<<<static_cast<unsigned>((threads + 255) / 256), 256, 0, s>>>(
+        static_cast<uint32_t*>(dst), static_cast<const uint32_t*>(src), words);
+}
 
 void launch_rmsnorm(const void* x, bool x_f32, const void* g, void* y, int rows, int d, float eps,
                     hipStream_t s) {

@@ -26,7 +26,12 @@ namespace {
 
 constexpr int kRing = 4;                 // pinned staging buffers in flight
 constexpr int kDecodeTargetWaves = 4096; // decode work-groups aimed for per iteration
-constexpr int kChunkTargetWgs = 512;     // chunk-attention work-groups aimed for per iteration
+// Chunk attention runs one work-group per CU (its register use allows no
+// more), so a launch of kChunkSlots work-groups with equal work finishes in
+// one round on a 256-CU part.  A work-group takes at least kChunkMinTiles
+// 64-key tiles, which keeps its fixed costs (Q load, partial write) small.
+constexpr int kChunkSlots = 256;
+constexpr int kChunkMinTiles = 4;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -53,7 +58,8 @@ struct slw_ctx {
 
     // HIP resources, created on first device use
     bool hip_ready = false;
-    int32_t* staging[kRing] = {};
+    int32_t* staging[kRing] = {};      // coherent pinned host memory
+    int32_t* staging_dev[kRing] = {};  // the same memory's device address
     size_t staging_cap[kRing] = {};
     hipEvent_t staged[kRing] = {};
     int ring = 0;
@@ -97,8 +103,9 @@ int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
 int chunk_tiles(const slw_model_cfg& c, int C) {
     return static_cast<int>(ceil_div(C, chunk_tile_positions(c.n_q_heads / c.n_kv_heads)));
 }
+int chunk_slot_cap(const slw_model_cfg& c) { return std::max(1, kChunkSlots / c.n_kv_heads); }
 int chunk_item_cap(const slw_model_cfg& c, int C) {
-    return C > 0 ? chunk_tiles(c, C) + static_cast<int>(ceil_div(kChunkTargetWgs, c.n_kv_heads)) + 1 : 0;
+    return C > 0 ? chunk_tiles(c, C) + chunk_slot_cap(c) : 0;
 }
 
 size_t meta_ints(const slw_model_cfg& c, int C, int B) {
@@ -106,7 +113,7 @@ size_t meta_ints(const slw_model_cfg& c, int C, int B) {
     const size_t mb = static_cast<size_t>(max_blocks(c));
     return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + mb +
            2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + 3 * static_cast<size_t>(chunk_item_cap(c, C)) +
-           chunk_tiles(c, C) + 1;
+           chunk_tiles(c, C) + 1 + chunk_slot_cap(c) + 1;
 }
 
 struct Layout {
@@ -174,7 +181,9 @@ int ensure_hip(slw_ctx* ctx) {
     return SLW_OK;
 }
 
-// Pinned buffer of the next ring slot with room for n ints (waits for its last copy).
+// Pinned buffer of the next ring slot with room for n ints (waits for its
+// last copy).  The buffers are coherent and mapped: the iteration's first
+// kernel reads them over the bus, so the upload needs no copy engine.
 int next_staging(slw_ctx* ctx, size_t n, int32_t** buf, int* slot_out) {
     const int slot = ctx->ring;
     ctx->ring = (ctx->ring + 1) % kRing;
@@ -182,11 +191,15 @@ int next_staging(slw_ctx* ctx, size_t n, int32_t** buf, int* slot_out) {
     if (ctx->staging_cap[slot] < n) {
         if (ctx->staging[slot]) HIP_TRY(hipHostFree(ctx->staging[slot]));
         ctx->staging[slot] = nullptr;
+        ctx->staging_dev[slot] = nullptr;
         ctx->staging_cap[slot] = 0;
         size_t cap = std::max<size_t>(n, 1 << 16);
         void* p = nullptr;
-        HIP_TRY(hipHostMalloc(&p, cap * 4, hipHostMallocDefault));
+        HIP_TRY(hipHostMalloc(&p, cap * 4, hipHostMallocMapped | hipHostMallocCoherent));
         ctx->staging[slot] = static_cast<int32_t*>(p);
+        void* dp = nullptr;
+        HIP_TRY(hipHostGetDevicePointer(&dp, p, 0));
+        ctx->staging_dev[slot] = static_cast<int32_t*>(dp);
         ctx->staging_cap[slot] = cap;
     }
     *buf = ctx->staging[slot];
@@ -314,32 +327,62 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
         }
         m[o_workoff + B] = w;
     }
-    // chunk attention work items: (query tile, key range); split the key axis
-    // when the query tiles alone give too few work-groups
+    // Chunk attention work.  The 64-key tiles of every query tile, laid end
+    // to end, are cut into equal runs, one per work-group of each kv head; a
+    // run that crosses query tiles becomes one item per query tile it
+    // touches.  A query tile covered by one item is written directly, one
+    // covered by several is combined by the merge kernel.
     const int n_qt = C > 0 ? chunk_tiles(c, C) : 0;
     const int pwg = chunk_tile_positions(c.n_q_heads / c.n_kv_heads);
-    int64_t ckeys = 0;
-    for (int q = 0; q < n_qt; ++q) ckeys += P + std::min(C, (q + 1) * pwg);
-    int64_t span = INT64_MAX;
-    if (static_cast<int64_t>(n_qt) * c.n_kv_heads < kChunkTargetWgs && n_qt > 0) {
-        span = ceil_div(ckeys * c.n_kv_heads, kChunkTargetWgs);
-        span = std::max<int64_t>(256, ceil_div(span, 64) * 64);
-    }
+    std::vector<int64_t> tile_end(n_qt + 1, 0);
+    for (int q = 0; q < n_qt; ++q) tile_end[q + 1] = tile_end[q] + ceil_div(P + std::min(C, (q + 1) * pwg), 64);
+    const int64_t total_tiles = tile_end[n_qt];
+    int n_slots = 0;
     std::vector<int32_t>& it = ctx->items;
     it.clear();
+    std::vector<int32_t> slot_off;
+    if (n_qt > 0) {
+        int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
+        const int64_t per = ceil_div(total_tiles, want);
+        n_slots = static_cast<int>(ceil_div(total_tiles, per));
+        slot_off.resize(n_slots + 1);
+        int q = 0;
+        for (int sl = 0; sl < n_slots; ++sl) {
+            slot_off[sl] = static_cast<int32_t>(it.size() / 3);
+            int64_t t0 = sl * per;
+            const int64_t t1 = std::min(total_tiles, t0 + per);
+            while (t0 < t1) {
+                while (tile_end[q + 1] <= t0) ++q;
+                const int64_t seg_end = std::min(t1, tile_end[q + 1]);
+                const int64_t ke_q = P + std::min(C, (q + 1) * pwg);
+                it.push_back(q);
+                it.push_back(static_cast<int32_t>((t0 - tile_end[q]) * 64));
+                it.push_back(static_cast<int32_t>(std::min(ke_q, (seg_end - tile_end[q]) * 64)));
+                t0 = seg_end;
+            }
+        }
+        slot_off[n_slots] = static_cast<int32_t>(it.size() / 3);
+    }
     std::vector<int32_t> qt_off(n_qt + 1);
-    for (int q = 0; q < n_qt; ++q) {
-        qt_off[q] = static_cast<int32_t>(it.size() / 3);
-        const int64_t ke = P + std::min(C, (q + 1) * pwg);
-        for (int64_t kb = 0; kb < ke; kb += span) {
-            it.push_back(q);
-            it.push_back(static_cast<int32_t>(kb));
-            it.push_back(static_cast<int32_t>(std::min(ke, kb + span)));
+    {
+        int i = 0;
+        const int n_it = static_cast<int>(it.size() / 3);
+        for (int q = 0; q <= n_qt; ++q) {
+            while (i < n_it && it[3 * i] < q) ++i;
+            qt_off[q] = i;
         }
     }
-    qt_off[n_qt] = static_cast<int32_t>(it.size() / 3);
     const int n_items = static_cast<int>(it.size() / 3);
-    if (n_items > chunk_item_cap(c, C)) return fail(SLW_EINVAL, "internal: chunk items %d above cap", n_items);
+    if (n_items > chunk_item_cap(c, C) || n_slots > chunk_slot_cap(c))
+        return fail(SLW_EINVAL, "internal: chunk items %d / slots %d above cap", n_items, n_slots);
+    for (int q = 0; q < n_qt; ++q) {  // the items of each query tile tile its key range
+        int64_t at = 0;
+        for (int i = qt_off[q]; i < qt_off[q + 1]; ++i) {
+            if (it[3 * i + 1] != at || it[3 * i + 2] <= at) return fail(SLW_EINVAL, "internal: chunk plan");
+            at = it[3 * i + 2];
+        }
+        if (at != P + std::min(C, (q + 1) * pwg)) return fail(SLW_EINVAL, "internal: chunk plan");
+    }
     const size_t o_item = m.size();
     m.resize(m.size() + 3 * static_cast<size_t>(n_items));
     for (int i = 0; i < n_items; ++i) {
@@ -347,8 +390,12 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
         m[o_item + n_items + i] = it[3 * i + 1];
         m[o_item + 2 * n_items + i] = it[3 * i + 2];
     }
+    const size_t o_slot = m.size();
+    m.insert(m.end(), slot_off.begin(), slot_off.end());
     const size_t o_qtoff = m.size();
     m.insert(m.end(), qt_off.begin(), qt_off.end());
+
+    if (m.size() > meta_ints(c, C, B)) return fail(SLW_EINVAL, "internal: metadata %zu ints above its region", m.size());
 
     // ---- upload ----
     int32_t* stage = nullptr;
@@ -358,7 +405,8 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     std::memcpy(stage, m.data(), m.size() * 4);
     char* wsb = static_cast<char*>(ws);
     int32_t* dmeta = reinterpret_cast<int32_t*>(wsb + L.meta);
-    HIP_TRY(hipMemcpyAsync(dmeta, stage, m.size() * 4, hipMemcpyHostToDevice, stream));
+    launch_copy_from_host(dmeta, ctx->staging_dev[slot], m.size(), stream);
+    HIP_TRY(hipGetLastError());
     HIP_TRY(hipEventRecord(ctx->staged[slot], stream));
 
     const int32_t* d_slot = dmeta;
@@ -437,7 +485,9 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             ca.hkv = hkv;
             ca.hd = hd;
             ca.ld_qkv = qw;
+            ca.slot_off = dmeta + o_slot;
             ca.n_items = n_items;
+            ca.n_slots = n_slots;
             ca.split = n_items > n_qt ? 1 : 0;
             launch_chunk_attention(ca, stream);
         }

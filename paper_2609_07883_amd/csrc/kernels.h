@@ -68,10 +68,12 @@ struct ChunkAttnArgs {
     const int32_t* item_kb;   // [n_items] multiple of 64
     const int32_t* item_ke;   // [n_items]
     const int32_t* qt_off;    // [n_qt + 1] first item of each query tile
-    float* part_o;            // [n_items][hkv][256][hd]   (split mode)
+    const int32_t* slot_off;  // [n_slots + 1] first item of each work-group (per kv head)
+    float* part_o;            // [n_items][hkv][256][hd]   (items of split query tiles)
     float* part_ml;           // [n_items][hkv][256][2]
     int c, prefix, hq, hkv, hd, ld_qkv;
-    int n_items, split;       // split: partials + merge instead of direct stores
+    int n_items, n_slots;
+    int split;                // some query tile has several items: the merge kernel runs
 };
 // Query positions per work-group for a group size (rows / group).
 inline int chunk_tile_positions(int group) { return 256 / group; }
@@ -95,6 +97,10 @@ struct DecodeAttnArgs {
 };
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
 void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s);
+
+// Copy `words` 32-bit words from coherent, mapped host memory (its device
+// address; both pointers 16-byte aligned) to device memory, as a kernel.
+void launch_copy_from_host(void* dst, const void* src, size_t words, hipStream_t s);
 
 // Read `bytes` of device memory (last-level cache flush that leaves no dirty
 // lines); the buffer is written only if a thread's xor of its words equals key.
