@@ -78,12 +78,12 @@ def stage_work(shape, C, P, B, ctx_sum):
     kvb = hkv * hd * 2 * 2                      # K and V bytes per token
     w = {}
     w["rmsnorm_attn"] = (0, M * d * 2 * 2)
-    w["rope_table"] = (0, M * hd // 2 * 8)
+    w["rope_table"] = (0, 0)    # the table is filled by the iteration's setup kernel, before the stage events
     w["qkv_gemm"] = (2 * M * qw * d, qw * d * 2 + M * d * 2 + M * qw * 2 + M * kvb // 2 * 2)
     w["chunk_attn"] = (4 * hq * hd * (C * P + C * (C + 1) // 2),
                        (P + C) * kvb + C * hq * hd * 2 * 2)
     w["decode_attn"] = (4 * hq * hd * ctx_sum, ctx_sum * kvb + B * hq * hd * 2)
-    w["decode_merge"] = (0, 0)
+    w["attn_merge"] = (0, 0)
     w["o_gemm"] = (2 * M * d * hq * hd, d * hq * hd * 2 + M * hq * hd * 2 + M * d * (2 + 4))
     w["rmsnorm_mlp"] = (0, M * d * (4 + 2))
     w["gateup_gemm"] = (2 * M * 2 * F * d, 2 * F * d * 2 + M * d * 2 + M * F * 2)

@@ -211,9 +211,13 @@ int slw_workspace_view(slw_ctx* ctx, int32_t which, int32_t C, int32_t B, size_t
  * before the most recent one (0 = most recent) and writes, per stage, its
  * elapsed milliseconds summed over layers:
  *   0 RMSNorm (attention)  1 RoPE table    2 QKV GEMM with RoPE and KV append
- *   3 chunk attention      4 decode attention  5 decode merge  6 output GEMM
+ *   3 chunk attention      4 decode attention  5 attention merges (split
+ *   chunk query tiles and decode key splits, one launch)  6 output GEMM
  *   7 RMSNorm (MLP)        8 gate/up GEMM  9 down GEMM
- * Stages absent from that iteration (C == 0 or B == 0) read 0.
+ * Stages absent from that iteration (C == 0 or B == 0) read 0.  Stage 1 is
+ * kept for the layout of the array and reads (close to) 0: the RoPE table is
+ * filled by the iteration's first kernel, together with the metadata copy,
+ * before stage 0 of layer 0.
  */
 #define SLW_N_STAGES 10
 int slw_set_stage_timing(slw_ctx* ctx, int32_t depth);

@@ -37,7 +37,7 @@ EXPORTS = (
     "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
     "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
 )
-STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "decode_merge",
+STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "attn_merge",
           "o_gemm", "rmsnorm_mlp", "gateup_gemm", "down_gemm")
 
 

@@ -81,7 +81,7 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // host cuts the keys of all query tiles into equal runs, one per work-group).
 // A query tile covered by one item is normalised and stored directly; the
 // items of a query tile split over several write fp32 partials (running max,
-// sum, unnormalised output) that chunk_merge_kernel combines.
+// sum, unnormalised output) that attn_merge_kernel combines.
 // ---------------------------------------------------------------------------
 
 // Keys of the two score tiles of a pair of pages (32 keys): row r of tile
@@ -374,11 +374,10 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     }  // items of this work-group
 }
 
-// Combine the key-range partials of one (chunk position, q head).
+// Combine the key-range partials of one (chunk position, q head); 64 threads.
 template <int HD, int GROUP>
-__global__ __launch_bounds__(64) void chunk_merge_kernel(ChunkAttnArgs a) {
+__device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int pos, int h) {
     constexpr int PWG = 256 / GROUP;
-    const int pos = blockIdx.x, h = blockIdx.y;
     const int kvh = h / GROUP;
     const int qt = pos / PWG;
     const int row = (pos % PWG) * GROUP + h % GROUP;
@@ -564,8 +563,7 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
 
 // Merge the splits of one (decode, q head): weights 2^(m_s - max m).
 template <int HD>
-__global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
-    const int b = blockIdx.x, h = blockIdx.y;
+__device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b, int h) {
     const int w0 = a.work_off[b], w1 = a.work_off[b + 1];
     float mmax = -INFINITY;
     for (int w = w0; w < w1; ++w) mmax = fmaxf(mmax, a.part_ml[(static_cast<size_t>(w) * a.hq + h) * 2]);
@@ -585,10 +583,36 @@ __global__ __launch_bounds__(64) void decode_merge_kernel(DecodeAttnArgs a) {
     for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
 }
 
+// One launch for both merges of a layer: blocks x < chunk_rows combine the
+// partials of chunk position x (query tiles split over several items), the
+// rest those of decode x - chunk_rows; y is the q head.
+template <int HD, int GROUP>
+__global__ __launch_bounds__(64) void attn_merge_kernel(ChunkAttnArgs ca, DecodeAttnArgs da, int chunk_rows) {
+    const int x = blockIdx.x, h = blockIdx.y;
+    if (x < chunk_rows) chunk_merge_row<HD, GROUP>(ca, x, h);
+    else decode_merge_row<HD>(da, x - chunk_rows, h);
+}
+
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
     chunk_attn_kernel<HD, GROUP, kChunkStages><<<dim3(a.n_slots, a.hkv), 512, 0, s>>>(a);
-    if (a.split) chunk_merge_kernel<HD, GROUP><<<dim3(a.c, a.hq), 64, 0, s>>>(a);
+}
+
+template <int HD, int GROUP>
+void launch_merge_g(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, int chunk_rows, int hq, hipStream_t s) {
+    attn_merge_kernel<HD, GROUP><<<dim3(chunk_rows + da.b, hq), 64, 0, s>>>(ca, da, chunk_rows);
+}
+
+template <int HD>
+void launch_merge_hd(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, int chunk_rows, int group, int hq,
+                     hipStream_t s) {
+    switch (group) {
+        case 1: launch_merge_g<HD, 1>(ca, da, chunk_rows, hq, s); break;
+        case 2: launch_merge_g<HD, 2>(ca, da, chunk_rows, hq, s); break;
+        case 4: launch_merge_g<HD, 4>(ca, da, chunk_rows, hq, s); break;
+        case 8: launch_merge_g<HD, 8>(ca, da, chunk_rows, hq, s); break;
+        default: launch_merge_g<HD, 16>(ca, da, chunk_rows, hq, s); break;
+    }
 }
 
 template <int HD>
@@ -617,11 +641,16 @@ void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s) {
     else decode_attn_kernel<64><<<grid, 64, 0, s>>>(a);
 }
 
-void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s) {
-    if (a.b <= 0) return;
-    dim3 grid(a.b, a.hq);
-    if (a.hd == 128) decode_merge_kernel<128><<<grid, 64, 0, s>>>(a);
-    else decode_merge_kernel<64><<<grid, 64, 0, s>>>(a);
+void launch_attention_merge(const ChunkAttnArgs* ca, const DecodeAttnArgs* da, hipStream_t s) {
+    const int chunk_rows = ca && ca->c > 0 && ca->split ? ca->c : 0;
+    DecodeAttnArgs dd{};
+    if (da && da->b > 0) dd = *da;
+    if (chunk_rows + dd.b == 0) return;
+    ChunkAttnArgs cc{};
+    if (ca) cc = *ca;
+    const int hq = chunk_rows ? cc.hq : dd.hq, hkv = chunk_rows ? cc.hkv : dd.hkv, hd = chunk_rows ? cc.hd : dd.hd;
+    if (hd == 128) launch_merge_hd<128>(cc, dd, chunk_rows, hq / hkv, hq, s);
+    else launch_merge_hd<64>(cc, dd, chunk_rows, hq / hkv, hq, s);
 }
 
 }  // namespace slw

@@ -71,10 +71,9 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const T* __restri
 
 // One thread per (row, frequency): angle p * theta^(-2i/hd) formed and
 // reduced in double precision so that large positions keep full accuracy.
-__global__ void rope_table_kernel(const int32_t* __restrict__ pos, float2* __restrict__ cs, int rows,
-                                  int half, double theta) {
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= rows * half) return;
+// cos and sin of position pos[r] times theta^(-i/half), in fp64 so that large
+// positions keep their accuracy.
+__device__ __forceinline__ void rope_entry(const int32_t* pos, float2* cs, int idx, int half, double theta) {
     const int r = idx / half, i = idx % half;
     const double ang = static_cast<double>(pos[r]) * pow(theta, -static_cast<double>(i) / half);
     double s, c;
@@ -96,29 +95,43 @@ __global__ void sweep_kernel(uint32_t* p, size_t n4, uint32_t key) {
     if (x == key) p[0] = x;
 }
 
-// Copy n words from coherent host memory mapped into the device's address
-// space: one 16-byte read per thread over the bus, then a tail of single
-// words.  Done by a kernel rather than the copy engine so that the copy is
-// ordered with the kernels around it on the stream without a hand-off
-// between engines.
-__global__ void copy_from_host_kernel(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src, size_t n) {
-    const size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
-    const size_t n4 = n / 4;
-    if (i < n4) {
-        reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
-    } else if (i < n4 + (n & 3)) {
-        const size_t w = 4 * n4 + (i - n4);
-        dst[w] = src[w];
+// First kernel of an iteration.  Blocks [0, copy_blocks) copy n words of
+// metadata from coherent host memory mapped into the device's address space
+// (one 16-byte read per thread over the bus, then a tail of single words);
+// done by a kernel rather than the copy engine, the copy is ordered with the
+// kernels around it on the stream without a hand-off between engines.  The
+// other blocks fill the RoPE table, reading the positions from the host copy
+// (the device copy is not complete while this kernel runs).
+__global__ void iteration_setup_kernel(uint32_t* __restrict__ dst, const uint32_t* __restrict__ src, size_t n,
+                                       unsigned copy_blocks, const int32_t* __restrict__ pos_host,
+                                       float2* __restrict__ cs, int rows, int half, double theta) {
+    if (blockIdx.x < copy_blocks) {
+        const size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
+        const size_t n4 = n / 4;
+        if (i < n4) {
+            reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+        } else if (i < n4 + (n & 3)) {
+            const size_t w = 4 * n4 + (i - n4);
+            dst[w] = src[w];
+        }
+        return;
     }
+    const int idx = static_cast<int>(blockIdx.x - copy_blocks) * blockDim.x + threadIdx.x;
+    if (idx < rows * half) rope_entry(pos_host, cs, idx, half, theta);
 }
 
 }  // namespace
 
-void launch_copy_from_host(void* dst, const void* src, size_t words, hipStream_t s) {
-    if (words == 0) return;
-    const size_t threads = words / 4 + (words & 3);
-    copy_from_host_kernel<<<static_cast<unsigned>((threads + 255) / 256), 256, 0, s>>>(
-        static_cast<uint32_t*>(dst), static_cast<const uint32_t*>(src), words);
+void launch_iteration_setup(void* dst, const void* src, size_t words, const int32_t* pos_host, float2* cs,
+                            int rows, int hd, double theta, hipStream_t s) {
+    const size_t copy_threads = words / 4 + (words & 3);
+    const unsigned copy_blocks = static_cast<unsigned>((copy_threads + 255) / 256);
+    const int half = hd / 2;
+    const unsigned rope_blocks = static_cast<unsigned>((static_cast<size_t>(rows) * half + 255) / 256);
+    if (copy_blocks + rope_blocks == 0) return;
+    iteration_setup_kernel<<<copy_blocks + rope_blocks, 256, 0, s>>>(
+        static_cast<uint32_t*>(dst), static_cast<const uint32_t*>(src), words, copy_blocks, pos_host, cs, rows,
+        half, theta);
 }
 
 void launch_rmsnorm(const void* x, bool x_f32, const void* g, void* y, int rows, int d, float eps,
@@ -132,12 +145,6 @@ void launch_rmsnorm(const void* x, bool x_f32, const void* g, void* y, int rows,
         rmsnorm_kernel<bf16><<<rows, kNormThreads, 0, s>>>(static_cast<const bf16*>(x),
                                                            static_cast<const bf16*>(g),
                                                            static_cast<bf16*>(y), d, eps);
-}
-
-void launch_rope_table(const int32_t* pos, float2* cs, int rows, int hd, double theta, hipStream_t s) {
-    if (rows <= 0) return;
-    const int half = hd / 2, n = rows * half;
-    rope_table_kernel<<<(n + 255) / 256, 256, 0, s>>>(pos, cs, rows, half, theta);
 }
 
 void launch_cache_sweep(void* p, size_t bytes, uint32_t key, hipStream_t s) {

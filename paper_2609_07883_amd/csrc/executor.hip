@@ -405,18 +405,19 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     std::memcpy(stage, m.data(), m.size() * 4);
     char* wsb = static_cast<char*>(ws);
     int32_t* dmeta = reinterpret_cast<int32_t*>(wsb + L.meta);
-    launch_copy_from_host(dmeta, ctx->staging_dev[slot], m.size(), stream);
+    float2* rope = reinterpret_cast<float2*>(wsb + L.rope);
+    // metadata copy and RoPE table (positions follow the M slots) in one kernel
+    launch_iteration_setup(dmeta, ctx->staging_dev[slot], m.size(), ctx->staging_dev[slot] + M, rope, M, c.head_dim,
+                           static_cast<double>(c.rope_theta), stream);
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipEventRecord(ctx->staged[slot], stream));
 
     const int32_t* d_slot = dmeta;
-    const int32_t* d_pos = dmeta + M;
     void* xn = wsb + L.xn;
     void* qkv = wsb + L.qkv;
     void* attn = wsb + L.attn;
     void* hbuf = wsb + L.h;
     void* act = wsb + L.act;
-    float2* rope = reinterpret_cast<float2*>(wsb + L.rope);
     void* gpartp = wsb + L.gemm_part;
 
     const int d = c.d_model, hq = c.n_q_heads, hkv = c.n_kv_heads, hd = c.head_dim, F = c.ffn_dim;
@@ -451,8 +452,7 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
 
         if ((rc = mark(l, 0))) return rc;
         launch_rmsnorm(cur, false, wl.g1, xn, M, d, c.rms_eps, stream);
-        if ((rc = mark(l, 1))) return rc;
-        if (l == 0) launch_rope_table(d_pos, rope, M, hd, static_cast<double>(c.rope_theta), stream);
+        if ((rc = mark(l, 1))) return rc;  // the RoPE table stage is empty: the setup kernel fills the table
         if ((rc = mark(l, 2))) return rc;
         {
             GemmArgs ga{xn, wl.wqkv, qkv, nullptr, M, qw, d, d, qw, EPI_QKV};
@@ -466,8 +466,8 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             launch_gemm(ga, p_qkv, gpartp, stream);
         }
         if ((rc = mark(l, 3))) return rc;
+        ChunkAttnArgs ca{};
         if (C > 0) {
-            ChunkAttnArgs ca{};
             ca.qkv = qkv;
             ca.out = attn;
             ca.k_pool = kp;
@@ -492,8 +492,8 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             launch_chunk_attention(ca, stream);
         }
         if ((rc = mark(l, 4))) return rc;
+        DecodeAttnArgs da{};
         if (B > 0) {
-            DecodeAttnArgs da{};
             da.q = static_cast<const char*>(qkv) + static_cast<size_t>(C) * qw * 2;
             da.out = static_cast<char*>(attn) + static_cast<size_t>(C) * hq * hd * 2;
             da.k_pool = kp;
@@ -514,11 +514,9 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             da.hd = hd;
             da.ld_q = qw;
             launch_decode_attention_split(da, stream);
-            if ((rc = mark(l, 5))) return rc;
-            launch_decode_merge(da, stream);
-        } else if ((rc = mark(l, 5))) {
-            return rc;
         }
+        if ((rc = mark(l, 5))) return rc;
+        launch_attention_merge(&ca, &da, stream);
         if ((rc = mark(l, 6))) return rc;
         launch_gemm(GemmArgs{attn, wl.wo, hbuf, cur, M, d, hq * hd, hq * hd, d, EPI_RESID_F32OUT}, p_o, gpartp,
                     stream);

@@ -12,8 +12,6 @@ namespace slw {
 void launch_rmsnorm(const void* x, bool x_f32, const void* g, void* y, int rows, int d, float eps,
                     hipStream_t s);
 
-// cs[r][i] = (cos, sin) of pos[r] * theta^(-2i/hd), i < hd/2, formed in double.
-void launch_rope_table(const int32_t* pos, float2* cs, int rows, int hd, double theta, hipStream_t s);
 
 // GEMM out = A W^T with an epilogue:
 //   EPI_RESID_F32OUT  out fp32 = acc + resid (bf16)
@@ -96,11 +94,17 @@ struct DecodeAttnArgs {
     int b, n_work, split_tokens, hq, hkv, hd, ld_q;
 };
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
-void launch_decode_merge(const DecodeAttnArgs& a, hipStream_t s);
+// Combine the partials of both attentions in one launch: chunk positions of
+// query tiles split over several items (ca may be null or unsplit) and every
+// decode (da may be null or have b = 0).
+void launch_attention_merge(const ChunkAttnArgs* ca, const DecodeAttnArgs* da, hipStream_t s);
 
-// Copy `words` 32-bit words from coherent, mapped host memory (its device
-// address; both pointers 16-byte aligned) to device memory, as a kernel.
-void launch_copy_from_host(void* dst, const void* src, size_t words, hipStream_t s);
+// One kernel: copy `words` 32-bit words from coherent, mapped host memory
+// (its device address; both pointers 16-byte aligned) to device memory, and
+// fill the RoPE table: cs[r][i] = (cos, sin) of pos_host[r] * theta^(-2i/hd),
+// i < hd/2, formed in double (pos_host lies in that host memory).
+void launch_iteration_setup(void* dst, const void* src, size_t words, const int32_t* pos_host, float2* cs,
+                            int rows, int hd, double theta, hipStream_t s);
 
 // Read `bytes` of device memory (last-level cache flush that leaves no dirty
 // lines); the buffer is written only if a thread's xor of its words equals key.
