@@ -41,11 +41,19 @@ struct GemmPlan {
     int splits;   // split-K factor across work-groups (1: fused epilogue)
     size_t partial_bytes;
     int ks;     // weight-streaming kernel (m <= 32): k slices per work-group
+    int sk_workers = 0;  // stream-K: work-groups sharing the k steps of the last tiles (0: off)
+    int dp_tiles = 0;    // stream-K: tiles run whole before them
 };
+// CUs the stream-K schedule spreads its last round over (MI355X).
+constexpr int kStreamKCus = 256;
 constexpr int kSkinnyCfg = 99;
 GemmPlan plan_gemm(int m, int n, int k);
 // The plan for a given tile configuration (split-K chosen by tile count).
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k);
+// The configuration with a stream-K schedule: whole tiles for all rounds but
+// the last full one, whose tiles and the remainder share their k steps
+// equally over one round of work-groups (plain tiles when rounds are whole).
+GemmPlan plan_stream_k(int cfg, int m, int n, int k);
 // Whether the plan's tiles divide n and k.
 bool gemm_shape_ok(const GemmPlan& p, int n, int k);
 // Enqueue the GEMM; `partial` must hold plan.partial_bytes when plan.splits > 1.

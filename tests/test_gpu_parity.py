@@ -67,6 +67,30 @@ def test_tiny_prompt_in_chunks_with_decodes(tiny_sessions, qk_std):
         stream += 1
 
 
+def test_tiny_long_chunk_stream_k():
+    """903 rows (a 900-token chunk at prefix 100 and three decodes): the
+    output projection (256 x 256 wide) runs the stream-K schedule, whose
+    pieces and fixup must reproduce every row."""
+    _require_gpu()
+    from paper_2609_07883_amd.runtime import Session
+    sess = Session(synth.TINY, num_blocks=512, max_c=1024, max_b=4, qk_std=0.16)
+    mir = Mirror(sess)
+    pre = 7
+    mir.create(pre)
+    mir.install_context(pre, 100)
+    dec = [21, 22, 23]
+    ctx = [40, 130, 257]
+    for sid, L in zip(dec, ctx):
+        mir.create(sid)
+        mir.install_context(sid, L)
+    b = api.Batch(900, pre, 100, dec, ctx)
+    x = synth.embeddings(b.rows, synth.TINY.d_model, seed=1, stream=903)
+    y, yr, sg, sr = mir.step(b, x)
+    assert sg == sr
+    check(y, yr, "903-row iteration")
+    assert mir.kv_error(b) <= TOL
+
+
 @pytest.fixture(scope="module")
 def l8b():
     _require_gpu()
