@@ -54,13 +54,14 @@ __device__ __forceinline__ int w_row(const GemmArgs& g, int c) {
     return c;
 }
 
-// Rotate (x0, x1) = dims (d0, d0 + hd/2) of head hg of row `row` (q and k
-// heads) and store; k and v also go to their KV page at slot[row].
-__device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, int d0, float x0, float x1) {
+// Rotate (x0, x1) = dims (d0, d0 + hd/2) of head hg of row `row` by
+// cs = (cos, sin) (q and k heads; v heads are not rotated) and store; k and v
+// also go to their KV page at slot[row].
+__device__ __forceinline__ void qkv_store_cs(const GemmArgs& g, int row, int hg, int d0, float x0, float x1,
+                                             float2 cs, int slot) {
     const int d1 = d0 + g.hd / 2;
     bf16* out = static_cast<bf16*>(g.out) + static_cast<size_t>(row) * g.ldo + hg * g.hd;
     if (hg < g.hq + g.hkv) {
-        const float2 cs = g.rope_cs[row * (g.hd / 2) + d0];
         const float y0 = x0 * cs.x - x1 * cs.y;
         const float y1 = x1 * cs.x + x0 * cs.y;
         x0 = y0;
@@ -70,7 +71,6 @@ __device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, in
     out[d0] = b0;
     out[d1] = b1;
     if (hg < g.hq) return;
-    const int slot = g.slot[row];
     const size_t blk = slot >> 4, t = slot & 15;
     if (hg < g.hq + g.hkv) {
         bf16* pg = static_cast<bf16*>(g.k_pool) + (blk * g.hkv + (hg - g.hq)) * g.hd * 16;
@@ -81,6 +81,12 @@ __device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, in
         pg[d0 * 16 + t] = b0;
         pg[d1 * 16 + t] = b1;
     }
+}
+
+// The same with the rotation and the slot read from the iteration's tables.
+__device__ __forceinline__ void qkv_store(const GemmArgs& g, int row, int hg, int d0, float x0, float x1) {
+    const float2 cs = hg < g.hq + g.hkv ? g.rope_cs[row * (g.hd / 2) + d0] : make_float2(1.f, 0.f);
+    qkv_store_cs(g, row, hg, d0, x0, x1, cs, hg < g.hq ? 0 : g.slot[row]);
 }
 
 // LDS rows hold BK bf16 (BK/8 chunks of 16 bytes).  Chunk c of row r is
@@ -318,10 +324,14 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int m0, int n0,
 
 // Fused epilogue of one tile: element e of MFMA tile (i, j) of a wave is row
 // m0 + wm WM + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4, B column
-// n0 + wn WN + 32 j + lane % 32.
+// n0 + wn WN + 32 j + lane % 32.  The epilogue's inputs (RoPE table,
+// residual) are read for a whole block of rows before any of its stores:
+// the compiler cannot tell that the stores do not alias them, so reads and
+// stores interleaved per element would each wait out a memory round trip.
+// Reads of rows past m are clamped to row m - 1 and their stores skipped.
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 __device__ __forceinline__ void tile_store(const GemmArgs& g, int m0, int n0,
-                                       const f32x16 (&acc)[BM / WAVES_M / 32][BN / WAVES_N / 32]) {
+                                           const f32x16 (&acc)[BM / WAVES_M / 32][BN / WAVES_N / 32]) {
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -341,20 +351,42 @@ __device__ __forceinline__ void tile_store(const GemmArgs& g, int m0, int n0,
                 fcol = (c0 >> 1) + (lane & 31);
             }
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i) {
+                float2 cs[16];
+                int sl[16];
+                if (EPI == EPI_QKV) {
+                    const bool rot = hg < g.hq + g.hkv, paged = hg >= g.hq;
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int row = min(rbase + i * 32 + 8 * (e >> 2) + (e & 3), g.m - 1);
+                        cs[e] = rot ? g.rope_cs[row * (g.hd / 2) + d0] : make_float2(1.f, 0.f);
+                        sl[e] = paged ? g.slot[row] : 0;
+                    }
+                }
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int row = rbase + i * 32 + 8 * (e >> 2) + (e & 3);
                     if (row >= g.m) continue;
                     const float x0 = acc[i][2 * pr][e], x1 = acc[i][2 * pr + 1][e];
-                    if (EPI == EPI_QKV) qkv_store(g, row, hg, d0, x0, x1);
+                    if (EPI == EPI_QKV) qkv_store_cs(g, row, hg, d0, x0, x1, cs[e], sl[e]);
                     else out[static_cast<size_t>(row) * g.ldo + fcol] = f2bf(silu(x0) * x1);
                 }
+            }
         }
         return;
     }
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+        float r[TN][16];
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = min(rbase + i * 32 + 8 * (e >> 2) + (e & 3), g.m - 1);
+                const size_t o = static_cast<size_t>(row) * g.ldo + cbase + j * 32;
+                r[j][e] = EPI == EPI_RESID_F32OUT ? bf2f(static_cast<const bf16*>(g.resid)[o])
+                                                  : static_cast<const float*>(g.resid)[o];
+            }
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
@@ -363,10 +395,11 @@ __device__ __forceinline__ void tile_store(const GemmArgs& g, int m0, int n0,
                 if (row >= g.m) continue;
                 const size_t o = static_cast<size_t>(row) * g.ldo + cbase + j * 32;
                 if (EPI == EPI_RESID_F32OUT)
-                    static_cast<float*>(g.out)[o] = acc[i][j][e] + bf2f(static_cast<const bf16*>(g.resid)[o]);
+                    static_cast<float*>(g.out)[o] = acc[i][j][e] + r[j][e];
                 else
-                    static_cast<bf16*>(g.out)[o] = f2bf(acc[i][j][e] + static_cast<const float*>(g.resid)[o]);
+                    static_cast<bf16*>(g.out)[o] = f2bf(acc[i][j][e] + r[j][e]);
             }
+    }
 }
 
 // Split-K partial of one tile into P [m][n] (B column order).
@@ -731,24 +764,48 @@ __global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restri
                         f32x4{acc[c][t][4 * e4], acc[c][t][4 * e4 + 1], acc[c][t][4 * e4 + 2], acc[c][t][4 * e4 + 3]};
                 continue;
             }
+            if (EPI == EPI_QKV) {
+                // rotations (and the KV slot) read before any store, which the
+                // compiler cannot tell apart from the tables
+                const int hg = c0 / g.hd, d0 = ((c0 % g.hd) / 64) * 32 + i0;
+                const bool rot = hg < g.hq + g.hkv;
+                float2 cs[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int e = 4 * e4 + q;
-                const float x0 = acc[0][t][e], x1 = acc[1][t][e];
-                if (EPI == EPI_QKV) {
-                    qkv_store(g, row, c0 / g.hd, ((c0 % g.hd) / 64) * 32 + i0 + q, x0, x1);
-                } else if (EPI == EPI_SWIGLU) {
+                for (int q = 0; q < 4; ++q)
+                    cs[q] = rot ? g.rope_cs[row * (g.hd / 2) + d0 + q] : make_float2(1.f, 0.f);
+                const int slot = hg < g.hq ? 0 : g.slot[row];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    qkv_store_cs(g, row, hg, d0 + q, acc[0][t][4 * e4 + q], acc[1][t][4 * e4 + q], cs[q], slot);
+            } else if (EPI == EPI_SWIGLU) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
                     static_cast<bf16*>(g.out)[static_cast<size_t>(row) * g.ldo + (c0 >> 1) + i0 + q] =
-                        f2bf(silu(x0) * x1);
-                } else {
+                        f2bf(silu(acc[0][t][4 * e4 + q]) * acc[1][t][4 * e4 + q]);
+            } else {
+                // four consecutive output columns per lane: one vector read of
+                // the residual and one vector store for each 32-column group
+                f32x4 rv[2];
 #pragma unroll
-                    for (int c = 0; c < 2; ++c) {
-                        const size_t o = static_cast<size_t>(row) * g.ldo + c0 + 32 * c + i0 + q;
-                        const float v = c ? x1 : x0;
-                        if (EPI == EPI_RESID_F32OUT)
-                            static_cast<float*>(g.out)[o] = v + bf2f(static_cast<const bf16*>(g.resid)[o]);
-                        else
-                            static_cast<bf16*>(g.out)[o] = f2bf(v + static_cast<const float*>(g.resid)[o]);
+                for (int c = 0; c < 2; ++c) {
+                    const size_t o = static_cast<size_t>(row) * g.ldo + c0 + 32 * c + i0;
+                    if (EPI == EPI_RESID_F32OUT) {
+                        const bf16x4 rb = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.resid) + o);
+                        rv[c] = f32x4{bf2f(rb[0]), bf2f(rb[1]), bf2f(rb[2]), bf2f(rb[3])};
+                    } else {
+                        rv[c] = *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.resid) + o);
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < 2; ++c) {
+                    const size_t o = static_cast<size_t>(row) * g.ldo + c0 + 32 * c + i0;
+                    const f32x4 v = f32x4{acc[c][t][4 * e4], acc[c][t][4 * e4 + 1], acc[c][t][4 * e4 + 2],
+                                          acc[c][t][4 * e4 + 3]} + rv[c];
+                    if (EPI == EPI_RESID_F32OUT) {
+                        *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + o) = v;
+                    } else {
+                        const bf16x4 ob = {f2bf(v[0]), f2bf(v[1]), f2bf(v[2]), f2bf(v[3])};
+                        *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + o) = ob;
                     }
                 }
             }
