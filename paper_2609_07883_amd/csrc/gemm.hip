@@ -903,30 +903,36 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 
 }  // namespace
 
-// Tile and split choice, from timings of every configuration on the
-// 8B-layer shapes (m = 96 .. 4104, caches swept with reads between runs):
-// the weight-streaming kernel up to 32 rows on the narrower projections,
-// 64-row tiles with split-K while weight streaming dominates, then whichever
-// tile measured fastest in each band of m; from m = 1600 on the 256 x 256
-// tile fed by a two-buffer direct-load ring of k-64 steps.  n must be a
-// multiple of 128 and k of 64.
+// Tile and split choice, from timings of every configuration, with and
+// without the stream-K schedule, on the 8B-layer shapes (m = 96 .. 4104,
+// caches swept with reads between runs; one run for all, as timings vary
+// between boxes): the weight-streaming kernel up to 32 rows on the narrower
+// projections, then whichever configuration measured fastest in each band of
+// m.  The 128 x 128 tiles (two work-groups per CU) win wherever their tiles
+// fit one round of 512; the 256 x 256 ring tile from about 2000 rows (3500
+// for qkv); stream-K where 256 x 256 tiles are too few for the CUs on the
+// narrow projections.  n must be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     // Up to 32 rows the weight-streaming kernel wins on the narrower
     // projections (o, down: 12-16% at m <= 32, qkv even); on gate/up the
-    // 64 x 128 tiles keep up with it.
+    // 128 x 128 tiles keep up with it.
     if (m <= 32 && n < 16384 && n % 64 == 0) return plan_with_cfg(kSkinnyCfg, m, n, k);
-    // Where the 256 x 256 tiles are too few for the CUs and split-K would
-    // need four or more partial slabs (down from m = 450, o from m = 800, up
-    // to about 3000 rows), the stream-K schedule measured 9-20% faster; with
-    // many tiles per CU, or on gate/up and qkv, its partials cost more than
-    // the imbalance they remove.
-    const bool sk_band = n % 256 == 0 && n < 6144 && m < 3000 && (k >= 8192 ? m >= 450 : m >= 800);
-    if (sk_band) return plan_stream_k(11, m, n, k);
+    constexpr int SK = -1;  // stream-K with the 256 x 256 ring tile
     int cfg;
-    if (k >= 8192) cfg = m <= 160 ? 1 : m < 450 ? 8 : m < 800 ? 10 : 11;                 // deep k (down)
-    else if (n >= 16384) cfg = m <= 160 ? 1 : m <= 400 ? 10 : m < 800 ? 1 : m < 1600 ? 7 : 11;  // gate/up
-    else if (n >= 6144) cfg = m <= 400 ? 1 : m < 1600 ? 0 : 11;                          // qkv
-    else cfg = m <= 400 ? 0 : m < 800 ? 1 : m < 1600 ? 10 : 11;                         // o
+    if (k >= 8192)  // deep k (down)
+        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 450 ? 11 : SK;
+    else if (n >= 16384)  // gate/up
+        cfg = m <= 200 ? 0 : m <= 650 ? 1 : m < 950 ? 11 : m < 1800 ? 7 : 11;
+    else if (n >= 6144)  // qkv
+        cfg = m <= 128 ? 0 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 10 : m < 1300 ? 0 : m < 1800 ? 1
+            : m < 2500 ? 7 : m < 3500 ? 0 : 11;
+    else  // o
+        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 700 ? 1 : m < 950 ? 0 : m < 1300 ? SK : m < 1800 ? 0
+            : m < 3500 ? SK : 0;
+    if (cfg == SK) {
+        if (n % 256 == 0) return plan_stream_k(11, m, n, k);
+        cfg = 11;
+    }
     if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
     return plan_with_cfg(cfg, m, n, k);
 }
