@@ -464,7 +464,7 @@ def serve_main(args):
                 f"P99 TTFT {m['p99_ttft_ms']:.0f} ms, P99 TPOT {m['p99_tpot_ms']:.2f} ms, missed TTFT {m['ttft_missed']} / "
                 f"TPOT {m['tpot_missed']}, {len(it)} iterations, "
                 f"{wall:.1f}s")
-    best = {D: max((r for r in runs if r["tpot_slo_ms"] == D and r["policy"] != "SLOWeave"),
+    best = {D: max((r for r in runs if r["tpot_slo_ms"] == D and not r["policy"].startswith("SLOWeave")),
                    key=lambda r: r["goodput_req_s"]) for D in (25.0, 10.0)}
     gain = {}
     for name in ("SLOWeave", "SLOWeave+telemetry"):
