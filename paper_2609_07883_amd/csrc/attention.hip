@@ -374,7 +374,52 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     }  // items of this work-group
 }
 
-// Combine the key-range partials of one (chunk position, q head); 64 threads.
+// Combine n partials (running max, sum and unnormalised output) of one
+// row and write it normalised; 64 threads, HD / 64 dims each.  Partial w
+// sits at row r0 + w * stride of ml [.][2] and po [.][HD]; a max of -inf
+// means every key of that range was masked for the row.  The loads are
+// issued eight partials at a time before any is used, so a list costs a few
+// memory round trips rather than one per partial.
+template <int HD>
+__device__ __forceinline__ void merge_row(const float* __restrict__ ml, const float* __restrict__ po, size_t r0,
+                                          size_t stride, int n, bf16* __restrict__ out) {
+    constexpr int CH = 8, PER = HD / 64;
+    float mmax = -INFINITY;
+    for (int c = 0; c < n; c += CH) {
+        float m[CH];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) m[j] = c + j < n ? ml[(r0 + (c + j) * stride) * 2] : -INFINITY;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) mmax = fmaxf(mmax, m[j]);
+    }
+    float acc[PER] = {};
+    float lsum = 0.f;
+    for (int c = 0; c < n; c += CH) {
+        float m[CH], l[CH], v[CH][PER];
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            const bool ok = c + j < n;
+            const size_t r = r0 + (c + j) * stride;
+            m[j] = ok ? ml[r * 2] : -INFINITY;
+            l[j] = ok ? ml[r * 2 + 1] : 0.f;
+#pragma unroll
+            for (int p = 0; p < PER; ++p) v[j][p] = ok ? po[r * HD + threadIdx.x + 64 * p] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < CH; ++j) {
+            if (m[j] == -INFINITY) continue;
+            const float sc = fast_exp2(m[j] - mmax);
+            lsum += sc * l[j];
+#pragma unroll
+            for (int p = 0; p < PER; ++p) acc[p] += sc * v[j][p];
+        }
+    }
+    const float inv = 1.0f / lsum;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) out[threadIdx.x + 64 * p] = f2bf(acc[p] * inv);
+}
+
+// Combine the key-range partials of one (chunk position, q head).
 template <int HD, int GROUP>
 __device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int pos, int h) {
     constexpr int PWG = 256 / GROUP;
@@ -383,25 +428,9 @@ __device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int pos,
     const int row = (pos % PWG) * GROUP + h % GROUP;
     const int w0 = a.qt_off[qt], w1 = a.qt_off[qt + 1];
     if (w1 - w0 == 1) return;  // written by the attention kernel
-    float mmax = -INFINITY;
-    for (int w = w0; w < w1; ++w)
-        mmax = fmaxf(mmax, a.part_ml[((static_cast<size_t>(w) * a.hkv + kvh) * 256 + row) * 2]);
-    constexpr int PER = HD / 64;
-    float acc[PER] = {};
-    float lsum = 0.f;
-    for (int w = w0; w < w1; ++w) {
-        const size_t r = (static_cast<size_t>(w) * a.hkv + kvh) * 256 + row;
-        const float mw = a.part_ml[r * 2];
-        if (mw == -INFINITY) continue;  // every key of this range was masked for the row
-        const float sc = exp2f(mw - mmax);
-        lsum += sc * a.part_ml[r * 2 + 1];
-#pragma unroll
-        for (int j = 0; j < PER; ++j) acc[j] += sc * a.part_o[r * HD + threadIdx.x + 64 * j];
-    }
-    bf16* out = static_cast<bf16*>(a.out) + static_cast<size_t>(pos) * a.hq * HD + h * HD;
-    const float inv = 1.0f / lsum;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
+    merge_row<HD>(a.part_ml, a.part_o, (static_cast<size_t>(w0) * a.hkv + kvh) * 256 + row,
+                  static_cast<size_t>(a.hkv) * 256, w1 - w0,
+                  static_cast<bf16*>(a.out) + static_cast<size_t>(pos) * a.hq * HD + h * HD);
 }
 
 // ---------------------------------------------------------------------------
@@ -565,22 +594,8 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
 template <int HD>
 __device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b, int h) {
     const int w0 = a.work_off[b], w1 = a.work_off[b + 1];
-    float mmax = -INFINITY;
-    for (int w = w0; w < w1; ++w) mmax = fmaxf(mmax, a.part_ml[(static_cast<size_t>(w) * a.hq + h) * 2]);
-    float lsum = 0.f;
-    constexpr int PER = HD / 64;
-    float acc[PER] = {};
-    for (int w = w0; w < w1; ++w) {
-        const size_t r = static_cast<size_t>(w) * a.hq + h;
-        const float sc = exp2f(a.part_ml[r * 2] - mmax);
-        lsum += sc * a.part_ml[r * 2 + 1];
-#pragma unroll
-        for (int j = 0; j < PER; ++j) acc[j] += sc * a.part_o[r * HD + threadIdx.x + 64 * j];
-    }
-    bf16* out = static_cast<bf16*>(a.out) + static_cast<size_t>(b) * a.hq * HD + h * HD;
-    const float inv = 1.0f / lsum;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) out[threadIdx.x + 64 * j] = f2bf(acc[j] * inv);
+    merge_row<HD>(a.part_ml, a.part_o, static_cast<size_t>(w0) * a.hq + h, a.hq, w1 - w0,
+                  static_cast<bf16*>(a.out) + static_cast<size_t>(b) * a.hq * HD + h * HD);
 }
 
 // One launch for both merges of a layer: blocks x < chunk_rows combine the

@@ -91,6 +91,30 @@ def test_tiny_long_chunk_stream_k():
     assert mir.kv_error(b) <= TOL
 
 
+@pytest.mark.parametrize("C", [100, 150, 600, 850, 1000])
+def test_tiny_gemm_plan_bands(C):
+    """Row counts on both sides of the GEMM planner's bands (128 x 128 tiles
+    with split-K, 64 x 128 tiles, stream-K): every row of the iteration
+    against the oracle."""
+    _require_gpu()
+    from paper_2609_07883_amd.runtime import Session
+    sess = Session(synth.TINY, num_blocks=512, max_c=1024, max_b=4, qk_std=0.16)
+    mir = Mirror(sess)
+    pre = 7
+    mir.create(pre)
+    mir.install_context(pre, 64)
+    dec = [21, 22, 23]
+    ctx = [17, 300, 64]
+    for sid, L in zip(dec, ctx):
+        mir.create(sid)
+        mir.install_context(sid, L)
+    b = api.Batch(C, pre, 64, dec, ctx)
+    x = synth.embeddings(b.rows, synth.TINY.d_model, seed=1, stream=C)
+    y, yr, sg, sr = mir.step(b, x)
+    assert sg == sr
+    check(y, yr, f"{b.rows}-row iteration")
+
+
 @pytest.fixture(scope="module")
 def l8b():
     _require_gpu()
