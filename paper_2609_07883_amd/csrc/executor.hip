@@ -63,6 +63,10 @@ struct slw_ctx {
     size_t staging_cap[kRing] = {};
     hipEvent_t staged[kRing] = {};
     int ring = 0;
+    // second stream for decode attention next to chunk attention, with a
+    // fork and a join event per layer
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> fork_ev, join_ev;
 
     // stage telemetry: a ring of `stage_depth` event sets, each [layer][stage boundary]
     int stage_depth = 0;
@@ -80,6 +84,12 @@ struct slw_ctx {
             if (staging[i]) (void)hipHostFree(staging[i]);
         }
         for (hipEvent_t e : stage_ev) (void)hipEventDestroy(e);
+        if (side) {
+            (void)hipStreamSynchronize(side);
+            (void)hipStreamDestroy(side);
+        }
+        for (hipEvent_t e : fork_ev) (void)hipEventDestroy(e);
+        for (hipEvent_t e : join_ev) (void)hipEventDestroy(e);
     }
 };
 
@@ -177,6 +187,13 @@ int check_cfg(const slw_model_cfg& c) {
 int ensure_hip(slw_ctx* ctx) {
     if (ctx->hip_ready) return SLW_OK;
     for (int i = 0; i < kRing; ++i) HIP_TRY(hipEventCreateWithFlags(&ctx->staged[i], hipEventDisableTiming));
+    HIP_TRY(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
+    ctx->fork_ev.assign(ctx->cfg.n_layers, nullptr);
+    ctx->join_ev.assign(ctx->cfg.n_layers, nullptr);
+    for (int l = 0; l < ctx->cfg.n_layers; ++l) {
+        HIP_TRY(hipEventCreateWithFlags(&ctx->fork_ev[l], hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&ctx->join_ev[l], hipEventDisableTiming));
+    }
     ctx->hip_ready = true;
     return SLW_OK;
 }
@@ -466,6 +483,16 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             launch_gemm(ga, p_qkv, gpartp, stream);
         }
         if ((rc = mark(l, 3))) return rc;
+        // With both attentions to run (and no per-stage events), decode
+        // attention goes to a second stream so that it fills the CUs a short
+        // chunk leaves idle; the merge waits for both.
+        const bool concurrent = C > 0 && B > 0 && !timing;
+        hipStream_t dstream = stream;
+        if (concurrent) {
+            HIP_TRY(hipEventRecord(ctx->fork_ev[l], stream));
+            HIP_TRY(hipStreamWaitEvent(ctx->side, ctx->fork_ev[l], 0));
+            dstream = ctx->side;
+        }
         ChunkAttnArgs ca{};
         if (C > 0) {
             ca.qkv = qkv;
@@ -513,7 +540,11 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
             da.hkv = hkv;
             da.hd = hd;
             da.ld_q = qw;
-            launch_decode_attention_split(da, stream);
+            launch_decode_attention_split(da, dstream);
+            if (concurrent) {
+                HIP_TRY(hipEventRecord(ctx->join_ev[l], dstream));
+                HIP_TRY(hipStreamWaitEvent(stream, ctx->join_ev[l], 0));
+            }
         }
         if ((rc = mark(l, 5))) return rc;
         launch_attention_merge(&ca, &da, stream);

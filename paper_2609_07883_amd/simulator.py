@@ -1,0 +1,99 @@
+"""The Sec. 4 simulator study on the library's serving loop.
+
+The loop in the library (slw_serve) runs on the analytic cost model of
+Sec. 4.1 (the simulator's executor), so the simulator is the same scheduler
+as the GPU runtime, not a second program.  This module sweeps the four
+workloads of Sec. 4.2 (``synth.SIM_WORKLOADS``: 1,000 requests per run, five
+seeds) over the TPOT objectives and the policies of Sec. 4.3 (full-prompt
+prefill, fixed chunks of 64, 256 and 1,024, SLOWeave with C_max 4,096) and
+reports the mean over seeds of P99 TTFT, P99 request-level TPOT, SLO
+attainment and goodput, the layout of the paper's Table 3 and Table 4.
+
+SLOWeave prices iterations with a table of the same analytic model on a
+dense grid (every decode batch up to 2,048, chunks every 16 tokens up to
+C_max, interpolated exactly since the model is linear in c), so its
+predictions equal the executor's costs, as in the paper's simulator.
+
+Run as ``python -m paper_2609_07883_amd.simulator [--requests N] [--seeds K]``.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import time
+
+import numpy as np
+
+from . import api, serving, synth
+
+C_MAX = 4096
+MAX_DECODE = 2048
+TPOTS_MS = (10.0, 25.0, 50.0)
+POLICIES = (("Full", "fixed", 1 << 30), ("Fixed-64", "fixed", 64), ("Fixed-256", "fixed", 256),
+            ("Fixed-1024", "fixed", 1024), ("SLOWeave", "sloweave", 0))
+
+
+def analytic_table() -> api.CostTable:
+    """The analytic model on a dense grid (exact under the table's lookups)."""
+    return api.CostTable.analytic(list(range(0, C_MAX + 1, 16)), list(range(0, MAX_DECODE + 1)))
+
+
+def run_one(trace, table, policy: str, chunk: int, tpot_ms: float, ttft_slo_ms: float) -> dict:
+    res = serving.run(trace, policy=policy, fixed_chunk=chunk, tpot_ms=tpot_ms, max_decode=MAX_DECODE,
+                      c_max=C_MAX, table=table if policy == "sloweave" else None)
+    return serving.metrics(trace, res.token_ns, ttft_slo_ms=ttft_slo_ms, tpot_slo_ms=tpot_ms)
+
+
+def study(workloads=tuple(synth.SIM_WORKLOADS), tpots=TPOTS_MS, policies=POLICIES, n: int = 1000,
+          seeds=(0, 1, 2, 3, 4), table: api.CostTable | None = None) -> list[dict]:
+    """Mean over seeds of each (workload, TPOT objective, policy)."""
+    table = table or analytic_table()
+    rows = []
+    for wname in workloads:
+        w = synth.SIM_WORKLOADS[wname]
+        traces = [synth.sim_trace(wname, n, s) for s in seeds]
+        for tpot in tpots:
+            for pname, pol, chunk in policies:
+                ms = [run_one(tr, table, pol, chunk, tpot, w.ttft_slo_ms) for tr in traces]
+                rows.append({"workload": wname, "tpot_slo_ms": tpot, "ttft_slo_ms": w.ttft_slo_ms,
+                             "policy": pname,
+                             "p99_ttft_ms": float(np.mean([m["p99_ttft_ms"] for m in ms])),
+                             "p99_tpot_ms": float(np.mean([m["p99_tpot_ms"] for m in ms])),
+                             "slo_attainment": float(np.mean([m["slo_attainment"] for m in ms])),
+                             "goodput_req_s": float(np.mean([m["goodput_req_s"] for m in ms])),
+                             "throughput_req_s": float(np.mean([m["throughput_req_s"] for m in ms]))})
+    return rows
+
+
+def gains(rows: list[dict]) -> dict:
+    """SLOWeave goodput over the best non-SLOWeave policy, per (workload, TPOT)."""
+    out = {}
+    for r in rows:
+        if r["policy"] != "SLOWeave":
+            continue
+        others = [o for o in rows if o["workload"] == r["workload"] and o["tpot_slo_ms"] == r["tpot_slo_ms"]
+                  and o["policy"] != "SLOWeave"]
+        best = max(others, key=lambda o: o["goodput_req_s"])
+        out[f'{r["workload"]} {r["tpot_slo_ms"]:g}ms'] = {
+            "vs": best["policy"],
+            "ratio": round(r["goodput_req_s"] / best["goodput_req_s"], 3) if best["goodput_req_s"] > 0 else None}
+    return out
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--requests", type=int, default=1000)
+    ap.add_argument("--seeds", type=int, default=5)
+    args = ap.parse_args(argv)
+    t0 = time.time()
+    rows = study(n=args.requests, seeds=tuple(range(args.seeds)))
+    for r in rows:
+        print(f'{r["workload"]:7s} TPOT {r["tpot_slo_ms"]:4.0f} ms  {r["policy"]:10s}  '
+              f'P99 TTFT {r["p99_ttft_ms"]:8.1f} ms  P99 TPOT {r["p99_tpot_ms"]:6.1f} ms  '
+              f'SLO {100 * r["slo_attainment"]:5.1f}%  goodput {r["goodput_req_s"]:6.1f} req/s')
+    print(json.dumps({"rows": rows, "sloweave_vs_best_other": gains(rows), "requests": args.requests,
+                      "seeds": args.seeds, "wall_s": round(time.time() - t0, 1)}))
+
+
+if __name__ == "__main__":
+    main()

@@ -190,3 +190,64 @@ def request_trace(n: int, rate_per_s: float, seed: int = 3, burst_factor: float 
     prompt = np.where(coin, short, long_).astype(np.int64)
     output = np.minimum(rng.geometric(1.0 / output_mean, size=n), output_cap).astype(np.int64)
     return RequestTrace(arrival, prompt, output)
+
+
+# The simulator's four workloads (Sec. 4.2): median prompt and output
+# lengths, the share of long prompts, the offered rate and the TTFT
+# objective.  The spread of the clipped log-normals, the clipping bounds and
+# the bursty workload's two arrival states are not given; the readings are
+# sigma 0.8, prompts in [1, 16384], outputs in [1, 4096], and states of
+# 1.6x and 0.4x the offered rate with exponential dwell times of mean 1 s
+# (so the long-run rate is the offered one).
+@dataclass(frozen=True)
+class SimWorkload:
+    name: str
+    prompt_median: float
+    long_share: float        # share of prompts drawn around long_median instead
+    long_median: float
+    output_median: float
+    rate_per_s: float
+    ttft_slo_ms: float
+    bursty: bool = False
+
+
+SIM_WORKLOADS = {
+    "chat": SimWorkload("chat", 256, 0.0, 1800, 96, 110.0, 1000.0),
+    "mixed": SimWorkload("mixed", 256, 0.3, 1800, 100, 90.0, 1000.0),
+    "long": SimWorkload("long", 1800, 0.0, 1800, 180, 60.0, 5000.0),
+    "bursty": SimWorkload("bursty", 256, 0.3, 1800, 100, 70.0, 1500.0, bursty=True),
+}
+SIM_SIGMA = 0.8
+SIM_PROMPT_CAP = 16384
+SIM_OUTPUT_CAP = 4096
+SIM_BURST_HIGH, SIM_BURST_LOW, SIM_BURST_DWELL_S = 1.6, 0.4, 1.0
+
+
+def sim_trace(workload: str, n: int = 1000, seed: int = 0) -> RequestTrace:
+    """n requests of one of the simulator workloads (SIM_WORKLOADS)."""
+    w = SIM_WORKLOADS[workload]
+    rng = np.random.default_rng(seed)
+    times = np.empty(n)
+    t = 0.0
+    if w.bursty:
+        high = bool(rng.random() < 0.5)
+        edge = rng.exponential(SIM_BURST_DWELL_S)
+        for k in range(n):
+            while True:        # memoryless: restart the draw at every state change
+                rate = w.rate_per_s * (SIM_BURST_HIGH if high else SIM_BURST_LOW)
+                dt = rng.exponential(1.0 / rate)
+                if t + dt < edge:
+                    t += dt
+                    break
+                t = edge
+                high = not high
+                edge = t + rng.exponential(SIM_BURST_DWELL_S)
+            times[k] = t
+    else:
+        times = np.cumsum(rng.exponential(1.0 / w.rate_per_s, size=n))
+    arrival = np.rint((times - times[0]) * 1e9).astype(np.int64)
+    long_ = rng.random(n) < w.long_share
+    med = np.where(long_, w.long_median, w.prompt_median)
+    prompt = np.clip(np.rint(med * np.exp(SIM_SIGMA * rng.standard_normal(n))), 1, SIM_PROMPT_CAP)
+    output = np.clip(np.rint(w.output_median * np.exp(SIM_SIGMA * rng.standard_normal(n))), 1, SIM_OUTPUT_CAP)
+    return RequestTrace(arrival, prompt.astype(np.int64), output.astype(np.int64))
