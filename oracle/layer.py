@@ -206,17 +206,26 @@ def append_kv(shape: LayerShape, kv: KVState, seqs, pos, k, v) -> None:
     tokens before this iteration's rows are written (positions are dense).
     """
     hkv, hd = shape.n_kv_heads, shape.head_dim
+    grown = {}      # sequence -> rows that extend it, in position order
     for r, (s, p) in enumerate(zip(seqs, pos)):
         if s not in kv.seqs:
             kv.seqs[s] = SeqCache(np.zeros((0, hkv, hd)), np.zeros((0, hkv, hd)))
         c = kv.seqs[s]
-        if p > c.length:
-            raise ValueError(f"seq {s}: row at position {p} but only {c.length} cached")
-        if p == c.length:
-            c.k = np.concatenate([c.k, np.zeros((1, hkv, hd))])
-            c.v = np.concatenate([c.v, np.zeros((1, hkv, hd))])
-        c.k[p] = k[r]
-        c.v[p] = v[r]
+        new = grown.setdefault(s, [])
+        if p > c.length + len(new):
+            raise ValueError(f"seq {s}: row at position {p} but only {c.length + len(new)} cached")
+        if p == c.length + len(new):
+            new.append(r)
+        elif p >= c.length:
+            new[p - c.length] = r
+        else:
+            c.k[p] = k[r]
+            c.v[p] = v[r]
+    for s, new in grown.items():     # one copy per sequence, not one per row
+        if new:
+            c = kv.seqs[s]
+            c.k = np.concatenate([c.k, np.asarray(k)[new]])
+            c.v = np.concatenate([c.v, np.asarray(v)[new]])
 
 
 def mlp_rows(shape: LayerShape, w: LayerWeights, x: np.ndarray, o: np.ndarray) -> np.ndarray:

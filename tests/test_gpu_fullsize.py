@@ -52,11 +52,13 @@ def _run(C, P, ctx, seed):
     for sid, L in zip(dec, ctx):
         mir.create(sid)
         mir.install_context(sid, int(L))
+    print(f"C={C} P={P} B={B}: contexts installed", flush=True)
     batch = api.Batch(C, pre, P, dec, [int(L) for L in ctx])
     x = synth.embeddings(batch.rows, shape.d_model, seed=1, stream=seed)
     rng = np.random.default_rng(seed)
     rows = _sample_rows(C, B, rng)
     y, yr, sg, sr = mir.step(batch, x, rows=rows)
+    print(f"C={C} P={P} B={B}: iteration and oracle done", flush=True)
     assert sg == sr, "slot mapping differs"
     for sid in [pre] + dec:
         assert sess.ctx.block_table(sid) == mir.mgr.block_table(sid)
