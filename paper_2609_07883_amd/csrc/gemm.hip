@@ -913,10 +913,11 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 // for qkv); stream-K where 256 x 256 tiles are too few for the CUs on the
 // narrow projections.  n must be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
-    // Up to 32 rows the weight-streaming kernel wins on the narrower
-    // projections (o, down: 12-16% at m <= 32, qkv even); on gate/up the
-    // 128 x 128 tiles keep up with it.
-    if (m <= 32 && n < 16384 && n % 64 == 0) return plan_with_cfg(kSkinnyCfg, m, n, k);
+    // The weight-streaming kernel wins on the narrow projections up to 32
+    // rows (o, down: 10-20%) and on gate/up up to 16 rows (13% at one row);
+    // on qkv the 64 x 128 tiles with split-K measured 3-13% faster.
+    const bool wide = n >= 16384, qkv_like = n >= 6144 && !wide;
+    if (n % 64 == 0 && (wide ? m <= 16 : m <= 32 && !qkv_like)) return plan_with_cfg(kSkinnyCfg, m, n, k);
     constexpr int SK = -1;  // stream-K with the 256 x 256 ring tile
     int cfg;
     if (k >= 8192)  // deep k (down)
@@ -924,7 +925,7 @@ GemmPlan plan_gemm(int m, int n, int k) {
     else if (n >= 16384)  // gate/up
         cfg = m <= 200 ? 0 : m <= 650 ? 1 : m < 950 ? 11 : m < 1800 ? 7 : 11;
     else if (n >= 6144)  // qkv
-        cfg = m <= 128 ? 0 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 10 : m < 1300 ? 0 : m < 1800 ? 1
+        cfg = m <= 32 ? 1 : m <= 128 ? 0 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 10 : m < 1300 ? 0 : m < 1800 ? 1
             : m < 2500 ? 7 : m < 3500 ? 0 : 11;
     else  // o
         cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 700 ? 1 : m < 950 ? 0 : m < 1300 ? SK : m < 1800 ? 0
