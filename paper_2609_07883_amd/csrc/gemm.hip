@@ -226,6 +226,28 @@ __device__ __forceinline__ void tile_mainloop(const GemmArgs& g, int m0, int n0,
 #pragma unroll
                 for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[c][i], fb[c][j], acc[i][j]);
         }
+        // Instruction order for the scheduler: the first slice's reads, then
+        // per slice one next-slice read after each of the first TM + TN
+        // MFMAs.  Left alone, the compiler issues each slice's reads right
+        // before the MFMAs that use them and waits for them there (gate/up
+        // and down +4-5% with the interleave).
+        constexpr int NR = TM + TN, NM = TM * TN;
+        if constexpr (NM >= NR) {
+            __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);  // 0x100: LDS reads
+#pragma unroll
+            for (int s = 0; s < BK / 16; ++s) {
+                if (s + 1 < BK / 16) {
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) {
+                        __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);  // 0x8: MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    }
+                    if constexpr (NM > NR) __builtin_amdgcn_sched_group_barrier(0x8, NM - NR, 0);
+                } else {
+                    __builtin_amdgcn_sched_group_barrier(0x8, NM, 0);
+                }
+            }
+        }
     };
 
     if constexpr (RING == 0) {
