@@ -365,6 +365,18 @@ typedef struct slw_request {
     int32_t output_len;  /* output tokens, >= 1; the first one comes from the prefill */
 } slw_request;
 
+/*
+ * Optional per-request objectives (Sec. 3.5), parallel to the request array.
+ * A chunk is admissible when T_hat + delta_i <= d_i - s_t for every active
+ * request i, with d_i = l_i + D_i: the loop runs Alg. 1 on the deadlines
+ * d_i - (delta_i - opts->margin_ns) with margin opts->margin_ns.
+ */
+typedef struct slw_request_slo {
+    int64_t tpot_ns;     /* D_i (> 0), or 0 for opts->tpot_ns                       */
+    int64_t margin_ns;   /* delta_i of the request's class (>= 0), or < 0 for opts  */
+    int64_t ttft_ns;     /* TTFT objective for SLW_QUEUE_EDF (> 0), or 0 for none   */
+} slw_request_slo;
+
 #define SLW_POLICY_SLOWEAVE 0 /* Alg. 1 over opts->table with margin and cap       */
 #define SLW_POLICY_FIXED 1    /* chunks of opts->fixed_chunk tokens                */
 
@@ -376,6 +388,13 @@ typedef struct slw_request {
 #define SLW_SERVE_KV_WAIT 0x100u      /* the oldest prompt waits for KV blocks      */
 #define SLW_SERVE_DECODE_CAP 0x200u   /* the oldest prompt waits: decode batch full */
 #define SLW_SERVE_UNPRICED 0x400u     /* decode batch above the table: decode-only  */
+#define SLW_SERVE_AGED 0x800u         /* chunk forced by the aging threshold         */
+
+/* Queue disciplines (Sec. 3.4): which pending prompt is served first.  Ties
+ * go to the older request (arrival, then id). */
+#define SLW_QUEUE_OLDEST 0   /* earliest arrival                                    */
+#define SLW_QUEUE_SRPT 1     /* fewest remaining prompt tokens                      */
+#define SLW_QUEUE_EDF 2      /* earliest arrival + TTFT objective (none: last)      */
 
 typedef struct slw_serve_opts {
     int32_t policy;          /* SLW_POLICY_*                                            */
@@ -404,6 +423,31 @@ typedef struct slw_serve_opts {
      * P99 of the window).  0 = off. */
     int32_t residual_window;
     const slw_cost_table* exec_table;  /* SLW_EXEC_TABLE: the iteration times */
+    /* Policy variants (Sec. 3.3-3.5).  Zero-initialised fields leave the
+     * loop as described above. */
+    const slw_request_slo* slo; /* host [n] per-request objectives, or NULL            */
+    int32_t queue;           /* SLW_QUEUE_*                                             */
+    /* Admission control: a request that becomes eligible is refused when
+     * T_hat(n, 0) + delta_i > D_i * admit_ppm / 1e6 (table lookup at prefix 0),
+     * n counting the active decodes, the admitted pending prompts and the
+     * request; also refused when n is beyond the table.  A refused request
+     * emits no token: its token_ns entries are -1.  0 = off; needs table. */
+    int32_t admit_ppm;
+    /* Aging (SLOWeave): when Alg. 1 gives no chunk to a head that may run and
+     * that has waited aging_ns since it became eligible or last ran a chunk,
+     * min(aging_chunk, remaining, c_max) tokens run anyway (SLW_SERVE_AGED): a
+     * bounded deadline violation recorded as such.  0 = off. */
+    int64_t aging_ns;
+    int32_t aging_chunk;
+    /* Prefill batching by first fit (SLOWeave, virtual-clock executors only;
+     * SLW_EUNSUPPORTED with the GPU executor): when the head's chunk finishes
+     * its prompt, the next pending prompts in queue order join while the
+     * decode cap allows (counting prompts that finish earlier in the
+     * iteration), up to max_prefills prompts, each with the largest chunk c
+     * for which T_hat(n, S + c) still meets the budget, S being the tokens
+     * already placed; a prompt that does not finish ends the list.  The
+     * iteration is priced at the total.  0 or 1 = one prompt. */
+    int32_t max_prefills;
 } slw_serve_opts;
 
 /* One iteration of a serving run (host memory). */
@@ -420,13 +464,16 @@ typedef struct slw_iteration_record {
                              (0 when none may run)                                       */
     uint32_t flags;       /* SLW_FLAG_* of the decision | SLW_SERVE_*                    */
     int64_t rel_margin_ppm; /* telemetry margin q used by the decision (0 when off)       */
+    int32_t n_prefill;    /* prompts served (chunk is their total; prefill_id the first)  */
+    int32_t reserved;
 } slw_iteration_record;
 
 /*
  * Serve a trace to completion (synchronous).  Each iteration decodes one
  * token for every active request (decode rows in ascending id order) and
  * runs at most one prefill chunk of the oldest eligible prompt (by arrival,
- * then id); requests that arrive during an iteration become eligible when
+ * then id; opts->queue and opts->max_prefills change which and how many
+ * prompts); requests that arrive during an iteration become eligible when
  * it ends; the first output token is emitted by the iteration that finishes
  * the prompt, which also sets l_i; a prompt may start only while fewer than
  * max_decode requests decode and (GPU) while the pool can hold every
@@ -435,7 +482,7 @@ typedef struct slw_iteration_record {
  * it.  The table executor advances the clock by exec_table's T_hat(n, c)
  * (a stand-in for hardware whose cost differs from the controller's table).
  * With a context axis in the table, decisions and predictions are priced
- * at the oldest eligible prompt's cached prefix (0 with none).
+ * at the cached prefix of the first prompt the iteration serves (0 with none).
  * The GPU executor synchronises `stream` after every iteration, creates
  * a KV sequence per request when its prompt starts and frees it when its
  * last token is out; ctx may be NULL with SLW_EXEC_ANALYTIC.

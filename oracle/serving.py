@@ -54,53 +54,102 @@ class Request:
     arrival_ns: int
     prompt: int      # prompt tokens (>= 1)
     output: int      # output tokens (>= 1), the first one emitted by the prefill
+    tpot_ns: int = 0     # D_i (Sec. 3.5); 0: the run's D
+    margin_ns: int = -1  # the request class's margin delta_i (Sec. 3.5); < 0: the run's delta
+    ttft_ns: int = 0     # TTFT objective used by earliest-deadline queueing; 0: none
 
 
 @dataclass
 class Iteration:
     start_ns: int
     end_ns: int
-    chunk: int
+    chunk: int           # prefill tokens run (over every prompt of the iteration)
     n_decode: int
-    prefill_rid: int     # -1 when the iteration runs no chunk
+    prefill_rid: int     # first prompt served, -1 when the iteration runs no chunk
     budget_ns: int       # earliest deadline minus start (0 with no active decode)
     rel_margin_ppm: int = 0  # telemetry margin used by the decision
+    n_prefill: int = 0   # prompts served
+    aged: bool = False   # the chunk was forced by the aging threshold
 
 
 @dataclass
 class Trace:
     token_ns: dict = field(default_factory=dict)    # rid -> [completion time of each output token]
     iterations: list = field(default_factory=list)
+    rejected: set = field(default_factory=set)      # rids refused by admission control
+
+
+QUEUES = ("oldest", "srpt", "edf")
+
+
+def _queue_key(queue, r: Request, remaining: int):
+    """Sec. 3.4: the order in which pending prompts are served.  Ties go to
+    the older request (arrival, then id)."""
+    if queue == "srpt":             # shortest remaining prefill first
+        return (remaining, r.arrival_ns, r.rid)
+    if queue == "edf":              # earliest TTFT deadline first (none: last)
+        return (r.arrival_ns + r.ttft_ns if r.ttft_ns > 0 else float("inf"), r.arrival_ns, r.rid)
+    return (r.arrival_ns, r.rid)    # oldest first
 
 
 def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed_chunk: int = 0,
              predict=None, c_last: int | None = None, c_max: int = 4096, margin_ns: int = 0,
              max_decode: int | None = None, residual_window: int = 0, prefix_aware: bool = False,
-             max_iterations: int = 10_000_000) -> Trace:
+             queue: str = "oldest", admit_ppm: int = 0, aging_ns: int = 0, aging_chunk: int = 0,
+             max_prefills: int = 1, max_iterations: int = 10_000_000) -> Trace:
     """Run the trace through the iteration-level loop of Sec. 4.1.
 
-    cost_ns(n, c) -> ns is how long an iteration with n decodes and a chunk
-    of c tokens takes (the simulator's cost model); predict(n, c) -> ns is
+    cost_ns(n, c) -> ns is how long an iteration with n decodes and c
+    prefill tokens takes (the simulator's cost model); predict(n, c) -> ns is
     what the SLOWeave controller believes (defaults to cost_ns) and c_last
     the largest chunk it can price.  policy is "sloweave" (Alg. 1 with margin
     margin_ns and cap c_max) or "fixed" (chunks of fixed_chunk tokens).
     residual_window > 0 turns on the telemetry margin (module docstring).
     With prefix_aware, cost_ns and predict take a third argument, the cached
-    prefix the iteration is priced at: that of the oldest eligible prompt
+    prefix the iteration is priced at: that of the first prompt it serves
     (its tokens already processed), 0 with none.
+
+    Policy variants (Sec. 3.3-3.5; the paper gives no parameters, these are
+    the readings this loop implements):
+    * per-request objectives: request i's next-token deadline is
+      l_i + D_i and its class margin delta_i; a chunk is admissible when
+      T_hat + delta_i <= d_i - s_t for every active i, i.e. Alg. 1 runs on the
+      deadlines d_i - (delta_i - margin_ns) with margin margin_ns;
+    * queue: the pending prompt served first ("oldest", "srpt": fewest
+      remaining prompt tokens, "edf": earliest arrival + TTFT objective);
+    * admission control (admit_ppm > 0): a request that becomes eligible is
+      refused when T_hat(n, 0) + delta_i > D_i * admit_ppm / 1e6, n counting
+      the active decodes, the admitted pending prompts and itself (also
+      refused when n is beyond the predictor); refused requests emit no
+      token;
+    * aging (aging_ns > 0, SLOWeave only): when Alg. 1 gives no chunk to a
+      head that may run and that has waited aging_ns since it became eligible
+      or last ran, min(aging_chunk, remaining, c_max) tokens run anyway;
+    * prefill batching (max_prefills > 1, SLOWeave only): first fit.  When
+      the head's chunk finishes its prompt, the next pending prompts in queue
+      order join while the decode cap allows (counting the prompts that
+      finish earlier in the iteration), each with the largest chunk c for
+      which T_hat(n, S + c) still meets the budget, S being the tokens
+      already placed (Alg. 1's search with the predictor shifted by S, caps
+      c_max - S and c_last - S); a prompt that does not finish ends the list.
     """
     if policy not in ("sloweave", "fixed"):
         raise ValueError(policy)
     if policy == "fixed" and fixed_chunk <= 0:
         raise ValueError("fixed_chunk must be positive")
+    if queue not in QUEUES:
+        raise ValueError(queue)
     predict = predict or cost_ns
 
     def at(f, n, c, p):
         return f(n, c, p) if prefix_aware else f(n, c)
     reqs = sorted(requests, key=lambda r: (r.arrival_ns, r.rid))
+    D = {r.rid: r.tpot_ns if r.tpot_ns > 0 else tpot_ns for r in reqs}
+    delta = {r.rid: r.margin_ns if r.margin_ns >= 0 else margin_ns for r in reqs}
     out = Trace(token_ns={r.rid: [] for r in reqs})
-    pending = []            # eligible requests whose prompt is not finished, oldest first
+    pending = []            # eligible requests whose prompt is not finished
     done_prompt = {}        # rid -> prompt tokens already processed
+    waited = {}             # rid -> time it became eligible or last ran a chunk
     active = {}             # rid -> (request, time of its latest token l_i)
     t = reqs[0].arrival_ns if reqs else 0
     nxt = 0
@@ -110,20 +159,38 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
         if finished == len(reqs):
             return out
         while nxt < len(reqs) and reqs[nxt].arrival_ns <= t:
-            pending.append(reqs[nxt])
-            done_prompt[reqs[nxt].rid] = 0
+            r = reqs[nxt]
             nxt += 1
+            if admit_ppm > 0:
+                n_future = len(active) + len(pending) + 1
+                try:
+                    cost = at(predict, n_future, 0, 0)
+                except IndexError:                 # beyond the priced decode batches
+                    cost = None
+                if cost is None or (cost + delta[r.rid]) * 10**6 > D[r.rid] * admit_ppm:
+                    out.rejected.add(r.rid)
+                    finished += 1
+                    continue
+            pending.append(r)
+            done_prompt[r.rid] = 0
+            waited[r.rid] = t
+        if finished == len(reqs):
+            return out
         if not pending and not active:
             t = reqs[nxt].arrival_ns           # idle until the next arrival
             continue
         order = sorted(active)                 # decode rows in request-id order
-        deadlines = [active[r][1] + tpot_ns for r in order]
+        deadlines = [active[r][1] + D[r] for r in order]
+        eff = [active[r][1] + D[r] - (delta[r] - margin_ns) for r in order]
         n = len(order)
-        head = pending[0] if pending and (max_decode is None or n < max_decode) else None
+        queue_order = sorted(pending, key=lambda r: _queue_key(queue, r, r.prompt - done_prompt[r.rid]))
+        head = queue_order[0] if queue_order and (max_decode is None or n < max_decode) else None
         remaining = head.prompt - done_prompt[head.rid] if head else 0
         budget = min(deadlines) - t if deadlines else 0
         prefix = done_prompt[head.rid] if head else 0
         rel = 0
+        aged = False
+        plan = []                              # (request, tokens) served this iteration
         if head is None:
             chunk = 0
         elif policy == "fixed":
@@ -136,11 +203,41 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
                 v = at(predict, nn, cc, p)
                 return v + -(-q * v // 10**6)   # T_hat + ceil(q T_hat / 1e6)
             try:
-                chunk = select_chunk(with_margin, deadlines, t, remaining, c_max, margin_ns, c_last=c_last)[0]
+                chunk = select_chunk(with_margin, eff, t, remaining, c_max, margin_ns, c_last=c_last)[0]
             except IndexError:                 # n above the priced decode batches
                 chunk = 0
+            if chunk == 0 and aging_ns > 0 and t - waited[head.rid] >= aging_ns:
+                chunk = min(aging_chunk, remaining, c_max)
+                aged = True
+        if chunk > 0:
+            plan.append((head, chunk))
+        if policy == "sloweave" and max_prefills > 1 and chunk == remaining and chunk > 0 and not aged:
+            total = chunk
+            for r in queue_order[1:]:
+                if len(plan) >= max_prefills:
+                    break
+                if max_decode is not None and n + len(plan) >= max_decode:
+                    break
+                rem = r.prompt - done_prompt[r.rid]
+
+                def shifted(nn, cc, base=total, q=rel, p=prefix):
+                    v = at(predict, nn, base + cc, p)
+                    return v + -(-q * v // 10**6)
+                try:
+                    c = select_chunk(shifted, eff, t, rem, c_max - total, margin_ns,
+                                     c_last=None if c_last is None else c_last - total)[0]
+                except IndexError:
+                    c = 0
+                if c <= 0:
+                    break
+                plan.append((r, c))
+                total += c
+                if c < rem:
+                    break
+            chunk = total
         end = t + at(cost_ns, n, chunk, prefix)
-        out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget, rel))
+        out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget, rel,
+                                        len(plan), aged))
         if residual_window > 0 and chunk > 0:
             pred = at(predict, n, chunk, prefix)
             if pred > 0:
@@ -153,15 +250,16 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
                 finished += 1
             else:
                 active[rid] = (req, end)
-        if chunk > 0:
-            done_prompt[head.rid] += chunk
-            if done_prompt[head.rid] == head.prompt:
-                pending.pop(0)
-                out.token_ns[head.rid].append(end)     # first output token
-                if head.output == 1:
+        for r, c in plan:
+            done_prompt[r.rid] += c
+            waited[r.rid] = end
+            if done_prompt[r.rid] == r.prompt:
+                pending.remove(r)
+                out.token_ns[r.rid].append(end)     # first output token
+                if r.output == 1:
                     finished += 1
                 else:
-                    active[head.rid] = (head, end)
+                    active[r.rid] = (r, end)
         t = end
     raise RuntimeError("iteration limit reached")
 
@@ -185,28 +283,31 @@ def request_metrics(req: Request, token_ns, ttft_slo_ns: int, tpot_slo_ns: int) 
     return RequestMetrics(req.rid, ttft, tpot, token_ns[-1], ttft <= ttft_slo_ns and tpot <= tpot_slo_ns)
 
 
-def summarize(requests, token_ns: dict, ttft_slo_ns: int, tpot_slo_ns: int) -> dict:
+def summarize(requests, token_ns: dict, ttft_slo_ns: int, tpot_slo_ns: int, rejected=()) -> dict:
     """Request-level results of one run (Sec. 4.3), integer ns and exact ratios.
 
     goodput_num / goodput_den_ns is requests meeting both SLOs per
-    nanosecond of arrival span.
+    nanosecond of arrival span.  Requests refused by admission control
+    count as missed and are left out of the latency percentiles.
     """
     reqs = sorted(requests, key=lambda r: (r.arrival_ns, r.rid))
-    ms = [request_metrics(r, token_ns[r.rid], ttft_slo_ns, tpot_slo_ns) for r in reqs]
+    rejected = set(rejected)
+    ms = [request_metrics(r, token_ns[r.rid], ttft_slo_ns, tpot_slo_ns) for r in reqs if r.rid not in rejected]
     span = reqs[-1].arrival_ns - reqs[0].arrival_ns
     if span <= 0:
         raise ValueError("the arrival span must be positive")
-    makespan = max(m.finish_ns for m in ms) - reqs[0].arrival_ns
+    makespan = max(m.finish_ns for m in ms) - reqs[0].arrival_ns if ms else 0
     met = sum(m.meets for m in ms)
     return {
-        "requests": len(ms),
+        "requests": len(reqs),
+        "rejected": len(rejected),
         "met": met,
         "goodput_num": met,
         "goodput_den_ns": span,
         "makespan_ns": makespan,
-        "p50_ttft_ns": nearest_rank([m.ttft_ns for m in ms], 1, 2),
-        "p99_ttft_ns": nearest_rank([m.ttft_ns for m in ms], 99, 100),
-        "p99_tpot_ns": nearest_rank([m.tpot_p99_ns for m in ms], 99, 100),
-        "output_tokens": sum(r.output for r in reqs),
-        "prompt_tokens": sum(r.prompt for r in reqs),
+        "p50_ttft_ns": nearest_rank([m.ttft_ns for m in ms], 1, 2) if ms else 0,
+        "p99_ttft_ns": nearest_rank([m.ttft_ns for m in ms], 99, 100) if ms else 0,
+        "p99_tpot_ns": nearest_rank([m.tpot_p99_ns for m in ms], 99, 100) if ms else 0,
+        "output_tokens": sum(r.output for r in reqs if r.rid not in rejected),
+        "prompt_tokens": sum(r.prompt for r in reqs if r.rid not in rejected),
     }

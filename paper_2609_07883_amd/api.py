@@ -84,19 +84,27 @@ class ServeOpts(C.Structure):
                 ("table", C.c_void_p), ("executor", C.c_int32), ("skip_idle", C.c_int32),
                 ("x_in", C.c_void_p), ("x_out", C.c_void_p), ("max_rows", C.c_int32),
                 ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p),
-                ("residual_window", C.c_int32), ("exec_table", C.c_void_p)]
+                ("residual_window", C.c_int32), ("exec_table", C.c_void_p), ("slo", C.c_void_p),
+                ("queue", C.c_int32), ("admit_ppm", C.c_int32), ("aging_ns", C.c_int64),
+                ("aging_chunk", C.c_int32), ("max_prefills", C.c_int32)]
+
+
+class RequestSloC(C.Structure):
+    _fields_ = [("tpot_ns", C.c_int64), ("margin_ns", C.c_int64), ("ttft_ns", C.c_int64)]
 
 
 class IterationRecord(C.Structure):
     _fields_ = [("start_ns", C.c_int64), ("end_ns", C.c_int64), ("budget_ns", C.c_int64),
                 ("decide_ns", C.c_int64), ("predicted_ns", C.c_int64), ("prefill_id", C.c_int64),
                 ("chunk", C.c_int32), ("n_decode", C.c_int32), ("remaining", C.c_int32),
-                ("flags", C.c_uint32), ("rel_margin_ppm", C.c_int64)]
+                ("flags", C.c_uint32), ("rel_margin_ppm", C.c_int64), ("n_prefill", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 POLICY_SLOWEAVE, POLICY_FIXED = 0, 1
 EXEC_GPU, EXEC_ANALYTIC, EXEC_TABLE = 0, 1, 2
-SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED = 0x100, 0x200, 0x400
+SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED, SERVE_AGED = 0x100, 0x200, 0x400, 0x800
+QUEUES = {"oldest": 0, "srpt": 1, "edf": 2}
 
 _lib = None
 
@@ -300,7 +308,8 @@ def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_
 ITERATION_DTYPE = np.dtype([("start_ns", np.int64), ("end_ns", np.int64), ("budget_ns", np.int64),
                             ("decide_ns", np.int64), ("predicted_ns", np.int64), ("prefill_id", np.int64),
                             ("chunk", np.int32), ("n_decode", np.int32), ("remaining", np.int32),
-                            ("flags", np.uint32), ("rel_margin_ppm", np.int64)])
+                            ("flags", np.uint32), ("rel_margin_ppm", np.int64), ("n_prefill", np.int32),
+                            ("reserved", np.int32)])
 assert ITERATION_DTYPE.itemsize == C.sizeof(IterationRecord)
 
 
@@ -309,17 +318,28 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
           executor: int = EXEC_ANALYTIC, ctx: "Context | None" = None, skip_idle: bool = True,
           x_in: int = 0, x_out: int = 0, max_rows: int = 0, ws: int = 0, ws_bytes: int = 0,
           stream: int = 0, iter_cap: int | None = None, residual_window: int = 0,
-          exec_table: CostTable | None = None):
+          exec_table: CostTable | None = None, slo_tpot_ns=None, slo_margin_ns=None, slo_ttft_ns=None,
+          queue: str = "oldest", admit_ppm: int = 0, aging_ns: int = 0, aging_chunk: int = 0,
+          max_prefills: int = 1):
     """slw_serve over a trace given as arrays.
 
+    slo_tpot_ns / slo_margin_ns / slo_ttft_ns are optional per-request
+    objectives (0 / -1 / 0 entries defer to the run's values).
     Returns (token_ns, iterations): token_ns is a list of int64 arrays, one per
-    request in the given order; iterations is a structured array of
-    ITERATION_DTYPE records.
+    request in the given order (all -1 for a request refused by admission
+    control); iterations is a structured array of ITERATION_DTYPE records.
     """
     n = len(ids)
     reqs = (RequestC * max(n, 1))()
     for k in range(n):
         reqs[k] = RequestC(int(ids[k]), int(arrival_ns[k]), int(prompt[k]), int(output[k]))
+    slo = None
+    if slo_tpot_ns is not None or slo_margin_ns is not None or slo_ttft_ns is not None:
+        slo = (RequestSloC * max(n, 1))()
+        for k in range(n):
+            slo[k] = RequestSloC(int(slo_tpot_ns[k]) if slo_tpot_ns is not None else 0,
+                                 int(slo_margin_ns[k]) if slo_margin_ns is not None else -1,
+                                 int(slo_ttft_ns[k]) if slo_ttft_ns is not None else 0)
     out = np.asarray(output, dtype=np.int64)
     tok = np.zeros(max(int(out.sum()), 1), np.int64)
     cap = int(iter_cap if iter_cap is not None else 4 * (int(out.sum()) + int(np.sum(prompt))) + 16)
@@ -327,7 +347,9 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
     o = ServeOpts(policy, fixed_chunk, c_max, max_decode, int(tpot_ns), int(margin_ns),
                   table.handle if table is not None else None, executor, int(skip_idle),
                   x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None,
-                  residual_window, exec_table.handle if exec_table is not None else None)
+                  residual_window, exec_table.handle if exec_table is not None else None,
+                  C.cast(slo, C.c_void_p) if slo is not None else None, QUEUES[queue], int(admit_ppm),
+                  int(aging_ns), int(aging_chunk), int(max_prefills))
     nit = C.c_int64()
     _check(lib().slw_serve(ctx._h if ctx is not None else None, reqs, n, C.byref(o), _ptr(tok, C.c_int64),
                            len(tok), its.ctypes.data_as(C.POINTER(IterationRecord)), len(its), C.byref(nit)))

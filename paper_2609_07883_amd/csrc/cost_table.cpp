@@ -151,6 +151,13 @@ int64_t analytic_iteration_ns(int32_t n, int32_t c) {
 int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
                       int32_t prefix, int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm,
                       int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
+    return select_chunk_after(t, deadlines_ns, n_active, now_ns, prefix, 0, remaining, c_max, margin_ns,
+                              rel_margin_ppm, chunk, flags, n_lookups);
+}
+
+int select_chunk_after(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
+                       int32_t prefix, int32_t base, int32_t remaining, int32_t c_max, int64_t margin_ns,
+                       int64_t rel_margin_ppm, int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
     if (!t || !chunk || !flags) return fail(SLW_EINVAL, "null argument");
     *chunk = 0;
     *flags = 0;
@@ -158,14 +165,15 @@ int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int3
     if (n_active < 0 || (n_active > 0 && !deadlines_ns)) return fail(SLW_EINVAL, "bad active set");
     if (prefix < 0) return fail(SLW_EINVAL, "negative prefix");
     if (rel_margin_ppm < 0 || rel_margin_ppm > 100000000) return fail(SLW_ERANGE, "relative margin out of range");
+    if (base < 0) return fail(SLW_EINVAL, "negative base chunk");
     if (remaining <= 0) {  // no pending prefill
         *flags = SLW_FLAG_NO_PENDING;
         return SLW_OK;
     }
-    int32_t cap = std::min(c_max, remaining);
+    int32_t cap = std::min(c_max - base, remaining);
     uint32_t fl = 0;
-    if (t->c_grid.back() < cap) {
-        cap = t->c_grid.back();
+    if (t->c_grid.back() - base < cap) {
+        cap = t->c_grid.back() - base;
         fl |= SLW_FLAG_CAPPED_BY_GRID;
     }
     if (cap < 0) cap = 0;
@@ -181,7 +189,7 @@ int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int3
     const int64_t budget = earliest - now_ns;
     // predicted time plus the relative margin ceil(rel * T_hat / 1e6) (monotone in c like T_hat)
     auto predict = [&](int32_t c) {
-        const int64_t v = lookup_row(t, row, c);
+        const int64_t v = lookup_row(t, row, base + c);
         return v + (rel_margin_ppm * v + 999999) / 1000000;
     };
     int32_t lo = 0, hi = cap, lookups = 0;

@@ -39,6 +39,14 @@ int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int3
                       int32_t prefix, int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm,
                       int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
 
+// The same search with base tokens already placed in the iteration: the
+// largest c <= min(remaining, c_max - base, last grid chunk - base) with
+// T_hat(prefix, n, base + c) + ceil(rel * T_hat / 1e6) + margin_ns <= budget
+// (first-fit prefill batching, Sec. 3.3).  select_chunk_core is base 0.
+int select_chunk_after(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
+                       int32_t prefix, int32_t base, int32_t remaining, int32_t c_max, int64_t margin_ns,
+                       int64_t rel_margin_ppm, int32_t* chunk, uint32_t* flags, int32_t* n_lookups);
+
 // T_hat at (prefix, n, c) with the lookup rules of the ABI; SLW_ERANGE outside the grids.
 int lookup_ctx(const slw_cost_table* t, int32_t prefix, int32_t n, int32_t c, int64_t* t_ns);
 

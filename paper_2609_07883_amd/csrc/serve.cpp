@@ -12,7 +12,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cstdint>
-#include <deque>
+#include <limits>
 #include <map>
 #include <thread>
 #include <vector>
@@ -35,6 +35,7 @@ struct Live {
     int32_t prompt_done;  // prompt tokens processed
     int32_t emitted;      // output tokens emitted
     int64_t last_ns;      // l_i: time of the latest token
+    int64_t waited_ns;    // pending: when it became eligible or last ran a chunk
     bool started;         // prompt begun (KV sequence exists)
 };
 
@@ -58,6 +59,14 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     if (o->executor == SLW_EXEC_TABLE && !o->exec_table) return fail(SLW_EINVAL, "table executor needs exec_table");
     if (o->residual_window < 0 || o->residual_window > 65536)
         return fail(SLW_ERANGE, "residual_window must be in [0, 65536]");
+    if (o->queue < SLW_QUEUE_OLDEST || o->queue > SLW_QUEUE_EDF) return fail(SLW_EINVAL, "unknown queue %d", o->queue);
+    if (o->admit_ppm < 0 || o->admit_ppm > 10000000) return fail(SLW_ERANGE, "admit_ppm must be in [0, 1e7]");
+    if (o->admit_ppm > 0 && !o->table) return fail(SLW_EINVAL, "admission control needs a cost table");
+    if (o->aging_ns < 0 || (o->aging_ns > 0 && o->aging_chunk < 1))
+        return fail(SLW_EINVAL, "aging needs aging_ns >= 0 and aging_chunk >= 1");
+    if (o->max_prefills < 0) return fail(SLW_EINVAL, "max_prefills must be >= 0");
+    if (o->max_prefills > 1 && o->executor == SLW_EXEC_GPU)
+        return fail(SLW_EUNSUPPORTED, "prefill batching runs on the virtual-clock executors only");
     if (o->executor == SLW_EXEC_GPU) {
         if (!ctx || !o->x_in || !o->x_out || !o->ws) return fail(SLW_EINVAL, "GPU executor needs ctx and buffers");
         const int64_t cap = o->policy == SLW_POLICY_FIXED ? o->fixed_chunk : o->c_max;
@@ -71,6 +80,8 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         if (r.prompt_len < 1 || r.output_len < 1 || r.arrival_ns < 0)
             return fail(SLW_EINVAL, "request %lld: bad lengths or arrival", static_cast<long long>(r.id));
         if (seen[r.id]++) return fail(SLW_EINVAL, "duplicate request id %lld", static_cast<long long>(r.id));
+        if (o->slo && (o->slo[i].tpot_ns < 0 || o->slo[i].ttft_ns < 0))
+            return fail(SLW_EINVAL, "request %lld: negative objective", static_cast<long long>(r.id));
     }
     return SLW_OK;
 }
@@ -108,7 +119,29 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
                                                         : reqs[a].id < reqs[b].id;
     });
 
-    std::deque<Live> pending;            // eligible, prompt not finished, oldest first
+    // per-request objectives (Sec. 3.5)
+    auto D_of = [&](int32_t i) { return o->slo && o->slo[i].tpot_ns > 0 ? o->slo[i].tpot_ns : o->tpot_ns; };
+    auto delta_of = [&](int32_t i) { return o->slo && o->slo[i].margin_ns >= 0 ? o->slo[i].margin_ns : o->margin_ns; };
+    auto edf_key = [&](int32_t i) {
+        return o->slo && o->slo[i].ttft_ns > 0 ? reqs[i].arrival_ns + o->slo[i].ttft_ns
+                                               : std::numeric_limits<int64_t>::max();
+    };
+    // queue order (Sec. 3.4), ties to the older request
+    auto before = [&](const Live& x, const Live& y) {
+        const slw_request& a = reqs[x.req];
+        const slw_request& b = reqs[y.req];
+        if (o->queue == SLW_QUEUE_SRPT) {
+            const int32_t ra = a.prompt_len - x.prompt_done, rb = b.prompt_len - y.prompt_done;
+            if (ra != rb) return ra < rb;
+        } else if (o->queue == SLW_QUEUE_EDF) {
+            const int64_t ea = edf_key(x.req), eb = edf_key(y.req);
+            if (ea != eb) return ea < eb;
+        }
+        return a.arrival_ns != b.arrival_ns ? a.arrival_ns < b.arrival_ns : a.id < b.id;
+    };
+    const int32_t max_prefills = std::max(o->max_prefills, 1);
+
+    std::vector<Live> pending;           // eligible, prompt not finished (queue order once sorted)
     std::map<int64_t, Live> active;      // decoding, keyed (and batched) by id
     int64_t committed_blocks = 0;        // KV blocks every started request may reach
     int32_t next = 0, finished = 0;
@@ -120,20 +153,43 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     int64_t host_shift = virt;  // trace time = host_ns() - t0_host + host_shift
     auto now = [&]() { return gpu ? host_ns() - t0_host + host_shift : virt; };
 
-    std::vector<int64_t> dec_ids, deadlines;
+    std::vector<int64_t> dec_ids, deadlines, eff;
     std::vector<int32_t> ctx_lens;
+    std::vector<std::pair<int32_t, int32_t>> plan;  // (index into pending, tokens) served this iteration
     // telemetry: relative residuals (ppm) of the last residual_window chunked iterations
     const int32_t W = o->residual_window;
     std::vector<int64_t> resid(std::max(W, 1)), scratch;
     int64_t n_resid = 0;
     const hipStream_t stream = static_cast<hipStream_t>(o->stream);
 
+    auto finish = [&](const slw_request& r) {
+        if (gpu) {
+            const int e = slw_seq_free(ctx, r.id);
+            if (e) return e;
+            committed_blocks -= kv_blocks_for(r);
+        }
+        ++finished;
+        return SLW_OK;
+    };
+
     while (finished < n) {
         int64_t t = now();
         while (next < n && reqs[order[next]].arrival_ns <= t) {
-            pending.push_back(Live{order[next], 0, 0, 0, false});
-            ++next;
+            const int32_t i = order[next++];
+            if (o->admit_ppm > 0) {  // admission control (Sec. 3.4)
+                const int32_t nf = static_cast<int32_t>(active.size() + pending.size() + 1);
+                int64_t cost = 0;
+                const bool priced = lookup_ctx(o->table, 0, nf, 0, &cost) == SLW_OK;
+                if (!priced) clear_error();
+                if (!priced || (cost + delta_of(i)) * 1000000 > D_of(i) * o->admit_ppm) {
+                    std::fill(token_ns + tok_off[i], token_ns + tok_off[i + 1], int64_t{-1});
+                    ++finished;
+                    continue;
+                }
+            }
+            pending.push_back(Live{i, 0, 0, 0, t, false});
         }
+        if (finished == n) break;
         if (pending.empty() && active.empty()) {
             const int64_t arr = reqs[order[next]].arrival_ns;  // next < n: someone is still to come
             if (!gpu) {
@@ -154,16 +210,19 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         const int64_t t_dec0 = host_ns();
         dec_ids.clear();
         deadlines.clear();
+        eff.clear();
         ctx_lens.clear();
         for (const auto& kv : active) {
             const Live& a = kv.second;
             const slw_request& r = reqs[a.req];
             dec_ids.push_back(r.id);
-            deadlines.push_back(a.last_ns + o->tpot_ns);
+            deadlines.push_back(a.last_ns + D_of(a.req));
+            eff.push_back(a.last_ns + D_of(a.req) - (delta_of(a.req) - o->margin_ns));
             ctx_lens.push_back(r.prompt_len + a.emitted - 1);
         }
         const int32_t nd = static_cast<int32_t>(dec_ids.size());
         if (nd > 0) rec.budget_ns = *std::min_element(deadlines.begin(), deadlines.end()) - t;
+        if (o->queue != SLW_QUEUE_OLDEST) std::sort(pending.begin(), pending.end(), before);
 
         Live* head = nullptr;
         if (!pending.empty()) {
@@ -177,21 +236,23 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             }
         }
         int32_t chunk = 0;
+        int64_t rel = 0;
+        plan.clear();
+        const int32_t prefix = head ? head->prompt_done : 0;  // context the iteration is priced at
         if (head) {
             const int32_t remaining = reqs[head->req].prompt_len - head->prompt_done;
             rec.remaining = remaining;
             if (o->policy == SLW_POLICY_FIXED) {
                 chunk = std::min(o->fixed_chunk, remaining);
             } else {
-                int64_t rel = 0;
                 if (W > 0 && n_resid > 0) {
                     scratch.assign(resid.begin(), resid.begin() + std::min<int64_t>(n_resid, W));
                     rel = std::min<int64_t>(std::max<int64_t>(nearest_rank(scratch, 99, 100), 0), 100000000);
                 }
                 rec.rel_margin_ppm = rel;
                 uint32_t fl = 0;
-                rc = select_chunk_core(o->table, deadlines.data(), nd, t, head->prompt_done, remaining, o->c_max,
-                                       o->margin_ns, rel, &chunk, &fl, nullptr);
+                rc = select_chunk_core(o->table, eff.data(), nd, t, prefix, remaining, o->c_max, o->margin_ns, rel,
+                                       &chunk, &fl, nullptr);
                 if (rc == SLW_ERANGE) {  // more decodes than the table prices
                     clear_error();
                     chunk = 0;
@@ -200,12 +261,40 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
                     return rc;
                 }
                 rec.flags |= fl;
+                if (chunk == 0 && o->aging_ns > 0 && t - head->waited_ns >= o->aging_ns) {
+                    chunk = std::min({o->aging_chunk, remaining, o->c_max});
+                    rec.flags |= SLW_SERVE_AGED;
+                }
+            }
+            if (chunk > 0) plan.emplace_back(0, chunk);
+            // first-fit prefill batching (Sec. 3.3)
+            if (o->policy == SLW_POLICY_SLOWEAVE && max_prefills > 1 && chunk > 0 && chunk == remaining &&
+                !(rec.flags & SLW_SERVE_AGED)) {
+                for (size_t k = 1; k < pending.size(); ++k) {
+                    if (static_cast<int32_t>(plan.size()) >= max_prefills) break;
+                    if (nd + static_cast<int32_t>(plan.size()) >= o->max_decode) break;
+                    const int32_t rem = reqs[pending[k].req].prompt_len - pending[k].prompt_done;
+                    int32_t c = 0;
+                    uint32_t fl = 0;
+                    rc = select_chunk_after(o->table, eff.data(), nd, t, prefix, chunk, rem, o->c_max, o->margin_ns,
+                                            rel, &c, &fl, nullptr);
+                    if (rc == SLW_ERANGE) {
+                        clear_error();
+                        c = 0;
+                    } else if (rc) {
+                        return rc;
+                    }
+                    if (c <= 0) break;
+                    plan.emplace_back(static_cast<int32_t>(k), c);
+                    chunk += c;
+                    if (c < rem) break;
+                }
             }
         }
         rec.decide_ns = host_ns() - t_dec0;
         rec.chunk = chunk;
         rec.n_decode = nd;
-        const int32_t prefix = head ? head->prompt_done : 0;  // context the iteration is priced at
+        rec.n_prefill = static_cast<int32_t>(plan.size());
         if (o->table) {
             int64_t p = 0;
             if (lookup_ctx(o->table, prefix, nd, chunk, &p) == SLW_OK) rec.predicted_ns = p;
@@ -259,41 +348,37 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             ++a.emitted;
             a.last_ns = end;
             if (a.emitted == r.output_len) {
-                if (gpu) {
-                    rc = slw_seq_free(ctx, r.id);
-                    if (rc) return rc;
-                    committed_blocks -= kv_blocks_for(r);
-                }
-                ++finished;
+                rc = finish(r);
+                if (rc) return rc;
                 it = active.erase(it);
             } else {
                 ++it;
             }
         }
-        // the chunk: the prompt's last chunk emits the first token
-        if (chunk > 0) {
-            Live h = *head;
-            h.prompt_done += chunk;
+        // the chunks: a prompt's last chunk emits its first token
+        bool any_done = false;
+        for (const auto& pc : plan) {
+            Live& h = pending[pc.first];
+            h.prompt_done += pc.second;
+            h.waited_ns = end;
             const slw_request& r = reqs[h.req];
             if (h.prompt_done == r.prompt_len) {
-                pending.pop_front();
+                any_done = true;
                 token_ns[tok_off[h.req]] = end;
                 h.emitted = 1;
                 h.last_ns = end;
                 if (r.output_len == 1) {
-                    if (gpu) {
-                        rc = slw_seq_free(ctx, r.id);
-                        if (rc) return rc;
-                        committed_blocks -= kv_blocks_for(r);
-                    }
-                    ++finished;
+                    rc = finish(r);
+                    if (rc) return rc;
                 } else {
                     active.emplace(r.id, h);
                 }
-            } else {
-                *head = h;
             }
         }
+        if (any_done)
+            pending.erase(std::remove_if(pending.begin(), pending.end(),
+                                         [&](const Live& x) { return x.prompt_done == reqs[x.req].prompt_len; }),
+                          pending.end());
     }
     return SLW_OK;
 }
