@@ -129,3 +129,42 @@ def test_telemetry_margin_on_gpu(setup):
             pred = int(r["predicted_ns"])
             resid.append((int(r["end_ns"]) - int(r["start_ns"]) - pred) * 10**6 // pred)
     assert checked > 10
+
+
+def test_policy_variants_on_gpu(setup):
+    """Request classes, shortest-remaining-prompt queueing, admission control
+    and aging on the GPU executor: every chunk goes to the waiting prompt with
+    the fewest remaining tokens, aged chunks are min(aging_chunk, remaining),
+    refused requests emit nothing and the pool is whole at the end."""
+    sess, ct, tr = setup
+    n = len(tr)
+    rng = np.random.default_rng(12)
+    inter = rng.random(n) < 0.5
+    tpot_ms = np.where(inter, 1.5, 6.0)
+    margin = np.where(inter, 100_000, 0)
+    res = serving.run(tr, policy="sloweave", tpot_ms=4.0, max_decode=16, c_max=256, table=ct, session=sess,
+                      slo_tpot_ms=tpot_ms, slo_margin_ns=margin, queue="srpt", admit_ppm=600_000,
+                      aging_ns=5_000_000, aging_chunk=32)
+    torch.cuda.synchronize()
+    served = [i for i in range(n) if res.token_ns[i][0] >= 0]
+    for i in range(n):
+        t = res.token_ns[i]
+        if i in served:
+            assert t[0] > tr.arrival_ns[i] and np.all(np.diff(t) > 0)
+        else:
+            assert np.all(t == -1)
+    it = res.iterations
+    assert it["n_decode"].max() <= 16 and np.all(it["n_prefill"] <= 1)
+    done = np.zeros(n, np.int64)
+    for r in it:
+        if r["chunk"] > 0:
+            waiting = [i for i in served if tr.arrival_ns[i] <= r["start_ns"] and done[i] < tr.prompt[i]]
+            best = min(waiting, key=lambda i: (tr.prompt[i] - done[i], tr.arrival_ns[i], i))
+            assert r["prefill_id"] == best
+            if r["flags"] & api.SERVE_AGED:
+                assert r["chunk"] == min(32, tr.prompt[best] - done[best])
+            done[best] += r["chunk"]
+    assert done[served].tolist() == [int(tr.prompt[i]) for i in served]
+    assert sess.ctx.free_blocks() == sess.num_blocks
+    print(f"variants: {n - len(served)} refused, {int(np.sum((it['flags'] & api.SERVE_AGED) != 0))} aged, "
+          f"{serving.metrics(tr, res.token_ns, 1000, tpot_ms)}")
