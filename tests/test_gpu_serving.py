@@ -131,21 +131,8 @@ def test_telemetry_margin_on_gpu(setup):
     assert checked > 10
 
 
-def test_policy_variants_on_gpu(setup):
-    """Request classes, shortest-remaining-prompt queueing, admission control
-    and aging on the GPU executor: every chunk goes to the waiting prompt with
-    the fewest remaining tokens, aged chunks are min(aging_chunk, remaining),
-    refused requests emit nothing and the pool is whole at the end."""
-    sess, ct, tr = setup
+def _check_variant_run(sess, tr, res, queue_key):
     n = len(tr)
-    rng = np.random.default_rng(12)
-    inter = rng.random(n) < 0.5
-    tpot_ms = np.where(inter, 1.5, 6.0)
-    margin = np.where(inter, 100_000, 0)
-    res = serving.run(tr, policy="sloweave", tpot_ms=4.0, max_decode=16, c_max=256, table=ct, session=sess,
-                      slo_tpot_ms=tpot_ms, slo_margin_ns=margin, queue="srpt", admit_ppm=600_000,
-                      aging_ns=5_000_000, aging_chunk=32)
-    torch.cuda.synchronize()
     served = [i for i in range(n) if res.token_ns[i][0] >= 0]
     for i in range(n):
         t = res.token_ns[i]
@@ -156,15 +143,59 @@ def test_policy_variants_on_gpu(setup):
     it = res.iterations
     assert it["n_decode"].max() <= 16 and np.all(it["n_prefill"] <= 1)
     done = np.zeros(n, np.int64)
+    aged = 0
     for r in it:
         if r["chunk"] > 0:
             waiting = [i for i in served if tr.arrival_ns[i] <= r["start_ns"] and done[i] < tr.prompt[i]]
-            best = min(waiting, key=lambda i: (tr.prompt[i] - done[i], tr.arrival_ns[i], i))
+            best = min(waiting, key=lambda i: queue_key(i, done))
             assert r["prefill_id"] == best
             if r["flags"] & api.SERVE_AGED:
                 assert r["chunk"] == min(32, tr.prompt[best] - done[best])
+                aged += 1
             done[best] += r["chunk"]
     assert done[served].tolist() == [int(tr.prompt[i]) for i in served]
     assert sess.ctx.free_blocks() == sess.num_blocks
-    print(f"variants: {n - len(served)} refused, {int(np.sum((it['flags'] & api.SERVE_AGED) != 0))} aged, "
-          f"{serving.metrics(tr, res.token_ns, 1000, tpot_ms)}")
+    return n - len(served), aged
+
+
+def test_policy_variants_on_gpu(setup):
+    """Request classes with shortest-remaining-prompt queueing and admission
+    control, then aging, on the GPU executor: every chunk goes to the prompt
+    the queue puts first, refused requests emit nothing, aged chunks are
+    min(aging_chunk, remaining) and the pool is whole at the end.
+
+    Admission: twelve requests arrive together, so every admission decision
+    is taken before anything runs and the refused set follows from the
+    measured table alone (interactive D = 4 T_hat(1, 0), admitted while the
+    decode batch they join costs at most halfway between the cheapest and the
+    dearest decode-only row; batch D 20x larger)."""
+    sess, ct, tr = setup
+    t_dec = ct.lookup(1, 0)
+    n = 12
+    burst = synth.RequestTrace(np.full(n, 1000, np.int64), np.arange(20, 20 + 7 * n, 7, dtype=np.int64),
+                               np.full(n, 8, np.int64))
+    inter = np.arange(n) % 2 == 0
+    d_ns = np.where(inter, 4 * t_dec, 80 * t_dec).astype(np.int64)
+    # threshold halfway between the cheapest and the dearest decode-only row
+    rows = [ct.lookup(b, 0) for b in (1, 2, 4, 8, 16)]
+    assert max(rows) > min(rows)
+    admit = int((min(rows) + max(rows)) // 2 * 1_000_000 // (4 * t_dec))
+    res = serving.run(burst, policy="sloweave", tpot_ms=4.0, max_decode=16, c_max=256, table=ct, session=sess,
+                      slo_tpot_ms=d_ns / 1e6, queue="srpt", admit_ppm=admit)
+    torch.cuda.synchronize()
+    refused, _ = _check_variant_run(sess, burst, res,
+                                    lambda i, done: (burst.prompt[i] - done[i], burst.arrival_ns[i], i))
+    expect, admitted = [], 0
+    for i in range(n):
+        if ct.lookup(admitted + 1, 0) * 1_000_000 > d_ns[i] * admit:
+            expect.append(i)
+        else:
+            admitted += 1
+    assert [i for i in range(n) if res.token_ns[i][0] < 0] == expect and refused == len(expect) > 0
+    # aging: a D below one decode-only iteration leaves no admissible chunk
+    res = serving.run(tr, policy="sloweave", tpot_ms=0.5 * t_dec / 1e6, max_decode=16, c_max=256, table=ct,
+                      session=sess, aging_ns=int(2 * t_dec), aging_chunk=32)
+    torch.cuda.synchronize()
+    _, aged = _check_variant_run(sess, tr, res, lambda i, done: (tr.arrival_ns[i], i))
+    assert aged > 0
+    print(f"variants: {refused} refused, {aged} aged chunks")
