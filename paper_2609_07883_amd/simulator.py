@@ -14,7 +14,8 @@ dense grid (every decode batch up to 2,048, chunks every 16 tokens up to
 C_max, interpolated exactly since the model is linear in c), so its
 predictions equal the executor's costs, as in the paper's simulator.
 
-Run as ``python -m paper_2609_07883_amd.simulator [--requests N] [--seeds K]``.
+Run as ``python -m paper_2609_07883_amd.simulator [--requests N] [--seeds K]``;
+``--classes`` runs the two-class study of Sec. 3.5 (``classes_study``) instead.
 """
 from __future__ import annotations
 
@@ -80,12 +81,67 @@ def gains(rows: list[dict]) -> dict:
     return out
 
 
+CLASS_POLICIES = (("SLOWeave per-request D", "sloweave", 0, "classes"),
+                  ("SLOWeave D = 10 ms for all", "sloweave", 0, 10.0),
+                  ("SLOWeave D = 50 ms for all", "sloweave", 0, 50.0),
+                  ("Fixed-256", "fixed", 256, "classes"), ("Fixed-1024", "fixed", 1024, "classes"))
+
+
+def _subset(trace, idx):
+    return synth.RequestTrace(trace.arrival_ns[idx], trace.prompt[idx], trace.output[idx])
+
+
+def classes_study(workload: str = "mixed", n: int = 1000, seeds=(0, 1, 2, 3, 4), interactive: float = 0.5,
+                  d_ms=(10.0, 50.0), rate_scale: float = 1.0, table: api.CostTable | None = None,
+                  policies=CLASS_POLICIES) -> list[dict]:
+    """Sec. 3.5 on the simulator: a fraction `interactive` of the requests
+    (a seeded coin per request) carries the tight objective d_ms[0], the
+    others d_ms[1].  The controller either sees each request's own D (its
+    budget is the earliest of the active requests' deadlines) or one D for
+    all; each class is scored against its own objective."""
+    table = table or analytic_table()
+    w = synth.SIM_WORKLOADS[workload]
+    rows = []
+    for pname, pol, chunk, ctl in policies:
+        acc = {"interactive": [], "batch": [], "all": []}
+        for seed in seeds:
+            tr = synth.sim_trace(workload, n, seed, rate_scale)
+            inter = np.random.default_rng(10_000 + seed).random(len(tr)) < interactive
+            d = np.where(inter, d_ms[0], d_ms[1])
+            kw = dict(slo_tpot_ms=d, tpot_ms=d_ms[1]) if ctl == "classes" else dict(tpot_ms=float(ctl))
+            res = serving.run(tr, policy=pol, fixed_chunk=chunk, max_decode=MAX_DECODE, c_max=C_MAX,
+                              table=table if pol == "sloweave" else None, **kw)
+            acc["all"].append(serving.metrics(tr, res.token_ns, w.ttft_slo_ms, d))
+            for cname, mask in (("interactive", inter), ("batch", ~inter)):
+                idx = np.nonzero(mask)[0]
+                acc[cname].append(serving.metrics(_subset(tr, idx), [res.token_ns[i] for i in idx],
+                                                  w.ttft_slo_ms, d[idx]))
+        row = {"workload": workload, "policy": pname}
+        for cname, ms in acc.items():
+            row[f"{cname}_slo_attainment"] = float(np.mean([m["slo_attainment"] for m in ms]))
+            row[f"{cname}_p99_ttft_ms"] = float(np.mean([m["p99_ttft_ms"] for m in ms]))
+        row["goodput_req_s"] = float(np.mean([m["goodput_req_s"] for m in acc["all"]]))
+        rows.append(row)
+    return rows
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--requests", type=int, default=1000)
     ap.add_argument("--seeds", type=int, default=5)
+    ap.add_argument("--classes", action="store_true", help="the two-class study of Sec. 3.5 instead")
+    ap.add_argument("--interactive", type=float, default=0.03, help="share of 10 ms requests (--classes)")
     args = ap.parse_args(argv)
     t0 = time.time()
+    if args.classes:
+        rows = classes_study(n=args.requests, seeds=tuple(range(args.seeds)), interactive=args.interactive)
+        for r in rows:
+            print(f'{r["policy"]:28s} SLO interactive {100 * r["interactive_slo_attainment"]:5.1f}%  '
+                  f'batch {100 * r["batch_slo_attainment"]:5.1f}%  all {100 * r["all_slo_attainment"]:5.1f}%  '
+                  f'P99 TTFT {r["all_p99_ttft_ms"]:8.1f} ms  goodput {r["goodput_req_s"]:6.1f} req/s')
+        print(json.dumps({"rows": rows, "requests": args.requests, "seeds": args.seeds,
+                          "interactive": args.interactive, "wall_s": round(time.time() - t0, 1)}))
+        return
     rows = study(n=args.requests, seeds=tuple(range(args.seeds)))
     for r in rows:
         print(f'{r["workload"]:7s} TPOT {r["tpot_slo_ms"]:4.0f} ms  {r["policy"]:10s}  '

@@ -223,8 +223,9 @@ SIM_OUTPUT_CAP = 4096
 SIM_BURST_HIGH, SIM_BURST_LOW, SIM_BURST_DWELL_S = 1.6, 0.4, 1.0
 
 
-def sim_trace(workload: str, n: int = 1000, seed: int = 0) -> RequestTrace:
-    """n requests of one of the simulator workloads (SIM_WORKLOADS)."""
+def sim_trace(workload: str, n: int = 1000, seed: int = 0, rate_scale: float = 1.0) -> RequestTrace:
+    """n requests of one of the simulator workloads (SIM_WORKLOADS), arriving
+    at rate_scale times the workload's rate."""
     w = SIM_WORKLOADS[workload]
     rng = np.random.default_rng(seed)
     times = np.empty(n)
@@ -234,7 +235,7 @@ def sim_trace(workload: str, n: int = 1000, seed: int = 0) -> RequestTrace:
         edge = rng.exponential(SIM_BURST_DWELL_S)
         for k in range(n):
             while True:        # memoryless: restart the draw at every state change
-                rate = w.rate_per_s * (SIM_BURST_HIGH if high else SIM_BURST_LOW)
+                rate = w.rate_per_s * rate_scale * (SIM_BURST_HIGH if high else SIM_BURST_LOW)
                 dt = rng.exponential(1.0 / rate)
                 if t + dt < edge:
                     t += dt
@@ -244,7 +245,7 @@ def sim_trace(workload: str, n: int = 1000, seed: int = 0) -> RequestTrace:
                 edge = t + rng.exponential(SIM_BURST_DWELL_S)
             times[k] = t
     else:
-        times = np.cumsum(rng.exponential(1.0 / w.rate_per_s, size=n))
+        times = np.cumsum(rng.exponential(1.0 / (w.rate_per_s * rate_scale), size=n))
     arrival = np.rint((times - times[0]) * 1e9).astype(np.int64)
     long_ = rng.random(n) < w.long_share
     med = np.where(long_, w.long_median, w.prompt_median)

@@ -75,3 +75,20 @@ def test_study_trends_at_25ms():
     assert good[("chat", "SLOWeave")] >= 0.97 * best_chat
     slw = [r for r in rows if r["policy"] == "SLOWeave"]
     assert all(r["p99_tpot_ms"] <= 25.0 + 1e-6 for r in slw)   # the controller keeps every gap within D
+
+
+def test_request_classes_trend():
+    """Sec. 3.5 on the simulator (mixed workload, 3% of requests interactive at
+    D = 10 ms, the rest at 50 ms): with each request's own objective the
+    controller keeps far more interactive requests within their SLOs than a
+    controller told D = 50 ms for all, and serves both classes at least as
+    well as one told D = 10 ms for all (it uses the batch slack whenever no
+    interactive request decodes)."""
+    from paper_2609_07883_amd import simulator as M
+    rows = {r["policy"]: r for r in M.classes_study(workload="mixed", n=1000, seeds=(0,), interactive=0.03)}
+    per, tight, loose = (rows["SLOWeave per-request D"], rows["SLOWeave D = 10 ms for all"],
+                         rows["SLOWeave D = 50 ms for all"])
+    assert per["interactive_slo_attainment"] >= loose["interactive_slo_attainment"] + 0.2
+    assert per["interactive_slo_attainment"] >= tight["interactive_slo_attainment"]
+    assert per["batch_slo_attainment"] >= tight["batch_slo_attainment"]
+    assert per["goodput_req_s"] > tight["goodput_req_s"]
