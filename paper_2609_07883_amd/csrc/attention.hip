@@ -377,23 +377,17 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
 // Combine n partials (running max, sum and unnormalised output) of one
 // row and write it normalised; 64 threads, HD / 64 dims each.  Partial w
 // sits at row r0 + w * stride of ml [.][2] and po [.][HD]; a max of -inf
-// means every key of that range was masked for the row.  The loads are
-// issued eight partials at a time before any is used, so a list costs a few
-// memory round trips rather than one per partial.
+// means every key of that range was masked for the row.
 template <int HD>
 __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const float* __restrict__ po, size_t r0,
                                           size_t stride, int n, bf16* __restrict__ out) {
     constexpr int CH = 8, PER = HD / 64;
-    float mmax = -INFINITY;
-    for (int c = 0; c < n; c += CH) {
-        float m[CH];
-#pragma unroll
-        for (int j = 0; j < CH; ++j) m[j] = c + j < n ? ml[(r0 + (c + j) * stride) * 2] : -INFINITY;
-#pragma unroll
-        for (int j = 0; j < CH; ++j) mmax = fmaxf(mmax, m[j]);
-    }
+    // One pass with a running maximum: each group of CH partials is loaded
+    // at once, the sums so far are rescaled to the group's new maximum and
+    // the group is added, so a list of up to CH partials costs one memory
+    // round trip.
+    float mmax = -INFINITY, lsum = 0.f;
     float acc[PER] = {};
-    float lsum = 0.f;
     for (int c = 0; c < n; c += CH) {
         float m[CH], l[CH], v[CH][PER];
 #pragma unroll
@@ -405,14 +399,24 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const fl
 #pragma unroll
             for (int p = 0; p < PER; ++p) v[j][p] = ok ? po[r * HD + threadIdx.x + 64 * p] : 0.f;
         }
+        float mc = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < CH; ++j) mc = fmaxf(mc, m[j]);
+        if (mc == -INFINITY) continue;  // every key of these ranges masked
+        const float mn = fmaxf(mmax, mc);
+        const float rs = fast_exp2(mmax - mn);  // 0 while nothing has been added
+        lsum *= rs;
+#pragma unroll
+        for (int p = 0; p < PER; ++p) acc[p] *= rs;
 #pragma unroll
         for (int j = 0; j < CH; ++j) {
             if (m[j] == -INFINITY) continue;
-            const float sc = fast_exp2(m[j] - mmax);
+            const float sc = fast_exp2(m[j] - mn);
             lsum += sc * l[j];
 #pragma unroll
             for (int p = 0; p < PER; ++p) acc[p] += sc * v[j][p];
         }
+        mmax = mn;
     }
     const float inv = 1.0f / lsum;
 #pragma unroll
