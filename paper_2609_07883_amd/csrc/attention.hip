@@ -382,6 +382,7 @@ template <int HD>
 __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const float* __restrict__ po, size_t r0,
                                           size_t stride, int n, bf16* __restrict__ out) {
     constexpr int CH = 8, PER = HD / 64;
+    const int lane = threadIdx.x & 63;
     // One pass with a running maximum: each group of CH partials is loaded
     // at once, the sums so far are rescaled to the group's new maximum and
     // the group is added, so a list of up to CH partials costs one memory
@@ -397,7 +398,7 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const fl
             m[j] = ok ? ml[r * 2] : -INFINITY;
             l[j] = ok ? ml[r * 2 + 1] : 0.f;
 #pragma unroll
-            for (int p = 0; p < PER; ++p) v[j][p] = ok ? po[r * HD + threadIdx.x + 64 * p] : 0.f;
+            for (int p = 0; p < PER; ++p) v[j][p] = ok ? po[r * HD + lane + 64 * p] : 0.f;
         }
         float mc = -INFINITY;
 #pragma unroll
@@ -420,7 +421,7 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const fl
     }
     const float inv = 1.0f / lsum;
 #pragma unroll
-    for (int p = 0; p < PER; ++p) out[threadIdx.x + 64 * p] = f2bf(acc[p] * inv);
+    for (int p = 0; p < PER; ++p) out[lane + 64 * p] = f2bf(acc[p] * inv);
 }
 
 // Combine the key-range partials of one (chunk position, q head).
@@ -604,10 +605,12 @@ __device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b,
 
 // One launch for both merges of a layer: blocks x < chunk_rows combine the
 // partials of chunk position x (query tiles split over several items), the
-// rest those of decode x - chunk_rows; y is the q head.
-template <int HD, int GROUP>
-__global__ __launch_bounds__(64) void attn_merge_kernel(ChunkAttnArgs ca, DecodeAttnArgs da, int chunk_rows) {
-    const int x = blockIdx.x, h = blockIdx.y;
+// rest those of decode x - chunk_rows; wave w of block (x, y) takes q head
+// y * WAVES + w.
+template <int HD, int GROUP, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void attn_merge_kernel(ChunkAttnArgs ca, DecodeAttnArgs da,
+                                                                int chunk_rows) {
+    const int x = blockIdx.x, h = blockIdx.y * WAVES + (threadIdx.x >> 6);
     if (x < chunk_rows) chunk_merge_row<HD, GROUP>(ca, x, h);
     else decode_merge_row<HD>(da, x - chunk_rows, h);
 }
@@ -619,7 +622,12 @@ void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
 
 template <int HD, int GROUP>
 void launch_merge_g(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, int chunk_rows, int hq, hipStream_t s) {
-    attn_merge_kernel<HD, GROUP><<<dim3(chunk_rows + da.b, hq), 64, 0, s>>>(ca, da, chunk_rows);
+    // four heads per work-group where they divide evenly: a quarter of the
+    // (tiny) work-groups to dispatch
+    if (hq % 4 == 0)
+        attn_merge_kernel<HD, GROUP, 4><<<dim3(chunk_rows + da.b, hq / 4), 256, 0, s>>>(ca, da, chunk_rows);
+    else
+        attn_merge_kernel<HD, GROUP, 1><<<dim3(chunk_rows + da.b, hq), 64, 0, s>>>(ca, da, chunk_rows);
 }
 
 template <int HD>
