@@ -10,6 +10,11 @@ Test infrastructure only (see ``oracle/__init__``).
   chunk is Alg. 1 over a cost predictor (SLOWeave) or a fixed size.
 * ``request_metrics`` / ``summarize``: TTFT, within-request P99 TPOT, SLO
   attainment and goodput of Sec. 4.3.
+* The policy variants of Sec. 3.3-3.5 (per-request objectives and class
+  margins, queue disciplines, admission control, aging, first-fit prefill
+  batching) are options of ``simulate``; its docstring states the reading
+  of each.  Pinned by brute-force replay and closed-form cases in the tests
+  of the policy variants.
 
 Times are integer nanoseconds throughout, so two implementations of the
 same loop agree exactly.

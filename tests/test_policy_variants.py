@@ -101,6 +101,18 @@ def test_oracle_decisions_by_brute_force(queue):
     assert _replay(reqs, ref, 25 * MS, 100_000, 2048, queue) > 50
 
 
+@pytest.mark.parametrize("queue,expect", [("oldest", [0, 1, 2]), ("srpt", [1, 2, 0]), ("edf", [2, 1, 0])])
+def test_oracle_queue_order_closed_form(queue, expect):
+    """Three one-token requests at t = 0 with prompts 300 / 100 / 200 and TTFT
+    objectives none / 300 ms / 100 ms: with no decode active each iteration
+    runs one whole prompt, in the queue's order (a request without a TTFT
+    objective goes last under earliest-deadline queueing)."""
+    reqs = [V.Request(0, 0, 300, 1), V.Request(1, 0, 100, 1, ttft_ns=300 * MS), V.Request(2, 0, 200, 1, ttft_ns=100 * MS)]
+    tr = V.simulate(reqs, cost_ns=_t, tpot_ns=25 * MS, policy="sloweave", c_max=4096, queue=queue)
+    assert [it.prefill_rid for it in tr.iterations] == expect
+    assert [it.chunk for it in tr.iterations] == [reqs[i].prompt for i in expect]
+
+
 def test_oracle_admission_closed_form():
     """20 requests at t = 0, D = 2 ms, admit at D: T(n, 0) = 1.25 + 0.055 n ms
     admits n <= 13 with delta 0 and n <= 10 with delta 0.2 ms (even ids)."""
