@@ -848,13 +848,15 @@ struct TileCfg {
 // 11: 256x256 / 8 waves, k 64, 2-buffer ring (128 KB)
 // 12: 256x256 / 4 waves (128x128), k 32, 4-buffer ring (128 KB)
 // 13: 256x256 / 4 waves (128x128), k 64, 2-buffer ring (128 KB)
+// 14: 192x256 / 8 waves (96x64), k 64, 2-buffer ring (112 KB): less row
+//     padding than 256 where m is just past a multiple of 256
 // The register-staged k-32 tiles (6, 7) use 48 KB of LDS, so two
 // work-groups share a CU and one's loads overlap the other's matrix work.
 constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 0}, {64, 128, 2, 2, 64, 0}, {32, 256, 1, 4, 64, 0},
                              {256, 256, 2, 4, 64, 0}, {256, 256, 2, 2, 64, 0}, {128, 256, 2, 4, 64, 0},
                              {256, 128, 2, 2, 32, 0}, {128, 256, 2, 2, 32, 0}, {256, 256, 2, 4, 32, 4},
                              {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}, {256, 256, 2, 4, 64, 2},
-                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}};
+                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}, {192, 256, 2, 4, 64, 2}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int EPI>
@@ -931,30 +933,36 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 // between boxes): the weight-streaming kernel up to 32 rows on the narrower
 // projections, then whichever configuration measured fastest in each band of
 // m.  The 128 x 128 tiles (two work-groups per CU) win wherever their tiles
-// fit one round of 512; the 256 x 256 ring tile from about 2000 rows (3500
-// for qkv); stream-K where 256 x 256 tiles are too few for the CUs on the
-// narrow projections.  n must be a multiple of 128 and k of 64.
+// fit one round of 512; the 256 x 256 ring tile from about 2000 rows on
+// gate/up; the 192 x 256 ring tile in the bands where m sits just past a
+// multiple of 256 or where its row bands fill whole rounds; stream-K where
+// the ring tiles are too few for the CUs on the narrow projections.  The
+// bands follow the measurements, so they are not monotone in m.  n must be
+// a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     // The weight-streaming kernel wins on the narrow projections up to 32
     // rows (o, down: 10-20%) and on gate/up up to 16 rows (13% at one row);
     // on qkv the 64 x 128 tiles with split-K measured 3-13% faster.
     const bool wide = n >= 16384, qkv_like = n >= 6144 && !wide;
     if (n % 64 == 0 && (wide ? m <= 16 : m <= 32 && !qkv_like)) return plan_with_cfg(kSkinnyCfg, m, n, k);
-    constexpr int SK = -1;  // stream-K with the 256 x 256 ring tile
+    constexpr int SK = -1;   // stream-K with the 256 x 256 ring tile
+    constexpr int SK14 = -2; // stream-K with the 192 x 256 ring tile
     int cfg;
     if (k >= 8192)  // deep k (down)
-        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 450 ? 11 : SK;
+        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 420 ? 14 : m < 700 ? SK14 : m < 930 ? SK : m < 1200 ? SK14
+            : m < 3800 ? SK : 14;
     else if (n >= 16384)  // gate/up
-        cfg = m <= 200 ? 0 : m <= 650 ? 1 : m < 950 ? 11 : m < 1800 ? 7 : 11;
+        cfg = m <= 200 ? 0 : m <= 650 ? 14 : m < 950 ? 11 : m < 1200 ? 14 : 11;
     else if (n >= 6144)  // qkv
-        cfg = m <= 32 ? 1 : m <= 128 ? 0 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 10 : m < 1300 ? 0 : m < 1800 ? 1
-            : m < 2500 ? 7 : m < 3500 ? 0 : 11;
+        cfg = m <= 32 ? 1 : m <= 128 ? 0 : m <= 220 ? 14 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 14 : m < 1200 ? 0
+            : m < 1400 ? 14 : m < 1650 ? 1 : m < 1950 ? 14 : m < 2500 ? 7 : m < 3250 ? 0 : m < 3800 ? 14 : 11;
     else  // o
-        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 700 ? 1 : m < 950 ? 0 : m < 1300 ? SK : m < 1800 ? 0
-            : m < 3500 ? SK : 0;
-    if (cfg == SK) {
-        if (n % 256 == 0) return plan_stream_k(11, m, n, k);
-        cfg = 11;
+        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 700 ? 1 : m < 950 ? 0 : m < 1180 ? SK14 : m < 1400 ? 14
+            : m < 1950 ? 0 : m < 2700 ? SK : m < 3250 ? 14 : m < 3800 ? 7 : 14;
+    if (cfg == SK || cfg == SK14) {
+        const int sk_cfg = cfg == SK ? 11 : 14;
+        if (n % 256 == 0) return plan_stream_k(sk_cfg, m, n, k);
+        cfg = sk_cfg;
     }
     if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
     return plan_with_cfg(cfg, m, n, k);
@@ -1036,7 +1044,8 @@ void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_
         case 10: launch_cfg<128, 128, 2, 2, 32, 4>(g, p, partial, s); break;
         case 11: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
         case 12: launch_cfg<256, 256, 2, 2, 32, 4>(g, p, partial, s); break;
-        default: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 13: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
+        default: launch_cfg<192, 256, 2, 4, 64, 2>(g, p, partial, s); break;
     }
 }
 

@@ -106,3 +106,12 @@ def test_small_chunk_with_decodes():
 def test_single_decode():
     """C = 0, B = 1: one row through every kernel."""
     _run(0, 0, [1500], seed=17)
+
+
+@pytest.mark.parametrize("C,P", [(128, 0), (512, 2048), (768, 0), (1268, 0)])
+def test_gemm_band_points(C, P):
+    """Layer points whose GEMMs take the 192 x 256 ring tile (plain, with
+    split-K and with stream-K) and the other bands of the planner: M = 160,
+    544, 800 and 1300 with B = 32 decodes."""
+    ctx = synth.uniform_lengths(32, 512, 2048, seed=2)
+    _run(C, P, ctx, seed=20 + C // 64)
