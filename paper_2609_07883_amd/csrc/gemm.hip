@@ -850,13 +850,16 @@ struct TileCfg {
 // 13: 256x256 / 4 waves (128x128), k 64, 2-buffer ring (128 KB)
 // 14: 192x256 / 8 waves (96x64), k 64, 2-buffer ring (112 KB): less row
 //     padding than 256 where m is just past a multiple of 256
+// 15: 128x128 / 4 waves (64x64), k 64, 2-buffer ring (64 KB: two
+//     work-groups per CU)
 // The register-staged k-32 tiles (6, 7) use 48 KB of LDS, so two
 // work-groups share a CU and one's loads overlap the other's matrix work.
 constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 0}, {64, 128, 2, 2, 64, 0}, {32, 256, 1, 4, 64, 0},
                              {256, 256, 2, 4, 64, 0}, {256, 256, 2, 2, 64, 0}, {128, 256, 2, 4, 64, 0},
                              {256, 128, 2, 2, 32, 0}, {128, 256, 2, 2, 32, 0}, {256, 256, 2, 4, 32, 4},
                              {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}, {256, 256, 2, 4, 64, 2},
-                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}, {192, 256, 2, 4, 64, 2}};
+                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}, {192, 256, 2, 4, 64, 2},
+                             {128, 128, 2, 2, 64, 2}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int EPI>
@@ -952,12 +955,12 @@ GemmPlan plan_gemm(int m, int n, int k) {
         cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 420 ? 14 : m < 700 ? SK14 : m < 930 ? SK : m < 1200 ? SK14
             : m < 3800 ? SK : 14;
     else if (n >= 16384)  // gate/up
-        cfg = m <= 200 ? 0 : m <= 650 ? 14 : m < 950 ? 11 : m < 1200 ? 14 : 11;
+        cfg = m <= 128 ? 0 : m <= 200 ? 15 : m <= 650 ? 14 : m < 950 ? 11 : m < 1200 ? 14 : 11;
     else if (n >= 6144)  // qkv
         cfg = m <= 32 ? 1 : m <= 128 ? 0 : m <= 220 ? 14 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 14 : m < 1200 ? 0
-            : m < 1400 ? 14 : m < 1650 ? 1 : m < 1950 ? 14 : m < 2500 ? 7 : m < 3250 ? 0 : m < 3800 ? 14 : 11;
+            : m < 1400 ? 14 : m < 1650 ? 1 : m < 1950 ? 14 : m < 3250 ? 15 : m < 3800 ? 14 : 11;
     else  // o
-        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 700 ? 1 : m < 950 ? 0 : m < 1180 ? SK14 : m < 1400 ? 14
+        cfg = m <= 128 ? 10 : m < 400 ? 15 : m < 700 ? 1 : m < 950 ? 0 : m < 1180 ? SK14 : m < 1400 ? 14
             : m < 1950 ? 0 : m < 2700 ? SK : m < 3250 ? 14 : m < 3800 ? 7 : 14;
     if (cfg == SK || cfg == SK14) {
         const int sk_cfg = cfg == SK ? 11 : 14;
@@ -1045,7 +1048,8 @@ void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_
         case 11: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
         case 12: launch_cfg<256, 256, 2, 2, 32, 4>(g, p, partial, s); break;
         case 13: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
-        default: launch_cfg<192, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 14: launch_cfg<192, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        default: launch_cfg<128, 128, 2, 2, 64, 2>(g, p, partial, s); break;
     }
 }
 
