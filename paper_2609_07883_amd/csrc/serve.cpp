@@ -1,7 +1,9 @@
 // Serving loop: the iteration-level scheduler that drives the mixed iteration
 // (Sec. 3.1 deadline model, Sec. 3.2 / Alg. 1 chunk choice, Sec. 4.1 iteration
-// semantics, Sec. 4.3 oldest-first queueing).  It uses only the public calls
-// of this library: the KV manager, slw_select_chunk and slw_mixed_iteration.
+// semantics, Sec. 4.3 oldest-first queueing), with the policy variants of
+// Sec. 3.3-3.5 as options (per-request objectives and class margins, queue
+// disciplines, admission control, aging, first-fit prefill batching).  It
+// uses the KV manager, the chunk search of Alg. 1 and slw_mixed_iteration.
 //
 // Two executors share every scheduling decision: the GPU one runs each
 // iteration on the device and reads the host clock once the stream drains;
