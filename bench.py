@@ -125,8 +125,19 @@ def roof_time(flops, nbytes):
     return max(flops / PEAK_BF16, nbytes / PEAK_HBM)
 
 
-def cpu_baseline(shape, ctx_lens, budget_s=30.0):
-    """The oracle on the host cores over the P = 0 column of the sweep (bounded)."""
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(shape, ctx_lens, budget_s=30.0, min_s=12.0):
+    """The oracle on the host cores over the P = 0 column of the sweep, in
+    passes until at least min_s seconds of oracle time (bounded by budget_s)."""
     from oracle import layer as OL
     from paper_2609_07883_amd import synth
     from tests.parity import oracle_shape, oracle_weights
@@ -141,23 +152,35 @@ def cpu_baseline(shape, ctx_lens, budget_s=30.0):
     for i, L in enumerate(ctx_lens):
         kb, vb = synth.cached_kv(int(L), shape.n_kv_heads, shape.head_dim, 3, 0, 100 + i)
         kv.seqs[100 + i] = OL.SeqCache(synth.bf16_to_f64(kb), synth.bf16_to_f64(vb))
-    rows, secs, done = 0, 0.0, []
-    for C in C_SWEEP:
+    rows, secs, done, passes = 0, 0.0, [], 0
+    while secs < min_s and passes < 8:
+        passes += 1
+        for C in C_SWEEP:
+            if secs > budget_s:
+                break
+            rows, secs = _oracle_point(OL, sh, w, kv, shape, ctx_lens, C, rows, secs)
+            if passes == 1:
+                done.append(C)
         if secs > budget_s:
             break
-        k2 = kv.copy()
-        k2.seqs[1] = OL.SeqCache(np.zeros((0, shape.n_kv_heads, shape.head_dim)),
-                                 np.zeros((0, shape.n_kv_heads, shape.head_dim)))
-        b = OL.MixedBatch(C, 1, 0, list(range(100, 100 + len(ctx_lens))), [int(x) for x in ctx_lens])
-        x = synth.bf16_to_f64(synth.embeddings(C + len(ctx_lens), shape.d_model, seed=1, stream=C))
-        t0 = time.perf_counter()
-        OL.mixed_iteration(sh, w, x, k2, b)
-        secs += time.perf_counter() - t0
-        rows += C + len(ctx_lens)
-        done.append(C)
     return {"value": rows / secs, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": _cpu_model(),
             "sample": f"float64 oracle, one mixed iteration at each C in {done} with P=0 and the same "
-                      f"B={len(ctx_lens)} decodes ({rows} rows, {secs:.1f} s)"}
+                      f"B={len(ctx_lens)} decodes, {passes} pass(es) ({rows} rows, {secs:.1f} s)"}
+
+
+def _oracle_point(OL, sh, w, kv, shape, ctx_lens, C, rows, secs):
+    """One timed oracle iteration at chunk C (fresh prefill sequence, shared decodes)."""
+    from paper_2609_07883_amd import synth
+    k2 = kv.copy()
+    k2.seqs[1] = OL.SeqCache(np.zeros((0, shape.n_kv_heads, shape.head_dim)),
+                             np.zeros((0, shape.n_kv_heads, shape.head_dim)))
+    b = OL.MixedBatch(C, 1, 0, list(range(100, 100 + len(ctx_lens))), [int(x) for x in ctx_lens])
+    x = synth.bf16_to_f64(synth.embeddings(C + len(ctx_lens), shape.d_model, seed=1, stream=C))
+    t0 = time.perf_counter()
+    OL.mixed_iteration(sh, w, x, k2, b)
+    secs += time.perf_counter() - t0
+    return rows + C + len(ctx_lens), secs
 
 
 def main():
