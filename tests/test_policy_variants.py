@@ -50,7 +50,6 @@ def _reqs(tr, tpot=None, margin=None, ttft=None):
 def _replay(reqs, tr, D, margin, c_max, queue="oldest"):
     """Brute-force re-derivation of every decision of an oracle run (oldest /
     srpt / edf queue, no decode cap, no aging, one prompt per iteration)."""
-    by = {r.rid: r for r in reqs}
     tok = {rid: np.asarray(v, dtype=np.int64) for rid, v in tr.token_ns.items()}
     done = {r.rid: 0 for r in reqs}
     decided = 0
