@@ -214,3 +214,48 @@ def test_rejects_inconsistent_context():
     _prefill_into(shape, w, kv, 1, x_rows(10, model.d_model))
     with pytest.raises(ValueError):
         L.mixed_iteration(shape, w, x_rows(1, model.d_model), kv, L.MixedBatch(0, -1, 0, [1], [9]))
+
+
+def test_append_kv_equals_row_by_row_writes():
+    """Step 4 writes row r's K/V at position pos[r] of its sequence, in row
+    order: a row at the current length extends the sequence, one inside it
+    overwrites, one beyond it is an error.  The append (one copy per
+    sequence) must leave exactly what a row-by-row write does."""
+    from oracle.layer import LayerShape
+    rng = np.random.default_rng(5)
+    hkv, hd = 2, 4
+    shape = LayerShape(d_model=8, n_q_heads=2, n_kv_heads=hkv, head_dim=hd, ffn_dim=8, rms_eps=1e-5,
+                       rope_theta=10000.0)
+    for trial in range(40):
+        init = {s: int(rng.integers(0, 5)) for s in range(3)}
+        kv = L.KVState({s: L.SeqCache(rng.standard_normal((n, hkv, hd)), rng.standard_normal((n, hkv, hd)))
+                        for s, n in init.items()})
+        ref = {s: [c.k[i].copy() for i in range(c.length)] for s, c in kv.seqs.items()}
+        refv = {s: [c.v[i].copy() for i in range(c.length)] for s, c in kv.seqs.items()}
+        seqs, pos = [], []
+        length = dict(init)
+        for _ in range(int(rng.integers(1, 12))):
+            s = int(rng.integers(0, 3))
+            p = int(rng.integers(0, length[s] + 1))   # inside or at the end: always valid
+            seqs.append(s)
+            pos.append(p)
+            length[s] = max(length[s], p + 1)
+        k = rng.standard_normal((len(seqs), hkv, hd))
+        v = rng.standard_normal((len(seqs), hkv, hd))
+        for r, (s, p) in enumerate(zip(seqs, pos)):       # row-by-row reference
+            if p == len(ref[s]):
+                ref[s].append(k[r].copy())
+                refv[s].append(v[r].copy())
+            else:
+                ref[s][p] = k[r].copy()
+                refv[s][p] = v[r].copy()
+        L.append_kv(shape, kv, seqs, pos, k, v)
+        for s in range(3):
+            assert kv.seqs[s].length == len(ref[s])
+            if ref[s]:
+                np.testing.assert_array_equal(kv.seqs[s].k, np.stack(ref[s]))
+                np.testing.assert_array_equal(kv.seqs[s].v, np.stack(refv[s]))
+    # a row beyond the current length (counting earlier rows) is refused
+    kv = L.KVState({0: L.SeqCache(np.zeros((2, hkv, hd)), np.zeros((2, hkv, hd)))})
+    with pytest.raises(ValueError):
+        L.append_kv(shape, kv, [0, 0], [2, 4], np.zeros((2, hkv, hd)), np.zeros((2, hkv, hd)))
