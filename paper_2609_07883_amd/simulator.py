@@ -32,6 +32,8 @@ MAX_DECODE = 2048
 TPOTS_MS = (10.0, 25.0, 50.0)
 POLICIES = (("Full", "fixed", 1 << 30), ("Fixed-64", "fixed", 64), ("Fixed-256", "fixed", 256),
             ("Fixed-1024", "fixed", 1024), ("SLOWeave", "sloweave", 0))
+# Sec. 3.3 prefill batching by first fit (up to four prompts per iteration)
+BATCHING_POLICY = ("SLOWeave + first-fit batching", "sloweave", 0, {"max_prefills": 4})
 
 
 def analytic_table() -> api.CostTable:
@@ -39,9 +41,9 @@ def analytic_table() -> api.CostTable:
     return api.CostTable.analytic(list(range(0, C_MAX + 1, 16)), list(range(0, MAX_DECODE + 1)))
 
 
-def run_one(trace, table, policy: str, chunk: int, tpot_ms: float, ttft_slo_ms: float) -> dict:
+def run_one(trace, table, policy: str, chunk: int, tpot_ms: float, ttft_slo_ms: float, **variants) -> dict:
     res = serving.run(trace, policy=policy, fixed_chunk=chunk, tpot_ms=tpot_ms, max_decode=MAX_DECODE,
-                      c_max=C_MAX, table=table if policy == "sloweave" else None)
+                      c_max=C_MAX, table=table if policy == "sloweave" else None, **variants)
     return serving.metrics(trace, res.token_ns, ttft_slo_ms=ttft_slo_ms, tpot_slo_ms=tpot_ms)
 
 
@@ -54,8 +56,9 @@ def study(workloads=tuple(synth.SIM_WORKLOADS), tpots=TPOTS_MS, policies=POLICIE
         w = synth.SIM_WORKLOADS[wname]
         traces = [synth.sim_trace(wname, n, s) for s in seeds]
         for tpot in tpots:
-            for pname, pol, chunk in policies:
-                ms = [run_one(tr, table, pol, chunk, tpot, w.ttft_slo_ms) for tr in traces]
+            for pname, pol, chunk, *opt in policies:
+                kw = opt[0] if opt else {}
+                ms = [run_one(tr, table, pol, chunk, tpot, w.ttft_slo_ms, **kw) for tr in traces]
                 rows.append({"workload": wname, "tpot_slo_ms": tpot, "ttft_slo_ms": w.ttft_slo_ms,
                              "policy": pname,
                              "p99_ttft_ms": float(np.mean([m["p99_ttft_ms"] for m in ms])),
@@ -73,7 +76,7 @@ def gains(rows: list[dict]) -> dict:
         if r["policy"] != "SLOWeave":
             continue
         others = [o for o in rows if o["workload"] == r["workload"] and o["tpot_slo_ms"] == r["tpot_slo_ms"]
-                  and o["policy"] != "SLOWeave"]
+                  and not o["policy"].startswith("SLOWeave")]
         best = max(others, key=lambda o: o["goodput_req_s"])
         out[f'{r["workload"]} {r["tpot_slo_ms"]:g}ms'] = {
             "vs": best["policy"],
@@ -131,6 +134,8 @@ def main(argv=None):
     ap.add_argument("--seeds", type=int, default=5)
     ap.add_argument("--classes", action="store_true", help="the two-class study of Sec. 3.5 instead")
     ap.add_argument("--interactive", type=float, default=0.03, help="share of 10 ms requests (--classes)")
+    ap.add_argument("--batching", action="store_true",
+                    help="add SLOWeave with first-fit prefill batching (Sec. 3.3) to the study")
     args = ap.parse_args(argv)
     t0 = time.time()
     if args.classes:
@@ -142,7 +147,8 @@ def main(argv=None):
         print(json.dumps({"rows": rows, "requests": args.requests, "seeds": args.seeds,
                           "interactive": args.interactive, "wall_s": round(time.time() - t0, 1)}))
         return
-    rows = study(n=args.requests, seeds=tuple(range(args.seeds)))
+    rows = study(n=args.requests, seeds=tuple(range(args.seeds)),
+                 policies=POLICIES + ((BATCHING_POLICY,) if args.batching else ()))
     for r in rows:
         print(f'{r["workload"]:7s} TPOT {r["tpot_slo_ms"]:4.0f} ms  {r["policy"]:10s}  '
               f'P99 TTFT {r["p99_ttft_ms"]:8.1f} ms  P99 TPOT {r["p99_tpot_ms"]:6.1f} ms  '

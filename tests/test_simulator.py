@@ -92,3 +92,16 @@ def test_request_classes_trend():
     assert per["interactive_slo_attainment"] >= tight["interactive_slo_attainment"]
     assert per["batch_slo_attainment"] >= tight["batch_slo_attainment"]
     assert per["goodput_req_s"] > tight["goodput_req_s"]
+
+
+def test_first_fit_batching_trend():
+    """Sec. 3.3 prefill batching on the simulator: with up to four prompts per
+    iteration SLOWeave's goodput on the mixed workload at 25 ms is higher
+    than with one (the fixed per-chunk cost of the analytic model is paid
+    once for several short prompts), and no TPOT objective is missed more."""
+    from paper_2609_07883_amd import simulator as M
+    rows = {r["policy"]: r for r in M.study(workloads=("mixed",), tpots=(25.0,), n=1000, seeds=(0,),
+                                            policies=(M.POLICIES[-1], M.BATCHING_POLICY))}
+    one, batch = rows["SLOWeave"], rows[M.BATCHING_POLICY[0]]
+    assert batch["goodput_req_s"] > 1.2 * one["goodput_req_s"]
+    assert batch["p99_tpot_ms"] <= 25.0 + 1e-9
