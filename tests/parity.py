@@ -6,11 +6,17 @@ row of the layer output, or one head of an appended K/V row):
 
     rel = max over vectors v of  max_i |g_vi - r_vi| / max_i |r_vi|
 
-and must stay <= 2e-2.  An elementwise denominator (|r_i| + rms(r)) is also
-reported (``elementwise_err``); its maximum over ~10^6 outputs sits near 2e-2
-for any path that stores its GEMM inputs in bf16, as an exact CPU emulation
-of those rounding points shows, so it is reported rather than asserted.
-The rms error ||g - r|| / ||r|| must stay below 1e-2.
+and must stay <= 2e-2, and the rms error ||g - r|| / ||r|| below 1e-2.
+The elementwise form max_i |g_i - r_i| / (|r_i| + rms(r)) is asserted with a
+wider bound, ELEMENTWISE_TOL: an exact CPU emulation of a pipeline that
+stores its GEMM inputs and outputs in bf16 (tests/test_tolerance_reading.py)
+reaches 2.15e-2 on it over a 200-token chunk of the 8B-shaped layer (2.04e-2
+with the residual kept in fp32), so 2e-2 on that form is out of reach
+for any bf16 path; 3e-2 bounds an implementation to that floor plus the
+spread of its accumulation order.  Through a stack of n layers the rounding
+errors of the layers add along the residual stream roughly in quadrature
+(the same emulation over two stacked layers reaches 2.81e-2 against
+2.04e-2 for one), so a stack is held to ELEMENTWISE_TOL * sqrt(n).
 """
 from __future__ import annotations
 
@@ -22,6 +28,7 @@ from paper_2609_07883_amd import api, synth
 
 TOL = 2e-2
 RMS_TOL = 1e-2
+ELEMENTWISE_TOL = 3e-2
 
 
 def rel_err(got, ref) -> float:
@@ -53,10 +60,11 @@ def elementwise_err(got, ref) -> float:
     return float(np.max(np.abs(got - ref) / (np.abs(ref) + rms + 1e-30)))
 
 
-def check(got, ref, what: str = "") -> dict:
-    """Assert the parity bar; return the three error figures."""
+def check(got, ref, what: str = "", layers: int = 1) -> dict:
+    """Assert the parity bar (outputs of a stack of `layers` layers); return the three error figures."""
     e = {"rel": rel_err(got, ref), "rms": rms_err(got, ref), "elementwise": elementwise_err(got, ref)}
-    assert e["rel"] <= TOL and e["rms"] <= RMS_TOL, f"{what} parity: {e}"
+    ew_tol = ELEMENTWISE_TOL * float(np.sqrt(layers))
+    assert e["rel"] <= TOL and e["rms"] <= RMS_TOL and e["elementwise"] <= ew_tol, f"{what} parity: {e}"
     return e
 
 

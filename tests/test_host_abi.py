@@ -232,3 +232,18 @@ def test_select_chunk_ctx_bit_exact_vs_oracle():
         prefix = int(rng.integers(0, 16385))
         assert api.select_chunk(ct, dl, now, rem, cmax, margin, prefix=prefix)[:2] == \
             S.select_chunk_table(ot, dl, now, rem, cmax, margin, prefix=prefix)[:2]
+
+
+def test_cost_table_statistics_match_hand_worked_golden():
+    """The library's P50, P99, running max and monotonicity report on the
+    hand-worked table of tests/golden/monotone_table.txt."""
+    from tests.test_oracle_schedule import _golden_monotone
+    g, samples = _golden_monotone()
+    ct = api.CostTable.from_samples(g["c_grid"], g["b_grid"], np.asarray(samples, dtype=np.int64))
+    assert ct.values(api.TABLE_P50).tolist() == [g["p50"][b] for b in g["b_grid"]]
+    assert ct.values(api.TABLE_P99).tolist() == [g["p99"][b] for b in g["b_grid"]]
+    assert ct.values(api.TABLE_THAT).tolist() == [g["that"][b] for b in g["b_grid"]]
+    assert ct.monotone() == g["violations"]
+    ct2 = api.CostTable.from_samples(g["c_grid"], g["b_grid"], np.asarray([samples, samples], dtype=np.int64),
+                                     p_grid=[0, 4096])
+    assert ct2.monotone() == (2 * g["violations"][0], g["violations"][1])

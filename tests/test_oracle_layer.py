@@ -259,3 +259,67 @@ def test_append_kv_equals_row_by_row_writes():
     kv = L.KVState({0: L.SeqCache(np.zeros((2, hkv, hd)), np.zeros((2, hkv, hd)))})
     with pytest.raises(ValueError):
         L.append_kv(shape, kv, [0, 0], [2, 4], np.zeros((2, hkv, hd)), np.zeros((2, hkv, hd)))
+
+
+def _hf_kv(lay, rot, x: np.ndarray):
+    """K (after RoPE) and V that transformers' attention module forms from a
+    layer's input rows x [n][d] at positions 0..n-1: [n][Hkv][hd] each."""
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+    n = x.shape[0]
+    at = lay.self_attn
+    hs = torch.from_numpy(x)[None]
+    pos = torch.arange(n)[None]
+    cos, sin = rot(hs, pos)
+    with torch.no_grad():
+        u = lay.input_layernorm(hs)
+        hd = at.head_dim
+        q = at.q_proj(u).view(1, n, -1, hd).transpose(1, 2)
+        k = at.k_proj(u).view(1, n, -1, hd).transpose(1, 2)
+        v = at.v_proj(u).view(1, n, -1, hd).transpose(1, 2)
+        _, k = apply_rotary_pos_emb(q, k, cos, sin)
+    return k[0].transpose(0, 1).numpy(), v[0].transpose(0, 1).numpy()
+
+
+def test_stack_matches_stacked_transformers_layers():
+    """stack_iteration over three layers with their own weights and caches:
+    a prompt prefilled in two chunks, then one decode token, against three
+    transformers LlamaDecoderLayers applied in turn to the whole sequence.
+    Every layer's K/V is compared with the K/V transformers forms from that
+    layer's input, so a wrong hand-off between layers or a cache shared
+    between layers shows up."""
+    model = TINY_GQA
+    n_layers, n = 3, 90
+    bits = [synth.layer_weights(model, layer=l, weight_seed=6, qk_std=0.16) for l in range(n_layers)]
+    ws = [oracle_weights(b) for b in bits]
+    shape = oracle_shape(model)
+    x = x_rows(n + 1, model.d_model, stream=8)
+    # transformers: the whole sequence through each layer in turn
+    hf_in, hf_kv = [], []
+    h = x
+    for w in ws:
+        lay, rot = _hf_layer(model, w)
+        hf_in.append(h)
+        hf_kv.append(_hf_kv(lay, rot, h))
+        h = _hf_forward(lay, rot, h)
+    ref = h
+    # oracle: chunks of 40 and 50, then the decode of position 90
+    kvs = [L.KVState() for _ in ws]
+    ys = []
+    for p, c in ((0, 40), (40, 50)):
+        b = L.MixedBatch(chunk=c, prefill_seq=3, prefix_len=p, decode_seqs=[], context_lens=[])
+        ys.append(L.stack_iteration(shape, ws, x[p:p + c], kvs, b))
+    b = L.MixedBatch(chunk=0, prefill_seq=-1, prefix_len=0, decode_seqs=[3], context_lens=[n])
+    ys.append(L.stack_iteration(shape, ws, x[n:], kvs, b))
+    y = np.concatenate(ys)
+    scale = np.max(np.abs(ref))
+    assert np.max(np.abs(y - ref)) <= 1e-6 * scale
+    for l in range(n_layers):
+        k_ref, v_ref = hf_kv[l]
+        c = kvs[l].seqs[3]
+        assert c.length == n + 1
+        # K carries transformers' float32 RoPE frequencies directly (about
+        # 1e-6 relative at these positions); a structural mistake is O(1)
+        assert np.max(np.abs(c.k - k_ref)) <= 1e-5 * np.max(np.abs(k_ref))
+        assert np.max(np.abs(c.v - v_ref)) <= 1e-6 * np.max(np.abs(v_ref))
+    # the layers differ: a stack that reused one layer's weights would not match
+    assert np.max(np.abs(hf_kv[0][0] - hf_kv[1][0])) > 0.1 * np.max(np.abs(hf_kv[0][0]))

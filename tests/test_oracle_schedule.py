@@ -255,3 +255,39 @@ def test_context_planes_round_prefix_up():
     with pytest.raises(IndexError):
         S.select_chunk_table(t, [10**9 + 150], 10**9, 500, 128, prefix=5000)
     assert S.select_chunk_table(t, [], 10**9, 500, 128, prefix=5000)[0] == 128   # nothing to price
+
+
+def _golden_monotone():
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "monotone_table.txt")
+    g = {"sample": {}, "p50": {}, "p99": {}, "that": {}}
+    for line in open(path):
+        f = line.split()
+        if not f or f[0].startswith("#"):
+            continue
+        if f[0] in ("c_grid", "b_grid"):
+            g[f[0]] = [int(v) for v in f[1:]]
+        elif f[0] == "sample":
+            g["sample"][(int(f[1]), int(f[2]))] = [int(v) for v in f[3:]]
+        elif f[0] in ("p50", "p99", "that"):
+            g[f[0]][int(f[1])] = [int(v) for v in f[2:]]
+        elif f[0] == "violations":
+            g["violations"] = (int(f[1]), int(f[2]))
+    samples = [[g["sample"][(b, c)] for c in g["c_grid"]] for b in g["b_grid"]]
+    return g, samples
+
+
+def test_table_statistics_match_hand_worked_golden():
+    """P50, P99, running max and the count and size of raw P99 decreases along
+    c, against a table worked out by hand (tests/golden/monotone_table.txt):
+    an equal step is no decrease, the last column is scanned, and the largest
+    drop is the largest of all rows."""
+    g, samples = _golden_monotone()
+    t = S.CostTable(g["c_grid"], g["b_grid"], samples)
+    assert t.p50 == [g["p50"][b] for b in g["b_grid"]]
+    assert t.p99 == [g["p99"][b] for b in g["b_grid"]]
+    assert t.t_hat == [g["that"][b] for b in g["b_grid"]]
+    assert t.monotone_violations() == g["violations"]
+    # with a context axis every plane is scanned: two copies double the count
+    t2 = S.CostTable(g["c_grid"], g["b_grid"], [samples, samples], p_grid=[0, 4096])
+    assert t2.monotone_violations() == (2 * g["violations"][0], g["violations"][1])
