@@ -12,7 +12,9 @@
  *     pointers are ordinary CPU memory.  The library never allocates device
  *     memory: weights, KV pools, activations and the workspace all belong to
  *     the caller.  It owns only host state (sequence tables, cost tables) plus
- *     a small pinned host staging ring and HIP events, created on first use.
+ *     a small pinned host staging ring and HIP events, created on first use,
+ *     and the static workspace array of slw_mixed_iteration_static, which is
+ *     part of its device code (loaded with it, never allocated by a call).
  *   - Streams are passed as void* holding a hipStream_t (NULL = the null
  *     stream).  Device work is enqueued asynchronously; kernel faults surface
  *     at the caller's next synchronisation.
@@ -60,8 +62,9 @@ const char* slw_last_error(void);
  * causal attention over the paged cache, output projection + residual,
  * RMSNorm, SwiGLU MLP + residual.
  * Supported: head_dim in {64, 128}; n_q_heads % n_kv_heads == 0 with group
- * n_q_heads / n_kv_heads <= 16; d_model and ffn_dim multiples of 64;
- * block_size == 16; 1 <= max_pos <= 1048576.
+ * n_q_heads / n_kv_heads in {1, 2, 4, 8, 16}; d_model a multiple of 128 in
+ * [128, 8192]; ffn_dim a multiple of 64; (n_q_heads + 2 n_kv_heads) *
+ * head_dim a multiple of 128; block_size == 16; 1 <= max_pos <= 1048576.
  */
 typedef struct slw_model_cfg {
     int32_t n_layers;
@@ -171,7 +174,7 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  *   ws     device workspace of ws_bytes >= slw_workspace_size(ctx, C, B)
  * Reserves KV room (prefill_seq up to prefix_len + C, each decode up to
  * context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
- * it), builds the slot mapping and block tables on the host, writes them to
+ * it; a call that fails after reserving returns the blocks), builds the slot mapping and block tables on the host, writes them to
  * a coherent pinned staging ring that a first kernel copies into the
  * workspace, then enqueues per layer: RMSNorm, QKV GEMM
  * whose epilogue applies RoPE and appends K/V to the pages, chunk attention
@@ -182,6 +185,26 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  */
 int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const void* x_in, void* x_out,
                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The mixed iteration for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Same batch, inputs, outputs and results as
+ * slw_mixed_iteration, but it takes no workspace: it uses a device array of
+ * SLW_STATIC_WS_BYTES inside the library, one per GPU, which each GPU the
+ * library runs on holds until the process ends.  The call allocates nothing
+ * (no hipMalloc, no pinned host memory, no stream or event): the metadata is
+ * copied from host memory the context already holds, `stream` is
+ * synchronised once after that copy (the iteration's kernels then run
+ * asynchronously), both attentions run on `stream`, and no stage timing is
+ * recorded.  An iteration whose workspace would exceed the array
+ * (slw_workspace_size(ctx, C, B) gives an upper bound) is refused with
+ * SLW_ENOMEM before anything is reserved or enqueued.  Every call on a GPU
+ * shares that GPU's array, which keeps the last call's contents: calls that
+ * overlap on one GPU (several streams or threads) race.
+ */
+#define SLW_STATIC_WS_BYTES ((size_t)128 << 20)
+int slw_mixed_iteration_static(slw_ctx* ctx, const slw_batch* batch, const void* x_in, void* x_out, void* stream);
 
 /* Slot of every row of the last slw_mixed_iteration (host int32, chunk rows first). */
 int slw_last_slots(slw_ctx* ctx, int32_t* out, int32_t cap, int32_t* n);

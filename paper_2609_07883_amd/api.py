@@ -36,7 +36,9 @@ EXPORTS = (
     "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
     "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
     "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
+    "slw_mixed_iteration_static",
 )
+STATIC_WS_BYTES = 128 << 20
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "attn_merge",
           "o_gemm", "rmsnorm_mlp", "gateup_gemm", "down_gemm")
 
@@ -132,6 +134,7 @@ def lib() -> C.CDLL:
         "slw_seq_block_table": ([vp, i64, P(i32), i32, P(i32)], C.c_int),
         "slw_workspace_size": ([vp, i32, i32, P(sz)], C.c_int),
         "slw_mixed_iteration": ([vp, P(BatchC), vp, vp, vp, sz, vp], C.c_int),
+        "slw_mixed_iteration_static": ([vp, P(BatchC), vp, vp, vp], C.c_int),
         "slw_last_slots": ([vp, P(i32), i32, P(i32)], C.c_int),
         "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
@@ -461,6 +464,10 @@ class Context:
                         stream: int = 0):
         _check(lib().slw_mixed_iteration(self._h, C.byref(batch.c_struct()), x_in, x_out, ws, ws_bytes,
                                          stream or None))
+
+    def mixed_iteration_static(self, batch: Batch, x_in: int, x_out: int, stream: int = 0):
+        """The iteration on the library's static workspace (no allocation of any kind)."""
+        _check(lib().slw_mixed_iteration_static(self._h, C.byref(batch.c_struct()), x_in, x_out, stream or None))
 
     def set_stage_timing(self, depth: int):
         """Record per-stage HIP events for the last `depth` iterations (0: off)."""

@@ -11,6 +11,7 @@
 #include <chrono>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <random>
 #include <unordered_set>
 #include <vector>
@@ -53,6 +54,7 @@ struct slw_ctx {
     KvManager kv;
     bool kv_ready = false;
     std::vector<int32_t> last_slots;
+    std::vector<int32_t> slots_build;  // slots of the iteration being built
     std::vector<int32_t> meta;  // host build area
     std::vector<int32_t> items; // chunk-attention work items (host build area)
 
@@ -236,8 +238,19 @@ int ensure_stage_events(slw_ctx* ctx) {
     return SLW_OK;
 }
 
+int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
+                      const Layout& L, hipStream_t stream, bool no_alloc);
+
+// One iteration: validation, KV reservation (all or nothing), then the
+// metadata, its upload and the kernels.  A failure after the reservation
+// returns the reserved blocks, so a failed call leaves the block manager as
+// it found it.  no_alloc: the workspace is the static array, the metadata is
+// copied with hipMemcpyAsync from host memory the context holds, both
+// attentions run on `stream` and no stage events are recorded, so the call
+// creates no HIP object and allocates no memory of any kind on the device or
+// pinned on the host.
 int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
-                         size_t ws_bytes, hipStream_t stream) {
+                         size_t ws_bytes, hipStream_t stream, bool no_alloc = false) {
     const slw_model_cfg& c = ctx->cfg;
     if (!bt) return fail(SLW_EINVAL, "null batch");
     const int C = bt->C, B = bt->B, P = bt->prefix_len;
@@ -283,13 +296,32 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     const Layout L = layout(c, C, B);
     const size_t gpart = gemm_partial_bytes(c, C + B);
     if (ws_bytes < L.end_fixed + gpart)
-        return fail(SLW_ENOMEM, "workspace holds %zu bytes, this iteration needs %zu", ws_bytes,
+        return fail(SLW_ENOMEM, "%s holds %zu bytes, this iteration needs %zu",
+                    no_alloc ? "the static workspace (SLW_STATIC_WS_BYTES)" : "the workspace", ws_bytes,
                     L.end_fixed + gpart);
+    int rc = SLW_OK;
+    if (!no_alloc) {
+        rc = ensure_hip(ctx);
+        if (rc) return rc;
+        if (ctx->stage_depth > 0) {
+            rc = ensure_stage_events(ctx);
+            if (rc) return rc;
+        }
+    }
+    KvManager::Undo undo;
+    rc = ctx->kv.reserve_all(req, &undo);
+    if (rc) return rc;
+    rc = enqueue_iteration(ctx, bt, x_in, x_out, ws, L, stream, no_alloc);
+    if (rc) ctx->kv.rollback(undo);
+    return rc;
+}
 
-    int rc = ctx->kv.reserve_all(req);
-    if (rc) return rc;
-    rc = ensure_hip(ctx);
-    if (rc) return rc;
+// Metadata, upload and kernels of an iteration whose blocks are reserved.
+int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
+                      const Layout& L, hipStream_t stream, bool no_alloc) {
+    const slw_model_cfg& c = ctx->cfg;
+    const int C = bt->C, B = bt->B, P = bt->prefix_len;
+    int rc = SLW_OK;
 
     // ---- metadata (host) ----
     const int M = C + B;
@@ -302,10 +334,11 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     m.clear();
     m.reserve(meta_ints(c, C, B));
     // slot[M], pos[M]
-    ctx->last_slots.resize(M);
-    for (int j = 0; j < C; ++j) ctx->last_slots[j] = ctx->kv.slot(bt->prefill_seq, P + j);
-    for (int b = 0; b < B; ++b) ctx->last_slots[C + b] = ctx->kv.slot(bt->decode_seqs[b], bt->context_lens[b]);
-    m.insert(m.end(), ctx->last_slots.begin(), ctx->last_slots.end());
+    std::vector<int32_t>& slots = ctx->slots_build;
+    slots.resize(M);
+    for (int j = 0; j < C; ++j) slots[j] = ctx->kv.slot(bt->prefill_seq, P + j);
+    for (int b = 0; b < B; ++b) slots[C + b] = ctx->kv.slot(bt->decode_seqs[b], bt->context_lens[b]);
+    m.insert(m.end(), slots.begin(), slots.end());
     for (int j = 0; j < C; ++j) m.push_back(P + j);
     for (int b = 0; b < B; ++b) m.push_back(bt->context_lens[b]);
     const size_t o_kvlen = m.size();
@@ -415,19 +448,30 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     if (m.size() > meta_ints(c, C, B)) return fail(SLW_EINVAL, "internal: metadata %zu ints above its region", m.size());
 
     // ---- upload ----
-    int32_t* stage = nullptr;
-    int slot = 0;
-    rc = next_staging(ctx, m.size(), &stage, &slot);
-    if (rc) return rc;
-    std::memcpy(stage, m.data(), m.size() * 4);
     char* wsb = static_cast<char*>(ws);
     int32_t* dmeta = reinterpret_cast<int32_t*>(wsb + L.meta);
     float2* rope = reinterpret_cast<float2*>(wsb + L.rope);
-    // metadata copy and RoPE table (positions follow the M slots) in one kernel
-    launch_iteration_setup(dmeta, ctx->staging_dev[slot], m.size(), ctx->staging_dev[slot] + M, rope, M, c.head_dim,
-                           static_cast<double>(c.rope_theta), stream);
-    HIP_TRY(hipGetLastError());
-    HIP_TRY(hipEventRecord(ctx->staged[slot], stream));
+    if (no_alloc) {
+        // From the context's host vector, which the next call refills: a copy
+        // from pageable memory may still be reading it when hipMemcpyAsync
+        // returns, so the stream is synchronised right after it.
+        HIP_TRY(hipMemcpyAsync(dmeta, m.data(), m.size() * 4, hipMemcpyHostToDevice, stream));
+        HIP_TRY(hipStreamSynchronize(stream));
+        launch_iteration_setup(dmeta, nullptr, 0, dmeta + M, rope, M, c.head_dim, static_cast<double>(c.rope_theta),
+                               stream);
+        HIP_TRY(hipGetLastError());
+    } else {
+        int32_t* stage = nullptr;
+        int slot = 0;
+        rc = next_staging(ctx, m.size(), &stage, &slot);
+        if (rc) return rc;
+        std::memcpy(stage, m.data(), m.size() * 4);
+        // metadata copy and RoPE table (positions follow the M slots) in one kernel
+        launch_iteration_setup(dmeta, ctx->staging_dev[slot], m.size(), ctx->staging_dev[slot] + M, rope, M,
+                               c.head_dim, static_cast<double>(c.rope_theta), stream);
+        HIP_TRY(hipGetLastError());
+        HIP_TRY(hipEventRecord(ctx->staged[slot], stream));
+    }
 
     const int32_t* d_slot = dmeta;
     void* xn = wsb + L.xn;
@@ -445,12 +489,10 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     const GemmPlan p_d = plan_gemm(M, d, F);
     const size_t layer_pool = static_cast<size_t>(ctx->kv.num_blocks()) * hkv * hd * 16 * 2;
 
-    const bool timing = ctx->stage_depth > 0;
+    const bool timing = !no_alloc && ctx->stage_depth > 0;
     size_t set_base = 0;
     int set = 0;
     if (timing) {
-        rc = ensure_stage_events(ctx);
-        if (rc) return rc;
         set = static_cast<int>(ctx->stage_iter % ctx->stage_depth);
         set_base = static_cast<size_t>(set) * c.n_layers * (kStages + 1);
         ctx->stage_mask[set] = 0;
@@ -486,7 +528,7 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
         // With both attentions to run (and no per-stage events), decode
         // attention goes to a second stream so that it fills the CUs a short
         // chunk leaves idle; the merge waits for both.
-        const bool concurrent = C > 0 && B > 0 && !timing;
+        const bool concurrent = C > 0 && B > 0 && !timing && !no_alloc;
         hipStream_t dstream = stream;
         if (concurrent) {
             HIP_TRY(hipEventRecord(ctx->fork_ev[l], stream));
@@ -561,9 +603,13 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     }
     HIP_TRY(hipGetLastError());
     if (timing) {
-        ctx->stage_mask[set] = 0x3FFu & ~(C > 0 ? 0u : (1u << 3)) & ~(B > 0 ? 0u : (3u << 4));
+        // the merge stage (5) runs when decodes or split chunk query tiles need it
+        const bool merge = B > 0 || (C > 0 && n_items > n_qt);
+        ctx->stage_mask[set] = 0x3FFu & ~(C > 0 ? 0u : (1u << 3)) & ~(B > 0 ? 0u : (1u << 4)) &
+                               ~(merge ? 0u : (1u << 5));
         ++ctx->stage_iter;
     }
+    ctx->last_slots.swap(slots);
     return SLW_OK;
 }
 
@@ -699,6 +745,54 @@ extern "C" int slw_mixed_iteration(slw_ctx* ctx, const slw_batch* batch, const v
     return guarded([&] {
         if (!ctx) return fail(SLW_EINVAL, "null context");
         return mixed_iteration_impl(ctx, batch, x_in, x_out, ws, ws_bytes, static_cast<hipStream_t>(stream));
+    });
+}
+
+// ---------------------------------------------------------------------------
+// The allocation-free variant: the workspace is a file-scope device array of
+// SLW_STATIC_WS_BYTES, one copy per GPU, held until the process ends.  Its
+// address on each device is taken once, with that device current, through
+// hipGetSymbolAddress; host code uses only that address (the array's name
+// is a host-side stand-in).  No value in it needs to start at zero: every
+// word a kernel reads was written earlier in the same call.  Calls that
+// overlap on one GPU share the array and race.
+// ---------------------------------------------------------------------------
+
+namespace {
+
+constexpr size_t kStaticWsBytes = SLW_STATIC_WS_BYTES;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kStaticWsBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_workspace(void** out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(SLW_ERANGE, "device %d above %d", dev, kMaxDevices - 1);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(SLW_EHIP, "hipGetSymbolAddress gave a null address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return SLW_OK;
+}
+
+}  // namespace
+
+extern "C" int slw_mixed_iteration_static(slw_ctx* ctx, const slw_batch* batch, const void* x_in, void* x_out,
+                                          void* stream) {
+    return guarded([&] {
+        if (!ctx) return fail(SLW_EINVAL, "null context");
+        void* ws = nullptr;
+        int rc = static_workspace(&ws);
+        if (rc) return rc;
+        return mixed_iteration_impl(ctx, batch, x_in, x_out, ws, kStaticWsBytes, static_cast<hipStream_t>(stream),
+                                    true);
     });
 }
 

@@ -30,7 +30,8 @@ int KvManager::release(int64_t id) {
     return SLW_OK;
 }
 
-int KvManager::reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req) {
+int KvManager::reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req, Undo* undo) {
+    if (undo) undo->grown.clear();
     // Largest request per sequence, then the total number of new blocks.
     std::unordered_map<int64_t, int32_t> want;
     for (const auto& r : req) {
@@ -58,6 +59,7 @@ int KvManager::reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req) 
         Seq& s = seqs_.at(r.first);
         int32_t len = w->second > s.reserved ? w->second : s.reserved;
         int64_t need = ceil_div(len, block_size_) - static_cast<int64_t>(s.blocks.size());
+        if (undo) undo->grown.push_back({r.first, s.blocks.size(), s.reserved});
         for (int64_t i = 0; i < need; ++i) {
             s.blocks.push_back(free_.top());
             free_.pop();
@@ -66,6 +68,17 @@ int KvManager::reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req) 
         want.erase(w);
     }
     return SLW_OK;
+}
+
+void KvManager::rollback(const Undo& undo) {
+    for (auto e = undo.grown.rbegin(); e != undo.grown.rend(); ++e) {
+        Seq& s = seqs_.at(e->id);
+        while (s.blocks.size() > e->blocks) {
+            free_.push(s.blocks.back());
+            s.blocks.pop_back();
+        }
+        s.reserved = e->reserved;
+    }
 }
 
 }  // namespace slw

@@ -24,8 +24,22 @@ public:
     // Each returns an SLW_* code (and sets the error message on failure).
     int create(int64_t id);
     int release(int64_t id);
-    // Grows every (id, new_len) in order; all or nothing.
-    int reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req);
+    // What a reservation changed: per grown sequence, its block count and
+    // reserved length before the call.
+    struct Undo {
+        struct Entry {
+            int64_t id;
+            size_t blocks;
+            int32_t reserved;
+        };
+        std::vector<Entry> grown;
+    };
+    // Grows every (id, new_len) in order; all or nothing.  With `undo`, the
+    // changes are recorded so that rollback() can return them.
+    int reserve_all(const std::vector<std::pair<int64_t, int32_t>>& req, Undo* undo = nullptr);
+    // Returns the blocks a reservation took and restores the lengths; the
+    // free set, and so every later allocation, is as before the reservation.
+    void rollback(const Undo& undo);
 
     const std::vector<int32_t>& table(int64_t id) const { return seqs_.at(id).blocks; }
     int32_t reserved(int64_t id) const { return seqs_.at(id).reserved; }
