@@ -412,6 +412,7 @@ typedef struct slw_request_slo {
 #define SLW_SERVE_DECODE_CAP 0x200u   /* the oldest prompt waits: decode batch full */
 #define SLW_SERVE_UNPRICED 0x400u     /* decode batch above the table: decode-only  */
 #define SLW_SERVE_AGED 0x800u         /* chunk forced by the aging threshold         */
+#define SLW_SERVE_FALLBACK 0x1000u    /* decode-only: residual P99 above the margin  */
 
 /* Queue disciplines (Sec. 3.4): which pending prompt is served first.  Ties
  * go to the older request (arrival, then id). */
@@ -471,6 +472,17 @@ typedef struct slw_serve_opts {
      * already placed; a prompt that does not finish ends the list.  The
      * iteration is priced at the total.  0 or 1 = one prompt. */
     int32_t max_prefills;
+    /* Telemetry fallback (Sec. 5.1: the scheduler falls back to decode-only
+     * execution when telemetry residuals exceed the configured margin;
+     * Table 1: telemetry records fallback events).  Every iteration whose
+     * time `table` predicts leaves observed - predicted (ns) in a window of
+     * the last fallback_window such values; while the window's nearest-rank
+     * P99 exceeds margin_ns, a SLOWeave decision with a prompt to serve and
+     * active decodes runs no chunk and its record carries SLW_SERVE_FALLBACK
+     * (with no active decode there is no deadline to protect).  Decode-only
+     * iterations keep filling the window, so chunks return once the observed
+     * residuals are back within the margin.  0 = off. */
+    int32_t fallback_window;
 } slw_serve_opts;
 
 /* One iteration of a serving run (host memory). */
@@ -489,6 +501,8 @@ typedef struct slw_iteration_record {
     int64_t rel_margin_ppm; /* telemetry margin q used by the decision (0 when off)       */
     int32_t n_prefill;    /* prompts served (chunk is their total; prefill_id the first)  */
     int32_t reserved;
+    int64_t resid_p99_ns; /* fallback window's P99 tested by the decision (0 when off, when
+                             the window is empty, or with no prompt to serve or no decode) */
 } slw_iteration_record;
 
 /*

@@ -44,7 +44,19 @@ Readings (the paper is silent or ambiguous here):
   last W of them form the window, and a decision adds
   ceil(q * T_hat(n, c) / 1e6) to every prediction it tests, q being the
   nearest-rank P99 of the window clamped to [0, 1e8] (0 while the window is
-  empty).
+  empty);
+* the telemetry fallback (Sec. 5.1: the scheduler may fall back to
+  decode-only execution when telemetry residuals exceed the configured
+  margin; Table 1: telemetry records predicted and observed durations and
+  fallback events) compares absolute residuals with the margin delta: every
+  iteration the predictor prices leaves observed - predicted in ns, the last
+  F of them form the fallback window, and while the window's nearest-rank
+  P99 exceeds delta a SLOWeave decision that has a prompt to serve and
+  active decodes to protect runs no chunk and is recorded as a fallback
+  event (no fallback while the window is empty; with no active decode there
+  is no deadline to protect and Alg. 1 runs as usual).  Decode-only
+  iterations keep filling the window, so chunks return once the observed
+  residuals are back within delta.
 """
 from __future__ import annotations
 
@@ -75,6 +87,8 @@ class Iteration:
     rel_margin_ppm: int = 0  # telemetry margin used by the decision
     n_prefill: int = 0   # prompts served
     aged: bool = False   # the chunk was forced by the aging threshold
+    fallback: bool = False   # decode-only because the residual P99 exceeded the margin
+    resid_p99_ns: int = 0    # fallback window's P99 tested by the decision
 
 
 @dataclass
@@ -101,7 +115,7 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
              predict=None, c_last: int | None = None, c_max: int = 4096, margin_ns: int = 0,
              max_decode: int | None = None, residual_window: int = 0, prefix_aware: bool = False,
              queue: str = "oldest", admit_ppm: int = 0, aging_ns: int = 0, aging_chunk: int = 0,
-             max_prefills: int = 1, max_iterations: int = 10_000_000) -> Trace:
+             max_prefills: int = 1, fallback_window: int = 0, max_iterations: int = 10_000_000) -> Trace:
     """Run the trace through the iteration-level loop of Sec. 4.1.
 
     cost_ns(n, c) -> ns is how long an iteration with n decodes and c
@@ -109,7 +123,8 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
     what the SLOWeave controller believes (defaults to cost_ns) and c_last
     the largest chunk it can price.  policy is "sloweave" (Alg. 1 with margin
     margin_ns and cap c_max) or "fixed" (chunks of fixed_chunk tokens).
-    residual_window > 0 turns on the telemetry margin (module docstring).
+    residual_window > 0 turns on the telemetry margin and fallback_window > 0
+    the telemetry fallback (module docstring).
     With prefix_aware, cost_ns and predict take a third argument, the cached
     prefix the iteration is priced at: that of the first prompt it serves
     (its tokens already processed), 0 with none.
@@ -160,6 +175,7 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
     nxt = 0
     finished = 0
     residuals = []          # relative residuals (ppm) of chunked iterations, oldest first
+    fb_resid = []           # absolute residuals (ns) of priced iterations, oldest first
     for _ in range(max_iterations):
         if finished == len(reqs):
             return out
@@ -195,6 +211,8 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
         prefix = done_prompt[head.rid] if head else 0
         rel = 0
         aged = False
+        fallback = False
+        fb_p99 = 0
         plan = []                              # (request, tokens) served this iteration
         if head is None:
             chunk = 0
@@ -203,14 +221,20 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
         else:
             if residual_window > 0 and residuals:
                 rel = min(max(nearest_rank(residuals[-residual_window:], 99, 100), 0), 10**8)
+            if fallback_window > 0 and fb_resid and n > 0:
+                fb_p99 = nearest_rank(fb_resid[-fallback_window:], 99, 100)
+                fallback = fb_p99 > margin_ns
 
             def with_margin(nn, cc, q=rel, p=prefix):
                 v = at(predict, nn, cc, p)
                 return v + -(-q * v // 10**6)   # T_hat + ceil(q T_hat / 1e6)
-            try:
-                chunk = select_chunk(with_margin, eff, t, remaining, c_max, margin_ns, c_last=c_last)[0]
-            except IndexError:                 # n above the priced decode batches
+            if fallback:
                 chunk = 0
+            else:
+                try:
+                    chunk = select_chunk(with_margin, eff, t, remaining, c_max, margin_ns, c_last=c_last)[0]
+                except IndexError:             # n above the priced decode batches
+                    chunk = 0
             if chunk == 0 and aging_ns > 0 and t - waited[head.rid] >= aging_ns:
                 chunk = min(aging_chunk, remaining, c_max)
                 aged = True
@@ -242,11 +266,21 @@ def simulate(requests, *, cost_ns, tpot_ns: int, policy: str = "sloweave", fixed
             chunk = total
         end = t + at(cost_ns, n, chunk, prefix)
         out.iterations.append(Iteration(t, end, chunk, n, head.rid if chunk > 0 else -1, budget, rel,
-                                        len(plan), aged))
+                                        len(plan), aged, fallback, fb_p99))
         if residual_window > 0 and chunk > 0:
-            pred = at(predict, n, chunk, prefix)
+            try:
+                pred = at(predict, n, chunk, prefix)
+            except IndexError:                 # an aged chunk beside unpriced decodes
+                pred = 0
             if pred > 0:
                 residuals.append((end - t - pred) * 10**6 // pred)
+        if fallback_window > 0:
+            try:
+                pred = at(predict, n, chunk, prefix)
+            except IndexError:                 # not priced: no residual
+                pred = 0
+            if pred > 0:
+                fb_resid.append(end - t - pred)
         for rid in order:
             req, _ = active[rid]
             out.token_ns[rid].append(end)

@@ -88,7 +88,7 @@ class ServeOpts(C.Structure):
                 ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p),
                 ("residual_window", C.c_int32), ("exec_table", C.c_void_p), ("slo", C.c_void_p),
                 ("queue", C.c_int32), ("admit_ppm", C.c_int32), ("aging_ns", C.c_int64),
-                ("aging_chunk", C.c_int32), ("max_prefills", C.c_int32)]
+                ("aging_chunk", C.c_int32), ("max_prefills", C.c_int32), ("fallback_window", C.c_int32)]
 
 
 class RequestSloC(C.Structure):
@@ -100,12 +100,12 @@ class IterationRecord(C.Structure):
                 ("decide_ns", C.c_int64), ("predicted_ns", C.c_int64), ("prefill_id", C.c_int64),
                 ("chunk", C.c_int32), ("n_decode", C.c_int32), ("remaining", C.c_int32),
                 ("flags", C.c_uint32), ("rel_margin_ppm", C.c_int64), ("n_prefill", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("reserved", C.c_int32), ("resid_p99_ns", C.c_int64)]
 
 
 POLICY_SLOWEAVE, POLICY_FIXED = 0, 1
 EXEC_GPU, EXEC_ANALYTIC, EXEC_TABLE = 0, 1, 2
-SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED, SERVE_AGED = 0x100, 0x200, 0x400, 0x800
+SERVE_KV_WAIT, SERVE_DECODE_CAP, SERVE_UNPRICED, SERVE_AGED, SERVE_FALLBACK = 0x100, 0x200, 0x400, 0x800, 0x1000
 QUEUES = {"oldest": 0, "srpt": 1, "edf": 2}
 
 _lib = None
@@ -312,7 +312,7 @@ ITERATION_DTYPE = np.dtype([("start_ns", np.int64), ("end_ns", np.int64), ("budg
                             ("decide_ns", np.int64), ("predicted_ns", np.int64), ("prefill_id", np.int64),
                             ("chunk", np.int32), ("n_decode", np.int32), ("remaining", np.int32),
                             ("flags", np.uint32), ("rel_margin_ppm", np.int64), ("n_prefill", np.int32),
-                            ("reserved", np.int32)])
+                            ("reserved", np.int32), ("resid_p99_ns", np.int64)])
 assert ITERATION_DTYPE.itemsize == C.sizeof(IterationRecord)
 
 
@@ -323,7 +323,7 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
           stream: int = 0, iter_cap: int | None = None, residual_window: int = 0,
           exec_table: CostTable | None = None, slo_tpot_ns=None, slo_margin_ns=None, slo_ttft_ns=None,
           queue: str = "oldest", admit_ppm: int = 0, aging_ns: int = 0, aging_chunk: int = 0,
-          max_prefills: int = 1):
+          max_prefills: int = 1, fallback_window: int = 0):
     """slw_serve over a trace given as arrays.
 
     slo_tpot_ns / slo_margin_ns / slo_ttft_ns are optional per-request
@@ -352,7 +352,7 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
                   x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None,
                   residual_window, exec_table.handle if exec_table is not None else None,
                   C.cast(slo, C.c_void_p) if slo is not None else None, QUEUES[queue], int(admit_ppm),
-                  int(aging_ns), int(aging_chunk), int(max_prefills))
+                  int(aging_ns), int(aging_chunk), int(max_prefills), int(fallback_window))
     nit = C.c_int64()
     _check(lib().slw_serve(ctx._h if ctx is not None else None, reqs, n, C.byref(o), _ptr(tok, C.c_int64),
                            len(tok), its.ctypes.data_as(C.POINTER(IterationRecord)), len(its), C.byref(nit)))

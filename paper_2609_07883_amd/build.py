@@ -1,7 +1,7 @@
 """Build libsloweave.so (gfx950) in-tree.
 
-    python -m paper_2609_07883_amd.build          # library only
-    python -m paper_2609_07883_amd.build --all    # also the C oracle helpers, if any
+    python -m paper_2609_07883_amd.build            # every source
+    python -m paper_2609_07883_amd.build --changed  # only sources newer than their objects
 
 HIP sources are compiled with hipcc for gfx950; the host-only C++ sources
 with g++.  Objects go to ``_build/`` at the repository root; the shared
@@ -43,8 +43,17 @@ def _sources():
     return hip, cxx
 
 
-def _compile(src: str) -> str:
+def _newest_header() -> float:
+    hs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
+    hs += [os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
+    return max(os.path.getmtime(h) for h in hs)
+
+
+def _compile(src: str, changed_only: bool = False) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+    if changed_only and os.path.exists(obj) and \
+            os.path.getmtime(obj) > max(os.path.getmtime(src), _newest_header()):
+        return obj
     if src.endswith(".hip"):
         cmd = [HIPCC, *HIP_FLAGS, "-c", src, "-o", obj]
     else:
@@ -59,11 +68,11 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build_library(jobs: int = 8) -> str:
+def build_library(jobs: int = 8, changed_only: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     hip, cxx = _sources()
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(_compile, hip + cxx))
+        objs = list(ex.map(lambda f: _compile(f, changed_only), hip + cxx))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -76,8 +85,9 @@ def build_library(jobs: int = 8) -> str:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("-j", type=int, default=8)
+    ap.add_argument("--changed", action="store_true", help="compile only sources newer than their objects")
     args = ap.parse_args()
-    print(build_library(args.j))
+    print(build_library(args.j, args.changed))
 
 
 if __name__ == "__main__":

@@ -67,6 +67,9 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     if (o->aging_ns < 0 || (o->aging_ns > 0 && o->aging_chunk < 1))
         return fail(SLW_EINVAL, "aging needs aging_ns >= 0 and aging_chunk >= 1");
     if (o->max_prefills < 0) return fail(SLW_EINVAL, "max_prefills must be >= 0");
+    if (o->fallback_window < 0 || o->fallback_window > 65536)
+        return fail(SLW_ERANGE, "fallback_window must be in [0, 65536]");
+    if (o->fallback_window > 0 && !o->table) return fail(SLW_EINVAL, "the telemetry fallback needs a cost table");
     if (o->max_prefills > 1 && o->executor == SLW_EXEC_GPU)
         return fail(SLW_EUNSUPPORTED, "prefill batching runs on the virtual-clock executors only");
     if (o->executor == SLW_EXEC_GPU) {
@@ -162,6 +165,10 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     const int32_t W = o->residual_window;
     std::vector<int64_t> resid(std::max(W, 1)), scratch;
     int64_t n_resid = 0;
+    // telemetry fallback: absolute residuals (ns) of the last fallback_window priced iterations
+    const int32_t FW = o->fallback_window;
+    std::vector<int64_t> fb_resid(std::max(FW, 1));
+    int64_t n_fb = 0;
     const hipStream_t stream = static_cast<hipStream_t>(o->stream);
 
     auto finish = [&](const slw_request& r) {
@@ -252,17 +259,28 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
                     rel = std::min<int64_t>(std::max<int64_t>(nearest_rank(scratch, 99, 100), 0), 100000000);
                 }
                 rec.rel_margin_ppm = rel;
-                uint32_t fl = 0;
-                rc = select_chunk_core(o->table, eff.data(), nd, t, prefix, remaining, o->c_max, o->margin_ns, rel,
-                                       &chunk, &fl, nullptr);
-                if (rc == SLW_ERANGE) {  // more decodes than the table prices
-                    clear_error();
-                    chunk = 0;
-                    fl = SLW_SERVE_UNPRICED;
-                } else if (rc) {
-                    return rc;
+                bool fallback = false;
+                if (FW > 0 && n_fb > 0 && nd > 0) {  // with no decode there is no deadline to protect
+                    scratch.assign(fb_resid.begin(), fb_resid.begin() + std::min<int64_t>(n_fb, FW));
+                    rec.resid_p99_ns = nearest_rank(scratch, 99, 100);
+                    fallback = rec.resid_p99_ns > o->margin_ns;
                 }
-                rec.flags |= fl;
+                if (fallback) {
+                    chunk = 0;
+                    rec.flags |= SLW_SERVE_FALLBACK;
+                } else {
+                    uint32_t fl = 0;
+                    rc = select_chunk_core(o->table, eff.data(), nd, t, prefix, remaining, o->c_max, o->margin_ns,
+                                           rel, &chunk, &fl, nullptr);
+                    if (rc == SLW_ERANGE) {  // more decodes than the table prices
+                        clear_error();
+                        chunk = 0;
+                        fl = SLW_SERVE_UNPRICED;
+                    } else if (rc) {
+                        return rc;
+                    }
+                    rec.flags |= fl;
+                }
                 if (chunk == 0 && o->aging_ns > 0 && t - head->waited_ns >= o->aging_ns) {
                     chunk = std::min({o->aging_chunk, remaining, o->c_max});
                     rec.flags |= SLW_SERVE_AGED;
@@ -340,6 +358,10 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             if (num % rec.predicted_ns != 0 && num < 0) --q;  // floor
             resid[n_resid % W] = q;
             ++n_resid;
+        }
+        if (FW > 0 && rec.predicted_ns > 0) {
+            fb_resid[n_fb % FW] = end - t - rec.predicted_ns;
+            ++n_fb;
         }
 
         // decodes: one token each

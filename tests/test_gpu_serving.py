@@ -199,3 +199,44 @@ def test_policy_variants_on_gpu(setup):
     _, aged = _check_variant_run(sess, tr, res, lambda i, done: (tr.arrival_ns[i], i))
     assert aged > 0
     print(f"variants: {refused} refused, {aged} aged chunks")
+
+
+def test_telemetry_fallback_on_gpu(setup):
+    """Sec. 5.1's decode-only fallback on measured iterations: the controller
+    reads a table at half the measured times, so observed residuals exceed the
+    50 us margin.  Replayed from the records: each decision's window P99 is
+    the nearest-rank P99 of the absolute residuals of the priced iterations
+    before it; above the margin (with a prompt to serve and decodes active)
+    the iteration is decode-only and flagged, otherwise the chunk is Alg. 1
+    on the optimistic table.  Prompts still finish."""
+    sess, ct, tr = setup
+    FW, margin = 4, 50_000
+    samples = ct.values(api.TABLE_SAMPLES)
+    fast = api.CostTable.from_samples(C_GRID, B_GRID, samples // 2)
+    res = serving.run(tr, policy="sloweave", tpot_ms=3.0, max_decode=16, c_max=256, table=fast,
+                      margin_ns=margin, fallback_window=FW, session=sess)
+    torch.cuda.synchronize()
+    _check_run(sess, tr, res, 16)
+    ot = S.CostTable(C_GRID, B_GRID, (samples // 2).tolist())
+    window, events, decided = [], 0, 0
+    for r in res.iterations:
+        fb = bool(int(r["flags"]) & api.SERVE_FALLBACK)
+        if r["remaining"] > 0:
+            n = int(r["n_decode"])
+            p99 = S.nearest_rank(window[-FW:], 99, 100) if window and n > 0 else 0
+            assert int(r["resid_p99_ns"]) == p99
+            if n > 0 and window and p99 > margin:
+                assert fb and int(r["chunk"]) == 0
+                events += 1
+            else:
+                assert not fb
+                exp = S.select_chunk_table(ot, [int(r["start_ns"] + r["budget_ns"])] * n, int(r["start_ns"]),
+                                           int(r["remaining"]), 256, margin)
+                assert int(r["chunk"]) == exp[0]
+                decided += 1
+        else:
+            assert not fb
+        if r["predicted_ns"] > 0:
+            window.append(int(r["end_ns"]) - int(r["start_ns"]) - int(r["predicted_ns"]))
+    print(f"fallback: {events} events, {decided} Alg. 1 decisions, {len(res.iterations)} iterations")
+    assert events > 0 and decided > 0

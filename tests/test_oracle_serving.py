@@ -233,3 +233,60 @@ def test_telemetry_window_uses_nearest_rank_p99():
     assert [i.chunk for i in tr.iterations] == [100, 100, 100]
     # residuals: 0, 1e6 ppm, 0.5e6 ppm; margins seen by the 2nd and 3rd decisions
     assert [i.rel_margin_ppm for i in tr.iterations] == [0, 0, 1_000_000]
+
+
+def _slow_chunks(n, c):
+    """Hardware stand-in: the analytic model plus 1.5 ms on every iteration that runs a chunk."""
+    return S.analytic_cost_ns(n, c) + (1_500_000 if c > 0 else 0)
+
+
+def test_telemetry_fallback_by_hand():
+    """Sec. 5.1's decode-only fallback, stepped by hand.  The controller
+    predicts the analytic model T(n, c) (in ns: 350000 + [n>0](900000 +
+    55000 n) + [c>0](400000 + 6000 c)); every chunked iteration really takes
+    1.5 ms longer.  Margin delta = 1 ms, fallback window of one residual,
+    TPOT 50 ms; A (prompt 100, output 5) and B (prompt 200, output 3) arrive
+    at 0.
+
+      1. t=0: no decode, window empty: A's whole prompt, 100 tokens.  Cost
+         T(0,100) + 1.5 ms = 1350000 + 1500000 = 2850000; residual 1500000.
+      2. t=2850000: window P99 1500000 > delta: decode-only fallback for B's
+         turn.  Cost T(1,0) = 1305000, end 4155000; residual 0.
+      3. t=4155000: window P99 0 <= delta: Alg. 1 gives B's 200 tokens
+         (T(1,200) + 1 ms = 3905000 within 50 ms).  Cost 2905000 + 1500000,
+         end 8560000; B's first token.
+      4. t=8560000: nothing pending: decode-only, T(2,0) = 1360000, end 9920000.
+      5. t=9920000: decode-only, end 11280000: A's fifth and B's third token.
+    """
+    reqs = [V.Request(0, 0, 100, 5), V.Request(1, 0, 200, 3)]
+    tr = V.simulate(reqs, cost_ns=_slow_chunks, predict=S.analytic_cost_ns, tpot_ns=50_000_000,
+                    margin_ns=1_000_000, fallback_window=1)
+    got = [(i.start_ns, i.end_ns, i.chunk, i.n_decode, i.prefill_rid, i.fallback, i.resid_p99_ns)
+           for i in tr.iterations]
+    assert got == [(0, 2_850_000, 100, 0, 0, False, 0),
+                   (2_850_000, 4_155_000, 0, 1, -1, True, 1_500_000),
+                   (4_155_000, 8_560_000, 200, 1, 1, False, 0),
+                   (8_560_000, 9_920_000, 0, 2, -1, False, 0),
+                   (9_920_000, 11_280_000, 0, 2, -1, False, 0)]
+    assert tr.token_ns[0] == [2_850_000, 4_155_000, 8_560_000, 9_920_000, 11_280_000]
+    assert tr.token_ns[1] == [8_560_000, 9_920_000, 11_280_000]
+    # without the fallback B's chunk runs at once, ending at 2850000 + 4405000
+    tr0 = V.simulate(reqs, cost_ns=_slow_chunks, predict=S.analytic_cost_ns, tpot_ns=50_000_000,
+                     margin_ns=1_000_000)
+    assert tr0.token_ns[1][0] == 7_255_000
+    assert not any(i.fallback for i in tr0.iterations)
+
+
+def test_telemetry_fallback_is_inert_within_the_margin():
+    """Residuals at most delta never trigger the fallback: the run equals one without it."""
+    tr = synth.request_trace(120, 6.0, seed=4)
+    reqs = [V.Request(i, int(a), int(p), int(o)) for i, (a, p, o) in
+            enumerate(zip(tr.arrival_ns, tr.prompt, tr.output))]
+    cost = lambda n, c: S.analytic_cost_ns(n, c) + (700_000 if c > 0 else 0)
+    base = V.simulate(reqs, cost_ns=cost, predict=S.analytic_cost_ns, tpot_ns=25_000_000, margin_ns=700_000,
+                      max_decode=256)
+    fb = V.simulate(reqs, cost_ns=cost, predict=S.analytic_cost_ns, tpot_ns=25_000_000, margin_ns=700_000,
+                    max_decode=256, fallback_window=16)
+    assert base.token_ns == fb.token_ns
+    assert not any(i.fallback for i in fb.iterations)
+    assert max(i.resid_p99_ns for i in fb.iterations) == 700_000

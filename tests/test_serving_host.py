@@ -239,3 +239,46 @@ def test_context_axis_removes_long_prefix_misses():
         gaps = np.concatenate([np.diff(t) for t in res.token_ns if len(t) > 1])
         miss[name] = int(np.sum(gaps > 25 * MS))
     assert miss["flat"] > 0 and miss["ctx"] == 0
+
+
+@pytest.mark.parametrize("window,num,den,margin_ms", [(1, 6, 5, 0), (16, 11, 10, 1), (64, 5, 4, 2), (8, 9, 10, 0)])
+def test_telemetry_fallback_matches_oracle(window, num, den, margin_ms):
+    """The absolute-residual window, its P99, the decode-only fallback and its
+    record flag are the oracle's bit for bit, on hardware faster or slower
+    than the table."""
+    tr = _trace(250, 6.0, seed=12)
+    ctl, hw, octl, ohw = _scaled_tables(COARSE_C, COARSE_B, num, den)
+    res = serving.run(tr, policy="sloweave", tpot_ms=25, max_decode=256, table=ctl, exec_table=hw,
+                      margin_ns=margin_ms * MS, fallback_window=window)
+    ref = V.simulate(_oracle_reqs(tr), cost_ns=ohw.lookup, predict=octl.lookup, c_last=COARSE_C[-1],
+                     tpot_ns=25 * MS, max_decode=256, margin_ns=margin_ms * MS, fallback_window=window)
+    _compare(tr, res, ref)
+    it = res.iterations
+    fb = (it["flags"] & api.SERVE_FALLBACK) != 0
+    assert fb.tolist() == [r.fallback for r in ref.iterations]
+    assert it["resid_p99_ns"].tolist() == [r.resid_p99_ns for r in ref.iterations]
+    assert np.all(it["chunk"][fb] == 0)
+    if num > den:
+        assert fb.any()
+    else:
+        assert not fb.any()
+
+
+def test_telemetry_fallback_hand_worked_case():
+    """The hand-stepped oracle case (tests/test_oracle_serving.py) on the
+    library's table executor: a controller table over the analytic model and
+    a hardware table 1.5 ms slower wherever a chunk runs."""
+    cg, bg = [0, 1, 100, 200], [0, 1, 2]
+    ctl = api.CostTable.from_samples(cg, bg, np.array([[S.analytic_cost_ns(b, c)] * 1 for b in bg for c in cg],
+                                                      dtype=np.int64).reshape(len(bg), len(cg), 1))
+    hw = api.CostTable.from_samples(cg, bg, np.array([[S.analytic_cost_ns(b, c) + (1_500_000 if c else 0)]
+                                                      for b in bg for c in cg], dtype=np.int64)
+                                    .reshape(len(bg), len(cg), 1))
+    tok, its = api.serve([0, 1], [0, 0], [100, 200], [5, 3], policy=api.POLICY_SLOWEAVE, tpot_ns=50 * MS,
+                         max_decode=8, margin_ns=MS, table=ctl, executor=api.EXEC_TABLE, exec_table=hw,
+                         fallback_window=1)
+    assert tok[0].tolist() == [2_850_000, 4_155_000, 8_560_000, 9_920_000, 11_280_000]
+    assert tok[1].tolist() == [8_560_000, 9_920_000, 11_280_000]
+    assert its["chunk"].tolist() == [100, 0, 200, 0, 0]
+    assert ((its["flags"] & api.SERVE_FALLBACK) != 0).tolist() == [False, True, False, False, False]
+    assert its["resid_p99_ns"].tolist() == [0, 1_500_000, 0, 0, 0]
