@@ -121,6 +121,21 @@ def measured_traffic(stage, workload):
     return float(fields["bytes per launch"])
 
 
+def reserve_round_robin(ctx, lengths):
+    """Reserve {sid: n_positions} one block at a time across the sequences,
+    so that consecutive pages of a sequence are not neighbours in the pool
+    (the placement a server that grows many sequences together produces)."""
+    todo = {sid: int(n) for sid, n in lengths.items() if n > 0}
+    k = 1
+    while todo:
+        for sid in list(todo):
+            n = todo[sid]
+            ctx.seq_reserve(sid, min(n, 16 * k))
+            if 16 * k >= n:
+                del todo[sid]
+        k += 1
+
+
 def roof_time(flops, nbytes):
     return max(flops / PEAK_BF16, nbytes / PEAK_HBM)
 
@@ -137,14 +152,17 @@ def _cpu_model():
 
 def cpu_baseline(shape, ctx_lens, budget_s=30.0, min_s=12.0):
     """The oracle on the host cores over the P = 0 column of the sweep, in
-    passes until at least min_s seconds of oracle time (bounded by budget_s)."""
+    passes until at least min_s seconds of oracle time (bounded by budget_s);
+    then two more points: one iteration (C = 64, P = 0) on a single thread,
+    and one iteration with a cached prefix (C = 256, P = 2048) on all threads."""
     from oracle import layer as OL
     from paper_2609_07883_amd import synth
     from tests.parity import oracle_shape, oracle_weights
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         threads = len(os.sched_getaffinity(0))
     sh = oracle_shape(shape)
     w = oracle_weights(synth.layer_weights(shape, weight_seed=0))
@@ -163,19 +181,33 @@ def cpu_baseline(shape, ctx_lens, budget_s=30.0, min_s=12.0):
                 done.append(C)
         if secs > budget_s:
             break
-    return {"value": rows / secs, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "cpu_model": _cpu_model(),
-            "sample": f"float64 oracle, one mixed iteration at each C in {done} with P=0 and the same "
-                      f"B={len(ctx_lens)} decodes, {passes} pass(es) ({rows} rows, {secs:.1f} s)"}
+    out = {"value": rows / secs, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "cpu_model": _cpu_model(),
+           "sample": f"float64 oracle, one mixed iteration at each C in {done} with P=0 and the same "
+                     f"B={len(ctx_lens)} decodes, {passes} pass(es) ({rows} rows, {secs:.1f} s)"}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            r1, s1 = _oracle_point(OL, sh, w, kv, shape, ctx_lens, 64, 0, 0.0)
+        out["single_thread"] = {"value": round(r1 / s1, 1), "unit": "tokens/s", "cores": 1,
+                                "sample": f"one iteration at C=64, P=0, B={len(ctx_lens)} ({s1:.2f} s)"}
+    rp, sp = _oracle_point(OL, sh, w, kv, shape, ctx_lens, 256, 0, 0.0, prefix=2048)
+    out["prefix_point"] = {"value": round(rp / sp, 1), "unit": "tokens/s", "cores": threads,
+                           "sample": f"one iteration at C=256, P=2048, B={len(ctx_lens)} ({sp:.2f} s)"}
+    return out
 
 
-def _oracle_point(OL, sh, w, kv, shape, ctx_lens, C, rows, secs):
-    """One timed oracle iteration at chunk C (fresh prefill sequence, shared decodes)."""
+def _oracle_point(OL, sh, w, kv, shape, ctx_lens, C, rows, secs, prefix=0):
+    """One timed oracle iteration at chunk C over a fresh prefill sequence
+    holding `prefix` seeded cached tokens, beside the shared decodes."""
     from paper_2609_07883_amd import synth
     k2 = kv.copy()
-    k2.seqs[1] = OL.SeqCache(np.zeros((0, shape.n_kv_heads, shape.head_dim)),
-                             np.zeros((0, shape.n_kv_heads, shape.head_dim)))
-    b = OL.MixedBatch(C, 1, 0, list(range(100, 100 + len(ctx_lens))), [int(x) for x in ctx_lens])
+    if prefix:
+        kb, vb = synth.cached_kv(prefix, shape.n_kv_heads, shape.head_dim, 3, 0, 1)
+        k2.seqs[1] = OL.SeqCache(synth.bf16_to_f64(kb), synth.bf16_to_f64(vb))
+    else:
+        k2.seqs[1] = OL.SeqCache(np.zeros((0, shape.n_kv_heads, shape.head_dim)),
+                                 np.zeros((0, shape.n_kv_heads, shape.head_dim)))
+    b = OL.MixedBatch(C, 1, prefix, list(range(100, 100 + len(ctx_lens))), [int(x) for x in ctx_lens])
     x = synth.bf16_to_f64(synth.embeddings(C + len(ctx_lens), shape.d_model, seed=1, stream=C))
     t0 = time.perf_counter()
     OL.mixed_iteration(sh, w, x, k2, b)
@@ -249,14 +281,14 @@ def main():
     ctx = sess.ctx
     # pre-existing contexts: seeded N(0,1) bf16 K/V
     pre = 1
+    dec = list(range(100, 100 + max_b))
     ctx.seq_create(pre)
-    ctx.seq_reserve(pre, pre_len)
+    for sid in dec:
+        ctx.seq_create(sid)
+    reserve_round_robin(ctx, {pre: pre_len, **{sid: int(L) + 1 for sid, L in zip(dec, ctx_lens)}})
     kb, vb = synth.cached_kv(pre_len, shape.n_kv_heads, shape.head_dim, 3, 0, pre)
     sess.write_kv(0, pre, kb, vb)
-    dec = list(range(100, 100 + max_b))
     for sid, L in zip(dec, ctx_lens):
-        ctx.seq_create(sid)
-        ctx.seq_reserve(sid, int(L) + 1)
         kb, vb = synth.cached_kv(int(L), shape.n_kv_heads, shape.head_dim, 3, 0, sid)
         sess.write_kv(0, sid, kb, vb)
     x = synth.embeddings(sess.x_in.shape[0], shape.d_model, seed=1, stream=0)
@@ -297,56 +329,80 @@ def main():
     stage_ms = [ctx.stage_times(ago) for ago in range(n_iter)][::-1]  # oldest first
     ctx.set_stage_timing(0)
 
+    # timed region 3 (flushed): every iteration preceded by a 1 GiB read
+    # sweep that evicts the last-level cache without dirtying it, per-stage
+    # events as in region 2; the flush runs outside the iteration's events
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    ctx.set_stage_timing(n_iter)
+    torch.cuda.synchronize()
+    for _ in range(args.steps):
+        for b in batches:
+            api.flush_cache(flush.data_ptr(), flush.numel(), stream)
+            ctx.mixed_iteration(b, sess.x_in.data_ptr(), sess.x_out.data_ptr(), sess.ws.data_ptr(),
+                                sess.ws_bytes, stream)
+    torch.cuda.synchronize()
+    stage_ms_flushed = [ctx.stage_times(ago) for ago in range(n_iter)][::-1]
+    ctx.set_stage_timing(0)
+    del flush
+
     rows_per_step = sum(C + B for C, _, B in points)
     tokens_s = rows_per_step * args.steps / elapsed
     ms_per_step = elapsed * 1e3 / args.steps
 
-    # per-point iteration ms (sum of stage events) and per-stage totals
-    per_point = []
-    stage_tot = {s: 0.0 for s in api.STAGES}
-    stage_roof = {s: 0.0 for s in api.STAGES}
-    stage_flops = {s: 0.0 for s in api.STAGES}
-    stage_bytes = {s: 0.0 for s in api.STAGES}
-    for i, st in enumerate(stage_ms):
-        C, P, B = points[i % len(points)]
-        work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
+    def analyse(stage_ms):
+        """Per-point iteration ms (sum of stage events, median over steps),
+        per-stage totals and rates, and the roofline entry of the dominant stage."""
+        per_point = []
+        stage_tot = {s: 0.0 for s in api.STAGES}
+        stage_roof = {s: 0.0 for s in api.STAGES}
+        stage_flops = {s: 0.0 for s in api.STAGES}
+        stage_bytes = {s: 0.0 for s in api.STAGES}
+        for i, st in enumerate(stage_ms):
+            C, P, B = points[i % len(points)]
+            work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
+            for s in api.STAGES:
+                stage_tot[s] += st[s]
+                f, b = work[s]
+                stage_flops[s] += f
+                stage_bytes[s] += b
+                stage_roof[s] += roof_time(f, b) * 1e3
+        for j, (C, P, B) in enumerate(points):
+            its = [stage_ms[k] for k in range(j, n_iter, len(points))]
+            ms = float(np.median([sum(st.values()) for st in its]))
+            work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
+            roof = sum(roof_time(*work[s]) for s in api.STAGES) * 1e3
+            per_point.append({"C": C, "P": P, "B": B, "ms": round(ms, 4),
+                              "tokens_s": round((C + B) / ms * 1e3, 1),
+                              "roofline_frac": round(roof / ms, 3)})
+        kernels = {}
         for s in api.STAGES:
-            stage_tot[s] += st[s]
-            f, b = work[s]
-            stage_flops[s] += f
-            stage_bytes[s] += b
-            stage_roof[s] += roof_time(f, b) * 1e3
-    for j, (C, P, B) in enumerate(points):
-        its = [stage_ms[k] for k in range(j, n_iter, len(points))]
-        ms = float(np.median([sum(st.values()) for st in its]))
-        work = stage_work(shape, C, P, B, int(np.sum(ctx_lens[:B] + 1)))
-        roof = sum(roof_time(*work[s]) for s in api.STAGES) * 1e3
-        per_point.append({"C": C, "P": P, "B": B, "ms": round(ms, 4),
-                          "tokens_s": round((C + B) / ms * 1e3, 1),
-                          "roofline_frac": round(roof / ms, 3)})
-    kernels = {}
-    for s in api.STAGES:
-        t = stage_tot[s] / 1e3
-        if t <= 0:
-            continue
-        kernels[s] = {"ms_total": round(stage_tot[s], 4),
-                      "tflops": round(stage_flops[s] / t / 1e12, 2),
-                      "gbps": round(stage_bytes[s] / t / 1e9, 1),
-                      "roofline_frac": round(stage_roof[s] / stage_tot[s], 3)}
-    dom = max(kernels, key=lambda s: kernels[s]["ms_total"])
-    t_dom = stage_tot[dom] / 1e3
-    mfma_time = stage_flops[dom] / PEAK_BF16
-    hbm_time = stage_bytes[dom] / PEAK_HBM
-    if mfma_time >= hbm_time:
-        roofline = {"kernel": dom, "bound": "mfma", "achieved": round(stage_flops[dom] / t_dom / 1e12, 2),
+            t = stage_tot[s] / 1e3
+            if t <= 0:
+                continue
+            kernels[s] = {"ms_total": round(stage_tot[s], 4),
+                          "tflops": round(stage_flops[s] / t / 1e12, 2),
+                          "gbps": round(stage_bytes[s] / t / 1e9, 1),
+                          "roofline_frac": round(stage_roof[s] / stage_tot[s], 3)}
+        dom = max(kernels, key=lambda s: kernels[s]["ms_total"])
+        t_dom = stage_tot[dom] / 1e3
+        if stage_flops[dom] / PEAK_BF16 >= stage_bytes[dom] / PEAK_HBM:
+            roof = {"kernel": dom, "bound": "mfma", "achieved": round(stage_flops[dom] / t_dom / 1e12, 2),
                     "peak": 2500.0, "unit": "TFLOP/s"}
-    else:
-        roofline = {"kernel": dom, "bound": "hbm", "achieved": round(stage_bytes[dom] / t_dom / 1e9, 1),
+        else:
+            roof = {"kernel": dom, "bound": "hbm", "achieved": round(stage_bytes[dom] / t_dom / 1e9, 1),
                     "peak": 8000.0, "unit": "GB/s"}
-    roofline["frac"] = round(roofline["achieved"] / roofline["peak"], 4)
-    roofline["traffic"] = measured_traffic(dom, args.workload)
-    roofline["launches"] = n_iter
-    roofline["avg_launch_us"] = round(t_dom / n_iter * 1e6, 2)
+        roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+        roof["traffic"] = measured_traffic(dom, args.workload)
+        roof["launches"] = n_iter
+        roof["avg_launch_us"] = round(t_dom / n_iter * 1e6, 2)
+        return per_point, kernels, roof, sum(stage_tot.values())
+
+    per_point, kernels, roofline_unflushed, kern_ms = analyse(stage_ms)
+    per_point_fl, kernels_fl, roofline, kern_ms_fl = analyse(stage_ms_flushed)
+    roofline["timing"] = ("per-stage HIP events on the iteration stream, each iteration preceded by a 1 GiB "
+                          "read sweep of the last-level cache")
+    flushed = {"per_point": per_point_fl, "kernels": kernels_fl, "kernel_ms_per_step": round(kern_ms_fl / args.steps, 4),
+               "tokens_s_kernel_time": round(rows_per_step * args.steps / kern_ms_fl * 1e3, 1)}
     log(f"{args.workload}: timed {args.steps} steps x {len(points)} iterations: {elapsed * 1e3:.1f} ms, "
         f"{tokens_s:.0f} tokens/s")
 
@@ -391,13 +447,13 @@ def main():
     out = {"metric": METRIC, "value": round(tokens_s, 1), "unit": "tokens/s", "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
            "instrumented_ms_per_step": round(elapsed_ev * 1e3 / args.steps, 4),
-           "kernel_ms_per_step": round(sum(stage_tot.values()) / args.steps, 4),
+           "kernel_ms_per_step": round(kern_ms / args.steps, 4),
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
            "config": {"workload": WORKLOADS[args.workload], "block_size": 16,
                       "seeds": {"weights": 0, "embeddings": 1, "contexts": 2, "kv": 3}},
-           "roofline": roofline, "cpu_baseline": cpu, "sweep": per_point, "kernels": kernels,
-           "cost_table": table}
+           "roofline": roofline, "roofline_unflushed": roofline_unflushed, "cpu_baseline": cpu,
+           "sweep": per_point, "kernels": kernels, "flushed": flushed, "cost_table": table}
     print(json.dumps(out))
 
 

@@ -346,6 +346,15 @@ int slw_cost_table_monotone(const slw_cost_table* t, int32_t* violations, int64_
 int slw_cost_table_save(const slw_cost_table* t, const char* path);
 int slw_cost_table_load(const char* path, slw_cost_table** out);
 
+/*
+ * Read `bytes` of the device buffer `buf` on `stream` (asynchronous): the
+ * last-level cache sweep the profiler runs before every timed repeat (it
+ * evicts cached weights and K/V without leaving dirty lines behind; only
+ * the buffer's first word may be overwritten), for callers that time
+ * iterations from a cold cache themselves.  buf is 16-byte aligned.
+ */
+int slw_flush_cache(void* buf, size_t bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Controller (Eq. 1 by the binary search of Alg. 1, margin of Sec. 3.3)    */
 /* ------------------------------------------------------------------------ */

@@ -1,13 +1,15 @@
 // Paged attention on gfx950 matrix cores (v_mfma_f32_16x16x32_bf16).
 //
-// Both kernels compute transposed scores S^T = K Q^T: K (16 tokens of a page)
-// is the A operand and Q^T the B operand, so lane l holds, for query (or
-// head) l % 16, the scores of tokens 4 (l / 16) .. 4 (l / 16) + 3 of the page.
-// Those four scores from two pages are exactly the eight k-values lane l must
-// supply as the A operand (P) of the P V product, whose k index runs over the
-// same tokens; the V operand reads the matching tokens of one head dimension,
-// which are contiguous in the dim-major V page.  The softmax is online
-// (running max and sum per query, base-2 exponentials) in fp32.
+// Both kernels compute transposed scores S^T = K Q^T: 16 keys are the A
+// operand and Q^T the B operand, so lane l holds, for query (or head)
+// l % 16, the scores of rows 4 (l / 16) .. 4 (l / 16) + 3 of the key tile.
+// Two such tiles over a pair of pages take their keys in an order that
+// leaves lane group g with keys 8 g .. 8 g + 7 of the pair (pair_key below):
+// exactly the eight k-values lane l must supply as the A operand (P) of the
+// P V product, whose k index runs over the same keys, and eight consecutive
+// tokens of one page, so the V operand is one 16-byte piece of the
+// dim-major V page.  The softmax is online (running max and sum per query,
+// base-2 exponentials) in fp32.
 //
 // Page layouts (one (layer, block, kv head) page of 16 tokens):
 //   K: [hd/32][16][32]  element (t, d) at (d/32)*512 + t*32 + d%32
@@ -32,6 +34,10 @@ constexpr int kChunkStages = 2;
 // instruction, five more VALU operations per call.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Block tables read through the scalar cache: a wave-uniform index into
+// constant-address-space memory.
+typedef const int32_t __attribute__((address_space(4))) const_i32;
+
 // Max and sum over lanes l, l ^ 16, l ^ 32 and l ^ 48 (the four 16-lane rows
 // of a wave), with the gfx950 row-swap instructions instead of LDS permutes:
 // a swap of a register with itself leaves, in every lane, its own value in
@@ -47,10 +53,6 @@ __device__ __forceinline__ float rows4_sum(float x) {
     x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
     const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
-__device__ __forceinline__ bf16x8 cat44(bf16x4 lo, bf16x4 hi) {
-    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
 __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
@@ -172,7 +174,6 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // Block-table entries are read through the scalar cache (a uniform index
     // into constant memory): a vector load here would make the compiler wait
     // for every direct load in flight before using its result.
-    typedef const int32_t __attribute__((address_space(4))) const_i32;
     const const_i32* bt_s = (const const_i32*)a.bt;
     const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
     for (int item = i0; item < i1; ++item) {
@@ -445,37 +446,48 @@ __device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int pos,
 // taken 32 at a time (two pages) straight from the pages into MFMA operand
 // registers, with the next step's pages requested before the current step is
 // multiplied (two register sets), so every wave keeps 16 KB of loads in
-// flight while it computes.
+// flight while it computes.  The two score tiles of a step take their keys
+// in the pair_key order of chunk attention: lane group g then holds the
+// scores of keys 8 g .. 8 g + 7, eight consecutive tokens of one page, and
+// its V operand of the P V product is one 16-byte piece of the dim-major V
+// page.
 // ---------------------------------------------------------------------------
 template <int HD>
 struct DecodeStep {
-    bf16x8 k[2][HD / 32];
-    bf16x4 v[2][HD / 16];
+    bf16x8 k[2][HD / 32];  // [score tile][32-dim slab]
+    bf16x8 v[HD / 16];     // [16-dim output tile]
 };
+
+// The loads of one step.  The two block-table entries of the pair come
+// through the scalar cache (bt_s is wave-uniform): a vector load there would
+// make the wave wait for every load in flight, the previous step's prefetch
+// included, before it could address the next pages.  Pages past the split's
+// last page load that page instead, so every load is unconditional and the
+// waits can count; keys at or past tok1 are masked (scores) and zeroed (V)
+// by the caller.
 
 template <int HD>
 __device__ __forceinline__ void decode_load(DecodeStep<HD>& st, const bf16* kpool, const bf16* vpool,
-                                            const int* bt, int c0, int tok1, int hkv, int kvh, int col,
+                                            const const_i32* bt_s, int c0, int last_pg, int hkv, int kvh, int col,
                                             int grp) {
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
+    const int pg0 = c0 >> 4;
+    const int b0 = bt_s[min(pg0, last_pg)], b1 = bt_s[min(pg0 + 1, last_pg)];
+    // K: row `col` of score tile tau is key pair_key(col, tau) of the 32-key pair
+    const size_t kpage = (static_cast<size_t>((col >> 3) ? b1 : b0) * hkv + kvh) * PAGE;
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        const int pg = (c0 >> 4) + p;
-        if (pg * 16 < tok1) {
-            const size_t page = (static_cast<size_t>(bt[pg]) * hkv + kvh) * PAGE;
+    for (int tau = 0; tau < 2; ++tau) {
+        const int tok = pair_key(col, tau) & 15;
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk)
-                st.k[p][kk] = *reinterpret_cast<const bf16x8*>(kpool + page + kk * 512 + col * 32 + grp * 8);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                st.v[p][nt] = *reinterpret_cast<const bf16x4*>(vpool + page + (nt * 16 + col) * 16 + grp * 4);
-        } else {
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) st.k[p][kk] = bf16x8{};
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) st.v[p][nt] = bf16x4{};
-        }
+        for (int kk = 0; kk < KK; ++kk)
+            st.k[tau][kk] = *reinterpret_cast<const bf16x8*>(kpool + kpage + kk * 512 + tok * 32 + grp * 8);
     }
+    // V: lane group grp covers keys 8 grp .. 8 grp + 7 of the pair, tokens
+    // 8 (grp % 2) .. + 7 of page grp / 2, for dim nt * 16 + col
+    const size_t vpage = (static_cast<size_t>((grp >> 1) ? b1 : b0) * hkv + kvh) * PAGE;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+        st.v[nt] = *reinterpret_cast<const bf16x8*>(vpool + vpage + (nt * 16 + col) * 16 + 8 * (grp & 1));
 }
 
 template <int HD>
@@ -489,7 +501,8 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
     const int kv_len = a.kv_len[b];
     const int tok0 = split * a.split_tokens;
     const int tok1 = min(tok0 + a.split_tokens, kv_len);
-    const int* bt = a.bt + a.bt_off[b];
+    const int last_pg = (tok1 - 1) >> 4;
+    const const_i32* bt_s = (const const_i32*)(a.bt + a.bt_off[b]);
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
 
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
@@ -510,32 +523,36 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
     for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{};
     float m_run = -INFINITY, l_run = 0.f;
 
+    // lane (grp, col): element e of score tile tau is key 8 grp + 4 tau + e of
+    // the step.  Keys at or past tok1 (the split's end; stand-in pages and
+    // unwritten slots lie there) get score -inf and V 0, without branches: a
+    // branch that rewrites loaded registers makes the compiler's wait counts
+    // conservative and stalls on the prefetch in flight.
     auto compute = [&](DecodeStep<HD>& st, int c0) {
-        const bool tail = c0 + 32 > tok1;
-        if (tail) {  // zero V of keys past the split (possibly unwritten slots)
+        const int nv = min(max(tok1 - c0 - 8 * grp, 0), 8);  // valid keys of this lane group
+        u32x4 vmask;
 #pragma unroll
-            for (int p = 0; p < 2; ++p)
+        for (int j = 0; j < 4; ++j)
+            vmask[j] = (2 * j < nv ? 0x0000FFFFu : 0u) | (2 * j + 1 < nv ? 0xFFFF0000u : 0u);
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (c0 + p * 16 + grp * 4 + e >= tok1)
-#pragma unroll
-                        for (int nt = 0; nt < NT; ++nt) st.v[p][nt][e] = bf16(0.0f);
+        for (int nt = 0; nt < NT; ++nt) {
+            u32x4 bits = __builtin_bit_cast(u32x4, st.v[nt]) & vmask;
+            st.v[nt] = __builtin_bit_cast(bf16x8, bits);
         }
         f32x4 s[2];
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            s[p] = f32x4{};
+        for (int tau = 0; tau < 2; ++tau) {
+            s[tau] = f32x4{};
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) s[p] = mfma16(st.k[p][kk], qf[kk], s[p]);
+            for (int kk = 0; kk < KK; ++kk) s[tau] = mfma16(st.k[tau][kk], qf[kk], s[tau]);
         }
         float mx = -INFINITY;
 #pragma unroll
-        for (int p = 0; p < 2; ++p)
+        for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                float x = s[p][e];
-                if (tail && c0 + p * 16 + grp * 4 + e >= tok1) x = -INFINITY;
-                s[p][e] = x;
+                const float x = 4 * tau + e < nv ? s[tau][e] : -INFINITY;
+                s[tau][e] = x;
                 mx = fmaxf(mx, x);
             }
         mx = rows4_max(mx);
@@ -555,27 +572,32 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
         const float m_use = m_run == -INFINITY ? 0.f : m_run;
         float ls = 0.f;
 #pragma unroll
-        for (int p = 0; p < 2; ++p)
+        for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float v = fast_exp2(fmaf(s[p][e], sl2, -m_use));
-                s[p][e] = v;
+                const float v = fast_exp2(fmaf(s[tau][e], sl2, -m_use));
+                s[tau][e] = v;
                 ls += v;
             }
         l_run += ls;
-        const bf16x8 pf = to_bf16x8(s[0], s[1]);
+        const bf16x8 pf = to_bf16x8(s[0], s[1]);  // keys 8 grp .. 8 grp + 7 in order
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, cat44(st.v[0][nt], st.v[1][nt]), o[nt]);
+        for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, st.v[nt], o[nt]);
     };
 
+    // The next step's loads are issued before every step's compute, also
+    // past the split's end (they then re-read its last page, still in L2):
+    // no branch skips a load, so the compiler's counted waits leave the
+    // prefetched step in flight while the current one is multiplied.
     DecodeStep<HD> sa, sb;
-    decode_load<HD>(sa, kpool, vpool, bt, tok0, tok1, a.hkv, kvh, col, grp);
-    for (int c0 = tok0; c0 < tok1; c0 += 64) {
-        if (c0 + 32 < tok1) decode_load<HD>(sb, kpool, vpool, bt, c0 + 32, tok1, a.hkv, kvh, col, grp);
+    decode_load<HD>(sa, kpool, vpool, bt_s, tok0, last_pg, a.hkv, kvh, col, grp);
+    for (int c0 = tok0;; c0 += 64) {
+        decode_load<HD>(sb, kpool, vpool, bt_s, c0 + 32, last_pg, a.hkv, kvh, col, grp);
         compute(sa, c0);
         if (c0 + 32 >= tok1) break;
-        if (c0 + 64 < tok1) decode_load<HD>(sa, kpool, vpool, bt, c0 + 64, tok1, a.hkv, kvh, col, grp);
+        decode_load<HD>(sa, kpool, vpool, bt_s, c0 + 64, last_pg, a.hkv, kvh, col, grp);
         compute(sb, c0 + 32);
+        if (c0 + 64 >= tok1) break;
     }
 
     float l = l_run;

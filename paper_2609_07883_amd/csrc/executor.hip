@@ -796,6 +796,16 @@ extern "C" int slw_mixed_iteration_static(slw_ctx* ctx, const slw_batch* batch, 
     });
 }
 
+extern "C" int slw_flush_cache(void* buf, size_t bytes, void* stream) {
+    return guarded([&] {
+        if (!buf && bytes) return fail(SLW_EINVAL, "null buffer");
+        if (reinterpret_cast<uintptr_t>(buf) % 16) return fail(SLW_EINVAL, "buffer must be 16-byte aligned");
+        launch_cache_sweep(buf, bytes, 0x9e3779b9u, static_cast<hipStream_t>(stream));
+        HIP_TRY(hipGetLastError());
+        return SLW_OK;
+    });
+}
+
 extern "C" int slw_set_stage_timing(slw_ctx* ctx, int32_t depth) {
     return guarded([&] {
         if (!ctx) return fail(SLW_EINVAL, "null context");
