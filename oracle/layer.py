@@ -167,7 +167,9 @@ class MixedBatch:
     Rows 0..C-1 are the prefill chunk of ``prefill_seq`` at positions
     prefix_len..prefix_len+C-1; rows C..C+B-1 are one decode token each for
     ``decode_seqs[b]`` at position ``context_lens[b]`` (tokens cached before
-    this iteration).
+    this iteration).  With prefill batching (Sec. 3.3) ``prefills`` lists
+    several (sequence, prefix, chunk) triples instead: the chunk rows are
+    those of each triple in turn and ``chunk`` is their total.
     """
 
     chunk: int
@@ -175,15 +177,25 @@ class MixedBatch:
     prefix_len: int
     decode_seqs: list
     context_lens: list
+    prefills: list | None = None
+
+    @property
+    def prefill_list(self):
+        """The (sequence, prefix, chunk) triples whose rows come first."""
+        if self.prefills is not None:
+            return [tuple(p) for p in self.prefills if p[2] > 0]
+        return [(self.prefill_seq, self.prefix_len, self.chunk)] if self.chunk > 0 else []
 
     @property
     def rows(self) -> int:
         return self.chunk + len(self.decode_seqs)
 
     def row_seq_pos(self):
-        seqs = [self.prefill_seq] * self.chunk + list(self.decode_seqs)
-        pos = [self.prefix_len + j for j in range(self.chunk)] + list(self.context_lens)
-        return seqs, pos
+        seqs, pos = [], []
+        for sid, p0, c in self.prefill_list:
+            seqs += [sid] * c
+            pos += list(range(p0, p0 + c))
+        return seqs + list(self.decode_seqs), pos + list(self.context_lens)
 
 
 def qkv_rope(shape: LayerShape, w: LayerWeights, x: np.ndarray, pos):
@@ -250,17 +262,20 @@ def mixed_iteration(shape: LayerShape, w: LayerWeights, x: np.ndarray,
     m = batch.rows
     assert x.shape == (m, shape.d_model)
     seqs, pos = batch.row_seq_pos()
-    if len(set(batch.decode_seqs)) != len(batch.decode_seqs) or (
-            batch.chunk > 0 and batch.prefill_seq in batch.decode_seqs):
+    pre = batch.prefill_list
+    if sum(c for _, _, c in pre) != batch.chunk:
+        raise ValueError("the prefills' chunks must add up to the chunk rows")
+    listed = [sid for sid, _, _ in pre] + list(batch.decode_seqs)
+    if len(set(listed)) != len(listed):
         raise ValueError("a sequence may appear at most once per iteration")
     for s, p in zip(batch.decode_seqs, batch.context_lens):
         have = kv.seqs[s].length if s in kv.seqs else 0
         if have != p:
             raise ValueError(f"decode seq {s}: context_len {p} but {have} cached")
-    if batch.chunk > 0:
-        have = kv.seqs[batch.prefill_seq].length if batch.prefill_seq in kv.seqs else 0
-        if have != batch.prefix_len:
-            raise ValueError(f"prefill seq: prefix_len {batch.prefix_len} but {have} cached")
+    for sid, p0, _ in pre:
+        have = kv.seqs[sid].length if sid in kv.seqs else 0
+        if have != p0:
+            raise ValueError(f"prefill seq {sid}: prefix_len {p0} but {have} cached")
 
     q, k, v = qkv_rope(shape, w, x, pos)
     append_kv(shape, kv, seqs, pos, k, v)

@@ -11,8 +11,8 @@ allocation order, so this takes the following reading:
   block first;
 * a reservation that the free pool cannot cover fails and changes nothing;
   a group of reservations made for one iteration is all-or-nothing, taken
-  in the order given (the prefill sequence first, then the decodes in batch
-  order);
+  in the order given (the prefill sequences first, in the order their rows
+  come, then the decodes in batch order);
 * freeing a sequence returns all its blocks to the pool.
 
 The slot of position p of a sequence is bt[p // bs] * bs + p % bs.
@@ -96,23 +96,28 @@ class BlockManager:
 
 
 def iteration_metadata(mgr: BlockManager, chunk: int, prefill_seq: int, prefix_len: int,
-                       decode_seqs, context_lens):
+                       decode_seqs, context_lens, prefills=None):
     """Reservations and slot mapping of one mixed iteration.
 
-    Reserves the prefill sequence up to prefix_len + chunk (if chunk > 0) and
-    each decode b up to context_lens[b] + 1, then returns the slot of every
-    row (chunk rows first) and each participating sequence's block table.
+    Reserves the prefill sequence up to prefix_len + chunk (if chunk > 0), or
+    with prefill batching each (sequence, prefix, chunk) of ``prefills`` in
+    turn up to prefix + chunk, then each decode b up to context_lens[b] + 1;
+    returns the slot of every row (chunk rows first, in prefill order) and
+    each participating sequence's block table.
     """
-    req = []
-    if chunk > 0:
-        req.append((prefill_seq, prefix_len + chunk))
+    if prefills is None:
+        prefills = [(prefill_seq, prefix_len, chunk)]
+    prefills = [(s, p, c) for s, p, c in prefills if c > 0]
+    req = [(s, p + c) for s, p, c in prefills]
     req += [(s, L + 1) for s, L in zip(decode_seqs, context_lens)]
     mgr.reserve_many(req)
-    slots = [mgr.slot(prefill_seq, prefix_len + j) for j in range(chunk)]
+    slots = []
+    for s, p, c in prefills:
+        slots += [mgr.slot(s, p + j) for j in range(c)]
     slots += [mgr.slot(s, L) for s, L in zip(decode_seqs, context_lens)]
     tables = {}
-    if chunk > 0:
-        tables[prefill_seq] = mgr.block_table(prefill_seq)
+    for s, _, _ in prefills:
+        tables[s] = mgr.block_table(s)
     for s in decode_seqs:
         tables[s] = mgr.block_table(s)
     return slots, tables

@@ -323,3 +323,39 @@ def test_stack_matches_stacked_transformers_layers():
         assert np.max(np.abs(c.v - v_ref)) <= 1e-6 * np.max(np.abs(v_ref))
     # the layers differ: a stack that reused one layer's weights would not match
     assert np.max(np.abs(hf_kv[0][0] - hf_kv[1][0])) > 0.1 * np.max(np.abs(hf_kv[0][0]))
+
+
+def test_prefill_batching_equals_each_prompt_alone():
+    """Several prompts' chunks in one iteration (Sec. 3.3 prefill batching)
+    give every row the output and K/V it gets when its prompt runs alone:
+    rows of different sequences do not interact."""
+    model = TINY_GQA
+    w = oracle_weights(synth.layer_weights(model, weight_seed=7, qk_std=0.16))
+    shape = oracle_shape(model)
+    base = L.KVState()
+    # sequence 1 holds 30 tokens, 3 holds 17, decode 9 holds 40; sequence 2 is new
+    for sid, n, st in ((1, 30, 21), (3, 17, 22), (9, 40, 23)):
+        b = L.MixedBatch(chunk=n, prefill_seq=sid, prefix_len=0, decode_seqs=[], context_lens=[])
+        L.mixed_iteration(shape, w, x_rows(n, model.d_model, stream=st), base, b)
+    pre = [(1, 30, 25), (2, 0, 40), (3, 17, 9)]
+    x = x_rows(75, model.d_model, stream=24)
+    xd = x_rows(1, model.d_model, stream=25)
+    kv = base.copy()
+    batch = L.MixedBatch(chunk=74, prefill_seq=-1, prefix_len=0, decode_seqs=[9], context_lens=[40], prefills=pre)
+    y = L.mixed_iteration(shape, w, np.concatenate([x[:74], xd]), kv, batch)
+    r0 = 0
+    scale = np.max(np.abs(y))
+    for sid, p0, c in pre:
+        alone = base.copy()
+        b = L.MixedBatch(chunk=c, prefill_seq=sid, prefix_len=p0, decode_seqs=[], context_lens=[])
+        ya = L.mixed_iteration(shape, w, x[r0:r0 + c], alone, b)
+        np.testing.assert_allclose(y[r0:r0 + c], ya, rtol=0, atol=1e-12 * scale)
+        np.testing.assert_allclose(kv.seqs[sid].k, alone.seqs[sid].k, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(kv.seqs[sid].v, alone.seqs[sid].v, rtol=0, atol=1e-12)
+        r0 += c
+    alone = base.copy()
+    yd = L.mixed_iteration(shape, w, xd, alone, L.MixedBatch(0, -1, 0, [9], [40]))
+    np.testing.assert_allclose(y[74:], yd, rtol=0, atol=1e-12 * scale)
+    with pytest.raises(ValueError):      # a sequence listed twice
+        L.mixed_iteration(shape, w, x[:20], base.copy(),
+                          L.MixedBatch(20, -1, 0, [], [], prefills=[(1, 30, 10), (1, 40, 10)]))

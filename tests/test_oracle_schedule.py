@@ -291,3 +291,27 @@ def test_table_statistics_match_hand_worked_golden():
     # with a context axis every plane is scanned: two copies double the count
     t2 = S.CostTable(g["c_grid"], g["b_grid"], [samples, samples], p_grid=[0, 4096])
     assert t2.monotone_violations() == (2 * g["violations"][0], g["violations"][1])
+
+
+def test_iteration_metadata_with_several_prefills_by_hand():
+    """Prefill batching (Sec. 3.3): the prefills' reservations come first, in
+    the order of their rows, then the decodes; slots worked out by hand on a
+    fresh pool of 20 blocks of 16 positions."""
+    mgr = paging.BlockManager(20, 16)
+    for sid in (1, 2, 3):
+        mgr.create(sid)
+    # seq 1: positions 0..19 -> blocks 0, 1; seq 2: 0..4 -> block 2; decode 3 at 0 -> block 3
+    slots, tables = paging.iteration_metadata(mgr, 25, -1, 0, [3], [0], prefills=[(1, 0, 20), (2, 0, 5)])
+    assert slots == list(range(0, 20)) + [32, 33, 34, 35, 36] + [48]
+    assert tables == {1: [0, 1], 2: [2], 3: [3]}
+    # seq 2: positions 5..16 -> block 2 then a new block 4; seq 1: position 20 in block 1
+    slots, tables = paging.iteration_metadata(mgr, 13, -1, 0, [], [], prefills=[(2, 5, 12), (1, 20, 1)])
+    assert slots == list(range(37, 48)) + [64] + [20]
+    assert tables == {2: [2, 4], 1: [0, 1]}
+    # one prefill given either way is the same iteration
+    m1, m2 = paging.BlockManager(8, 16), paging.BlockManager(8, 16)
+    for m in (m1, m2):
+        m.create(5)
+    a = paging.iteration_metadata(m1, 17, 5, 0, [], [])
+    b = paging.iteration_metadata(m2, 17, -1, 0, [], [], prefills=[(5, 0, 17)])
+    assert a == b
