@@ -151,7 +151,15 @@ int slw_seq_block_table(slw_ctx* ctx, int64_t id, int32_t* out, int32_t cap, int
  *   context_lens  [B] tokens cached for each decode BEFORE this iteration; the
  *                 decode token sits at position context_lens[b] and attends to
  *                 context_lens[b] + 1 keys
+ * Prefill batching (Sec. 3.3: several pending prompts in one iteration):
+ *   n_prefill     > 1: the C chunk rows come from n_prefill prompts (at most
+ *                 SLW_MAX_PREFILLS), prompt i's chunk_lens[i] >= 1 rows after
+ *                 those of prompts 0 .. i-1, at positions prefix_lens[i] ..
+ *                 prefix_lens[i] + chunk_lens[i] - 1 of prefill_seqs[i]; the
+ *                 chunk_lens add up to C and prefill_seq / prefix_len are
+ *                 ignored.  0 or 1: one prefill as above (the arrays are ignored).
  */
+#define SLW_MAX_PREFILLS 16
 typedef struct slw_batch {
     int32_t C;
     int64_t prefill_seq;
@@ -159,6 +167,10 @@ typedef struct slw_batch {
     int32_t B;
     const int64_t* decode_seqs;
     const int32_t* context_lens;
+    int32_t n_prefill;
+    const int64_t* prefill_seqs;
+    const int32_t* prefix_lens;
+    const int32_t* chunk_lens;
 } slw_batch;
 
 /*
@@ -172,8 +184,8 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  *   x_in   device bf16 [C + B][d]: chunk rows first, then decode rows
  *   x_out  device bf16 [C + B][d]; may equal x_in
  *   ws     device workspace of ws_bytes >= slw_workspace_size(ctx, C, B)
- * Reserves KV room (prefill_seq up to prefix_len + C, each decode up to
- * context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
+ * Reserves KV room (each prefill sequence up to its prefix + chunk, in row
+ * order, then each decode up to context_lens[b] + 1; all or nothing, SLW_ENOMEM if the pool cannot cover
  * it; a call that fails after reserving returns the blocks), builds the slot mapping and block tables on the host, writes them to
  * a coherent pinned staging ring that a first kernel copies into the
  * workspace, then enqueues per layer: RMSNorm, QKV GEMM
@@ -472,11 +484,12 @@ typedef struct slw_serve_opts {
      * bounded deadline violation recorded as such.  0 = off. */
     int64_t aging_ns;
     int32_t aging_chunk;
-    /* Prefill batching by first fit (SLOWeave, virtual-clock executors only;
-     * SLW_EUNSUPPORTED with the GPU executor): when the head's chunk finishes
+    /* Prefill batching by first fit (SLOWeave; at most SLW_MAX_PREFILLS
+     * prompts on the GPU executor): when the head's chunk finishes
      * its prompt, the next pending prompts in queue order join while the
      * decode cap allows (counting prompts that finish earlier in the
-     * iteration), up to max_prefills prompts, each with the largest chunk c
+     * iteration) and, on the GPU, while the KV pool can hold each prompt
+     * that starts to its last token, up to max_prefills prompts, each with the largest chunk c
      * for which T_hat(n, S + c) still meets the budget, S being the tokens
      * already placed; a prompt that does not finish ends the list.  The
      * iteration is priced at the total.  0 or 1 = one prompt. */

@@ -64,7 +64,12 @@ class LayerWeightsC(C.Structure):
 class BatchC(C.Structure):
     _fields_ = [("C", C.c_int32), ("prefill_seq", C.c_int64), ("prefix_len", C.c_int32),
                 ("B", C.c_int32), ("decode_seqs", C.POINTER(C.c_int64)),
-                ("context_lens", C.POINTER(C.c_int32))]
+                ("context_lens", C.POINTER(C.c_int32)), ("n_prefill", C.c_int32),
+                ("prefill_seqs", C.POINTER(C.c_int64)), ("prefix_lens", C.POINTER(C.c_int32)),
+                ("chunk_lens", C.POINTER(C.c_int32))]
+
+
+MAX_PREFILLS = 16
 
 
 class ProfileOpts(C.Structure):
@@ -373,16 +378,38 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
 @dataclass(frozen=True)
 class Batch:
     """One iteration's batch.  Immutable: its C struct is built on first use
-    and reused by every later call with the same batch."""
+    and reused by every later call with the same batch.  ``prefills``
+    (prefill batching) lists (sequence, prefix, chunk) triples whose rows come
+    first, in that order; chunk is then their total and prefill_seq /
+    prefix_len are ignored."""
     chunk: int
     prefill_seq: int
     prefix_len: int
     decode_seqs: tuple
     context_lens: tuple
+    prefills: tuple | None = None
 
     def __post_init__(self):
         object.__setattr__(self, "decode_seqs", tuple(int(v) for v in self.decode_seqs))
         object.__setattr__(self, "context_lens", tuple(int(v) for v in self.context_lens))
+        if self.prefills is not None:
+            object.__setattr__(self, "prefills", tuple((int(s), int(p), int(c)) for s, p, c in self.prefills))
+
+    @classmethod
+    def batched(cls, prefills, decode_seqs=(), context_lens=()) -> "Batch":
+        """A batch of several prefills (sequence, prefix, chunk) next to decodes."""
+        prefills = [tuple(p) for p in prefills if p[2] > 0]
+        if len(prefills) == 1:
+            (s, p, c), = prefills
+            return cls(c, s, p, decode_seqs, context_lens)
+        return cls(sum(c for _, _, c in prefills), -1, 0, decode_seqs, context_lens, tuple(prefills))
+
+    @property
+    def prefill_list(self):
+        """The (sequence, prefix, chunk) triples of the chunk rows, in row order."""
+        if self.prefills is not None:
+            return list(self.prefills)
+        return [(self.prefill_seq, self.prefix_len, self.chunk)] if self.chunk > 0 else []
 
     @property
     def rows(self) -> int:
@@ -392,8 +419,13 @@ class Batch:
         c = self.__dict__.get("_c")
         if c is None:
             ds, cl = _i64(self.decode_seqs), _i32(self.context_lens)
+            pre = list(self.prefills) if self.prefills is not None else []
+            ps = _i64([p[0] for p in pre])
+            pp = _i32([p[1] for p in pre])
+            pc = _i32([p[2] for p in pre])
             c = (BatchC(self.chunk, self.prefill_seq, self.prefix_len, len(ds), _ptr(ds, C.c_int64),
-                        _ptr(cl, C.c_int32)), ds, cl)   # the arrays keep the pointers alive
+                        _ptr(cl, C.c_int32), len(pre), _ptr(ps, C.c_int64), _ptr(pp, C.c_int32),
+                        _ptr(pc, C.c_int32)), ds, cl, ps, pp, pc)   # the arrays keep the pointers alive
             object.__setattr__(self, "_c", c)
         return c[0]
 

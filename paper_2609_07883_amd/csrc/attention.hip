@@ -132,8 +132,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     static_assert(SLABS % 8 == 0, "tile loads must split evenly over the waves");
     static_assert(ST >= 2 && ST <= 4, "ring of two to four tiles");
     constexpr int CT = 2;                 // 16-row column tiles per wave (32 rows)
-    constexpr int PW = 32 / GROUP;        // positions per wave
-    constexpr int PWG = 8 * PW;           // positions per work-group (eight waves)
+    constexpr int PW = 32 / GROUP;        // positions per wave (eight waves: a tile of 8 PW positions)
     // Lazy rescaling: a row keeps its running max until a tile exceeds it by
     // 2^kSlack, so probabilities stay <= 2^kSlack and most tiles skip the
     // rescale of the output accumulators.
@@ -174,28 +173,30 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // Block-table entries are read through the scalar cache (a uniform index
     // into constant memory): a vector load here would make the compiler wait
     // for every direct load in flight before using its result.
-    const const_i32* bt_s = (const const_i32*)a.bt;
     const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
     for (int item = i0; item < i1; ++item) {
         const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
-        const int p0 = qt * PWG + wave * PW; // first chunk position of this wave
+        // the query tile: rows row0 .. row0 + nrows - 1 at positions pos0 .. of one sequence
+        const int row0 = a.qt_row0[qt], nrows = a.qt_rows[qt], pos0 = a.qt_pos0[qt];
+        const const_i32* bt_s = (const const_i32*)(a.bt + a.qt_bt[qt]);
+        const int j0 = wave * PW;            // first tile position of this wave
         const int n_tiles = (ke - kb + 63) / 64;
-        const int wave_qpos_lo = a.prefix + p0, wave_qpos_hi = a.prefix + p0 + PW - 1;
-        const bool wave_live = p0 < a.c;
+        const int wave_qpos_lo = pos0 + j0, wave_qpos_hi = pos0 + j0 + PW - 1;
+        const bool wave_live = j0 < nrows;
         // a query tile covered by one item is written here, else as a partial
         const bool whole = a.qt_off[qt + 1] - a.qt_off[qt] == 1;
 
-        // Q^T operand: row r = ct*16 + col is position p0 + r / GROUP, head kvh*GROUP + r % GROUP
+        // Q^T operand: row r = ct*16 + col is tile position j0 + r / GROUP, head kvh*GROUP + r % GROUP
         bf16x8 qf[CT][KK];
         const bf16* qkv = static_cast<const bf16*>(a.qkv);
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
-            const int r = ct * 16 + col, qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
+            const int r = ct * 16 + col, j = j0 + r / GROUP, h = kvh * GROUP + r % GROUP;
 #pragma unroll
             for (int kk = 0; kk < KK; ++kk)
-                qf[ct][kk] = qi < a.c ? *reinterpret_cast<const bf16x8*>(
-                                            qkv + static_cast<size_t>(qi) * a.ld_qkv + h * HD + kk * 32 + grp * 8)
-                                      : bf16x8{};
+                qf[ct][kk] = j < nrows ? *reinterpret_cast<const bf16x8*>(
+                                             qkv + static_cast<size_t>(row0 + j) * a.ld_qkv + h * HD + kk * 32 + grp * 8)
+                                       : bf16x8{};
         }
 
         const int last_page = (ke - 1) >> 4;
@@ -362,12 +363,13 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int r = ct * 16 + grp * 4 + e;
-                    const int qi = p0 + r / GROUP, h = kvh * GROUP + r % GROUP;
+                    const int j = j0 + r / GROUP, h = kvh * GROUP + r % GROUP;
                     const float inv = 1.0f / __shfl(l, grp * 4 + e, 64);
-                    if (qi < a.c) {
+                    if (j < nrows) {
 #pragma unroll
                         for (int nt = 0; nt < NT; ++nt)
-                            out[static_cast<size_t>(qi) * ldo + h * HD + nt * 16 + col] = f2bf(o[ct][nt][e] * inv);
+                            out[static_cast<size_t>(row0 + j) * ldo + h * HD + nt * 16 + col] =
+                                f2bf(o[ct][nt][e] * inv);
                     }
                 }
             }
@@ -425,18 +427,20 @@ __device__ __forceinline__ void merge_row(const float* __restrict__ ml, const fl
     for (int p = 0; p < PER; ++p) out[lane + 64 * p] = f2bf(acc[p] * inv);
 }
 
-// Combine the key-range partials of one (chunk position, q head).
+// Combine the key-range partials of one (tile position, q head): position x
+// of the flattened tiles is position x % PWG of query tile x / PWG.
 template <int HD, int GROUP>
-__device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int pos, int h) {
+__device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int x, int h) {
     constexpr int PWG = 256 / GROUP;
     const int kvh = h / GROUP;
-    const int qt = pos / PWG;
-    const int row = (pos % PWG) * GROUP + h % GROUP;
+    const int qt = x / PWG, j = x % PWG;
+    if (j >= a.qt_rows[qt]) return;  // past the tile's last row
+    const int row = j * GROUP + h % GROUP;
     const int w0 = a.qt_off[qt], w1 = a.qt_off[qt + 1];
     if (w1 - w0 == 1) return;  // written by the attention kernel
     merge_row<HD>(a.part_ml, a.part_o, (static_cast<size_t>(w0) * a.hkv + kvh) * 256 + row,
                   static_cast<size_t>(a.hkv) * 256, w1 - w0,
-                  static_cast<bf16*>(a.out) + static_cast<size_t>(pos) * a.hq * HD + h * HD);
+                  static_cast<bf16*>(a.out) + static_cast<size_t>(a.qt_row0[qt] + j) * a.hq * HD + h * HD);
 }
 
 // ---------------------------------------------------------------------------
@@ -626,9 +630,9 @@ __device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b,
 }
 
 // One launch for both merges of a layer: blocks x < chunk_rows combine the
-// partials of chunk position x (query tiles split over several items), the
-// rest those of decode x - chunk_rows; wave w of block (x, y) takes q head
-// y * WAVES + w.
+// partials of position x of the flattened query tiles (tiles split over
+// several items), the rest those of decode x - chunk_rows; wave w of block
+// (x, y) takes q head y * WAVES + w.
 template <int HD, int GROUP, int WAVES>
 __global__ __launch_bounds__(64 * WAVES) void attn_merge_kernel(ChunkAttnArgs ca, DecodeAttnArgs da,
                                                                 int chunk_rows) {
@@ -691,7 +695,8 @@ void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s) {
 }
 
 void launch_attention_merge(const ChunkAttnArgs* ca, const DecodeAttnArgs* da, hipStream_t s) {
-    const int chunk_rows = ca && ca->c > 0 && ca->split ? ca->c : 0;
+    // every position of every query tile (positions past a tile's rows return at once)
+    const int chunk_rows = ca && ca->c > 0 && ca->split ? ca->n_qt * chunk_tile_positions(ca->hq / ca->hkv) : 0;
     DecodeAttnArgs dd{};
     if (da && da->b > 0) dd = *da;
     if (chunk_rows + dd.b == 0) return;

@@ -43,6 +43,15 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
         if (e_ != hipSuccess) return fail(SLW_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
     } while (0)
 
+// One prefill of an iteration: `c` chunk rows from row `row0` on, at positions
+// prefix .. prefix + c - 1 of sequence `seq`.
+struct Prefill {
+    int64_t seq;
+    int32_t prefix;
+    int32_t c;
+    int32_t row0;
+};
+
 }  // namespace
 
 struct slw_ctx {
@@ -55,6 +64,7 @@ struct slw_ctx {
     bool kv_ready = false;
     std::vector<int32_t> last_slots;
     std::vector<int32_t> slots_build;  // slots of the iteration being built
+    std::vector<Prefill> prefills;     // the iteration's prefills in row order
     std::vector<int32_t> meta;  // host build area
     std::vector<int32_t> items; // chunk-attention work items (host build area)
 
@@ -112,8 +122,12 @@ int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
     return static_cast<int>(s);
 }
 
+// Query tiles of the chunk rows: each prefill's rows are tiled on their own,
+// so up to SLW_MAX_PREFILLS - 1 tiles more than one prefill of C rows needs.
 int chunk_tiles(const slw_model_cfg& c, int C) {
-    return static_cast<int>(ceil_div(C, chunk_tile_positions(c.n_q_heads / c.n_kv_heads)));
+    if (C <= 0) return 0;
+    return static_cast<int>(ceil_div(C, chunk_tile_positions(c.n_q_heads / c.n_kv_heads))) +
+           std::min(C, static_cast<int>(SLW_MAX_PREFILLS)) - 1;
 }
 int chunk_slot_cap(const slw_model_cfg& c) { return std::max(1, kChunkSlots / c.n_kv_heads); }
 int chunk_item_cap(const slw_model_cfg& c, int C) {
@@ -123,9 +137,10 @@ int chunk_item_cap(const slw_model_cfg& c, int C) {
 size_t meta_ints(const slw_model_cfg& c, int C, int B) {
     const int M = C + B;
     const size_t mb = static_cast<size_t>(max_blocks(c));
-    return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + mb +
+    const size_t np = C > 0 ? static_cast<size_t>(std::min(C, static_cast<int>(SLW_MAX_PREFILLS))) : 0;
+    return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + np * mb +
            2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + 3 * static_cast<size_t>(chunk_item_cap(c, C)) +
-           chunk_tiles(c, C) + 1 + chunk_slot_cap(c) + 1;
+           5 * static_cast<size_t>(chunk_tiles(c, C)) + 1 + chunk_slot_cap(c) + 1;
 }
 
 struct Layout {
@@ -253,7 +268,7 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
                          size_t ws_bytes, hipStream_t stream, bool no_alloc = false) {
     const slw_model_cfg& c = ctx->cfg;
     if (!bt) return fail(SLW_EINVAL, "null batch");
-    const int C = bt->C, B = bt->B, P = bt->prefix_len;
+    const int C = bt->C, B = bt->B;
     if (C < 0 || B < 0) return fail(SLW_EINVAL, "negative C or B");
     if (C == 0 && B == 0) {
         ctx->last_slots.clear();
@@ -265,26 +280,43 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
     if (!x_in || !x_out || !ws) return fail(SLW_EINVAL, "null device buffer");
     if (B > 0 && (!bt->decode_seqs || !bt->context_lens)) return fail(SLW_EINVAL, "null decode arrays");
 
-    // validation
+    // validation; the chunk rows' prefills in row order
+    std::vector<Prefill>& pre = ctx->prefills;
+    pre.clear();
+    if (bt->n_prefill > 1) {
+        if (bt->n_prefill > SLW_MAX_PREFILLS) return fail(SLW_ERANGE, "n_prefill %d above %d", bt->n_prefill, SLW_MAX_PREFILLS);
+        if (!bt->prefill_seqs || !bt->prefix_lens || !bt->chunk_lens) return fail(SLW_EINVAL, "null prefill arrays");
+        int64_t rows = 0;
+        for (int i = 0; i < bt->n_prefill; ++i) {
+            if (bt->chunk_lens[i] < 1) return fail(SLW_EINVAL, "prefill %d has chunk_len %d", i, bt->chunk_lens[i]);
+            pre.push_back({bt->prefill_seqs[i], bt->prefix_lens[i], bt->chunk_lens[i], static_cast<int32_t>(rows)});
+            rows += bt->chunk_lens[i];
+        }
+        if (rows != C) return fail(SLW_EINVAL, "chunk_lens add up to %lld, C is %d", (long long)rows, C);
+    } else if (C > 0) {
+        pre.push_back({bt->prefill_seq, bt->prefix_len, C, 0});
+    }
     std::vector<std::pair<int64_t, int32_t>> req;
-    req.reserve(B + 1);
-    if (C > 0) {
-        if (P < 0) return fail(SLW_EINVAL, "negative prefix_len");
-        if (static_cast<int64_t>(P) + C > c.max_pos) return fail(SLW_ERANGE, "prefix_len + C exceeds max_pos");
-        if (!ctx->kv.exists(bt->prefill_seq)) return fail(SLW_EINVAL, "prefill sequence %lld unknown", (long long)bt->prefill_seq);
-        if (ctx->kv.reserved(bt->prefill_seq) < P)
-            return fail(SLW_EINVAL, "prefill sequence holds %d positions, prefix_len is %d",
-                        ctx->kv.reserved(bt->prefill_seq), P);
-        req.emplace_back(bt->prefill_seq, P + C);
+    req.reserve(B + pre.size());
+    std::unordered_set<int64_t> seen;
+    seen.reserve(2 * (B + pre.size()) + 2);
+    for (const Prefill& f : pre) {
+        if (f.prefix < 0) return fail(SLW_EINVAL, "negative prefix_len");
+        if (static_cast<int64_t>(f.prefix) + f.c > c.max_pos) return fail(SLW_ERANGE, "prefix_len + chunk exceeds max_pos");
+        if (!ctx->kv.exists(f.seq)) return fail(SLW_EINVAL, "prefill sequence %lld unknown", (long long)f.seq);
+        if (!seen.insert(f.seq).second)
+            return fail(SLW_EINVAL, "sequence %lld appears twice in the batch", (long long)f.seq);
+        if (ctx->kv.reserved(f.seq) < f.prefix)
+            return fail(SLW_EINVAL, "prefill sequence %lld holds %d positions, prefix_len is %d", (long long)f.seq,
+                        ctx->kv.reserved(f.seq), f.prefix);
+        req.emplace_back(f.seq, f.prefix + f.c);
     }
     {
-        std::unordered_set<int64_t> seen;
-        seen.reserve(2 * B + 2);
         for (int b = 0; b < B; ++b) {
             const int64_t id = bt->decode_seqs[b];
             const int32_t L = bt->context_lens[b];
             if (!ctx->kv.exists(id)) return fail(SLW_EINVAL, "decode sequence %lld unknown", (long long)id);
-            if ((C > 0 && id == bt->prefill_seq) || !seen.insert(id).second)
+            if (!seen.insert(id).second)
                 return fail(SLW_EINVAL, "sequence %lld appears twice in the batch", (long long)id);
             if (L < 0 || L + 1 > c.max_pos) return fail(SLW_ERANGE, "context_len %d out of range", L);
             if (ctx->kv.reserved(id) < L)
@@ -320,7 +352,8 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
 int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
                       const Layout& L, hipStream_t stream, bool no_alloc) {
     const slw_model_cfg& c = ctx->cfg;
-    const int C = bt->C, B = bt->B, P = bt->prefix_len;
+    const int C = bt->C, B = bt->B;
+    const std::vector<Prefill>& pre = ctx->prefills;
     int rc = SLW_OK;
 
     // ---- metadata (host) ----
@@ -336,10 +369,12 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     // slot[M], pos[M]
     std::vector<int32_t>& slots = ctx->slots_build;
     slots.resize(M);
-    for (int j = 0; j < C; ++j) slots[j] = ctx->kv.slot(bt->prefill_seq, P + j);
+    for (const Prefill& f : pre)
+        for (int j = 0; j < f.c; ++j) slots[f.row0 + j] = ctx->kv.slot(f.seq, f.prefix + j);
     for (int b = 0; b < B; ++b) slots[C + b] = ctx->kv.slot(bt->decode_seqs[b], bt->context_lens[b]);
     m.insert(m.end(), slots.begin(), slots.end());
-    for (int j = 0; j < C; ++j) m.push_back(P + j);
+    for (const Prefill& f : pre)
+        for (int j = 0; j < f.c; ++j) m.push_back(f.prefix + j);
     for (int b = 0; b < B; ++b) m.push_back(bt->context_lens[b]);
     const size_t o_kvlen = m.size();
     for (int b = 0; b < B; ++b) m.push_back(bt->context_lens[b] + 1);
@@ -353,10 +388,13 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
         m.insert(m.end(), t.begin(), t.begin() + nb);
     }
     m[o_btoff + B] = static_cast<int32_t>(m.size() - o_bt);
+    // block tables of the prefills, one after the other
     const size_t o_pre = m.size();
-    if (C > 0) {
-        const auto& t = ctx->kv.table(bt->prefill_seq);
-        const int nb = static_cast<int>(ceil_div(P + C, 16));
+    std::vector<int32_t> pre_bt(pre.size());
+    for (size_t i = 0; i < pre.size(); ++i) {
+        pre_bt[i] = static_cast<int32_t>(m.size() - o_pre);
+        const auto& t = ctx->kv.table(pre[i].seq);
+        const int nb = static_cast<int>(ceil_div(pre[i].prefix + pre[i].c, 16));
         m.insert(m.end(), t.begin(), t.begin() + nb);
     }
     const size_t o_workb = m.size();
@@ -377,15 +415,28 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
         }
         m[o_workoff + B] = w;
     }
-    // Chunk attention work.  The 64-key tiles of every query tile, laid end
-    // to end, are cut into equal runs, one per work-group of each kv head; a
-    // run that crosses query tiles becomes one item per query tile it
-    // touches.  A query tile covered by one item is written directly, one
-    // covered by several is combined by the merge kernel.
-    const int n_qt = C > 0 ? chunk_tiles(c, C) : 0;
+    // Chunk attention work.  Each prefill's rows are cut into query tiles of
+    // pwg positions (a tile never mixes sequences); query tile q covers chunk
+    // rows qt_row0 .. + qt_rows at positions from qt_pos0 on and reads the
+    // block table at qt_bt, over keys 0 .. qt_pos0 + qt_rows - 1.  The 64-key
+    // tiles of every query tile, laid end to end, are cut into equal runs, one
+    // per work-group of each kv head; a run that crosses query tiles becomes
+    // one item per query tile it touches.  A query tile covered by one item is
+    // written directly, one covered by several is combined by the merge kernel.
     const int pwg = chunk_tile_positions(c.n_q_heads / c.n_kv_heads);
+    std::vector<int32_t> qt_row0, qt_rows, qt_pos0, qt_bt;
+    for (size_t i = 0; i < pre.size(); ++i)
+        for (int j = 0; j < pre[i].c; j += pwg) {
+            qt_row0.push_back(pre[i].row0 + j);
+            qt_rows.push_back(std::min(pwg, pre[i].c - j));
+            qt_pos0.push_back(pre[i].prefix + j);
+            qt_bt.push_back(pre_bt[i]);
+        }
+    const int n_qt = static_cast<int>(qt_row0.size());
+    if (n_qt > chunk_tiles(c, C)) return fail(SLW_EINVAL, "internal: %d query tiles above cap", n_qt);
+    auto key_end = [&](int q) { return static_cast<int64_t>(qt_pos0[q]) + qt_rows[q]; };
     std::vector<int64_t> tile_end(n_qt + 1, 0);
-    for (int q = 0; q < n_qt; ++q) tile_end[q + 1] = tile_end[q] + ceil_div(P + std::min(C, (q + 1) * pwg), 64);
+    for (int q = 0; q < n_qt; ++q) tile_end[q + 1] = tile_end[q] + ceil_div(key_end(q), 64);
     const int64_t total_tiles = tile_end[n_qt];
     int n_slots = 0;
     std::vector<int32_t>& it = ctx->items;
@@ -404,7 +455,7 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             while (t0 < t1) {
                 while (tile_end[q + 1] <= t0) ++q;
                 const int64_t seg_end = std::min(t1, tile_end[q + 1]);
-                const int64_t ke_q = P + std::min(C, (q + 1) * pwg);
+                const int64_t ke_q = key_end(q);
                 it.push_back(q);
                 it.push_back(static_cast<int32_t>((t0 - tile_end[q]) * 64));
                 it.push_back(static_cast<int32_t>(std::min(ke_q, (seg_end - tile_end[q]) * 64)));
@@ -431,7 +482,7 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             if (it[3 * i + 1] != at || it[3 * i + 2] <= at) return fail(SLW_EINVAL, "internal: chunk plan");
             at = it[3 * i + 2];
         }
-        if (at != P + std::min(C, (q + 1) * pwg)) return fail(SLW_EINVAL, "internal: chunk plan");
+        if (at != key_end(q)) return fail(SLW_EINVAL, "internal: chunk plan");
     }
     const size_t o_item = m.size();
     m.resize(m.size() + 3 * static_cast<size_t>(n_items));
@@ -444,6 +495,11 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     m.insert(m.end(), slot_off.begin(), slot_off.end());
     const size_t o_qtoff = m.size();
     m.insert(m.end(), qt_off.begin(), qt_off.end());
+    const size_t o_qt = m.size();  // [4][n_qt]: first row, rows, first position, block-table offset
+    m.insert(m.end(), qt_row0.begin(), qt_row0.end());
+    m.insert(m.end(), qt_rows.begin(), qt_rows.end());
+    m.insert(m.end(), qt_pos0.begin(), qt_pos0.end());
+    m.insert(m.end(), qt_bt.begin(), qt_bt.end());
 
     if (m.size() > meta_ints(c, C, B)) return fail(SLW_EINVAL, "internal: metadata %zu ints above its region", m.size());
 
@@ -549,7 +605,11 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             ca.part_o = reinterpret_cast<float*>(wsb + L.cpart_o);
             ca.part_ml = reinterpret_cast<float*>(wsb + L.cpart_ml);
             ca.c = C;
-            ca.prefix = P;
+            ca.n_qt = n_qt;
+            ca.qt_row0 = dmeta + o_qt;
+            ca.qt_rows = dmeta + o_qt + n_qt;
+            ca.qt_pos0 = dmeta + o_qt + 2 * n_qt;
+            ca.qt_bt = dmeta + o_qt + 3 * n_qt;
             ca.hq = hq;
             ca.hkv = hkv;
             ca.hd = hd;

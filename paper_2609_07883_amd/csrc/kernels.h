@@ -59,17 +59,22 @@ bool gemm_shape_ok(const GemmPlan& p, int n, int k);
 // Enqueue the GEMM; `partial` must hold plan.partial_bytes when plan.splits > 1.
 void launch_gemm(const GemmArgs& g, const GemmPlan& plan, void* partial, hipStream_t s);
 
-// Causal chunk-vs-prefix attention over the prefill sequence's pages.
-// A work-group covers 256 (position, head) rows of one kv head: 256 / group
-// consecutive chunk positions times the group's q heads.  Work item i covers
-// query tile item_qt[i] against keys [item_kb[i], item_ke[i]); when a tile's
-// keys are split over several items, partials are merged afterwards.
+// Causal chunk-vs-prefix attention over the prefill sequences' pages.
+// A query tile holds up to 256 / group consecutive chunk rows of one prefill
+// sequence; a work-group covers 256 (position, head) rows of one kv head: the
+// tile's positions times the group's q heads.  Work item i covers query tile
+// item_qt[i] against keys [item_kb[i], item_ke[i]); when a tile's keys are
+// split over several items, partials are merged afterwards.
 struct ChunkAttnArgs {
     const void* qkv;       // bf16 rows 0..c-1 (q after RoPE), row stride ld_qkv
     void* out;             // bf16 [c][hq * hd]
     const void* k_pool;    // this layer
     const void* v_pool;
-    const int32_t* bt;     // block table of the prefill sequence
+    const int32_t* bt;     // block tables of the prefill sequences, one after the other
+    const int32_t* qt_row0;   // [n_qt] first chunk row of each query tile
+    const int32_t* qt_rows;   // [n_qt] rows of the tile (<= 256 / group)
+    const int32_t* qt_pos0;   // [n_qt] sequence position of the tile's first row
+    const int32_t* qt_bt;     // [n_qt] offset of the tile's sequence's block table in bt
     const int32_t* item_qt;   // [n_items]
     const int32_t* item_kb;   // [n_items] multiple of 64
     const int32_t* item_ke;   // [n_items]
@@ -77,8 +82,8 @@ struct ChunkAttnArgs {
     const int32_t* slot_off;  // [n_slots + 1] first item of each work-group (per kv head)
     float* part_o;            // [n_items][hkv][256][hd]   (items of split query tiles)
     float* part_ml;           // [n_items][hkv][256][2]
-    int c, prefix, hq, hkv, hd, ld_qkv;
-    int n_items, n_slots;
+    int c, hq, hkv, hd, ld_qkv;
+    int n_qt, n_items, n_slots;
     int split;                // some query tile has several items: the merge kernel runs
 };
 // Query positions per work-group for a group size (rows / group).
@@ -102,7 +107,7 @@ struct DecodeAttnArgs {
     int b, n_work, split_tokens, hq, hkv, hd, ld_q;
 };
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
-// Combine the partials of both attentions in one launch: chunk positions of
+// Combine the partials of both attentions in one launch: chunk rows of
 // query tiles split over several items (ca may be null or unsplit) and every
 // decode (da may be null or have b = 0).
 void launch_attention_merge(const ChunkAttnArgs* ca, const DecodeAttnArgs* da, hipStream_t s);

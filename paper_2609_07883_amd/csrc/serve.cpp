@@ -70,8 +70,8 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     if (o->fallback_window < 0 || o->fallback_window > 65536)
         return fail(SLW_ERANGE, "fallback_window must be in [0, 65536]");
     if (o->fallback_window > 0 && !o->table) return fail(SLW_EINVAL, "the telemetry fallback needs a cost table");
-    if (o->max_prefills > 1 && o->executor == SLW_EXEC_GPU)
-        return fail(SLW_EUNSUPPORTED, "prefill batching runs on the virtual-clock executors only");
+    if (o->max_prefills > SLW_MAX_PREFILLS && o->executor == SLW_EXEC_GPU)
+        return fail(SLW_ERANGE, "max_prefills %d above SLW_MAX_PREFILLS on the GPU executor", o->max_prefills);
     if (o->executor == SLW_EXEC_GPU) {
         if (!ctx || !o->x_in || !o->x_out || !o->ws) return fail(SLW_EINVAL, "GPU executor needs ctx and buffers");
         const int64_t cap = o->policy == SLW_POLICY_FIXED ? o->fixed_chunk : o->c_max;
@@ -161,6 +161,8 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     std::vector<int64_t> dec_ids, deadlines, eff;
     std::vector<int32_t> ctx_lens;
     std::vector<std::pair<int32_t, int32_t>> plan;  // (index into pending, tokens) served this iteration
+    std::vector<int64_t> pf_seq;                     // GPU batch: the plan's sequences, prefixes, chunks
+    std::vector<int32_t> pf_prefix, pf_chunk;
     // telemetry: relative residuals (ppm) of the last residual_window chunked iterations
     const int32_t W = o->residual_window;
     std::vector<int64_t> resid(std::max(W, 1)), scratch;
@@ -290,9 +292,16 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
             // first-fit prefill batching (Sec. 3.3)
             if (o->policy == SLW_POLICY_SLOWEAVE && max_prefills > 1 && chunk > 0 && chunk == remaining &&
                 !(rec.flags & SLW_SERVE_AGED)) {
+                // GPU: blocks committed by the prompts this iteration starts
+                int64_t starting = gpu && !head->started ? kv_blocks_for(reqs[head->req]) : 0;
                 for (size_t k = 1; k < pending.size(); ++k) {
                     if (static_cast<int32_t>(plan.size()) >= max_prefills) break;
                     if (nd + static_cast<int32_t>(plan.size()) >= o->max_decode) break;
+                    if (gpu && !pending[k].started) {  // the pool must hold it to its last token
+                        const int64_t need = kv_blocks_for(reqs[pending[k].req]);
+                        if (committed_blocks + starting + need > pool_blocks) break;
+                        starting += need;
+                    }
                     const int32_t rem = reqs[pending[k].req].prompt_len - pending[k].prompt_done;
                     int32_t c = 0;
                     uint32_t fl = 0;
@@ -322,19 +331,34 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         }
 
         if (gpu) {
-            if (chunk > 0 && !head->started) {
-                rc = slw_seq_create(ctx, reqs[head->req].id);
-                if (rc) return rc;
-                head->started = true;
-                committed_blocks += kv_blocks_for(reqs[head->req]);
+            pf_seq.clear();
+            pf_prefix.clear();
+            pf_chunk.clear();
+            for (const auto& pc : plan) {
+                Live& h = pending[pc.first];
+                if (!h.started) {
+                    rc = slw_seq_create(ctx, reqs[h.req].id);
+                    if (rc) return rc;
+                    h.started = true;
+                    committed_blocks += kv_blocks_for(reqs[h.req]);
+                }
+                pf_seq.push_back(reqs[h.req].id);
+                pf_prefix.push_back(h.prompt_done);
+                pf_chunk.push_back(pc.second);
             }
             slw_batch b{};
             b.C = chunk;
-            b.prefill_seq = chunk > 0 ? reqs[head->req].id : 0;
-            b.prefix_len = chunk > 0 ? head->prompt_done : 0;
+            b.prefill_seq = chunk > 0 ? pf_seq[0] : 0;
+            b.prefix_len = chunk > 0 ? pf_prefix[0] : 0;
             b.B = nd;
             b.decode_seqs = dec_ids.data();
             b.context_lens = ctx_lens.data();
+            if (plan.size() > 1) {
+                b.n_prefill = static_cast<int32_t>(plan.size());
+                b.prefill_seqs = pf_seq.data();
+                b.prefix_lens = pf_prefix.data();
+                b.chunk_lens = pf_chunk.data();
+            }
             rc = slw_mixed_iteration(ctx, &b, o->x_in, o->x_out, o->ws, o->ws_bytes, o->stream);
             if (rc) return rc;
             if (hipStreamSynchronize(stream) != hipSuccess)

@@ -110,9 +110,10 @@ class Mirror:
         y_gpu = self.s.output(batch.rows)
         slots_gpu = self.s.ctx.last_slots()
         slots_ref, _ = OP.iteration_metadata(self.mgr, batch.chunk, batch.prefill_seq,
-                                             batch.prefix_len, batch.decode_seqs, batch.context_lens)
+                                             batch.prefix_len, batch.decode_seqs, batch.context_lens,
+                                             prefills=batch.prefill_list)
         ob = OL.MixedBatch(batch.chunk, batch.prefill_seq, batch.prefix_len,
-                           list(batch.decode_seqs), list(batch.context_lens))
+                           list(batch.decode_seqs), list(batch.context_lens), prefills=batch.prefill_list)
         x = synth.bf16_to_f64(x_bits)
         for layer in range(len(self.w)):
             x = OL.mixed_iteration(self.shape, self.w[layer], x, self.kv[layer], ob,
@@ -121,8 +122,12 @@ class Mirror:
 
     def kv_error(self, batch: api.Batch, layer: int = 0, rows=None) -> float:
         """Largest per-head-vector relative error of the K/V the iteration appended."""
-        seqs = [batch.prefill_seq] * batch.chunk + list(batch.decode_seqs)
-        pos = [batch.prefix_len + j for j in range(batch.chunk)] + list(batch.context_lens)
+        seqs, pos = [], []
+        for sid, p0, c in batch.prefill_list:
+            seqs += [sid] * c
+            pos += list(range(p0, p0 + c))
+        seqs += list(batch.decode_seqs)
+        pos += list(batch.context_lens)
         idx = range(len(seqs)) if rows is None else rows
         err = 0.0
         by_seq = {}
@@ -146,7 +151,8 @@ def stage_errors(mir: Mirror, batch: api.Batch, x_bits) -> dict:
     s = mir.s.shape
     shape, w = mir.shape, mir.w[0]
     seqs, pos = OL.MixedBatch(batch.chunk, batch.prefill_seq, batch.prefix_len,
-                              list(batch.decode_seqs), list(batch.context_lens)).row_seq_pos()
+                              list(batch.decode_seqs), list(batch.context_lens),
+                              prefills=batch.prefill_list).row_seq_pos()
     x = synth.bf16_to_f64(x_bits)
     q, k, v = OL.qkv_rope(shape, w, x, pos)
     kv = mir.kv[0]

@@ -211,3 +211,55 @@ def test_errors_are_reported_not_faulted(l8b):
     with pytest.raises(api.SloweaveError) as e:       # an iteration that cannot be covered
         sess.run(api.Batch(16 * (free + 1), 3, 0, [], []))
     assert e.value.code == api.ENOMEM and sess.ctx.free_blocks() == free
+
+
+def test_tiny_batched_prefills():
+    """Prefill batching (Sec. 3.3): three prompts' chunks (one fresh, two at a
+    cached prefix) next to two decodes in one iteration, then two prompts
+    again with one chunk spanning two query tiles; every row against the
+    oracle, slots and block tables bit-exact."""
+    _require_gpu()
+    from paper_2609_07883_amd.runtime import Session
+    sess = Session(synth.TINY, num_blocks=512, max_c=400, max_b=4, qk_std=0.16)
+    mir = Mirror(sess)
+    for sid, L in ((1, 70), (2, 0), (3, 130), (21, 40), (22, 257)):
+        mir.create(sid)
+        mir.install_context(sid, L)
+    steps = [
+        api.Batch.batched([(1, 70, 100), (2, 0, 37), (3, 130, 64)], [21, 22], [40, 257]),
+        api.Batch.batched([(2, 37, 300), (1, 170, 5)], [21, 22], [41, 258]),
+    ]
+    for i, b in enumerate(steps):
+        x = synth.embeddings(b.rows, synth.TINY.d_model, seed=1, stream=500 + i)
+        y, yr, sg, sr = mir.step(b, x)
+        assert sg == sr
+        e = check(y, yr, f"batched prefills, iteration {i}")
+        assert mir.kv_error(b) <= TOL
+        for sid in (1, 2, 3, 21, 22):
+            assert sess.ctx.block_table(sid) == mir.mgr.block_table(sid)
+        print(f"batched prefills iteration {i}: {e}", flush=True)
+
+
+@pytest.mark.parametrize("pre", [
+    ((500, 3000, 70), (501, 0, 130), (502, 500, 1)),   # a long prefix: its tiles' keys split and merged
+    ((501, 0, 64), (502, 0, 63), (500, 16, 65), (503, 7, 33)),
+], ids=["split_keys", "tile_edges"])
+def test_8b_batched_prefills(l8b, pre):
+    sess = l8b
+    sess.ctx.kv_init(sess.k_pool.data_ptr(), sess.v_pool.data_ptr(), sess.num_blocks)
+    mir = Mirror(sess, seed=6)
+    for sid, p0, _ in pre:
+        mir.create(sid)
+        mir.install_context(sid, p0)
+    dec, ctx = [600, 601], [5, 1000]
+    for sid, L in zip(dec, ctx):
+        mir.create(sid)
+        mir.install_context(sid, L)
+    b = api.Batch.batched(pre, dec, ctx)
+    x = synth.embeddings(b.rows, synth.LLAMA8B_LAYER.d_model, seed=1, stream=b.rows)
+    y, yr, sg, sr = mir.step(b, x)
+    assert sg == sr
+    e = check(y, yr, f"8B batched prefills {pre}")
+    kv = mir.kv_error(b)
+    print(f"8B batched prefills {pre}: out {e} kv {kv:.3e}", flush=True)
+    assert kv <= TOL

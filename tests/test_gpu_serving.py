@@ -240,3 +240,33 @@ def test_telemetry_fallback_on_gpu(setup):
             window.append(int(r["end_ns"]) - int(r["start_ns"]) - int(r["predicted_ns"]))
     print(f"fallback: {events} events, {decided} Alg. 1 decisions, {len(res.iterations)} iterations")
     assert events > 0 and decided > 0
+
+
+def test_prefill_batching_on_gpu(setup):
+    """First-fit prefill batching (Sec. 3.3) on the GPU executor: iterations
+    that finish one prompt take the next ones in queue order.  Checked from
+    the records: some iterations serve several prompts; every prompt token
+    runs exactly once (the chunks add up to the prompts); every chunked
+    iteration beside decodes keeps its predicted time within the budget, the
+    total included (Prop. 1's safety on the table); tokens come in order; the
+    pool is whole at the end."""
+    sess, ct, _ = setup
+    # bursts of short prompts: several fit one iteration
+    n = 24
+    tr = synth.RequestTrace(np.repeat(np.arange(4, dtype=np.int64) * 30_000_000, 6),
+                            np.arange(n, dtype=np.int64) * 7 % 50 + 12, np.full(n, 3, np.int64))
+    res = serving.run(tr, policy="sloweave", tpot_ms=4.0, max_decode=16, c_max=256, table=ct, session=sess,
+                      max_prefills=4)
+    torch.cuda.synchronize()
+    for i in range(n):
+        t = res.token_ns[i]
+        assert len(t) == tr.output[i] and t[0] > tr.arrival_ns[i] and np.all(np.diff(t) > 0)
+    it = res.iterations
+    assert int(it["chunk"].sum()) == int(tr.prompt.sum())
+    assert it["n_prefill"].max() > 1 and np.all(it["n_prefill"][it["chunk"] > 0] >= 1)
+    assert np.all(it["chunk"] <= 256) and it["n_decode"].max() <= 16
+    chunked = it[(it["chunk"] > 0) & (it["n_decode"] > 0)]
+    assert np.all(chunked["predicted_ns"] <= chunked["budget_ns"])
+    assert sess.ctx.free_blocks() == sess.num_blocks
+    print(f"batching: {int(np.sum(it['n_prefill'] > 1))} of {len(it)} iterations serve several prompts "
+          f"(up to {int(it['n_prefill'].max())})")

@@ -247,3 +247,36 @@ def test_cost_table_statistics_match_hand_worked_golden():
     ct2 = api.CostTable.from_samples(g["c_grid"], g["b_grid"], np.asarray([samples, samples], dtype=np.int64),
                                      p_grid=[0, 4096])
     assert ct2.monotone() == (2 * g["violations"][0], g["violations"][1])
+
+
+def test_batched_prefill_validation_through_abi():
+    """Several prefills in one iteration: malformed batches are refused on the
+    host before anything is reserved (no device pointer is ever touched, so
+    placeholder addresses serve)."""
+    ctx = api.Context.from_shape(synth.TINY)
+    fake = 1 << 20
+    ctx.set_layer_weights(0, *([fake] * 6))
+    ctx.kv_init(fake, fake, 64)
+    for sid in (1, 2, 3):
+        ctx.seq_create(sid)
+    ctx.seq_reserve(1, 20)
+    free = ctx.free_blocks()
+
+    def run(batch):
+        ctx.mixed_iteration(batch, fake, fake, fake, 1 << 30)
+
+    cases = [
+        (api.Batch(30, -1, 0, [], [], ((1, 20, 10), (1, 30, 20))), api.EINVAL),       # sequence twice
+        (api.Batch(30, -1, 0, [2], [0], ((1, 20, 10), (2, 0, 20))), api.EINVAL),      # prefill and decode
+        (api.Batch(31, -1, 0, [], [], ((1, 20, 10), (2, 0, 20))), api.EINVAL),       # rows do not add up
+        (api.Batch(10, -1, 0, [], [], ((1, 20, 10), (2, 0, 0))), api.EINVAL),        # empty chunk
+        (api.Batch(30, -1, 0, [], [], ((1, 21, 10), (2, 0, 20))), api.EINVAL),       # prefix not cached
+        (api.Batch(17, -1, 0, [], [], tuple((100 + i, 0, 1) for i in range(17))), api.ERANGE),  # > 16
+    ]
+    for b, code in cases:
+        with pytest.raises(api.SloweaveError) as e:
+            run(b)
+        assert e.value.code == code, (b, e.value)
+        assert ctx.free_blocks() == free
+    assert api.Batch.batched([(1, 20, 5)]) == api.Batch(5, 1, 20, [], [])
+    assert api.Batch.batched([(1, 20, 5), (2, 0, 3)]).chunk == 8

@@ -245,7 +245,7 @@ def test_variant_argument_errors():
         serving.run(tr, aging_ns=MS, **base)
     with pytest.raises(api.SloweaveError):  # admission without a table
         serving.run(tr, policy="fixed", fixed_chunk=64, tpot_ms=25, max_decode=16, admit_ppm=500_000)
-    with pytest.raises(api.SloweaveError) as e:  # prefill batching is for the virtual-clock executors
+    with pytest.raises(api.SloweaveError) as e:  # a GPU iteration takes at most SLW_MAX_PREFILLS prompts
         api.serve(np.arange(10), tr.arrival_ns, tr.prompt, tr.output, policy=0, tpot_ns=25 * MS, max_decode=16,
-                  table=tab, executor=api.EXEC_GPU, max_prefills=2)
-    assert "virtual-clock" in str(e.value)
+                  table=tab, executor=api.EXEC_GPU, max_prefills=api.MAX_PREFILLS + 1)
+    assert e.value.code == api.ERANGE
