@@ -368,7 +368,7 @@ int slw_cost_table_load(const char* path, slw_cost_table** out);
 int slw_flush_cache(void* buf, size_t bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
-/* Controller (Eq. 1 by the binary search of Alg. 1, margin of Sec. 3.3)    */
+/* Controller (Eq. 1 solved by bisection as Alg. 1 does; margin of Sec. 3.3) */
 /* ------------------------------------------------------------------------ */
 
 /*

@@ -3,8 +3,10 @@
 // Sec. 5.1: the profiler keeps P50 and P99 per (decode batch, chunk) grid
 // point and applies a running maximum along the chunk axis, and the
 // runtime's table is indexed by decode batch, cached context and chunk;
-// Sec. 6.4: interpolate between profiled points.  Eq. 1 is solved by the
-// upper-mid binary search of Alg. 1 with the margin test of Sec. 3.3.
+// Sec. 6.4: interpolate between profiled points.  Eq. 1 (the largest chunk
+// whose predicted iteration, plus the margin of Sec. 3.3, meets the earliest
+// deadline) is found by bisection, which Sec. 3.2 allows because the
+// prediction is monotone in the chunk.
 #include "cost_table.h"
 
 #include <algorithm>
@@ -148,6 +150,24 @@ int64_t analytic_iteration_ns(int32_t n, int32_t c) {
     return t;
 }
 
+// First x in [lo, hi) with pred(x) false, for a predicate true on a prefix
+// of the range and false after it; hi if it holds everywhere.  Each probe
+// halves the interval, so ceil(log2(hi - lo + 1)) probes at most.
+template <class Pred>
+int32_t first_false(int32_t lo, int32_t hi, Pred pred) {
+    int32_t n = hi - lo;
+    while (n > 0) {
+        const int32_t half = n / 2;
+        if (pred(lo + half)) {
+            lo += half + 1;
+            n -= half + 1;
+        } else {
+            n = half;
+        }
+    }
+    return lo;
+}
+
 int select_chunk_core(const slw_cost_table* t, const int64_t* deadlines_ns, int32_t n_active, int64_t now_ns,
                       int32_t prefix, int32_t remaining, int32_t c_max, int64_t margin_ns, int64_t rel_margin_ppm,
                       int32_t* chunk, uint32_t* flags, int32_t* n_lookups) {
@@ -192,17 +212,16 @@ int select_chunk_after(const slw_cost_table* t, const int64_t* deadlines_ns, int
         const int64_t v = lookup_row(t, row, base + c);
         return v + (rel_margin_ppm * v + 999999) / 1000000;
     };
-    int32_t lo = 0, hi = cap, lookups = 0;
-    while (lo < hi) {
-        int32_t mid = lo + (hi - lo + 1) / 2;  // floor((lo + hi + 1) / 2) without overflow
+    // Eq. 1 over c in [0, cap]: feasible(c) = predict(c) + margin <= budget
+    // holds on a prefix of the range (predict is monotone in c), so the
+    // chunk is one less than the first c in [1, cap] that is infeasible.
+    int32_t lookups = 0;
+    auto feasible = [&](int32_t c) {
         ++lookups;
-        if (predict(mid) + margin_ns <= budget) lo = mid;
-        else hi = mid - 1;
-    }
-    if (lo == 0) {
-        ++lookups;
-        if (predict(0) + margin_ns > budget) fl |= SLW_FLAG_DECODE_INFEASIBLE;
-    }
+        return predict(c) + margin_ns <= budget;
+    };
+    const int32_t lo = first_false(1, cap + 1, feasible) - 1;
+    if (lo == 0 && !feasible(0)) fl |= SLW_FLAG_DECODE_INFEASIBLE;
     *chunk = lo;
     *flags = fl;
     if (n_lookups) *n_lookups = lookups;
