@@ -367,6 +367,18 @@ int slw_cost_table_load(const char* path, slw_cost_table** out);
  */
 int slw_flush_cache(void* buf, size_t bytes, void* stream);
 
+/*
+ * Fill device bf16 dst[0 .. n-1] with mean + std * z_i (asynchronous on
+ * `stream`): seeded synthetic weights for stacks too large to draw on the
+ * host, not a step of the iteration.  z is the standard-normal stream of
+ * the counter-based Philox4x32-10 generator (Salmon et al., SC 2011) keyed
+ * by `seed`: draw t (counter (t mod 2^32, t div 2^32, 0, 0)) gives words
+ * w0..w3, and elements 4t .. 4t+3 are Box-Muller pairs of the 24-bit
+ * uniforms u = ((w0 >> 8) + 1/2) 2^-24, v = (w1 >> 8) 2^-24 (then w2, w3):
+ * sqrt(-2 ln u) cos(2 pi v), sqrt(-2 ln u) sin(2 pi v), rounded to bf16.
+ */
+int slw_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Controller (Eq. 1 solved by bisection as Alg. 1 does; margin of Sec. 3.3) */
 /* ------------------------------------------------------------------------ */

@@ -36,7 +36,7 @@ EXPORTS = (
     "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
     "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
     "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
-    "slw_mixed_iteration_static", "slw_flush_cache",
+    "slw_mixed_iteration_static", "slw_flush_cache", "slw_fill_normal",
 )
 STATIC_WS_BYTES = 128 << 20
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "attn_merge",
@@ -141,6 +141,7 @@ def lib() -> C.CDLL:
         "slw_mixed_iteration": ([vp, P(BatchC), vp, vp, vp, sz, vp], C.c_int),
         "slw_mixed_iteration_static": ([vp, P(BatchC), vp, vp, vp], C.c_int),
         "slw_flush_cache": ([vp, sz, vp], C.c_int),
+        "slw_fill_normal": ([vp, sz, C.c_uint64, C.c_float, C.c_float, vp], C.c_int),
         "slw_last_slots": ([vp, P(i32), i32, P(i32)], C.c_int),
         "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
@@ -308,6 +309,11 @@ def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_
                                           int(remaining), int(c_max), int(margin_ns), C.byref(ch), C.byref(fl),
                                           C.byref(nl)))
     return ch.value, fl.value, nl.value
+
+
+def fill_normal(dst: int, n: int, seed: int, mean: float, std: float, stream: int = 0) -> None:
+    """Enqueue dst[i] = bf16(mean + std z_i), z the Philox4x32-10 normal stream of seed."""
+    _check(lib().slw_fill_normal(dst or None, int(n), int(seed), float(mean), float(std), stream or None))
 
 
 def flush_cache(buf: int, nbytes: int, stream: int = 0) -> None:

@@ -1,4 +1,5 @@
-// Small bandwidth-bound kernels: RMSNorm, the per-iteration RoPE table, fill.
+// Small bandwidth-bound kernels: RMSNorm, the per-iteration set-up (metadata
+// copy, RoPE table), the cache sweep, the seeded normal fill.
 #include <math.h>
 
 #include "device.h"
@@ -69,10 +70,8 @@ __global__ __launch_bounds__(kNormThreads) void rmsnorm_kernel(const T* __restri
     }
 }
 
-// One thread per (row, frequency): angle p * theta^(-2i/hd) formed and
-// reduced in double precision so that large positions keep full accuracy.
-// cos and sin of position pos[r] times theta^(-i/half), in fp64 so that large
-// positions keep their accuracy.
+// One thread per (row, frequency): cos and sin of position pos[r] times
+// theta^(-i/half), formed in fp64 so that large positions keep their accuracy.
 __device__ __forceinline__ void rope_entry(const int32_t* pos, float2* cs, int idx, int half, double theta) {
     const int r = idx / half, i = idx % half;
     const double ang = static_cast<double>(pos[r]) * pow(theta, -static_cast<double>(i) / half);
@@ -120,7 +119,57 @@ __global__ void iteration_setup_kernel(uint32_t* __restrict__ dst, const uint32_
     if (idx < rows * half) rope_entry(pos_host, cs, idx, half, theta);
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): a counter-based
+// generator, ten rounds of two 32x32->64-bit multiplies with a Weyl-sequence
+// key schedule.
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c[0];
+        const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c[2];
+        c = u32x4{static_cast<uint32_t>(p1 >> 32) ^ c[1] ^ k0, static_cast<uint32_t>(p1),
+                  static_cast<uint32_t>(p0 >> 32) ^ c[3] ^ k1, static_cast<uint32_t>(p0)};
+    }
+    return c;
+}
+
+// Element i of the stream: draw t = i / 4 gives four normals by Box-Muller
+// on the uniforms of its two word pairs (24-bit, exact in fp32):
+//   u = (w0 >> 8 + 1/2) 2^-24,  v = (w1 >> 8) 2^-24,
+//   z0 = sqrt(-2 ln u) cos(2 pi v),  z1 = sqrt(-2 ln u) sin(2 pi v).
+__global__ void fill_normal_kernel(bf16* __restrict__ dst, size_t n, uint32_t k0, uint32_t k1, float mean,
+                                   float std) {
+    const size_t t = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x;
+    if (4 * t >= n) return;
+    const u32x4 w = philox4x32_10(u32x4{static_cast<uint32_t>(t), static_cast<uint32_t>(t >> 32), 0u, 0u}, k0, k1);
+    float z[4];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const float u = (static_cast<float>(w[2 * p] >> 8) + 0.5f) * 0x1p-24f;
+        const float v = static_cast<float>(w[2 * p + 1] >> 8) * 0x1p-24f;
+        const float r = sqrtf(-2.0f * logf(u));
+        float sn, cs;
+        sincosf(6.2831853071795864f * v, &sn, &cs);
+        z[2 * p] = r * cs;
+        z[2 * p + 1] = r * sn;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        if (4 * t + e < n) dst[4 * t + e] = f2bf(mean + std * z[e]);
+}
+
 }  // namespace
+
+void launch_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, hipStream_t s) {
+    const size_t draws = (n + 3) / 4;
+    if (draws == 0) return;
+    fill_normal_kernel<<<static_cast<unsigned>((draws + 255) / 256), 256, 0, s>>>(
+        static_cast<bf16*>(dst), n, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), mean, std);
+}
 
 void launch_iteration_setup(void* dst, const void* src, size_t words, const int32_t* pos_host, float2* cs,
                             int rows, int hd, double theta, hipStream_t s) {

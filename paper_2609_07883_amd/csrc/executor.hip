@@ -856,6 +856,17 @@ extern "C" int slw_mixed_iteration_static(slw_ctx* ctx, const slw_batch* batch, 
     });
 }
 
+extern "C" int slw_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, void* stream) {
+    return guarded([&] {
+        if (!dst && n) return fail(SLW_EINVAL, "null buffer");
+        if (reinterpret_cast<uintptr_t>(dst) % 2) return fail(SLW_EINVAL, "buffer must be 2-byte aligned");
+        if (n / 4 >= (static_cast<size_t>(1) << 62)) return fail(SLW_ERANGE, "too many elements");
+        launch_fill_normal(dst, n, seed, mean, std, static_cast<hipStream_t>(stream));
+        HIP_TRY(hipGetLastError());
+        return SLW_OK;
+    });
+}
+
 extern "C" int slw_flush_cache(void* buf, size_t bytes, void* stream) {
     return guarded([&] {
         if (!buf && bytes) return fail(SLW_EINVAL, "null buffer");

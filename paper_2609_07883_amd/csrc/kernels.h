@@ -119,6 +119,10 @@ void launch_attention_merge(const ChunkAttnArgs* ca, const DecodeAttnArgs* da, h
 void launch_iteration_setup(void* dst, const void* src, size_t words, const int32_t* pos_host, float2* cs,
                             int rows, int hd, double theta, hipStream_t s);
 
+// dst[i] = bf16(mean + std z_i), z the standard normals of the Philox4x32-10
+// stream keyed by seed (element i from draw i / 4 by Box-Muller).
+void launch_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, hipStream_t s);
+
 // Read `bytes` of device memory (last-level cache flush that leaves no dirty
 // lines); the buffer is written only if a thread's xor of its words equals key.
 void launch_cache_sweep(void* p, size_t bytes, uint32_t key, hipStream_t s);

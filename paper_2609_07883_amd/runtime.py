@@ -36,10 +36,11 @@ class Session:
 
     def __init__(self, shape: synth.ModelShape, num_blocks: int, max_c: int, max_b: int,
                  layers=None, weight_seed: int = 0, qk_std=None, device_weights: bool = False):
-        """device_weights draws the weights on the GPU (torch's generator seeded
-        weight_seed + 1000 * layer; N(0, 0.02) matrices, 1 + N(0, 0.02) gains)
-        instead of the host recipe of ``synth.layer_weights``: for deep stacks
-        whose outputs are timed but never compared with the oracle."""
+        """device_weights draws the weights on the GPU (the library's Philox
+        generator, seeds derived from weight_seed + 1000 * layer; N(0, 0.02)
+        matrices, 1 + N(0, 0.02) gains) instead of the host recipe of
+        ``synth.layer_weights``: for deep stacks whose outputs are timed but
+        never compared with the oracle."""
         self.shape = shape
         self.dev = _dev()
         self.ctx = api.Context.from_shape(shape)
@@ -73,21 +74,20 @@ class Session:
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
 
     def _device_layer(self, seed: int) -> dict:
+        """One layer drawn on the device by the library's seeded generator:
+        matrix j of the layer (wqkv, wo, wgu, wd, g1, g2) from the stream
+        keyed by seed * 16 + j; N(0, 0.02) matrices, 1 + N(0, 0.02) gains."""
         s = self.shape
-        g = torch.Generator(device=self.dev)
-        g.manual_seed(seed)
         nqkv = (s.n_q_heads + 2 * s.n_kv_heads) * s.head_dim
         shapes = {"wqkv": (nqkv, s.d_model), "wo": (s.d_model, s.n_q_heads * s.head_dim),
-                  "wgu": (2 * s.ffn_dim, s.d_model), "wd": (s.d_model, s.ffn_dim)}
+                  "wgu": (2 * s.ffn_dim, s.d_model), "wd": (s.d_model, s.ffn_dim),
+                  "g1": (s.d_model,), "g2": (s.d_model,)}
+        stream = self.stream()
         w = {}
-        for k, shp in shapes.items():
+        for j, (k, shp) in enumerate(shapes.items()):
             t = torch.empty(shp, dtype=torch.bfloat16, device=self.dev)
-            for r0 in range(0, shp[0], 2048):      # bounded float32 staging
-                r1 = min(shp[0], r0 + 2048)
-                t[r0:r1] = (torch.randn((r1 - r0, shp[1]), generator=g, device=self.dev) * 0.02).bfloat16()
+            api.fill_normal(t.data_ptr(), t.numel(), seed * 16 + j, 1.0 if k in ("g1", "g2") else 0.0, 0.02, stream)
             w[k] = t
-        for k in ("g1", "g2"):
-            w[k] = (1.0 + 0.02 * torch.randn(s.d_model, generator=g, device=self.dev)).bfloat16()
         return w
 
     # -- iteration ------------------------------------------------------------
