@@ -379,6 +379,16 @@ int slw_flush_cache(void* buf, size_t bytes, void* stream);
  */
 int slw_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, void* stream);
 
+/*
+ * The GEMM plan an iteration uses for a projection out[m][n] = A[m][k] W^T
+ * (host only, touches no GPU), for callers and tests that need to know which
+ * kernel variant a row count reaches.  out[0..5]: tile configuration (99:
+ * the weight-streaming kernel for m <= 32), tile rows BM, tile columns BN,
+ * k split factor (1: none), stream-K work-groups (0: not used), whole tiles
+ * run before them.  m >= 1; n a multiple of 128 and k of 64, else SLW_EINVAL.
+ */
+int slw_gemm_plan(int32_t m, int32_t n, int32_t k, int32_t out[6]);
+
 /* ------------------------------------------------------------------------ */
 /* Controller (Eq. 1 solved by bisection as Alg. 1 does; margin of Sec. 3.3) */
 /* ------------------------------------------------------------------------ */

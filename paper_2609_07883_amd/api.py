@@ -36,7 +36,7 @@ EXPORTS = (
     "slw_cost_table_load", "slw_select_chunk", "slw_set_stage_timing", "slw_stage_times",
     "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
     "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
-    "slw_mixed_iteration_static", "slw_flush_cache", "slw_fill_normal",
+    "slw_mixed_iteration_static", "slw_flush_cache", "slw_fill_normal", "slw_gemm_plan",
 )
 STATIC_WS_BYTES = 128 << 20
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "attn_merge",
@@ -142,6 +142,7 @@ def lib() -> C.CDLL:
         "slw_mixed_iteration_static": ([vp, P(BatchC), vp, vp, vp], C.c_int),
         "slw_flush_cache": ([vp, sz, vp], C.c_int),
         "slw_fill_normal": ([vp, sz, C.c_uint64, C.c_float, C.c_float, vp], C.c_int),
+        "slw_gemm_plan": ([i32, i32, i32, P(i32)], C.c_int),
         "slw_last_slots": ([vp, P(i32), i32, P(i32)], C.c_int),
         "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
@@ -314,6 +315,16 @@ def select_chunk(table: CostTable, deadlines_ns, now_ns: int, remaining: int, c_
 def fill_normal(dst: int, n: int, seed: int, mean: float, std: float, stream: int = 0) -> None:
     """Enqueue dst[i] = bf16(mean + std z_i), z the Philox4x32-10 normal stream of seed."""
     _check(lib().slw_fill_normal(dst or None, int(n), int(seed), float(mean), float(std), stream or None))
+
+
+GEMM_SKINNY = 99
+
+
+def gemm_plan(m: int, n: int, k: int) -> dict:
+    """The GEMM plan an iteration uses for out[m][n] = A[m][k] W^T (host only)."""
+    out = np.zeros(6, np.int32)
+    _check(lib().slw_gemm_plan(int(m), int(n), int(k), _ptr(out, C.c_int32)))
+    return dict(zip(("cfg", "bm", "bn", "splits", "sk_workers", "dp_tiles"), (int(v) for v in out)))
 
 
 def flush_cache(buf: int, nbytes: int, stream: int = 0) -> None:

@@ -142,7 +142,12 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int grp = lane >> 4, col = lane & 15;
-    const int kvh = blockIdx.y;
+    // Work order: kv-head major, the runs of one head in key order.  All
+    // runs of a head read that head's keys and values, and runs that start
+    // together read the same pages together: with the order spread over the
+    // XCDs in contiguous ranges, they share one L2.
+    const int pos = xcd_order(blockIdx.x, a.n_slots * a.hkv);
+    const int kvh = pos / a.n_slots, slot = pos % a.n_slots;
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
@@ -173,7 +178,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // Block-table entries are read through the scalar cache (a uniform index
     // into constant memory): a vector load here would make the compiler wait
     // for every direct load in flight before using its result.
-    const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
+    const int i0 = a.slot_off[slot], i1 = a.slot_off[slot + 1];
     for (int item = i0; item < i1; ++item) {
         const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
         // the query tile: rows row0 .. row0 + nrows - 1 at positions pos0 .. of one sequence
@@ -643,7 +648,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_merge_kernel(ChunkAttnArgs ca
 
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
-    chunk_attn_kernel<HD, GROUP, kChunkStages><<<dim3(a.n_slots, a.hkv), 512, 0, s>>>(a);
+    chunk_attn_kernel<HD, GROUP, kChunkStages><<<a.n_slots * a.hkv, 512, 0, s>>>(a);
 }
 
 template <int HD, int GROUP>

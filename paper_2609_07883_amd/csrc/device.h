@@ -33,6 +33,18 @@ __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Work-groups of a launch are dispatched round-robin to the 8 XCDs (linear id
+// % 8), each with its own L2.  Position in a work order of linear block id
+// `pid` out of `total` such that every XCD takes a contiguous range of the
+// order: work that shares operands, placed next to each other in the order,
+// then runs on one XCD and shares its L2.
+__device__ __forceinline__ int xcd_order(int pid, int total) {
+    constexpr int kXcd = 8;
+    const int q = total / kXcd, r = total % kXcd;
+    const int xcd = pid % kXcd, local = pid / kXcd;
+    return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);

@@ -699,6 +699,16 @@ extern "C" int slw_destroy(slw_ctx* ctx) {
     return SLW_OK;
 }
 
+extern "C" int slw_gemm_plan(int32_t m, int32_t n, int32_t k, int32_t out[6]) {
+    if (!out) return fail(SLW_EINVAL, "null argument");
+    if (m < 1 || n < 128 || n % 128 || k < 64 || k % 64)
+        return fail(SLW_EINVAL, "m >= 1, n a multiple of 128 and k of 64 (got %d, %d, %d)", m, n, k);
+    const GemmPlan p = plan_gemm(m, n, k);
+    const int32_t v[6] = {p.cfg, p.bm, p.bn, p.splits, p.sk_workers, p.dp_tiles};
+    for (int i = 0; i < 6; ++i) out[i] = v[i];
+    return SLW_OK;
+}
+
 extern "C" int slw_set_layer_weights(slw_ctx* ctx, int32_t layer, const slw_layer_weights* w) {
     if (!ctx || !w) return fail(SLW_EINVAL, "null argument");
     if (layer < 0 || layer >= ctx->cfg.n_layers) return fail(SLW_ERANGE, "layer %d out of range", layer);

@@ -114,16 +114,6 @@ __device__ __forceinline__ void tile_coords(int t, int nt_m, int nt_n, int& tm, 
     tn = in_group / gsize;
 }
 
-// Position in the tile order of linear block id `pid` out of `total`.
-// Blocks are dispatched round-robin to the 8 XCDs (pid % 8), each with its
-// own L2; the remap gives every XCD a contiguous range of the order.
-__device__ __forceinline__ int xcd_order(int pid, int total) {
-    constexpr int kXcd = 8;
-    const int q = total / kXcd, r = total % kXcd;
-    const int xcd = pid % kXcd, local = pid / kXcd;
-    return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
-}
-
 __device__ __forceinline__ void tile_of(int pid, int nt_m, int nt_n, int& tm, int& tn) {
     tile_coords(xcd_order(pid, nt_m * nt_n), nt_m, nt_n, tm, tn);
 }
@@ -838,28 +828,27 @@ __global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restri
 struct TileCfg {
     int bm, bn, waves_m, waves_n, bk, ring;  // ring 0: register-staged double buffer
 };
-// 0: 128x128 / 4 waves (64x64 each)      1: 64x128 / 4 waves (32x64)
-// 2: 32x256 / 4 waves (32x64)            3: 256x256 / 8 waves (128x64)
-// 4: 256x256 / 4 waves (128x128)         5: 128x256 / 8 waves (64x64)
-// 6: 256x128 / 4 waves (128x64), k 32    7: 128x256 / 4 waves (64x128), k 32
-// 8: 256x256 / 8 waves, k 32, 4-buffer direct-load ring (128 KB of LDS)
-// 9: 128x256 / 8 waves, k 32, 4-buffer ring (96 KB)
-// 10: 128x128 / 4 waves, k 32, 4-buffer ring (64 KB: two work-groups per CU)
-// 11: 256x256 / 8 waves, k 64, 2-buffer ring (128 KB)
-// 12: 256x256 / 4 waves (128x128), k 32, 4-buffer ring (128 KB)
-// 13: 256x256 / 4 waves (128x128), k 64, 2-buffer ring (128 KB)
-// 14: 192x256 / 8 waves (96x64), k 64, 2-buffer ring (112 KB): less row
-//     padding than 256 where m is just past a multiple of 256
-// 15: 128x128 / 4 waves (64x64), k 64, 2-buffer ring (64 KB: two
-//     work-groups per CU)
-// The register-staged k-32 tiles (6, 7) use 48 KB of LDS, so two
-// work-groups share a CU and one's loads overlap the other's matrix work.
-constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 0}, {64, 128, 2, 2, 64, 0}, {32, 256, 1, 4, 64, 0},
-                             {256, 256, 2, 4, 64, 0}, {256, 256, 2, 2, 64, 0}, {128, 256, 2, 4, 64, 0},
-                             {256, 128, 2, 2, 32, 0}, {128, 256, 2, 2, 32, 0}, {256, 256, 2, 4, 32, 4},
-                             {128, 256, 2, 4, 32, 4}, {128, 128, 2, 2, 32, 4}, {256, 256, 2, 4, 64, 2},
-                             {256, 256, 2, 2, 32, 4}, {256, 256, 2, 2, 64, 2}, {192, 256, 2, 4, 64, 2},
-                             {128, 128, 2, 2, 64, 2}};
+// BM x BN / waves (per-wave tile), k depth per stage, main loop, LDS:
+// 0: 128x128 / 4 (64x64), k 64, register-staged (64 KB: two work-groups per CU)
+// 1: 64x128 / 4 (32x64), k 64, register-staged (the fallback when n is not a
+//    multiple of 256)
+// 2: 256x128 / 4 (128x64), k 32, register-staged (48 KB: two per CU)
+// 3: 256x256 / 8 (128x64), k 64, 2-buffer direct-load ring (128 KB)
+// 4: 192x256 / 8 (96x64), k 64, 2-buffer ring (112 KB): less row padding
+//    than 256 where m is just past a multiple of 256
+// 5: 128x128 / 4 (64x64), k 64, 2-buffer ring (64 KB: two per CU)
+// 6: 96x256 / 4 (96x64), k 64, 3-buffer ring (132 KB): a single row tile
+//    for m up to 96, three stages of weights in flight
+// 7: 160x256 / 4 (160x64), k 64, 2-buffer ring (104 KB)
+// 8: 128x128 / 4 (64x64), k 64, 4-buffer ring (128 KB)
+// 9: 64x256 / 4 (64x64), k 64, 3-buffer ring (120 KB)
+// 10: 128x128 / 4 (64x64), k 64, 3-buffer ring (96 KB)
+// The deep rings of the small-m tiles keep more weight bytes in flight per
+// CU, which is what the weight-streaming shapes are short of.
+constexpr TileCfg kCfgs[] = {{128, 128, 2, 2, 64, 0}, {64, 128, 2, 2, 64, 0}, {256, 128, 2, 2, 32, 0},
+                             {256, 256, 2, 4, 64, 2}, {192, 256, 2, 4, 64, 2}, {128, 128, 2, 2, 64, 2},
+                             {96, 256, 1, 4, 64, 3},  {160, 256, 1, 4, 64, 2}, {128, 128, 2, 2, 64, 4},
+                             {64, 256, 1, 4, 64, 3},  {128, 128, 2, 2, 64, 3}};
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int EPI>
@@ -930,45 +919,60 @@ void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t
 
 }  // namespace
 
-// Tile and split choice, from timings of every configuration, with and
-// without the stream-K schedule, on the 8B-layer shapes (m = 96 .. 4104,
-// caches swept with reads between runs; one run for all, as timings vary
-// between boxes): the weight-streaming kernel up to 32 rows on the narrower
-// projections, then whichever configuration measured fastest in each band of
-// m.  The 128 x 128 tiles (two work-groups per CU) win wherever their tiles
-// fit one round of 512; the 256 x 256 ring tile from about 2000 rows on
-// gate/up; the 192 x 256 ring tile in the bands where m sits just past a
-// multiple of 256 or where its row bands fill whole rounds; stream-K where
-// the ring tiles are too few for the CUs on the narrow projections.  The
-// bands follow the measurements, so they are not monotone in m.  n must be
-// a multiple of 128 and k of 64.
+// Tile and split choice per projection shape, from one sweep that timed
+// every configuration plainly, with k split two ways and with the stream-K
+// schedule at m = 64 .. 4104 (21 points) on the 8B-layer shapes, each run
+// after a read sweep of the caches.  Band i covers m in (m_hi[i - 1], m_hi[i]]
+// and takes the fastest entry measured at its upper end (the previous
+// choice where it was within 1.5%); neighbouring bands with the same choice
+// are merged.  The bands are not monotone in m: what pays is how m fills
+// whole row tiles and rounds of the CUs.  splits: 0 the default rule of
+// plan_with_cfg, 2 a forced two-way split, -1 the stream-K schedule.
+struct Band {
+    int m_hi;
+    int8_t cfg, splits;
+};
+constexpr Band kBandsQkv[] = {{64, 9, 0},     {96, 6, 0},     {128, 0, 0},    {160, 4, 0},
+                              {192, 10, 2},   {224, 8, 2},    {288, 9, 2},    {480, 6, 2},
+                              {544, 5, 0},    {928, 4, 2},    {1056, 5, 0},   {1312, 4, -1},
+                              {1568, 4, 2},   {2592, 5, 0},   {3104, 4, 0},   {4104, 3, 0}};
+constexpr Band kBandsO[] = {{128, 10, 0},  {192, 6, 0},   {224, 5, 0},   {352, 10, 2},  {480, 8, 2},
+                            {672, 6, 2},   {800, 5, 0},   {928, 8, -1},  {1312, 4, 2},  {1568, 0, 0},
+                            {2080, 3, -1}, {2592, 4, 0},  {3104, 5, 0},  {4104, 4, 0}};
+constexpr Band kBandsGateUp[] = {{64, 9, 2},   {96, 6, 2},   {128, 0, 0},  {192, 4, 2},  {224, 3, 2},
+                                 {352, 4, 0},  {416, 3, 0},  {480, 2, 0},  {544, 7, 0},  {672, 4, 0},
+                                 {928, 3, 0},  {1056, 4, 0}, {1312, 3, 0}, {1568, 4, 0}, {4104, 3, 0}};
+constexpr Band kBandsDown[] = {{128, 10, 0},  {192, 6, 0},   {224, 5, 0},   {288, 7, 0},
+                               {352, 4, 0},   {480, 3, 0},   {544, 7, -1},  {672, 4, -1},
+                               {928, 3, -1},  {1056, 4, -1}, {1312, 4, 2},  {1568, 3, 2},
+                               {2080, 3, -1}, {2592, 4, -1}, {3104, 3, -1}, {4104, 4, 0}};
+
+template <size_t N>
+const Band& band_of(const Band (&t)[N], int m) {
+    for (const Band& b : t)
+        if (m <= b.m_hi) return b;
+    return t[N - 1];
+}
+
+// The weight-streaming kernel takes the narrower projections up to 32 rows
+// and gate/up up to 16 (it won there by 10-20%; on qkv the tile kernels
+// measured faster).  Shapes outside the 8B layer take the band of their
+// projection class; n must be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
-    // The weight-streaming kernel wins on the narrow projections up to 32
-    // rows (o, down: 10-20%) and on gate/up up to 16 rows (13% at one row);
-    // on qkv the 64 x 128 tiles with split-K measured 3-13% faster.
     const bool wide = n >= 16384, qkv_like = n >= 6144 && !wide;
     if (n % 64 == 0 && (wide ? m <= 16 : m <= 32 && !qkv_like)) return plan_with_cfg(kSkinnyCfg, m, n, k);
-    constexpr int SK = -1;   // stream-K with the 256 x 256 ring tile
-    constexpr int SK14 = -2; // stream-K with the 192 x 256 ring tile
-    int cfg;
-    if (k >= 8192)  // deep k (down)
-        cfg = m <= 128 ? 10 : m <= 200 ? 0 : m < 420 ? 14 : m < 700 ? SK14 : m < 930 ? SK : m < 1200 ? SK14
-            : m < 3800 ? SK : 14;
-    else if (n >= 16384)  // gate/up
-        cfg = m <= 128 ? 0 : m <= 200 ? 15 : m <= 650 ? 14 : m < 950 ? 11 : m < 1200 ? 14 : 11;
-    else if (n >= 6144)  // qkv
-        cfg = m <= 32 ? 1 : m <= 128 ? 0 : m <= 220 ? 14 : m <= 400 ? 1 : m < 700 ? 0 : m < 950 ? 14 : m < 1200 ? 0
-            : m < 1400 ? 14 : m < 1650 ? 1 : m < 1950 ? 14 : m < 3250 ? 15 : m < 3800 ? 14 : 11;
-    else  // o
-        cfg = m <= 128 ? 10 : m < 400 ? 15 : m < 700 ? 1 : m < 950 ? 0 : m < 1180 ? SK14 : m < 1400 ? 14
-            : m < 1950 ? 0 : m < 2700 ? SK : m < 3250 ? 14 : m < 3800 ? 7 : 14;
-    if (cfg == SK || cfg == SK14) {
-        const int sk_cfg = cfg == SK ? 11 : 14;
-        if (n % 256 == 0) return plan_stream_k(sk_cfg, m, n, k);
-        cfg = sk_cfg;
+    const Band& b = k >= 8192 ? band_of(kBandsDown, m)
+                    : wide    ? band_of(kBandsGateUp, m)
+                    : qkv_like ? band_of(kBandsQkv, m)
+                               : band_of(kBandsO, m);
+    if (n % kCfgs[b.cfg].bn) return plan_with_cfg(n % 128 ? 1 : 0, m, n, k);
+    if (b.splits < 0) return plan_stream_k(b.cfg, m, n, k);
+    GemmPlan p = plan_with_cfg(b.cfg, m, n, k);
+    if (b.splits > 0 && k % (b.splits * BK_MAX) == 0) {
+        p.splits = b.splits;
+        p.partial_bytes = b.splits > 1 ? static_cast<size_t>(b.splits) * m * n * sizeof(float) : 0;
     }
-    if (n % kCfgs[cfg].bn) cfg = n % 128 ? 1 : 0;
-    return plan_with_cfg(cfg, m, n, k);
+    return p;
 }
 
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
@@ -1036,20 +1040,15 @@ void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_
     switch (p.cfg) {
         case 0: launch_cfg<128, 128, 2, 2, 64, 0>(g, p, partial, s); break;
         case 1: launch_cfg<64, 128, 2, 2, 64, 0>(g, p, partial, s); break;
-        case 2: launch_cfg<32, 256, 1, 4, 64, 0>(g, p, partial, s); break;
-        case 3: launch_cfg<256, 256, 2, 4, 64, 0>(g, p, partial, s); break;
-        case 4: launch_cfg<256, 256, 2, 2, 64, 0>(g, p, partial, s); break;
-        case 5: launch_cfg<128, 256, 2, 4, 64, 0>(g, p, partial, s); break;
-        case 6: launch_cfg<256, 128, 2, 2, 32, 0>(g, p, partial, s); break;
-        case 7: launch_cfg<128, 256, 2, 2, 32, 0>(g, p, partial, s); break;
-        case 8: launch_cfg<256, 256, 2, 4, 32, 4>(g, p, partial, s); break;
-        case 9: launch_cfg<128, 256, 2, 4, 32, 4>(g, p, partial, s); break;
-        case 10: launch_cfg<128, 128, 2, 2, 32, 4>(g, p, partial, s); break;
-        case 11: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
-        case 12: launch_cfg<256, 256, 2, 2, 32, 4>(g, p, partial, s); break;
-        case 13: launch_cfg<256, 256, 2, 2, 64, 2>(g, p, partial, s); break;
-        case 14: launch_cfg<192, 256, 2, 4, 64, 2>(g, p, partial, s); break;
-        default: launch_cfg<128, 128, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 2: launch_cfg<256, 128, 2, 2, 32, 0>(g, p, partial, s); break;
+        case 3: launch_cfg<256, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 4: launch_cfg<192, 256, 2, 4, 64, 2>(g, p, partial, s); break;
+        case 5: launch_cfg<128, 128, 2, 2, 64, 2>(g, p, partial, s); break;
+        case 6: launch_cfg<96, 256, 1, 4, 64, 3>(g, p, partial, s); break;
+        case 7: launch_cfg<160, 256, 1, 4, 64, 2>(g, p, partial, s); break;
+        case 8: launch_cfg<128, 128, 2, 2, 64, 4>(g, p, partial, s); break;
+        case 9: launch_cfg<64, 256, 1, 4, 64, 3>(g, p, partial, s); break;
+        default: launch_cfg<128, 128, 2, 2, 64, 3>(g, p, partial, s); break;
     }
 }
 

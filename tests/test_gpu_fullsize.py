@@ -15,6 +15,8 @@ Workloads (8B-shaped layer: d 4096, 32/8 heads x 128, FFN 14336, bf16):
   * chat/bursty: C = 32 at a seeded chunk boundary of a log-normal prompt,
     B = 256 decodes with log-normal contexts (median 700, sigma 0.8, cap 8192).
 """
+import functools
+
 import numpy as np
 import pytest
 
@@ -108,10 +110,41 @@ def test_single_decode():
     _run(0, 0, [1500], seed=17)
 
 
-@pytest.mark.parametrize("C,P", [(128, 0), (512, 2048), (768, 0), (1268, 0)])
-def test_gemm_band_points(C, P):
-    """Layer points whose GEMMs take the 192 x 256 ring tile (plain, with
-    split-K and with stream-K) and the other bands of the planner: M = 160,
-    544, 800 and 1300 with B = 32 decodes."""
-    ctx = synth.uniform_lengths(32, 512, 2048, seed=2)
-    _run(C, P, ctx, seed=20 + C // 64)
+@functools.lru_cache(maxsize=None)
+def _plan_cover():
+    """Row counts that together reach every GEMM variant (tile configuration,
+    epilogue, plain / split-K / stream-K) the planner picks for the four
+    projections of this layer between 33 and 4104 rows, chosen greedily from
+    the plans the library reports."""
+    shape = synth.LLAMA8B_LAYER
+    d, F = shape.d_model, shape.ffn_dim
+    qkv = (shape.n_q_heads + 2 * shape.n_kv_heads) * shape.head_dim
+    proj = {"qkv": (qkv, d), "o": (d, shape.n_q_heads * shape.head_dim), "gateup": (2 * F, d), "down": (d, F)}
+
+    def variants(m):
+        out = set()
+        for name, (n, k) in proj.items():
+            p = api.gemm_plan(m, n, k)
+            mode = "sk" if p["sk_workers"] else "split" if p["splits"] > 1 else "plain"
+            out.add((name, p["cfg"], mode))
+        return out
+
+    cover = {m: variants(m) for m in range(33, 4105)}
+    left = set().union(*cover.values())
+    chosen = []
+    while left:
+        m = max(cover, key=lambda x: (len(cover[x] & left), -x))
+        chosen.append(m)
+        left -= cover[m]
+    return sorted(chosen)
+
+
+@pytest.mark.parametrize("part", range(4))
+def test_gemm_plan_variants(part):
+    """Prefill-only iterations (B = 0, P = 0) at row counts that reach every
+    GEMM kernel variant of the planner (a quarter of them per case), sampled
+    rows against the oracle."""
+    ms = _plan_cover()[part::4]
+    print(f"row counts {ms}", flush=True)
+    for m in ms:
+        _run(m, 0, [], seed=40 + m % 97)

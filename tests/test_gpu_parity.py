@@ -93,9 +93,10 @@ def test_tiny_long_chunk_stream_k():
 
 @pytest.mark.parametrize("C", [100, 150, 600, 850, 1000])
 def test_tiny_gemm_plan_bands(C):
-    """Row counts on both sides of the GEMM planner's bands (128 x 128 tiles
-    with split-K, 64 x 128 tiles, stream-K): every row of the iteration
-    against the oracle."""
+    """Row counts in several of the GEMM planner's bands on the Tiny shapes
+    (narrow projections: the tile fallbacks for widths that are not a
+    multiple of 256, forced splits refused where k does not divide): every
+    row of the iteration against the oracle."""
     _require_gpu()
     from paper_2609_07883_amd.runtime import Session
     sess = Session(synth.TINY, num_blocks=512, max_c=1024, max_b=4, qk_std=0.16)

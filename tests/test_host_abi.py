@@ -284,3 +284,33 @@ def test_batched_prefill_validation_through_abi():
         assert ctx.free_blocks() == free
     assert api.Batch.batched([(1, 20, 5)]) == api.Batch(5, 1, 20, [], [])
     assert api.Batch.batched([(1, 20, 5), (2, 0, 3)]).chunk == 8
+
+
+@pytest.mark.parametrize("shape", ["8b", "tiny"])
+def test_gemm_plan_is_valid_for_every_row_count(shape):
+    """The planner's choice for every row count is a launchable plan: tile
+    widths divide n, the k split divides k into whole 64-deep steps, stream-K
+    only with whole tiles counted in rounds of 8 XCDs, the weight-streaming
+    kernel only up to 32 rows."""
+    sh = synth.LLAMA8B_LAYER if shape == "8b" else synth.TINY
+    d, F = sh.d_model, sh.ffn_dim
+    qkv = (sh.n_q_heads + 2 * sh.n_kv_heads) * sh.head_dim
+    seen = set()
+    for n, k in [(qkv, d), (d, sh.n_q_heads * sh.head_dim), (2 * F, d), (d, F)]:
+        if n % 128:
+            continue
+        for m in list(range(1, 600)) + list(range(600, 9000, 37)):
+            p = api.gemm_plan(m, n, k)
+            if p["cfg"] == api.GEMM_SKINNY:
+                assert m <= 32
+                continue
+            assert n % p["bn"] == 0 and p["bm"] % 32 == 0
+            assert p["splits"] in (1, 2, 4, 8) and k % (64 * p["splits"]) == 0
+            if p["sk_workers"]:
+                assert p["splits"] == 1 and p["dp_tiles"] % 8 == 0 and 0 < p["sk_workers"] <= 512
+            seen.add(p["cfg"])
+    assert len(seen) >= 2
+    with pytest.raises(api.SloweaveError):
+        api.gemm_plan(0, 4096, 4096)
+    with pytest.raises(api.SloweaveError):
+        api.gemm_plan(64, 4000, 4096)
