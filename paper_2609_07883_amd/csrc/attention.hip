@@ -205,12 +205,21 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
         }
 
         const int last_page = (ke - 1) >> 4;
+        // Block ids of the pages the wave's loads of a tile read, fetched
+        // through the scalar cache one tile before the loads that use them:
+        // the wait for a scalar load then costs nothing where the loads are
+        // issued (read there, it stalled every wave of the CU once per page).
+        int blk_next[PER_WAVE];
+        auto fetch = [&](int t) {
+#pragma unroll
+            for (int i = 0; i < PER_WAVE; ++i)
+                blk_next[i] = bt_s[__builtin_amdgcn_readfirstlane(min((kb >> 4) + 4 * t + l_page[i], last_page))];
+        };
         auto issue = [&](int t) {
             const int buf = t % ST;
 #pragma unroll
             for (int i = 0; i < PER_WAVE; ++i) {
-                const int pg = __builtin_amdgcn_readfirstlane(min((kb >> 4) + 4 * t + l_page[i], last_page));
-                const size_t blk = bt_s[pg];
+                const size_t blk = blk_next[i];
                 const bf16* src = (l_isv[i] ? vpool : kpool) + (blk * a.hkv + kvh) * PAGE + l_elem[i];
                 load_lds16(src, l_isv[i] ? &Vs[buf][l_dst[i]] : &Ks[buf][l_dst[i]]);
             }
@@ -237,7 +246,11 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
         if (item != i0) barrier_only();
 #pragma unroll
         for (int t = 0; t < ST - 1; ++t)
-            if (t < n_tiles) issue(t);
+            if (t < n_tiles) {
+                fetch(t);
+                issue(t);
+            }
+        if (ST - 1 < n_tiles) fetch(ST - 1);
         for (int t = 0; t < n_tiles; ++t) {
             const int buf = t % ST;
             // this wave's loads of tile t are done once at most the loads of the
@@ -344,6 +357,10 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
                     }
                 }
             }
+            // after the tile's last LDS read: scalar loads return out of
+            // order, so one in flight makes every wait for an LDS read a
+            // wait for it too
+            if (t + ST < n_tiles) fetch(t + ST);
         }
         if (!wave_live) continue;
 
