@@ -233,8 +233,8 @@ def main():
     ap.add_argument("--tpots", default="25,10", help="serve: comma-separated TPOT objectives (ms)")
     ap.add_argument("--table-save", default=None, help="serve: write the profiled cost table here")
     ap.add_argument("--table-load", default=None, help="serve: read the cost table from here instead of profiling")
-    ap.add_argument("--fallback-margin-ms", type=float, default=1.0,
-                    help="serve: configured margin delta of the fallback policy (ms)")
+    ap.add_argument("--fallback-margin-ms", type=float, default=None,
+                    help="serve: configured margin delta of the fallback policy (ms; default 10%% of the TPOT)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device copy (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -530,11 +530,12 @@ def serve_main(args):
     for D in tpots:
         for name in args.policies.split(","):
             pol, fc, window, fb = SERVE_POLICIES[name]
-            margin = int(args.fallback_margin_ms * 1e6) if fb else 0
+            delta_ms = args.fallback_margin_ms if args.fallback_margin_ms is not None else 0.1 * D
+            margin = int(round(delta_ms * 1e6)) if fb else 0
             t2 = time.time()
             res = serving.run(trace, policy=pol, fixed_chunk=fc, tpot_ms=D, max_decode=max_b, c_max=4096,
                               table=ct, session=sess, residual_window=window, fallback_window=fb,
-                              margin_ns=margin)
+                              margin_ns=margin, log_every=2000)
             wall = time.time() - t2
             m = serving.metrics(trace, res.token_ns, ttft_slo_ms=1000.0, tpot_slo_ms=D)
             it = res.iterations

@@ -527,6 +527,10 @@ typedef struct slw_serve_opts {
      * iterations keep filling the window, so chunks return once the observed
      * residuals are back within the margin.  0 = off. */
     int32_t fallback_window;
+    /* Progress: after every log_every-th iteration the loop writes one line
+     * to stderr (iterations so far, trace clock, requests done), so that a
+     * long run shows where it is.  0 = silent. */
+    int32_t log_every;
 } slw_serve_opts;
 
 /* One iteration of a serving run (host memory). */

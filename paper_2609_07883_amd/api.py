@@ -93,7 +93,8 @@ class ServeOpts(C.Structure):
                 ("ws", C.c_void_p), ("ws_bytes", C.c_size_t), ("stream", C.c_void_p),
                 ("residual_window", C.c_int32), ("exec_table", C.c_void_p), ("slo", C.c_void_p),
                 ("queue", C.c_int32), ("admit_ppm", C.c_int32), ("aging_ns", C.c_int64),
-                ("aging_chunk", C.c_int32), ("max_prefills", C.c_int32), ("fallback_window", C.c_int32)]
+                ("aging_chunk", C.c_int32), ("max_prefills", C.c_int32), ("fallback_window", C.c_int32),
+                ("log_every", C.c_int32)]
 
 
 class RequestSloC(C.Structure):
@@ -351,7 +352,7 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
           stream: int = 0, iter_cap: int | None = None, residual_window: int = 0,
           exec_table: CostTable | None = None, slo_tpot_ns=None, slo_margin_ns=None, slo_ttft_ns=None,
           queue: str = "oldest", admit_ppm: int = 0, aging_ns: int = 0, aging_chunk: int = 0,
-          max_prefills: int = 1, fallback_window: int = 0):
+          max_prefills: int = 1, fallback_window: int = 0, log_every: int = 0):
     """slw_serve over a trace given as arrays.
 
     slo_tpot_ns / slo_margin_ns / slo_ttft_ns are optional per-request
@@ -380,7 +381,7 @@ def serve(ids, arrival_ns, prompt, output, *, policy: int, tpot_ns: int, max_dec
                   x_in or None, x_out or None, max_rows, ws or None, ws_bytes, stream or None,
                   residual_window, exec_table.handle if exec_table is not None else None,
                   C.cast(slo, C.c_void_p) if slo is not None else None, QUEUES[queue], int(admit_ppm),
-                  int(aging_ns), int(aging_chunk), int(max_prefills), int(fallback_window))
+                  int(aging_ns), int(aging_chunk), int(max_prefills), int(fallback_window), int(log_every))
     nit = C.c_int64()
     _check(lib().slw_serve(ctx._h if ctx is not None else None, reqs, n, C.byref(o), _ptr(tok, C.c_int64),
                            len(tok), its.ctypes.data_as(C.POINTER(IterationRecord)), len(its), C.byref(nit)))

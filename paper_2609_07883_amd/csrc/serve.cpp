@@ -13,6 +13,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cstdio>
 #include <cstdint>
 #include <limits>
 #include <map>
@@ -67,6 +68,7 @@ int check_opts(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
     if (o->aging_ns < 0 || (o->aging_ns > 0 && o->aging_chunk < 1))
         return fail(SLW_EINVAL, "aging needs aging_ns >= 0 and aging_chunk >= 1");
     if (o->max_prefills < 0) return fail(SLW_EINVAL, "max_prefills must be >= 0");
+    if (o->log_every < 0) return fail(SLW_EINVAL, "log_every must be >= 0");
     if (o->fallback_window < 0 || o->fallback_window > 65536)
         return fail(SLW_ERANGE, "fallback_window must be in [0, 65536]");
     if (o->fallback_window > 0 && !o->table) return fail(SLW_EINVAL, "the telemetry fallback needs a cost table");
@@ -376,6 +378,9 @@ int serve_impl(slw_ctx* ctx, const slw_request* reqs, int32_t n, const slw_serve
         rec.end_ns = end;
         if (chunk > 0) rec.prefill_id = reqs[head->req].id;
         iters[(*n_iters)++] = rec;
+        if (o->log_every > 0 && *n_iters % o->log_every == 0)
+            std::fprintf(stderr, "slw_serve: %lld iterations, trace clock %.1f s, %d of %d requests done\n",
+                         static_cast<long long>(*n_iters), static_cast<double>(end) * 1e-9, finished, n);
         if (W > 0 && chunk > 0 && rec.predicted_ns > 0) {
             const int64_t num = (end - t - rec.predicted_ns) * 1000000;
             int64_t q = num / rec.predicted_ns;

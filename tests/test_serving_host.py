@@ -282,3 +282,18 @@ def test_telemetry_fallback_hand_worked_case():
     assert its["chunk"].tolist() == [100, 0, 200, 0, 0]
     assert ((its["flags"] & api.SERVE_FALLBACK) != 0).tolist() == [False, True, False, False, False]
     assert its["resid_p99_ns"].tolist() == [0, 1_500_000, 0, 0, 0]
+
+
+def test_progress_lines_leave_the_run_unchanged(capfd):
+    """log_every only writes status lines: the iteration records and token
+    times are those of a silent run; a negative period is refused."""
+    tr = synth.request_trace(12, 2.0, seed=5)
+    quiet = serving.run(tr, policy="fixed", fixed_chunk=256, tpot_ms=25, max_decode=64)
+    loud = serving.run(tr, policy="fixed", fixed_chunk=256, tpot_ms=25, max_decode=64, log_every=100)
+    err = capfd.readouterr().err
+    fields = [f for f in quiet.iterations.dtype.names if f != "decide_ns"]  # host timing of Alg. 1
+    assert np.array_equal(quiet.iterations[fields], loud.iterations[fields])
+    assert all(np.array_equal(a, b) for a, b in zip(quiet.token_ns, loud.token_ns))
+    assert err.count("slw_serve:") == len(loud.iterations) // 100
+    with pytest.raises(api.SloweaveError):
+        serving.run(tr, policy="fixed", fixed_chunk=256, tpot_ms=25, max_decode=64, log_every=-1)
