@@ -466,9 +466,13 @@ __device__ __forceinline__ void chunk_merge_row(const ChunkAttnArgs& a, int x, i
 }
 
 // ---------------------------------------------------------------------------
-// Decode attention, split over the key axis: one wave per (work item, kv
-// head); a work item is one split of `split_tokens` keys of one decode.  All
-// q heads of the kv head's group (<= 16) are the columns of Q^T.  Keys are
+// Decode attention, split over the key axis: one wave per (slot, kv head).
+// The host lays the keys of all decodes end to end and cuts them into equal
+// runs, one per slot; a slot's run is a list of work items (a key range of
+// one decode, starting on a multiple of 64), which the wave takes one after
+// the other, each leaving a partial for the merge.  Equal runs make every
+// wave of the launch finish together, where one wave per fixed-size split
+// left a ragged last round.  All q heads of the kv head's group (<= 16) are the columns of Q^T.  Keys are
 // taken 32 at a time (two pages) straight from the pages into MFMA operand
 // registers, with the next step's pages requested before the current step is
 // multiplied (two register sets), so every wave keeps 16 KB of loads in
@@ -487,7 +491,7 @@ struct DecodeStep {
 // The loads of one step.  The two block-table entries of the pair come
 // through the scalar cache (bt_s is wave-uniform): a vector load there would
 // make the wave wait for every load in flight, the previous step's prefetch
-// included, before it could address the next pages.  Pages past the split's
+// included, before it could address the next pages.  Pages past the item's
 // last page load that page instead, so every load is unconditional and the
 // waits can count; keys at or past tok1 are masked (scores) and zeroed (V)
 // by the caller.
@@ -521,129 +525,131 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
     constexpr int KK = HD / 32, NT = HD / 16;
     constexpr float kSlack = 8.0f;  // lazy rescaling threshold (log2 units)
     const int lane = threadIdx.x, grp = lane >> 4, col = lane & 15;
-    const int w = blockIdx.x, kvh = blockIdx.y;
-    const int b = a.work_b[w], split = a.work_s[w];
+    const int kvh = blockIdx.y;
     const int group = a.hq / a.hkv;
-    const int kv_len = a.kv_len[b];
-    const int tok0 = split * a.split_tokens;
-    const int tok1 = min(tok0 + a.split_tokens, kv_len);
-    const int last_pg = (tok1 - 1) >> 4;
-    const const_i32* bt_s = (const const_i32*)(a.bt + a.bt_off[b]);
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
-
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
 
-    bf16x8 qf[KK];
-    {
-        const bf16* q = static_cast<const bf16*>(a.q) + static_cast<size_t>(b) * a.ld_q;
-        const int h = kvh * group + col;
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk)
-            qf[kk] = col < group ? *reinterpret_cast<const bf16x8*>(q + h * HD + kk * 32 + grp * 8)
-                                 : bf16x8{};
-    }
+    // The wave's items one after the other: keys [tok0, tok1) of decode b,
+    // each leaving its partial (running max, sum, unnormalised output).
+    const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
+    for (int w = i0; w < i1; ++w) {
+        const int b = a.work_b[w], tok0 = a.work_kb[w], tok1 = a.work_ke[w];
+        const int last_pg = (tok1 - 1) >> 4;
+        const const_i32* bt_s = (const const_i32*)(a.bt + a.bt_off[b]);
 
-    f32x4 o[NT];
+        bf16x8 qf[KK];
+        {
+            const bf16* q = static_cast<const bf16*>(a.q) + static_cast<size_t>(b) * a.ld_q;
+            const int h = kvh * group + col;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{};
-    float m_run = -INFINITY, l_run = 0.f;
-
-    // lane (grp, col): element e of score tile tau is key 8 grp + 4 tau + e of
-    // the step.  Keys at or past tok1 (the split's end; stand-in pages and
-    // unwritten slots lie there) get score -inf and V 0, without branches: a
-    // branch that rewrites loaded registers makes the compiler's wait counts
-    // conservative and stalls on the prefetch in flight.
-    auto compute = [&](DecodeStep<HD>& st, int c0) {
-        const int nv = min(max(tok1 - c0 - 8 * grp, 0), 8);  // valid keys of this lane group
-        u32x4 vmask;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            vmask[j] = (2 * j < nv ? 0x0000FFFFu : 0u) | (2 * j + 1 < nv ? 0xFFFF0000u : 0u);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            u32x4 bits = __builtin_bit_cast(u32x4, st.v[nt]) & vmask;
-            st.v[nt] = __builtin_bit_cast(bf16x8, bits);
+            for (int kk = 0; kk < KK; ++kk)
+                qf[kk] = col < group ? *reinterpret_cast<const bf16x8*>(q + h * HD + kk * 32 + grp * 8)
+                                     : bf16x8{};
         }
-        f32x4 s[2];
-#pragma unroll
-        for (int tau = 0; tau < 2; ++tau) {
-            s[tau] = f32x4{};
-#pragma unroll
-            for (int kk = 0; kk < KK; ++kk) s[tau] = mfma16(st.k[tau][kk], qf[kk], s[tau]);
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float x = 4 * tau + e < nv ? s[tau][e] : -INFINITY;
-                s[tau][e] = x;
-                mx = fmaxf(mx, x);
-            }
-        mx = rows4_max(mx);
-        mx *= sl2;
-        if (__any(mx > m_run + kSlack)) {
-            const float m_new = fmaxf(m_run, mx);
-            const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
-            l_run *= alpha;
-            m_run = m_new;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float ae = __shfl(alpha, grp * 4 + e, 64);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) o[nt][e] *= ae;
-            }
-        }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        float ls = 0.f;
-#pragma unroll
-        for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float v = fast_exp2(fmaf(s[tau][e], sl2, -m_use));
-                s[tau][e] = v;
-                ls += v;
-            }
-        l_run += ls;
-        const bf16x8 pf = to_bf16x8(s[0], s[1]);  // keys 8 grp .. 8 grp + 7 in order
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, st.v[nt], o[nt]);
-    };
 
-    // The next step's loads are issued before every step's compute, also
-    // past the split's end (they then re-read its last page, still in L2):
-    // no branch skips a load, so the compiler's counted waits leave the
-    // prefetched step in flight while the current one is multiplied.
-    DecodeStep<HD> sa, sb;
-    decode_load<HD>(sa, kpool, vpool, bt_s, tok0, last_pg, a.hkv, kvh, col, grp);
-    for (int c0 = tok0;; c0 += 64) {
-        decode_load<HD>(sb, kpool, vpool, bt_s, c0 + 32, last_pg, a.hkv, kvh, col, grp);
-        compute(sa, c0);
-        if (c0 + 32 >= tok1) break;
-        decode_load<HD>(sa, kpool, vpool, bt_s, c0 + 64, last_pg, a.hkv, kvh, col, grp);
-        compute(sb, c0 + 32);
-        if (c0 + 64 >= tok1) break;
-    }
+        f32x4 o[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) o[nt] = f32x4{};
+        float m_run = -INFINITY, l_run = 0.f;
 
-    float l = l_run;
-    l = rows4_sum(l);
-    const size_t hbase = static_cast<size_t>(w) * a.hq + kvh * group;
-    if (grp == 0 && col < group) {
-        a.part_ml[(hbase + col) * 2 + 0] = m_run;
-        a.part_ml[(hbase + col) * 2 + 1] = l;
-    }
+        // lane (grp, col): element e of score tile tau is key 8 grp + 4 tau + e of
+        // the step.  Keys at or past tok1 (the item's end; stand-in pages and
+        // unwritten slots lie there) get score -inf and V 0, without branches: a
+        // branch that rewrites loaded registers makes the compiler's wait counts
+        // conservative and stalls on the prefetch in flight.
+        auto compute = [&](DecodeStep<HD>& st, int c0) {
+            const int nv = min(max(tok1 - c0 - 8 * grp, 0), 8);  // valid keys of this lane group
+            u32x4 vmask;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int h = grp * 4 + e;
-        if (h < group) {
+            for (int j = 0; j < 4; ++j)
+                vmask[j] = (2 * j < nv ? 0x0000FFFFu : 0u) | (2 * j + 1 < nv ? 0xFFFF0000u : 0u);
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) a.part_o[(hbase + h) * HD + nt * 16 + col] = o[nt][e];
+            for (int nt = 0; nt < NT; ++nt) {
+                u32x4 bits = __builtin_bit_cast(u32x4, st.v[nt]) & vmask;
+                st.v[nt] = __builtin_bit_cast(bf16x8, bits);
+            }
+            f32x4 s[2];
+#pragma unroll
+            for (int tau = 0; tau < 2; ++tau) {
+                s[tau] = f32x4{};
+#pragma unroll
+                for (int kk = 0; kk < KK; ++kk) s[tau] = mfma16(st.k[tau][kk], qf[kk], s[tau]);
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float x = 4 * tau + e < nv ? s[tau][e] : -INFINITY;
+                    s[tau][e] = x;
+                    mx = fmaxf(mx, x);
+                }
+            mx = rows4_max(mx);
+            mx *= sl2;
+            if (__any(mx > m_run + kSlack)) {
+                const float m_new = fmaxf(m_run, mx);
+                const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
+                l_run *= alpha;
+                m_run = m_new;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float ae = __shfl(alpha, grp * 4 + e, 64);
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) o[nt][e] *= ae;
+                }
+            }
+            const float m_use = m_run == -INFINITY ? 0.f : m_run;
+            float ls = 0.f;
+#pragma unroll
+            for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float v = fast_exp2(fmaf(s[tau][e], sl2, -m_use));
+                    s[tau][e] = v;
+                    ls += v;
+                }
+            l_run += ls;
+            const bf16x8 pf = to_bf16x8(s[0], s[1]);  // keys 8 grp .. 8 grp + 7 in order
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) o[nt] = mfma16(pf, st.v[nt], o[nt]);
+        };
+
+        // The next step's loads are issued before every step's compute, also
+        // past the item's end (they then re-read its last page, still in L2):
+        // no branch skips a load, so the compiler's counted waits leave the
+        // prefetched step in flight while the current one is multiplied.
+        DecodeStep<HD> sa, sb;
+        decode_load<HD>(sa, kpool, vpool, bt_s, tok0, last_pg, a.hkv, kvh, col, grp);
+        for (int c0 = tok0;; c0 += 64) {
+            decode_load<HD>(sb, kpool, vpool, bt_s, c0 + 32, last_pg, a.hkv, kvh, col, grp);
+            compute(sa, c0);
+            if (c0 + 32 >= tok1) break;
+            decode_load<HD>(sa, kpool, vpool, bt_s, c0 + 64, last_pg, a.hkv, kvh, col, grp);
+            compute(sb, c0 + 32);
+            if (c0 + 64 >= tok1) break;
+        }
+
+        float l = l_run;
+        l = rows4_sum(l);
+        const size_t hbase = static_cast<size_t>(w) * a.hq + kvh * group;
+        if (grp == 0 && col < group) {
+            a.part_ml[(hbase + col) * 2 + 0] = m_run;
+            a.part_ml[(hbase + col) * 2 + 1] = l;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int h = grp * 4 + e;
+            if (h < group) {
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) a.part_o[(hbase + h) * HD + nt * 16 + col] = o[nt][e];
+            }
         }
     }
 }
 
-// Merge the splits of one (decode, q head): weights 2^(m_s - max m).
+// Merge the items of one (decode, q head): weights 2^(m_s - max m).
 template <int HD>
 __device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b, int h) {
     const int w0 = a.work_off[b], w1 = a.work_off[b + 1];
@@ -711,7 +717,7 @@ void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s) {
 
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s) {
     if (a.b <= 0) return;
-    dim3 grid(a.n_work, a.hkv);
+    dim3 grid(a.n_slots, a.hkv);
     if (a.hd == 128) decode_attn_kernel<128><<<grid, 64, 0, s>>>(a);
     else decode_attn_kernel<64><<<grid, 64, 0, s>>>(a);
 }

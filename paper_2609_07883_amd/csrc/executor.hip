@@ -26,7 +26,12 @@ using namespace slw;
 namespace {
 
 constexpr int kRing = 4;                 // pinned staging buffers in flight
-constexpr int kDecodeTargetWaves = 4096; // decode work-groups aimed for per iteration
+// Decode attention runs one wave per work-group, two per SIMD (its register
+// use allows no more): kDecodeWaves of them fill a 256-CU part once.  Their
+// keys are cut into equal runs (at least kDecodeMinKeys each), so that every
+// wave of the launch finishes at about the same time.
+constexpr int kDecodeWaves = 2048;
+constexpr int kDecodeMinKeys = 128;
 // Chunk attention runs one work-group per CU (its register use allows no
 // more), so a launch of kChunkSlots work-groups with equal work finishes in
 // one round on a 256-CU part.  A work-group takes at least kChunkMinTiles
@@ -67,6 +72,8 @@ struct slw_ctx {
     std::vector<Prefill> prefills;     // the iteration's prefills in row order
     std::vector<int32_t> meta;  // host build area
     std::vector<int32_t> items; // chunk-attention work items (host build area)
+    // decode-attention work items and wave slots (host build area)
+    std::vector<int32_t> dwork_b, dwork_kb, dwork_ke, dwork_off, dslot_off;
 
     // HIP resources, created on first device use
     bool hip_ready = false;
@@ -109,18 +116,9 @@ namespace {
 
 int qkv_width(const slw_model_cfg& c) { return (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim; }
 int max_blocks(const slw_model_cfg& c) { return static_cast<int>(ceil_div(c.max_pos, 16)); }
-int decode_work_cap(const slw_model_cfg& c, int B) {
-    return std::max(1, kDecodeTargetWaves / c.n_kv_heads) + B + 1;
-}
-
-// Keys per split: a multiple of 64 chosen so that about kDecodeTargetWaves
-// work-groups cover all decodes' keys (at least 128 keys each).
-int decode_split_tokens(const slw_model_cfg& c, int64_t total_keys) {
-    const int64_t per_head = std::max(1, kDecodeTargetWaves / c.n_kv_heads);
-    int64_t s = ceil_div(total_keys, per_head);
-    s = ceil_div(std::max<int64_t>(s, 128), 64) * 64;
-    return static_cast<int>(s);
-}
+int decode_slot_cap(const slw_model_cfg& c) { return std::max(1, kDecodeWaves / c.n_kv_heads); }
+// A run crosses at most one decode boundary more than it has runs: items <= slots + B - 1.
+int decode_work_cap(const slw_model_cfg& c, int B) { return decode_slot_cap(c) + B + 1; }
 
 // Query tiles of the chunk rows: each prefill's rows are tiled on their own,
 // so up to SLW_MAX_PREFILLS - 1 tiles more than one prefill of C rows needs.
@@ -139,7 +137,8 @@ size_t meta_ints(const slw_model_cfg& c, int C, int B) {
     const size_t mb = static_cast<size_t>(max_blocks(c));
     const size_t np = C > 0 ? static_cast<size_t>(std::min(C, static_cast<int>(SLW_MAX_PREFILLS))) : 0;
     return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + np * mb +
-           2 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + 3 * static_cast<size_t>(chunk_item_cap(c, C)) +
+           3 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + decode_slot_cap(c) + 1 +
+           3 * static_cast<size_t>(chunk_item_cap(c, C)) +
            5 * static_cast<size_t>(chunk_tiles(c, C)) + 1 + chunk_slot_cap(c) + 1;
 }
 
@@ -359,9 +358,6 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     // ---- metadata (host) ----
     const int M = C + B;
     const int W_cap = decode_work_cap(c, B);
-    int64_t total_keys = 0;
-    for (int b = 0; b < B; ++b) total_keys += bt->context_lens[b] + 1;
-    const int split = B > 0 ? decode_split_tokens(c, total_keys) : 64;
 
     std::vector<int32_t>& m = ctx->meta;
     m.clear();
@@ -397,23 +393,74 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
         const int nb = static_cast<int>(ceil_div(pre[i].prefix + pre[i].c, 16));
         m.insert(m.end(), t.begin(), t.begin() + nb);
     }
+    // Decode attention work.  The keys of all decodes, laid end to end with
+    // each decode's range padded to a multiple of 64, are cut into n_dslots
+    // equal runs (multiples of 64 keys, so that every item starts on a page
+    // pair), one per wave of each kv head; a run that crosses decodes becomes
+    // one item per decode it touches, and padding alone makes no item.
+    // Items come out in decode order, so each decode's items are contiguous
+    // for the merge.
     const size_t o_workb = m.size();
-    int n_work = 0;
-    for (int b = 0; b < B; ++b) n_work += static_cast<int>(ceil_div(bt->context_lens[b] + 1, split));
-    if (n_work > W_cap) return fail(SLW_EINVAL, "internal: decode work %d above cap %d", n_work, W_cap);
-    m.resize(m.size() + 2 * static_cast<size_t>(n_work) + B + 1);
+    int n_work = 0, n_dslots = 0;
     {
-        int w = 0;
-        const size_t o_works = o_workb + n_work, o_workoff = o_workb + 2 * n_work;
-        for (int b = 0; b < B; ++b) {
-            m[o_workoff + b] = w;
-            const int ns = static_cast<int>(ceil_div(bt->context_lens[b] + 1, split));
-            for (int s = 0; s < ns; ++s, ++w) {
-                m[o_workb + w] = b;
-                m[o_works + w] = s;
+        std::vector<int32_t>& wb = ctx->dwork_b;
+        std::vector<int32_t>& wk0 = ctx->dwork_kb;
+        std::vector<int32_t>& wk1 = ctx->dwork_ke;
+        std::vector<int32_t>& woff = ctx->dwork_off;
+        std::vector<int32_t>& soff = ctx->dslot_off;
+        wb.clear();
+        wk0.clear();
+        wk1.clear();
+        woff.assign(B + 1, 0);
+        soff.clear();
+        int64_t padded = 0;
+        for (int b = 0; b < B; ++b) padded += ceil_div(bt->context_lens[b] + 1, 64) * 64;
+        if (B > 0) {
+            const int64_t want = std::min<int64_t>(decode_slot_cap(c), std::max<int64_t>(1, padded / kDecodeMinKeys));
+            const int64_t per = ceil_div(ceil_div(padded, want), 64) * 64;
+            n_dslots = static_cast<int>(ceil_div(padded, per));
+            int b = 0;
+            int64_t start_b = 0;  // first key of decode b in the padded layout
+            for (int sl = 0; sl < n_dslots; ++sl) {
+                soff.push_back(static_cast<int32_t>(wb.size()));
+                int64_t r0 = sl * per;
+                const int64_t r1 = std::min(padded, r0 + per);
+                while (r0 < r1) {
+                    const int32_t len = bt->context_lens[b] + 1;
+                    const int64_t span = ceil_div(len, 64) * 64;
+                    if (r0 >= start_b + span) {  // past decode b
+                        start_b += span;
+                        woff[++b] = static_cast<int32_t>(wb.size());
+                        continue;
+                    }
+                    const int64_t k0 = r0 - start_b, k1 = std::min<int64_t>(r1 - start_b, span);
+                    if (k0 < len) {
+                        wb.push_back(b);
+                        wk0.push_back(static_cast<int32_t>(k0));
+                        wk1.push_back(static_cast<int32_t>(std::min<int64_t>(k1, len)));
+                    }
+                    r0 = start_b + k1;
+                }
             }
+            soff.push_back(static_cast<int32_t>(wb.size()));
+            while (b < B) woff[++b] = static_cast<int32_t>(wb.size());
         }
-        m[o_workoff + B] = w;
+        n_work = static_cast<int>(wb.size());
+        if (n_work > W_cap || n_dslots > decode_slot_cap(c))
+            return fail(SLW_EINVAL, "internal: decode work %d / slots %d above cap", n_work, n_dslots);
+        for (int b = 0; b < B; ++b) {  // the items of each decode tile its keys
+            int64_t at = 0;
+            for (int i = woff[b]; i < woff[b + 1]; ++i) {
+                if (wb[i] != b || wk0[i] != at || wk1[i] <= at) return fail(SLW_EINVAL, "internal: decode plan");
+                at = wk1[i];
+            }
+            if (at != bt->context_lens[b] + 1) return fail(SLW_EINVAL, "internal: decode plan");
+        }
+        m.insert(m.end(), wb.begin(), wb.end());
+        m.insert(m.end(), wk0.begin(), wk0.end());
+        m.insert(m.end(), wk1.begin(), wk1.end());
+        m.insert(m.end(), woff.begin(), woff.end());
+        m.insert(m.end(), soff.begin(), soff.end());
     }
     // Chunk attention work.  Each prefill's rows are cut into query tiles of
     // pwg positions (a tile never mixes sequences); query tile q covers chunk
@@ -631,13 +678,15 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             da.bt_off = dmeta + o_btoff;
             da.bt = dmeta + o_bt;
             da.work_b = dmeta + o_workb;
-            da.work_s = dmeta + o_workb + n_work;
-            da.work_off = dmeta + o_workb + 2 * n_work;
+            da.work_kb = dmeta + o_workb + n_work;
+            da.work_ke = dmeta + o_workb + 2 * n_work;
+            da.work_off = dmeta + o_workb + 3 * n_work;
+            da.slot_off = dmeta + o_workb + 3 * n_work + B + 1;
+            da.n_slots = n_dslots;
             da.part_o = reinterpret_cast<float*>(wsb + L.part_o);
             da.part_ml = reinterpret_cast<float*>(wsb + L.part_ml);
             da.b = B;
             da.n_work = n_work;
-            da.split_tokens = split;
             da.hq = hq;
             da.hkv = hkv;
             da.hd = hd;

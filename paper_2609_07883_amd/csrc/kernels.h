@@ -100,11 +100,13 @@ struct DecodeAttnArgs {
     const int32_t* bt_off;   // [b + 1] offsets into bt
     const int32_t* bt;       // concatenated block tables
     const int32_t* work_b;   // [n_work] decode of each work item
-    const int32_t* work_s;   // [n_work] split index of each work item
+    const int32_t* work_kb;  // [n_work] first key of the item (a multiple of 64)
+    const int32_t* work_ke;  // [n_work] key past its last
     const int32_t* work_off; // [b + 1] first work item of each decode
+    const int32_t* slot_off; // [n_slots + 1] first work item of each wave (per kv head)
     float* part_o;           // [n_work][hq][hd]
     float* part_ml;          // [n_work][hq][2]
-    int b, n_work, split_tokens, hq, hkv, hd, ld_q;
+    int b, n_work, n_slots, hq, hkv, hd, ld_q;
 };
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
 // Combine the partials of both attentions in one launch: chunk rows of
