@@ -79,8 +79,9 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // chunk that belongs at its swizzled LDS slot; every wave issues the same
 // number of loads per tile, so a counted wait for its own loads plus a bare
 // barrier publishes a tile).  A work item covers one key range of one query
-// tile, and a work-group runs the items of its slot one after the other (the
-// host cuts the keys of all query tiles into equal runs, one per work-group).
+// tile, and a work-group runs the items its slot lists one after the other
+// (the host gives each work-group whole query tiles when they balance, and
+// otherwise cuts the keys of all query tiles into equal runs).
 // A query tile covered by one item is normalised and stored directly; the
 // items of a query tile split over several write fp32 partials (running max,
 // sum, unnormalised output) that attn_merge_kernel combines.
@@ -179,7 +180,8 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
     // into constant memory): a vector load here would make the compiler wait
     // for every direct load in flight before using its result.
     const int i0 = a.slot_off[slot], i1 = a.slot_off[slot + 1];
-    for (int item = i0; item < i1; ++item) {
+    for (int k = i0; k < i1; ++k) {
+        const int item = a.slot_items[k];
         const int qt = a.item_qt[item], kb = a.item_kb[item], ke = a.item_ke[item];
         // the query tile: rows row0 .. row0 + nrows - 1 at positions pos0 .. of one sequence
         const int row0 = a.qt_row0[qt], nrows = a.qt_rows[qt], pos0 = a.qt_pos0[qt];
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
         // loads of its own pending inside the loop, so it adds no waits there.
         wait_vmcnt<0>();
         // every wave is past the previous item's last tile before its buffers refill
-        if (item != i0) barrier_only();
+        if (k != i0) barrier_only();
 #pragma unroll
         for (int t = 0; t < ST - 1; ++t)
             if (t < n_tiles) {

@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <chrono>
 #include <cstring>
+#include <limits>
 #include <memory>
 #include <mutex>
 #include <random>
@@ -38,6 +39,9 @@ constexpr int kDecodeMinKeys = 128;
 // 64-key tiles, which keeps its fixed costs (Q load, partial write) small.
 constexpr int kChunkSlots = 256;
 constexpr int kChunkMinTiles = 4;
+// Whole query tiles per work-group when the largest group's load is within
+// 11/10 of an equal share.
+constexpr int64_t kChunkWholeSlackNum = 11, kChunkWholeSlackDen = 10;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -72,6 +76,7 @@ struct slw_ctx {
     std::vector<Prefill> prefills;     // the iteration's prefills in row order
     std::vector<int32_t> meta;  // host build area
     std::vector<int32_t> items; // chunk-attention work items (host build area)
+    std::vector<int32_t> chunk_slot_items;  // each chunk work-group's items (host build area)
     // decode-attention work items and wave slots (host build area)
     std::vector<int32_t> dwork_b, dwork_kb, dwork_ke, dwork_off, dslot_off;
 
@@ -138,7 +143,7 @@ size_t meta_ints(const slw_model_cfg& c, int C, int B) {
     const size_t np = C > 0 ? static_cast<size_t>(std::min(C, static_cast<int>(SLW_MAX_PREFILLS))) : 0;
     return 2 * static_cast<size_t>(M) + B + (B + 1) + static_cast<size_t>(B) * mb + np * mb +
            3 * static_cast<size_t>(decode_work_cap(c, B)) + (B + 1) + decode_slot_cap(c) + 1 +
-           3 * static_cast<size_t>(chunk_item_cap(c, C)) +
+           4 * static_cast<size_t>(chunk_item_cap(c, C)) +
            5 * static_cast<size_t>(chunk_tiles(c, C)) + 1 + chunk_slot_cap(c) + 1;
 }
 
@@ -489,7 +494,50 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     std::vector<int32_t>& it = ctx->items;
     it.clear();
     std::vector<int32_t> slot_off;
+    // Whole query tiles where they balance: the tiles, longest first, each
+    // go to the least loaded of `want` work-groups (LPT); when the largest
+    // load stays within kChunkWholeSlack of an equal share, no tile is split
+    // and nothing is merged (long prompts: many tiles of similar length).
+    // Otherwise (fewer tiles than work-groups, or tiles of very different
+    // lengths, as at the start of a prompt) the equal runs below split them.
+    // Items stay in tile order; slot_items lists each work-group's items.
+    std::vector<int32_t>& slot_items = ctx->chunk_slot_items;
+    slot_items.clear();
+    bool whole = false;
     if (n_qt > 0) {
+        const int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
+        const int64_t per = ceil_div(total_tiles, want);
+        if (n_qt >= want) {
+            std::vector<int32_t> order(n_qt);
+            for (int q = 0; q < n_qt; ++q) order[q] = q;
+            auto len = [&](int q) { return tile_end[q + 1] - tile_end[q]; };
+            std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return len(x) > len(y); });
+            std::vector<int64_t> load(want, 0);
+            std::vector<int32_t> owner(n_qt);
+            for (int q : order) {
+                const int g = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+                load[g] += len(q);
+                owner[q] = g;
+            }
+            const int64_t mx = *std::max_element(load.begin(), load.end());
+            if (mx * kChunkWholeSlackDen <= per * kChunkWholeSlackNum) {
+                whole = true;
+                n_slots = static_cast<int>(want);
+                for (int q = 0; q < n_qt; ++q) {
+                    it.push_back(q);
+                    it.push_back(0);
+                    it.push_back(static_cast<int32_t>(key_end(q)));
+                }
+                slot_off.assign(n_slots + 1, 0);
+                for (int q = 0; q < n_qt; ++q) ++slot_off[owner[q] + 1];
+                for (int g = 0; g < n_slots; ++g) slot_off[g + 1] += slot_off[g];
+                slot_items.resize(n_qt);
+                std::vector<int32_t> fill(slot_off.begin(), slot_off.end() - 1);
+                for (int q = 0; q < n_qt; ++q) slot_items[fill[owner[q]]++] = q;
+            }
+        }
+    }
+    if (n_qt > 0 && !whole) {
         int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
         const int64_t per = ceil_div(total_tiles, want);
         n_slots = static_cast<int>(ceil_div(total_tiles, per));
@@ -510,6 +558,8 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             }
         }
         slot_off[n_slots] = static_cast<int32_t>(it.size() / 3);
+        slot_items.resize(it.size() / 3);
+        for (size_t i = 0; i < slot_items.size(); ++i) slot_items[i] = static_cast<int32_t>(i);
     }
     std::vector<int32_t> qt_off(n_qt + 1);
     {
@@ -540,6 +590,8 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     }
     const size_t o_slot = m.size();
     m.insert(m.end(), slot_off.begin(), slot_off.end());
+    const size_t o_slot_items = m.size();
+    m.insert(m.end(), slot_items.begin(), slot_items.end());
     const size_t o_qtoff = m.size();
     m.insert(m.end(), qt_off.begin(), qt_off.end());
     const size_t o_qt = m.size();  // [4][n_qt]: first row, rows, first position, block-table offset
@@ -662,6 +714,7 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             ca.hd = hd;
             ca.ld_qkv = qw;
             ca.slot_off = dmeta + o_slot;
+            ca.slot_items = dmeta + o_slot_items;
             ca.n_items = n_items;
             ca.n_slots = n_slots;
             ca.split = n_items > n_qt ? 1 : 0;

@@ -79,7 +79,8 @@ struct ChunkAttnArgs {
     const int32_t* item_kb;   // [n_items] multiple of 64
     const int32_t* item_ke;   // [n_items]
     const int32_t* qt_off;    // [n_qt + 1] first item of each query tile
-    const int32_t* slot_off;  // [n_slots + 1] first item of each work-group (per kv head)
+    const int32_t* slot_off;  // [n_slots + 1] first entry of each work-group in slot_items (per kv head)
+    const int32_t* slot_items; // [n_items] the items of each work-group, in the order it takes them
     float* part_o;            // [n_items][hkv][256][hd]   (items of split query tiles)
     float* part_ml;           // [n_items][hkv][256][2]
     int c, hq, hkv, hd, ld_qkv;

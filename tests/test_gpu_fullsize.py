@@ -85,6 +85,14 @@ def test_long_context_point():
     _run(4096, 28672, ctx, seed=13)
 
 
+def test_whole_query_tiles_point():
+    """C = 2048 at prefix 16384, B = 8: query tiles of similar length, which
+    the planner hands out whole (longest first to the least loaded
+    work-group), so no tile is split and none is merged."""
+    ctx = synth.uniform_lengths(8, 16384, 32768, seed=2)
+    _run(2048, 16384, ctx, seed=18)
+
+
 def test_chat_bursty_point():
     ctx = synth.lognormal_lengths(256, 700, 0.8, 8192, seed=2)
     prompt = int(synth.lognormal_lengths(1, 1024, 0.8, 8192, seed=4)[0])
