@@ -389,6 +389,26 @@ int slw_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, v
  */
 int slw_gemm_plan(int32_t m, int32_t n, int32_t k, int32_t out[6]);
 
+/*
+ * The attention work lists an iteration would build (host only, touches no
+ * GPU), for B decodes with context_lens[b] cached tokens each and n_prefill
+ * prompts, prompt i running chunk_lens[i] rows after prefix_lens[i] cached
+ * tokens, under cfg.  out[0..11]:
+ *   decode attention: work items, wave slots per kv head, largest and
+ *     smallest number of keys a slot takes;
+ *   chunk attention: query tiles, work items, work-groups per kv head,
+ *     1 when every work-group takes whole query tiles (nothing to merge),
+ *     largest and smallest number of 64-key tiles a work-group takes, 64-key
+ *     tiles in all;
+ *   out[11] = 0.
+ * The same invariants the executor checks on every iteration are checked
+ * here (every item list tiles its keys exactly, caps respected).
+ * SLW_EINVAL for a bad cfg, negative sizes, prompts beyond max_pos or more
+ * than SLW_MAX_PREFILLS prompts.
+ */
+int slw_attention_plan(const slw_model_cfg* cfg, int32_t B, const int32_t* context_lens, int32_t n_prefill,
+                       const int32_t* prefix_lens, const int32_t* chunk_lens, int64_t out[12]);
+
 /* ------------------------------------------------------------------------ */
 /* Controller (Eq. 1 solved by bisection as Alg. 1 does; margin of Sec. 3.3) */
 /* ------------------------------------------------------------------------ */

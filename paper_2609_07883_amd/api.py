@@ -37,6 +37,7 @@ EXPORTS = (
     "slw_serve", "slw_cost_table_analytic", "slw_build_cost_table_ctx", "slw_cost_table_from_samples_ctx",
     "slw_cost_table_prefixes", "slw_cost_table_lookup_ctx", "slw_select_chunk_ctx",
     "slw_mixed_iteration_static", "slw_flush_cache", "slw_fill_normal", "slw_gemm_plan",
+    "slw_attention_plan",
 )
 STATIC_WS_BYTES = 128 << 20
 STAGES = ("rmsnorm_attn", "rope_table", "qkv_gemm", "chunk_attn", "decode_attn", "attn_merge",
@@ -144,6 +145,7 @@ def lib() -> C.CDLL:
         "slw_flush_cache": ([vp, sz, vp], C.c_int),
         "slw_fill_normal": ([vp, sz, C.c_uint64, C.c_float, C.c_float, vp], C.c_int),
         "slw_gemm_plan": ([i32, i32, i32, P(i32)], C.c_int),
+        "slw_attention_plan": ([P(ModelCfg), i32, P(i32), i32, P(i32), P(i32), P(i64)], C.c_int),
         "slw_last_slots": ([vp, P(i32), i32, P(i32)], C.c_int),
         "slw_workspace_view": ([vp, i32, i32, i32, P(sz), P(sz)], C.c_int),
         "slw_build_cost_table": ([vp, P(i32), i32, P(i32), i32, P(ProfileOpts), P(vp)], C.c_int),
@@ -326,6 +328,27 @@ def gemm_plan(m: int, n: int, k: int) -> dict:
     out = np.zeros(6, np.int32)
     _check(lib().slw_gemm_plan(int(m), int(n), int(k), _ptr(out, C.c_int32)))
     return dict(zip(("cfg", "bm", "bn", "splits", "sk_workers", "dp_tiles"), (int(v) for v in out)))
+
+
+ATTENTION_PLAN_FIELDS = ("decode_items", "decode_slots", "decode_max_keys", "decode_min_keys",
+                         "query_tiles", "chunk_items", "chunk_slots", "chunk_whole",
+                         "chunk_max_tiles", "chunk_min_tiles", "chunk_tiles")
+
+
+def attention_plan(shape, context_lens, prefills=()) -> dict:
+    """The attention work lists an iteration would build (host only).
+
+    shape: a model shape (synth.ModelShape); context_lens: cached tokens of
+    each decode; prefills: (prefix_len, chunk_len) per prompt."""
+    cfg = ModelCfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                   shape.ffn_dim, shape.rms_eps, shape.rope_theta, 16, shape.max_pos)
+    cl = _i32(context_lens)
+    pp = _i32([p for p, _ in prefills])
+    pc = _i32([c for _, c in prefills])
+    out = np.zeros(12, np.int64)
+    _check(lib().slw_attention_plan(C.byref(cfg), len(cl), _ptr(cl, C.c_int32), len(pp), _ptr(pp, C.c_int32),
+                                    _ptr(pc, C.c_int32), _ptr(out, C.c_int64)))
+    return dict(zip(ATTENTION_PLAN_FIELDS, (int(v) for v in out)))
 
 
 def flush_cache(buf: int, nbytes: int, stream: int = 0) -> None:

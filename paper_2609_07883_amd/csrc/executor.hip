@@ -63,6 +63,20 @@ struct Prefill {
 
 }  // namespace
 
+// Work lists of the two attentions of one iteration (host build areas).
+struct DecodePlan {
+    std::vector<int32_t> b, kb, ke;  // items: decode, first key (a multiple of 64), key past the last
+    std::vector<int32_t> off;        // [B + 1] first item of each decode
+    std::vector<int32_t> slot_off;   // [slots + 1] first item of each wave slot
+};
+struct ChunkPlan {
+    std::vector<int32_t> items;       // [3 n]: query tile, first key, key past the last
+    std::vector<int32_t> slot_off;    // [slots + 1] first entry of each work-group in slot_items
+    std::vector<int32_t> slot_items;  // [n] the items of each work-group in turn
+    std::vector<int32_t> qt_off;      // [n_qt + 1] first item of each query tile
+    bool whole = false;               // whole query tiles per work-group
+};
+
 struct slw_ctx {
     slw_model_cfg cfg{};
     std::vector<slw_layer_weights> w;
@@ -75,10 +89,8 @@ struct slw_ctx {
     std::vector<int32_t> slots_build;  // slots of the iteration being built
     std::vector<Prefill> prefills;     // the iteration's prefills in row order
     std::vector<int32_t> meta;  // host build area
-    std::vector<int32_t> items; // chunk-attention work items (host build area)
-    std::vector<int32_t> chunk_slot_items;  // each chunk work-group's items (host build area)
-    // decode-attention work items and wave slots (host build area)
-    std::vector<int32_t> dwork_b, dwork_kb, dwork_ke, dwork_off, dslot_off;
+    DecodePlan dplan;           // the iteration's attention work (host build areas)
+    ChunkPlan cplan;
 
     // HIP resources, created on first device use
     bool hip_ready = false;
@@ -353,6 +365,185 @@ int mixed_iteration_impl(slw_ctx* ctx, const slw_batch* bt, const void* x_in, vo
 }
 
 // Metadata, upload and kernels of an iteration whose blocks are reserved.
+// Query tiles of the chunk rows: each prefill's rows cut into tiles of
+// chunk_tile_positions(group) positions (a tile never mixes sequences).
+// Tile q: first chunk row, rows, first position and, when wanted, the offset
+// of its sequence's block table (bt_of_prefill[i] for prefill i).
+void query_tiles(const slw_model_cfg& c, const std::vector<Prefill>& pre, std::vector<int32_t>& row0,
+                 std::vector<int32_t>& rows, std::vector<int32_t>& pos0, std::vector<int32_t>* bt,
+                 const std::vector<int32_t>& bt_of_prefill) {
+    const int pwg = chunk_tile_positions(c.n_q_heads / c.n_kv_heads);
+    row0.clear();
+    rows.clear();
+    pos0.clear();
+    if (bt) bt->clear();
+    for (size_t i = 0; i < pre.size(); ++i)
+        for (int j = 0; j < pre[i].c; j += pwg) {
+            row0.push_back(pre[i].row0 + j);
+            rows.push_back(std::min(pwg, pre[i].c - j));
+            pos0.push_back(pre[i].prefix + j);
+            if (bt) bt->push_back(bt_of_prefill[i]);
+        }
+}
+
+// Decode attention work.  The keys of all decodes (decode b attends to
+// context_lens[b] + 1 of them), laid end to end with each decode's range
+// padded to a multiple of 64, are cut into equal runs (multiples of 64 keys,
+// so that every item starts on a page pair; at least kDecodeMinKeys each, at
+// most decode_slot_cap(c) runs), one per wave of each kv head; a run that
+// crosses decodes becomes one item per decode it touches, and padding alone
+// makes no item.  Items come out in decode order, so each decode's items are
+// contiguous for the merge.
+int plan_decode(const slw_model_cfg& c, int B, const int32_t* context_lens, DecodePlan& p) {
+    p.b.clear();
+    p.kb.clear();
+    p.ke.clear();
+    p.off.assign(B + 1, 0);
+    p.slot_off.assign(1, 0);
+    if (B <= 0) return SLW_OK;
+    int64_t padded = 0;
+    for (int b = 0; b < B; ++b) padded += ceil_div(context_lens[b] + 1, 64) * 64;
+    const int64_t want = std::min<int64_t>(decode_slot_cap(c), std::max<int64_t>(1, padded / kDecodeMinKeys));
+    const int64_t per = ceil_div(ceil_div(padded, want), 64) * 64;
+    const int n_slots = static_cast<int>(ceil_div(padded, per));
+    p.slot_off.clear();
+    int b = 0;
+    int64_t start_b = 0;  // first key of decode b in the padded layout
+    for (int sl = 0; sl < n_slots; ++sl) {
+        p.slot_off.push_back(static_cast<int32_t>(p.b.size()));
+        int64_t r0 = sl * per;
+        const int64_t r1 = std::min(padded, r0 + per);
+        while (r0 < r1) {
+            const int32_t len = context_lens[b] + 1;
+            const int64_t span = ceil_div(len, 64) * 64;
+            if (r0 >= start_b + span) {  // past decode b
+                start_b += span;
+                p.off[++b] = static_cast<int32_t>(p.b.size());
+                continue;
+            }
+            const int64_t k0 = r0 - start_b, k1 = std::min<int64_t>(r1 - start_b, span);
+            if (k0 < len) {
+                p.b.push_back(b);
+                p.kb.push_back(static_cast<int32_t>(k0));
+                p.ke.push_back(static_cast<int32_t>(std::min<int64_t>(k1, len)));
+            }
+            r0 = start_b + k1;
+        }
+    }
+    p.slot_off.push_back(static_cast<int32_t>(p.b.size()));
+    while (b < B) p.off[++b] = static_cast<int32_t>(p.b.size());
+    if (static_cast<int>(p.b.size()) > decode_work_cap(c, B) || n_slots > decode_slot_cap(c))
+        return fail(SLW_EINVAL, "internal: decode work %zu / slots %d above cap", p.b.size(), n_slots);
+    for (int d = 0; d < B; ++d) {  // the items of each decode tile its keys
+        int64_t at = 0;
+        for (int i = p.off[d]; i < p.off[d + 1]; ++i) {
+            if (p.b[i] != d || p.kb[i] != at || p.ke[i] <= at) return fail(SLW_EINVAL, "internal: decode plan");
+            at = p.ke[i];
+        }
+        if (at != context_lens[d] + 1) return fail(SLW_EINVAL, "internal: decode plan");
+    }
+    return SLW_OK;
+}
+
+// Chunk attention work over query tiles q (first position qt_pos0[q],
+// qt_rows[q] rows, keys 0 .. qt_pos0[q] + qt_rows[q] - 1).  Whole query tiles
+// where they balance: the tiles, longest first, each go to the least loaded
+// of `want` work-groups (LPT); when the largest load stays within
+// kChunkWholeSlack of an equal share, no tile is split and nothing is merged
+// (long prompts: many tiles of similar length).  Otherwise (fewer tiles than
+// work-groups, or tiles of very different lengths, as at the start of a
+// prompt) the 64-key tiles of every query tile, laid end to end, are cut into
+// equal runs, one per work-group of each kv head; a run that crosses query
+// tiles becomes one item per query tile it touches.  Items stay in query-tile
+// order; slot_items lists each work-group's items.
+int plan_chunk(const slw_model_cfg& c, int C, const std::vector<int32_t>& qt_pos0, const std::vector<int32_t>& qt_rows,
+               ChunkPlan& p) {
+    const int n_qt = static_cast<int>(qt_pos0.size());
+    p.items.clear();
+    p.slot_off.clear();
+    p.slot_items.clear();
+    p.whole = false;
+    auto key_end = [&](int q) { return static_cast<int64_t>(qt_pos0[q]) + qt_rows[q]; };
+    std::vector<int64_t> tile_end(n_qt + 1, 0);
+    for (int q = 0; q < n_qt; ++q) tile_end[q + 1] = tile_end[q] + ceil_div(key_end(q), 64);
+    const int64_t total_tiles = tile_end[n_qt];
+    std::vector<int32_t>& it = p.items;
+    int n_slots = 0;
+    if (n_qt > 0) {
+        const int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
+        const int64_t per = ceil_div(total_tiles, want);
+        if (n_qt >= want) {
+            std::vector<int32_t> order(n_qt);
+            for (int q = 0; q < n_qt; ++q) order[q] = q;
+            auto len = [&](int q) { return tile_end[q + 1] - tile_end[q]; };
+            std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return len(x) > len(y); });
+            std::vector<int64_t> load(want, 0);
+            std::vector<int32_t> owner(n_qt);
+            for (int q : order) {
+                const int g = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+                load[g] += len(q);
+                owner[q] = g;
+            }
+            const int64_t mx = *std::max_element(load.begin(), load.end());
+            if (mx * kChunkWholeSlackDen <= per * kChunkWholeSlackNum) {
+                p.whole = true;
+                n_slots = static_cast<int>(want);
+                for (int q = 0; q < n_qt; ++q) {
+                    it.push_back(q);
+                    it.push_back(0);
+                    it.push_back(static_cast<int32_t>(key_end(q)));
+                }
+                p.slot_off.assign(n_slots + 1, 0);
+                for (int q = 0; q < n_qt; ++q) ++p.slot_off[owner[q] + 1];
+                for (int g = 0; g < n_slots; ++g) p.slot_off[g + 1] += p.slot_off[g];
+                p.slot_items.resize(n_qt);
+                std::vector<int32_t> fill(p.slot_off.begin(), p.slot_off.end() - 1);
+                for (int q = 0; q < n_qt; ++q) p.slot_items[fill[owner[q]]++] = q;
+            }
+        }
+        if (!p.whole) {
+            n_slots = static_cast<int>(ceil_div(total_tiles, per));
+            p.slot_off.resize(n_slots + 1);
+            int q = 0;
+            for (int sl = 0; sl < n_slots; ++sl) {
+                p.slot_off[sl] = static_cast<int32_t>(it.size() / 3);
+                int64_t t0 = sl * per;
+                const int64_t t1 = std::min(total_tiles, t0 + per);
+                while (t0 < t1) {
+                    while (tile_end[q + 1] <= t0) ++q;
+                    const int64_t seg_end = std::min(t1, tile_end[q + 1]);
+                    it.push_back(q);
+                    it.push_back(static_cast<int32_t>((t0 - tile_end[q]) * 64));
+                    it.push_back(static_cast<int32_t>(std::min(key_end(q), (seg_end - tile_end[q]) * 64)));
+                    t0 = seg_end;
+                }
+            }
+            p.slot_off[n_slots] = static_cast<int32_t>(it.size() / 3);
+            p.slot_items.resize(it.size() / 3);
+            for (size_t i = 0; i < p.slot_items.size(); ++i) p.slot_items[i] = static_cast<int32_t>(i);
+        }
+    } else {
+        p.slot_off.assign(1, 0);
+    }
+    const int n_items = static_cast<int>(it.size() / 3);
+    p.qt_off.assign(n_qt + 1, 0);
+    for (int q = 0, i = 0; q <= n_qt; ++q) {
+        while (i < n_items && it[3 * i] < q) ++i;
+        p.qt_off[q] = i;
+    }
+    if (n_items > chunk_item_cap(c, C) || n_slots > chunk_slot_cap(c))
+        return fail(SLW_EINVAL, "internal: chunk items %d / slots %d above cap", n_items, n_slots);
+    for (int q = 0; q < n_qt; ++q) {  // the items of each query tile tile its key range
+        int64_t at = 0;
+        for (int i = p.qt_off[q]; i < p.qt_off[q + 1]; ++i) {
+            if (it[3 * i + 1] != at || it[3 * i + 2] <= at) return fail(SLW_EINVAL, "internal: chunk plan");
+            at = it[3 * i + 2];
+        }
+        if (at != key_end(q)) return fail(SLW_EINVAL, "internal: chunk plan");
+    }
+    return SLW_OK;
+}
+
 int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void* x_out, void* ws,
                       const Layout& L, hipStream_t stream, bool no_alloc) {
     const slw_model_cfg& c = ctx->cfg;
@@ -362,7 +553,6 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
 
     // ---- metadata (host) ----
     const int M = C + B;
-    const int W_cap = decode_work_cap(c, B);
 
     std::vector<int32_t>& m = ctx->meta;
     m.clear();
@@ -398,189 +588,34 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
         const int nb = static_cast<int>(ceil_div(pre[i].prefix + pre[i].c, 16));
         m.insert(m.end(), t.begin(), t.begin() + nb);
     }
-    // Decode attention work.  The keys of all decodes, laid end to end with
-    // each decode's range padded to a multiple of 64, are cut into n_dslots
-    // equal runs (multiples of 64 keys, so that every item starts on a page
-    // pair), one per wave of each kv head; a run that crosses decodes becomes
-    // one item per decode it touches, and padding alone makes no item.
-    // Items come out in decode order, so each decode's items are contiguous
-    // for the merge.
+    // Decode attention work (plan_decode).
     const size_t o_workb = m.size();
-    int n_work = 0, n_dslots = 0;
-    {
-        std::vector<int32_t>& wb = ctx->dwork_b;
-        std::vector<int32_t>& wk0 = ctx->dwork_kb;
-        std::vector<int32_t>& wk1 = ctx->dwork_ke;
-        std::vector<int32_t>& woff = ctx->dwork_off;
-        std::vector<int32_t>& soff = ctx->dslot_off;
-        wb.clear();
-        wk0.clear();
-        wk1.clear();
-        woff.assign(B + 1, 0);
-        soff.clear();
-        int64_t padded = 0;
-        for (int b = 0; b < B; ++b) padded += ceil_div(bt->context_lens[b] + 1, 64) * 64;
-        if (B > 0) {
-            const int64_t want = std::min<int64_t>(decode_slot_cap(c), std::max<int64_t>(1, padded / kDecodeMinKeys));
-            const int64_t per = ceil_div(ceil_div(padded, want), 64) * 64;
-            n_dslots = static_cast<int>(ceil_div(padded, per));
-            int b = 0;
-            int64_t start_b = 0;  // first key of decode b in the padded layout
-            for (int sl = 0; sl < n_dslots; ++sl) {
-                soff.push_back(static_cast<int32_t>(wb.size()));
-                int64_t r0 = sl * per;
-                const int64_t r1 = std::min(padded, r0 + per);
-                while (r0 < r1) {
-                    const int32_t len = bt->context_lens[b] + 1;
-                    const int64_t span = ceil_div(len, 64) * 64;
-                    if (r0 >= start_b + span) {  // past decode b
-                        start_b += span;
-                        woff[++b] = static_cast<int32_t>(wb.size());
-                        continue;
-                    }
-                    const int64_t k0 = r0 - start_b, k1 = std::min<int64_t>(r1 - start_b, span);
-                    if (k0 < len) {
-                        wb.push_back(b);
-                        wk0.push_back(static_cast<int32_t>(k0));
-                        wk1.push_back(static_cast<int32_t>(std::min<int64_t>(k1, len)));
-                    }
-                    r0 = start_b + k1;
-                }
-            }
-            soff.push_back(static_cast<int32_t>(wb.size()));
-            while (b < B) woff[++b] = static_cast<int32_t>(wb.size());
-        }
-        n_work = static_cast<int>(wb.size());
-        if (n_work > W_cap || n_dslots > decode_slot_cap(c))
-            return fail(SLW_EINVAL, "internal: decode work %d / slots %d above cap", n_work, n_dslots);
-        for (int b = 0; b < B; ++b) {  // the items of each decode tile its keys
-            int64_t at = 0;
-            for (int i = woff[b]; i < woff[b + 1]; ++i) {
-                if (wb[i] != b || wk0[i] != at || wk1[i] <= at) return fail(SLW_EINVAL, "internal: decode plan");
-                at = wk1[i];
-            }
-            if (at != bt->context_lens[b] + 1) return fail(SLW_EINVAL, "internal: decode plan");
-        }
-        m.insert(m.end(), wb.begin(), wb.end());
-        m.insert(m.end(), wk0.begin(), wk0.end());
-        m.insert(m.end(), wk1.begin(), wk1.end());
-        m.insert(m.end(), woff.begin(), woff.end());
-        m.insert(m.end(), soff.begin(), soff.end());
-    }
+    DecodePlan& dp = ctx->dplan;
+    if ((rc = plan_decode(c, B, bt->context_lens, dp))) return rc;
+    const int n_work = static_cast<int>(dp.b.size()), n_dslots = static_cast<int>(dp.slot_off.size()) - 1;
+    m.insert(m.end(), dp.b.begin(), dp.b.end());
+    m.insert(m.end(), dp.kb.begin(), dp.kb.end());
+    m.insert(m.end(), dp.ke.begin(), dp.ke.end());
+    m.insert(m.end(), dp.off.begin(), dp.off.end());
+    m.insert(m.end(), dp.slot_off.begin(), dp.slot_off.end());
     // Chunk attention work.  Each prefill's rows are cut into query tiles of
     // pwg positions (a tile never mixes sequences); query tile q covers chunk
     // rows qt_row0 .. + qt_rows at positions from qt_pos0 on and reads the
-    // block table at qt_bt, over keys 0 .. qt_pos0 + qt_rows - 1.  The 64-key
-    // tiles of every query tile, laid end to end, are cut into equal runs, one
-    // per work-group of each kv head; a run that crosses query tiles becomes
-    // one item per query tile it touches.  A query tile covered by one item is
-    // written directly, one covered by several is combined by the merge kernel.
-    const int pwg = chunk_tile_positions(c.n_q_heads / c.n_kv_heads);
+    // block table at qt_bt, over keys 0 .. qt_pos0 + qt_rows - 1; plan_chunk
+    // hands the tiles out to the work-groups.  A query tile covered by one
+    // item is written directly, one covered by several is combined by the
+    // merge kernel.
     std::vector<int32_t> qt_row0, qt_rows, qt_pos0, qt_bt;
-    for (size_t i = 0; i < pre.size(); ++i)
-        for (int j = 0; j < pre[i].c; j += pwg) {
-            qt_row0.push_back(pre[i].row0 + j);
-            qt_rows.push_back(std::min(pwg, pre[i].c - j));
-            qt_pos0.push_back(pre[i].prefix + j);
-            qt_bt.push_back(pre_bt[i]);
-        }
+    query_tiles(c, pre, qt_row0, qt_rows, qt_pos0, &qt_bt, pre_bt);
     const int n_qt = static_cast<int>(qt_row0.size());
     if (n_qt > chunk_tiles(c, C)) return fail(SLW_EINVAL, "internal: %d query tiles above cap", n_qt);
-    auto key_end = [&](int q) { return static_cast<int64_t>(qt_pos0[q]) + qt_rows[q]; };
-    std::vector<int64_t> tile_end(n_qt + 1, 0);
-    for (int q = 0; q < n_qt; ++q) tile_end[q + 1] = tile_end[q] + ceil_div(key_end(q), 64);
-    const int64_t total_tiles = tile_end[n_qt];
-    int n_slots = 0;
-    std::vector<int32_t>& it = ctx->items;
-    it.clear();
-    std::vector<int32_t> slot_off;
-    // Whole query tiles where they balance: the tiles, longest first, each
-    // go to the least loaded of `want` work-groups (LPT); when the largest
-    // load stays within kChunkWholeSlack of an equal share, no tile is split
-    // and nothing is merged (long prompts: many tiles of similar length).
-    // Otherwise (fewer tiles than work-groups, or tiles of very different
-    // lengths, as at the start of a prompt) the equal runs below split them.
-    // Items stay in tile order; slot_items lists each work-group's items.
-    std::vector<int32_t>& slot_items = ctx->chunk_slot_items;
-    slot_items.clear();
-    bool whole = false;
-    if (n_qt > 0) {
-        const int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
-        const int64_t per = ceil_div(total_tiles, want);
-        if (n_qt >= want) {
-            std::vector<int32_t> order(n_qt);
-            for (int q = 0; q < n_qt; ++q) order[q] = q;
-            auto len = [&](int q) { return tile_end[q + 1] - tile_end[q]; };
-            std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return len(x) > len(y); });
-            std::vector<int64_t> load(want, 0);
-            std::vector<int32_t> owner(n_qt);
-            for (int q : order) {
-                const int g = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
-                load[g] += len(q);
-                owner[q] = g;
-            }
-            const int64_t mx = *std::max_element(load.begin(), load.end());
-            if (mx * kChunkWholeSlackDen <= per * kChunkWholeSlackNum) {
-                whole = true;
-                n_slots = static_cast<int>(want);
-                for (int q = 0; q < n_qt; ++q) {
-                    it.push_back(q);
-                    it.push_back(0);
-                    it.push_back(static_cast<int32_t>(key_end(q)));
-                }
-                slot_off.assign(n_slots + 1, 0);
-                for (int q = 0; q < n_qt; ++q) ++slot_off[owner[q] + 1];
-                for (int g = 0; g < n_slots; ++g) slot_off[g + 1] += slot_off[g];
-                slot_items.resize(n_qt);
-                std::vector<int32_t> fill(slot_off.begin(), slot_off.end() - 1);
-                for (int q = 0; q < n_qt; ++q) slot_items[fill[owner[q]]++] = q;
-            }
-        }
-    }
-    if (n_qt > 0 && !whole) {
-        int64_t want = std::min<int64_t>(chunk_slot_cap(c), std::max<int64_t>(1, total_tiles / kChunkMinTiles));
-        const int64_t per = ceil_div(total_tiles, want);
-        n_slots = static_cast<int>(ceil_div(total_tiles, per));
-        slot_off.resize(n_slots + 1);
-        int q = 0;
-        for (int sl = 0; sl < n_slots; ++sl) {
-            slot_off[sl] = static_cast<int32_t>(it.size() / 3);
-            int64_t t0 = sl * per;
-            const int64_t t1 = std::min(total_tiles, t0 + per);
-            while (t0 < t1) {
-                while (tile_end[q + 1] <= t0) ++q;
-                const int64_t seg_end = std::min(t1, tile_end[q + 1]);
-                const int64_t ke_q = key_end(q);
-                it.push_back(q);
-                it.push_back(static_cast<int32_t>((t0 - tile_end[q]) * 64));
-                it.push_back(static_cast<int32_t>(std::min(ke_q, (seg_end - tile_end[q]) * 64)));
-                t0 = seg_end;
-            }
-        }
-        slot_off[n_slots] = static_cast<int32_t>(it.size() / 3);
-        slot_items.resize(it.size() / 3);
-        for (size_t i = 0; i < slot_items.size(); ++i) slot_items[i] = static_cast<int32_t>(i);
-    }
-    std::vector<int32_t> qt_off(n_qt + 1);
-    {
-        int i = 0;
-        const int n_it = static_cast<int>(it.size() / 3);
-        for (int q = 0; q <= n_qt; ++q) {
-            while (i < n_it && it[3 * i] < q) ++i;
-            qt_off[q] = i;
-        }
-    }
-    const int n_items = static_cast<int>(it.size() / 3);
-    if (n_items > chunk_item_cap(c, C) || n_slots > chunk_slot_cap(c))
-        return fail(SLW_EINVAL, "internal: chunk items %d / slots %d above cap", n_items, n_slots);
-    for (int q = 0; q < n_qt; ++q) {  // the items of each query tile tile its key range
-        int64_t at = 0;
-        for (int i = qt_off[q]; i < qt_off[q + 1]; ++i) {
-            if (it[3 * i + 1] != at || it[3 * i + 2] <= at) return fail(SLW_EINVAL, "internal: chunk plan");
-            at = it[3 * i + 2];
-        }
-        if (at != key_end(q)) return fail(SLW_EINVAL, "internal: chunk plan");
-    }
+    ChunkPlan& cp = ctx->cplan;
+    if ((rc = plan_chunk(c, C, qt_pos0, qt_rows, cp))) return rc;
+    const std::vector<int32_t>& it = cp.items;
+    const std::vector<int32_t>& slot_off = cp.slot_off;
+    const std::vector<int32_t>& slot_items = cp.slot_items;
+    const std::vector<int32_t>& qt_off = cp.qt_off;
+    const int n_items = static_cast<int>(it.size() / 3), n_slots = static_cast<int>(slot_off.size()) - 1;
     const size_t o_item = m.size();
     m.resize(m.size() + 3 * static_cast<size_t>(n_items));
     for (int i = 0; i < n_items; ++i) {
@@ -799,6 +834,62 @@ extern "C" int slw_create(const slw_model_cfg* cfg, slw_ctx** out) {
 extern "C" int slw_destroy(slw_ctx* ctx) {
     delete ctx;
     return SLW_OK;
+}
+
+extern "C" int slw_attention_plan(const slw_model_cfg* cfg, int32_t B, const int32_t* context_lens,
+                                  int32_t n_prefill, const int32_t* prefix_lens, const int32_t* chunk_lens,
+                                  int64_t out[12]) {
+    return guarded([&] {
+        if (!cfg || !out || (B > 0 && !context_lens) || (n_prefill > 0 && (!prefix_lens || !chunk_lens)))
+            return fail(SLW_EINVAL, "null argument");
+        int rc = check_cfg(*cfg);
+        if (rc) return rc;
+        if (B < 0 || n_prefill < 0 || n_prefill > SLW_MAX_PREFILLS)
+            return fail(SLW_EINVAL, "B >= 0 and 0 <= n_prefill <= %d", SLW_MAX_PREFILLS);
+        std::vector<Prefill> pre;
+        int C = 0;
+        for (int i = 0; i < n_prefill; ++i) {
+            if (chunk_lens[i] < 1 || prefix_lens[i] < 0 ||
+                static_cast<int64_t>(prefix_lens[i]) + chunk_lens[i] > cfg->max_pos)
+                return fail(SLW_EINVAL, "prefill %d: chunk >= 1, prefix >= 0, prefix + chunk <= max_pos", i);
+            pre.push_back(Prefill{i, prefix_lens[i], chunk_lens[i], C});
+            C += chunk_lens[i];
+        }
+        for (int b = 0; b < B; ++b)
+            if (context_lens[b] < 0 || context_lens[b] >= cfg->max_pos)
+                return fail(SLW_EINVAL, "decode %d: context in [0, max_pos)", b);
+        DecodePlan dp;
+        ChunkPlan cp;
+        std::vector<int32_t> row0, rows, pos0;
+        query_tiles(*cfg, pre, row0, rows, pos0, nullptr, {});
+        if ((rc = plan_decode(*cfg, B, context_lens, dp))) return rc;
+        if ((rc = plan_chunk(*cfg, C, pos0, rows, cp))) return rc;
+        const int dslots = static_cast<int>(dp.slot_off.size()) - 1;
+        int64_t dmax = 0, dmin = dslots > 0 ? std::numeric_limits<int64_t>::max() : 0;
+        for (int sl = 0; sl < dslots; ++sl) {
+            int64_t keys = 0;
+            for (int i = dp.slot_off[sl]; i < dp.slot_off[sl + 1]; ++i) keys += dp.ke[i] - dp.kb[i];
+            dmax = std::max(dmax, keys);
+            dmin = std::min(dmin, keys);
+        }
+        const int cslots = static_cast<int>(cp.slot_off.size()) - 1;
+        int64_t cmax = 0, cmin = cslots > 0 ? std::numeric_limits<int64_t>::max() : 0, ctot = 0;
+        for (int g = 0; g < cslots; ++g) {
+            int64_t tiles = 0;
+            for (int k = cp.slot_off[g]; k < cp.slot_off[g + 1]; ++k) {
+                const int i = cp.slot_items[k];
+                tiles += ceil_div(cp.items[3 * i + 2], 64) - cp.items[3 * i + 1] / 64;
+            }
+            cmax = std::max(cmax, tiles);
+            cmin = std::min(cmin, tiles);
+            ctot += tiles;
+        }
+        const int64_t v[12] = {static_cast<int64_t>(dp.b.size()), dslots, dmax, dmin,
+                               static_cast<int64_t>(rows.size()), static_cast<int64_t>(cp.items.size() / 3), cslots,
+                               cp.whole ? 1 : 0, cmax, cmin, ctot, 0};
+        for (int i = 0; i < 12; ++i) out[i] = v[i];
+        return SLW_OK;
+    });
 }
 
 extern "C" int slw_gemm_plan(int32_t m, int32_t n, int32_t k, int32_t out[6]) {

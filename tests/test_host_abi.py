@@ -314,3 +314,65 @@ def test_gemm_plan_is_valid_for_every_row_count(shape):
         api.gemm_plan(0, 4096, 4096)
     with pytest.raises(api.SloweaveError):
         api.gemm_plan(64, 4000, 4096)
+
+
+def _share(total, slots, quantum):
+    return -(-(-(-total // slots)) // quantum) * quantum
+
+
+@settings(max_examples=300, deadline=None)
+@given(ctx=st.lists(st.integers(0, 32766), max_size=300),
+       pre=st.lists(st.tuples(st.integers(0, 28000), st.integers(1, 4096)), max_size=4),
+       shape=st.sampled_from(["8b", "tiny"]))
+def test_attention_plans_cover_every_key_once_and_balance(ctx, pre, shape):
+    """The executor's attention work lists (the same code, run on the host):
+    every decode's keys and every query tile's keys are covered exactly once
+    (the call fails otherwise), the decode runs are equal shares of the
+    padded keys, the chunk work-groups take equal runs of 64-key tiles or,
+    when whole tiles balance, at most 1.1 equal shares each."""
+    sh = synth.LLAMA8B_LAYER if shape == "8b" else synth.TINY
+    ctx = [min(c, sh.max_pos - 1) for c in ctx]
+    pre = [(min(p, sh.max_pos - c), c) for p, c in pre if c <= sh.max_pos]
+    p = api.attention_plan(sh, ctx, pre)
+    B = len(ctx)
+    slots_cap = max(1, 2048 // sh.n_kv_heads)
+    if B:
+        padded = sum(-(-(c + 1) // 64) * 64 for c in ctx)
+        want = min(slots_cap, max(1, padded // 128))
+        assert 1 <= p["decode_slots"] <= slots_cap
+        assert B <= p["decode_items"] <= p["decode_slots"] + B
+        assert p["decode_max_keys"] <= _share(padded, want, 64)
+    else:
+        assert p["decode_items"] == p["decode_slots"] == 0
+    group = sh.n_q_heads // sh.n_kv_heads
+    pwg = 256 // group
+    tiles = [-(-(pp + min(pwg, cc - j) + j) // 64) for pp, cc in pre for j in range(0, cc, pwg)]
+    assert p["query_tiles"] == len(tiles) and p["chunk_tiles"] == sum(tiles)
+    if tiles:
+        total = sum(tiles)
+        want = min(max(1, 256 // sh.n_kv_heads), max(1, total // 4))
+        share = -(-total // want)
+        assert p["chunk_items"] >= len(tiles)
+        if p["chunk_whole"]:
+            assert p["chunk_items"] == len(tiles) and len(tiles) >= want
+            assert p["chunk_max_tiles"] * 10 <= share * 11
+        else:
+            assert p["chunk_max_tiles"] <= share
+
+
+def test_attention_plan_examples():
+    """Long prompts take whole query tiles (nothing to merge); the start of a
+    prompt, whose tiles grow with their position, is cut into runs; one
+    short decode is one item."""
+    sh = synth.LLAMA8B_LAYER
+    long = api.attention_plan(sh, [20000] * 8, [(28672, 4096)])
+    assert long["chunk_whole"] == 1 and long["chunk_items"] == long["query_tiles"] == 64
+    assert long["chunk_max_tiles"] == long["chunk_min_tiles"] == 961   # 64 tiles of 449..512 paired to 961
+    first = api.attention_plan(sh, [], [(0, 2048)])
+    assert first["chunk_whole"] == 0 and first["chunk_tiles"] == 528 and first["chunk_max_tiles"] == 17
+    one = api.attention_plan(sh, [0], [])
+    assert (one["decode_items"], one["decode_slots"], one["decode_max_keys"]) == (1, 1, 1)
+    with pytest.raises(api.SloweaveError):
+        api.attention_plan(sh, [sh.max_pos], [])
+    with pytest.raises(api.SloweaveError):
+        api.attention_plan(sh, [], [(0, 1)] * 17)
