@@ -121,3 +121,28 @@ def test_elementwise_floor_of_a_two_layer_stack():
     print(f"2-layer floor: elementwise {e:.4f} per-vector {rel_err(y, y_ref):.4f} rms {rms_err(y, y_ref):.5f}")
     assert 2.5e-2 < e <= ELEMENTWISE_TOL * np.sqrt(2)
     assert rel_err(y, y_ref) <= 1e-2 and rms_err(y, y_ref) <= 7e-3
+
+
+def test_elementwise_floor_grows_with_the_score_spread():
+    """The floor depends on how sharp attention is, not only on the shapes:
+    with 16 q heads per kv head at d_model 1024 and the q/k weights at
+    std 0.16, scores reach tens of units, softmax is nearly hard, and the
+    bf16 rounding of the normed rows and of q/k alone moves the output past
+    ELEMENTWISE_TOL; at the scale 0.16 sqrt(256 / d_model) (the spread of the
+    d_model-256 cases) the same pipeline stays far inside it.  GPU cases of
+    other widths scale their q/k weights that way."""
+    from tests.test_gpu_gqa import SHAPES
+    s = SHAPES["gqa16_hd64"]
+    sh = oracle_shape(s)
+    C = 150
+    x = synth.bf16_to_f64(synth.embeddings(C, s.d_model, seed=1, stream=3))
+    pos = np.arange(C)
+    errs = {}
+    for qk in (0.16, 0.16 * (256 / s.d_model) ** 0.5):
+        w = oracle_weights(synth.layer_weights(s, weight_seed=0, qk_std=qk))
+        ref, _, _ = _layer(sh, w, x, pos, _keep, _keep)
+        em, _, _ = _layer(sh, w, x, pos, _bf, _keep)
+        errs[qk] = elementwise_err(em, ref)
+    sharp, spread = errs.values()
+    assert sharp > ELEMENTWISE_TOL
+    assert spread < 0.5 * ELEMENTWISE_TOL
