@@ -217,15 +217,23 @@ int check_cfg(const slw_model_cfg& c) {
     return SLW_OK;
 }
 
+// The iteration's events order work on this device only: a staging event
+// tells the host that the set-up kernel has finished reading a pinned buffer
+// (nothing the GPU wrote has to reach the host), and the fork and join
+// events order the two streams' kernels.  Without the system-scope fence an
+// event record does no cache write-back and invalidation (the CUs sat idle
+// for 6-11 us at each record): 8B-layer sweep +1.4%, chat mix +1.6%.
+constexpr unsigned kSyncEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+
 int ensure_hip(slw_ctx* ctx) {
     if (ctx->hip_ready) return SLW_OK;
-    for (int i = 0; i < kRing; ++i) HIP_TRY(hipEventCreateWithFlags(&ctx->staged[i], hipEventDisableTiming));
+    for (int i = 0; i < kRing; ++i) HIP_TRY(hipEventCreateWithFlags(&ctx->staged[i], kSyncEventFlags));
     HIP_TRY(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
     ctx->fork_ev.assign(ctx->cfg.n_layers, nullptr);
     ctx->join_ev.assign(ctx->cfg.n_layers, nullptr);
     for (int l = 0; l < ctx->cfg.n_layers; ++l) {
-        HIP_TRY(hipEventCreateWithFlags(&ctx->fork_ev[l], hipEventDisableTiming));
-        HIP_TRY(hipEventCreateWithFlags(&ctx->join_ev[l], hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&ctx->fork_ev[l], kSyncEventFlags));
+        HIP_TRY(hipEventCreateWithFlags(&ctx->join_ev[l], kSyncEventFlags));
     }
     ctx->hip_ready = true;
     return SLW_OK;
