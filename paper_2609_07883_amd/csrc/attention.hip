@@ -125,8 +125,29 @@ __device__ __forceinline__ void wait_vmcnt() {
 // compiler from moving LDS or global accesses across it).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
-template <int HD, int GROUP, int ST>
-__global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a) {
+template <int HD>
+__device__ __forceinline__ void decode_attn_wave(const DecodeAttnArgs& a, int slot, int kvh, int lane);
+
+// With DECODE, the launch also runs decode attention: work-groups past the
+// n_slots * hkv chunk work-groups hold eight decode waves each (wave v of
+// that part takes slot v % n_slots of kv head v / n_slots).  They start as
+// chunk work-groups leave CUs free, so the decodes fill the chunk part's
+// tail and any CUs a short chunk leaves idle, with no second stream to fork
+// and join.  Decode waves need no barrier; the chunk part's barriers see all
+// eight waves of its work-groups, which come first in the grid, so the
+// hardware's round-robin over the XCDs sees them in order.  (The chunk code
+// stays in the kernel itself: compiled as a separate function and inlined,
+// it came out with different branch conversion and ran up to 4% slower.)
+template <int HD, int GROUP, int ST, bool DECODE>
+__global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, DecodeAttnArgs da) {
+    if constexpr (DECODE) {
+        const int n_chunk = a.n_slots * a.hkv;
+        if (static_cast<int>(blockIdx.x) >= n_chunk) {
+            const int v = (static_cast<int>(blockIdx.x) - n_chunk) * 8 + static_cast<int>(threadIdx.x >> 6);
+            if (v < da.n_slots * da.hkv) decode_attn_wave<HD>(da, v % da.n_slots, v / da.n_slots, threadIdx.x & 63);
+            return;
+        }
+    }
     constexpr int KK = HD / 32, NT = HD / 16, PAGE = HD * 16;
     constexpr int SLABS = 2 * 4 * PAGE / 512;  // 1 KB direct loads per tile (K and V of four pages)
     constexpr int PER_WAVE = SLABS / 8;        // loads each wave issues per tile
@@ -522,12 +543,12 @@ __device__ __forceinline__ void decode_load(DecodeStep<HD>& st, const bf16* kpoo
         st.v[nt] = *reinterpret_cast<const bf16x8*>(vpool + vpage + (nt * 16 + col) * 16 + 8 * (grp & 1));
 }
 
+// One decode-attention wave: the items of `slot` for kv head kvh.
 template <int HD>
-__global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
+__device__ __forceinline__ void decode_attn_wave(const DecodeAttnArgs& a, int slot, int kvh, int lane) {
     constexpr int KK = HD / 32, NT = HD / 16;
     constexpr float kSlack = 8.0f;  // lazy rescaling threshold (log2 units)
-    const int lane = threadIdx.x, grp = lane >> 4, col = lane & 15;
-    const int kvh = blockIdx.y;
+    const int grp = lane >> 4, col = lane & 15;
     const int group = a.hq / a.hkv;
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
@@ -535,7 +556,7 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
 
     // The wave's items one after the other: keys [tok0, tok1) of decode b,
     // each leaving its partial (running max, sum, unnormalised output).
-    const int i0 = a.slot_off[blockIdx.x], i1 = a.slot_off[blockIdx.x + 1];
+    const int i0 = a.slot_off[slot], i1 = a.slot_off[slot + 1];
     for (int w = i0; w < i1; ++w) {
         const int b = a.work_b[w], tok0 = a.work_kb[w], tok1 = a.work_ke[w];
         const int last_pg = (tok1 - 1) >> 4;
@@ -651,6 +672,11 @@ __global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
     }
 }
 
+template <int HD>
+__global__ __launch_bounds__(64, 2) void decode_attn_kernel(DecodeAttnArgs a) {
+    decode_attn_wave<HD>(a, blockIdx.x, blockIdx.y, threadIdx.x);
+}
+
 // Merge the items of one (decode, q head): weights 2^(m_s - max m).
 template <int HD>
 __device__ __forceinline__ void decode_merge_row(const DecodeAttnArgs& a, int b, int h) {
@@ -673,7 +699,13 @@ __global__ __launch_bounds__(64 * WAVES) void attn_merge_kernel(ChunkAttnArgs ca
 
 template <int HD, int GROUP>
 void launch_chunk_g(const ChunkAttnArgs& a, hipStream_t s) {
-    chunk_attn_kernel<HD, GROUP, kChunkStages><<<a.n_slots * a.hkv, 512, 0, s>>>(a);
+    chunk_attn_kernel<HD, GROUP, kChunkStages, false><<<a.n_slots * a.hkv, 512, 0, s>>>(a, DecodeAttnArgs{});
+}
+
+template <int HD, int GROUP>
+void launch_both_g(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, hipStream_t s) {
+    const int blocks = ca.n_slots * ca.hkv + (da.n_slots * da.hkv + 7) / 8;
+    chunk_attn_kernel<HD, GROUP, kChunkStages, true><<<blocks, 512, 0, s>>>(ca, da);
 }
 
 template <int HD, int GROUP>
@@ -709,7 +741,31 @@ void launch_chunk_hd(const ChunkAttnArgs& a, hipStream_t s) {
     }
 }
 
+template <int HD>
+void launch_both_hd(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, hipStream_t s) {
+    switch (ca.hq / ca.hkv) {
+        case 1: launch_both_g<HD, 1>(ca, da, s); break;
+        case 2: launch_both_g<HD, 2>(ca, da, s); break;
+        case 4: launch_both_g<HD, 4>(ca, da, s); break;
+        case 8: launch_both_g<HD, 8>(ca, da, s); break;
+        default: launch_both_g<HD, 16>(ca, da, s); break;
+    }
+}
+
 }  // namespace
+
+void launch_attention(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, hipStream_t s) {
+    if (ca.c <= 0 || ca.n_items <= 0) {
+        launch_decode_attention_split(da, s);
+        return;
+    }
+    if (da.b <= 0) {
+        launch_chunk_attention(ca, s);
+        return;
+    }
+    if (ca.hd == 128) launch_both_hd<128>(ca, da, s);
+    else launch_both_hd<64>(ca, da, s);
+}
 
 void launch_chunk_attention(const ChunkAttnArgs& a, hipStream_t s) {
     if (a.c <= 0 || a.n_items <= 0) return;

@@ -42,6 +42,15 @@ constexpr int kChunkMinTiles = 4;
 // Whole query tiles per work-group when the largest group's load is within
 // 11/10 of an equal share.
 constexpr int64_t kChunkWholeSlackNum = 11, kChunkWholeSlackDen = 10;
+// Chunk and decode attention share one launch (decode waves run as chunk
+// work-groups leave CUs free) unless the chunk holds at least this many
+// (query, key) pairs: then decode attention runs on a second stream beside
+// the chunk kernel for its whole length, which a long chunk kernel even
+// finishes sooner (8B layer, 4096-token chunk at a 28 K prefix with eight
+// 16-32 K decodes: 2256 us with the decodes beside it, 2432 us alone).  One
+// launch saves the fork and join, 9-20 us an iteration on the layer sweep's
+// and the chat mix's chunks; the two ways measured even at 8-9 M pairs.
+constexpr int64_t kTwoStreamMinPairs = int64_t{8} << 20;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -99,8 +108,8 @@ struct slw_ctx {
     size_t staging_cap[kRing] = {};
     hipEvent_t staged[kRing] = {};
     int ring = 0;
-    // second stream for decode attention next to chunk attention, with a
-    // fork and a join event per layer
+    // second stream for decode attention next to a long chunk's attention,
+    // with a fork and a join event per layer
     hipStream_t side = nullptr;
     std::vector<hipEvent_t> fork_ev, join_ev;
 
@@ -601,6 +610,8 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
     DecodePlan& dp = ctx->dplan;
     if ((rc = plan_decode(c, B, bt->context_lens, dp))) return rc;
     const int n_work = static_cast<int>(dp.b.size()), n_dslots = static_cast<int>(dp.slot_off.size()) - 1;
+    int64_t chunk_pairs = 0;  // (query, key) pairs of the chunk rows: c p + c (c + 1) / 2 per prefill
+    for (const auto& q : pre) chunk_pairs += int64_t{q.c} * q.prefix + int64_t{q.c} * (q.c + 1) / 2;
     m.insert(m.end(), dp.b.begin(), dp.b.end());
     m.insert(m.end(), dp.kb.begin(), dp.kb.end());
     m.insert(m.end(), dp.ke.begin(), dp.ke.end());
@@ -723,16 +734,8 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             launch_gemm(ga, p_qkv, gpartp, stream);
         }
         if ((rc = mark(l, 3))) return rc;
-        // With both attentions to run (and no per-stage events), decode
-        // attention goes to a second stream so that it fills the CUs a short
-        // chunk leaves idle; the merge waits for both.
-        const bool concurrent = C > 0 && B > 0 && !timing && !no_alloc;
-        hipStream_t dstream = stream;
-        if (concurrent) {
-            HIP_TRY(hipEventRecord(ctx->fork_ev[l], stream));
-            HIP_TRY(hipStreamWaitEvent(ctx->side, ctx->fork_ev[l], 0));
-            dstream = ctx->side;
-        }
+        // Both attentions in one launch, or on two streams for a long
+        // chunk (see kTwoStreamMinPairs); per-stage events separate them.
         ChunkAttnArgs ca{};
         if (C > 0) {
             ca.qkv = qkv;
@@ -761,9 +764,7 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             ca.n_items = n_items;
             ca.n_slots = n_slots;
             ca.split = n_items > n_qt ? 1 : 0;
-            launch_chunk_attention(ca, stream);
         }
-        if ((rc = mark(l, 4))) return rc;
         DecodeAttnArgs da{};
         if (B > 0) {
             da.q = static_cast<const char*>(qkv) + static_cast<size_t>(C) * qw * 2;
@@ -787,11 +788,20 @@ int enqueue_iteration(slw_ctx* ctx, const slw_batch* bt, const void* x_in, void*
             da.hkv = hkv;
             da.hd = hd;
             da.ld_q = qw;
-            launch_decode_attention_split(da, dstream);
-            if (concurrent) {
-                HIP_TRY(hipEventRecord(ctx->join_ev[l], dstream));
-                HIP_TRY(hipStreamWaitEvent(stream, ctx->join_ev[l], 0));
-            }
+        }
+        if (timing) {
+            if (C > 0) launch_chunk_attention(ca, stream);
+            if ((rc = mark(l, 4))) return rc;
+            if (B > 0) launch_decode_attention_split(da, stream);
+        } else if (C > 0 && B > 0 && !no_alloc && chunk_pairs >= kTwoStreamMinPairs) {
+            HIP_TRY(hipEventRecord(ctx->fork_ev[l], stream));
+            HIP_TRY(hipStreamWaitEvent(ctx->side, ctx->fork_ev[l], 0));
+            launch_chunk_attention(ca, stream);
+            launch_decode_attention_split(da, ctx->side);
+            HIP_TRY(hipEventRecord(ctx->join_ev[l], ctx->side));
+            HIP_TRY(hipStreamWaitEvent(stream, ctx->join_ev[l], 0));
+        } else {
+            launch_attention(ca, da, stream);
         }
         if ((rc = mark(l, 5))) return rc;
         launch_attention_merge(&ca, &da, stream);

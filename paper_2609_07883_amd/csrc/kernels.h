@@ -110,6 +110,9 @@ struct DecodeAttnArgs {
     int b, n_work, n_slots, hq, hkv, hd, ld_q;
 };
 void launch_decode_attention_split(const DecodeAttnArgs& a, hipStream_t s);
+// Both attentions of a layer in one launch (chunk work-groups first, decode
+// waves after them); either part may be empty.
+void launch_attention(const ChunkAttnArgs& ca, const DecodeAttnArgs& da, hipStream_t s);
 // Combine the partials of both attentions in one launch: chunk rows of
 // query tiles split over several items (ca may be null or unsplit) and every
 // decode (da may be null or have b = 0).
