@@ -12,7 +12,8 @@
  *     pointers are ordinary CPU memory.  The library never allocates device
  *     memory: weights, KV pools, activations and the workspace all belong to
  *     the caller.  It owns only host state (sequence tables, cost tables) plus
- *     a small pinned host staging ring and HIP events, created on first use,
+ *     a small pinned host staging ring, HIP events and one non-blocking
+ *     stream (decode attention beside a long chunk's), created on first use,
  *     and the static workspace array of slw_mixed_iteration_static, which is
  *     part of its device code (loaded with it, never allocated by a call).
  *   - Streams are passed as void* holding a hipStream_t (NULL = the null
@@ -190,8 +191,11 @@ int slw_workspace_size(slw_ctx* ctx, int32_t max_C, int32_t max_B, size_t* bytes
  * a coherent pinned staging ring that a first kernel copies into the
  * workspace, then enqueues per layer: RMSNorm, QKV GEMM
  * whose epilogue applies RoPE and appends K/V to the pages, chunk attention
- * and split decode attention, output GEMM + residual (kept in fp32 within the
- * layer), RMSNorm, gate/up GEMM with SiLU*mul, down GEMM + residual.
+ * and split decode attention (one launch; for a chunk of at least 8 M
+ * query-key pairs, decode attention on the context's own stream beside it,
+ * joined back to `stream` by an event before the merge), output GEMM +
+ * residual (kept in fp32 within the layer), RMSNorm, gate/up GEMM with
+ * SiLU*mul, down GEMM + residual.
  * Each row's K/V is written at slot(seq, pos) = bt[pos/16]*16 + pos%16 of its
  * sequence in every layer.  C == 0 and B == 0 together is a no-op.
  */
