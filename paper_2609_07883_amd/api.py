@@ -321,6 +321,7 @@ def fill_normal(dst: int, n: int, seed: int, mean: float, std: float, stream: in
 
 
 GEMM_SKINNY = 99
+GEMM_NARROW = 98
 
 
 def gemm_plan(m: int, n: int, k: int) -> dict:

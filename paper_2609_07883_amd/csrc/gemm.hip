@@ -825,6 +825,116 @@ __global__ __launch_bounds__(256) void skinny_kernel(GemmArgs g, float* __restri
     }
 }
 
+// Narrow GEMM for m <= 32 rows (decode-sized batches): a work-group of KS
+// waves owns 16 output columns (CG == 1) or a RoPE / SwiGLU pair of 16-column
+// groups 32 apart (CG == 2) and all m rows; each wave takes K / KS of the k
+// range, so every weight byte is read once, and the waves' sums are added in
+// LDS before the fused epilogue: no split of k across work-groups, no second
+// kernel.  16 x 16 x 32 MFMAs with the weights as the A operand: a 64-lane
+// operand load reads 64 contiguous bytes of each of 16 weight rows (16 cache
+// lines, against 32 for a 32-row operand).  Four k slices of 32 are kept in
+// flight per wave in a ring of registers.
+constexpr int kNarrowMaxWaves = 8;
+template <int T, int CG, int EPI>
+__global__ __launch_bounds__(64 * kNarrowMaxWaves) void narrow_kernel(GemmArgs g, int ks_count) {
+    constexpr int R = 4;  // slices in flight
+    __shared__ f32x4 red[kNarrowMaxWaves][CG * T][64];
+    const int lane = threadIdx.x & 63, ks = threadIdx.x >> 6;
+    const int j = lane & 15, grp = lane >> 4;
+    // first column of each group: CG == 2 takes 16 columns of a 64-column
+    // tile and their partners 32 further on
+    int col0[CG];
+    if constexpr (CG == 2) {
+        const int tile64 = (blockIdx.x >> 1) * 64, half = (blockIdx.x & 1) * 16;
+        col0[0] = tile64 + half;
+        col0[1] = tile64 + 32 + half;
+    } else {
+        col0[0] = blockIdx.x * 16;
+    }
+    const int k_wave = g.k / ks_count;
+    const int kbeg = ks * k_wave + 8 * grp;
+    const int nslice = k_wave / 32;
+    const bf16* W = static_cast<const bf16*>(g.w);
+    const bf16* A = static_cast<const bf16*>(g.a);
+    const bf16* wp[CG];
+#pragma unroll
+    for (int c = 0; c < CG; ++c) wp[c] = W + static_cast<size_t>(w_row<EPI>(g, col0[c] + j)) * g.k + kbeg;
+    const bf16* ap[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t)  // rows past m read row m - 1; their results are never stored
+        ap[t] = A + static_cast<size_t>(min(t * 16 + j, g.m - 1)) * g.lda + kbeg;
+
+    bf16x8 wf[R][CG], af[R][T];
+    auto load = [&](int sl, int b) {
+#pragma unroll
+        for (int c = 0; c < CG; ++c) wf[b][c] = *reinterpret_cast<const bf16x8*>(wp[c] + 32 * sl);
+#pragma unroll
+        for (int t = 0; t < T; ++t) af[b][t] = *reinterpret_cast<const bf16x8*>(ap[t] + 32 * sl);
+    };
+    f32x4 acc[CG][T];
+#pragma unroll
+    for (int c = 0; c < CG; ++c)
+#pragma unroll
+        for (int t = 0; t < T; ++t) acc[c][t] = f32x4{};
+#pragma unroll
+    for (int b = 0; b < R; ++b)
+        if (b < nslice) load(b, b);
+    for (int s0 = 0; s0 < nslice; s0 += R) {
+#pragma unroll
+        for (int b = 0; b < R; ++b) {
+            if (s0 + b < nslice) {
+#pragma unroll
+                for (int c = 0; c < CG; ++c)
+#pragma unroll
+                    for (int t = 0; t < T; ++t) acc[c][t] = mfma16(wf[b][c], af[b][t], acc[c][t]);
+                if (s0 + b + R < nslice) load(s0 + b + R, b);
+            }
+        }
+    }
+
+    // Sum over the waves; wave t then stores token group t.
+#pragma unroll
+    for (int c = 0; c < CG; ++c)
+#pragma unroll
+        for (int t = 0; t < T; ++t) red[ks][c * T + t][lane] = acc[c][t];
+    __syncthreads();
+    if (ks >= T) return;
+    const int t = ks;
+    f32x4 v[CG];
+#pragma unroll
+    for (int c = 0; c < CG; ++c) {
+        v[c] = red[0][c * T + t][lane];
+        for (int w = 1; w < ks_count; ++w) v[c] += red[w][c * T + t][lane];
+    }
+    const int row = t * 16 + j;
+    if (row >= g.m) return;
+    // element e of a lane: column col0[c] + 4 grp + e of row `row`
+    if constexpr (EPI == EPI_QKV) {
+        const int tile64 = col0[0] - (blockIdx.x & 1) * 16;
+        const int hg = tile64 / g.hd, d0 = ((tile64 % g.hd) / 64) * 32 + (col0[0] - tile64) + 4 * grp;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qkv_store(g, row, hg, d0 + e, v[0][e], v[CG - 1][e]);
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        const int tile64 = col0[0] - (blockIdx.x & 1) * 16;
+        bf16* out = static_cast<bf16*>(g.out) + static_cast<size_t>(row) * g.ldo + (tile64 >> 1) +
+                    (col0[0] - tile64) + 4 * grp;
+        bf16x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = f2bf(silu(v[0][e]) * v[CG - 1][e]);
+        *reinterpret_cast<bf16x4*>(out) = o;
+    } else {
+        const size_t o = static_cast<size_t>(row) * g.ldo + col0[0] + 4 * grp;
+        if constexpr (EPI == EPI_RESID_F32OUT) {
+            const bf16x4 rb = *reinterpret_cast<const bf16x4*>(static_cast<const bf16*>(g.resid) + o);
+            *reinterpret_cast<f32x4*>(static_cast<float*>(g.out) + o) =
+                v[0] + f32x4{bf2f(rb[0]), bf2f(rb[1]), bf2f(rb[2]), bf2f(rb[3])};
+        } else {
+            const f32x4 r = *reinterpret_cast<const f32x4*>(static_cast<const float*>(g.resid) + o) + v[0];
+            *reinterpret_cast<bf16x4*>(static_cast<bf16*>(g.out) + o) = bf16x4{f2bf(r[0]), f2bf(r[1]), f2bf(r[2]), f2bf(r[3])};
+        }
+    }
+}
+
 struct TileCfg {
     int bm, bn, waves_m, waves_n, bk, ring;  // ring 0: register-staged double buffer
 };
@@ -906,6 +1016,21 @@ void launch_skinny(const GemmArgs& g, const GemmPlan& p, void* partial, hipStrea
     }
 }
 
+template <int T, int CG, int EPI>
+void launch_narrow_epi(const GemmArgs& g, const GemmPlan& p, hipStream_t s) {
+    narrow_kernel<T, CG, EPI><<<g.n / (16 * CG), 64 * p.ks, 0, s>>>(g, p.ks);
+}
+
+template <int T>
+void launch_narrow(const GemmArgs& g, const GemmPlan& p, hipStream_t s) {
+    switch (g.epi) {
+        case EPI_RESID_F32OUT: launch_narrow_epi<T, 1, EPI_RESID_F32OUT>(g, p, s); break;
+        case EPI_RESID_F32IN: launch_narrow_epi<T, 1, EPI_RESID_F32IN>(g, p, s); break;
+        case EPI_SWIGLU: launch_narrow_epi<T, 2, EPI_SWIGLU>(g, p, s); break;
+        default: launch_narrow_epi<T, 2, EPI_QKV>(g, p, s); break;
+    }
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, int BK, int ST>
 void launch_cfg(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     float* part = static_cast<float*>(partial);
@@ -954,12 +1079,19 @@ const Band& band_of(const Band (&t)[N], int m) {
     return t[N - 1];
 }
 
-// The weight-streaming kernel takes the narrower projections up to 32 rows
-// and gate/up up to 16 (it won there by 10-20%; on qkv the tile kernels
-// measured faster).  Shapes outside the 8B layer take the band of their
-// projection class; n must be a multiple of 128 and k of 64.
+// The narrow kernel takes qkv, the output and the down projection up to 8
+// rows and the output projection up to 16 (8B layer, against the kernels
+// below: output -34% at 1 row, -18% at 16; down -22% at 1 row, -13% at 8;
+// qkv -12% at 1 row; it loses on gate/up and beyond those row counts, where
+// every work-group re-reads all the activation rows).  The weight-streaming
+// kernel takes the other narrow projections up to 32 rows and gate/up up to
+// 16 (it won there by 10-20%; on qkv the tile kernels measured faster).
+// Shapes outside the 8B layer take the band of their projection class; n must
+// be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     const bool wide = n >= 16384, qkv_like = n >= 6144 && !wide;
+    if (n % 64 == 0 && k % 32 == 0 && !wide && (m <= 8 || (m <= 16 && !qkv_like && k < 8192)))
+        return plan_with_cfg(kNarrowCfg, m, n, k);
     if (n % 64 == 0 && (wide ? m <= 16 : m <= 32 && !qkv_like)) return plan_with_cfg(kSkinnyCfg, m, n, k);
     const Band& b = k >= 8192 ? band_of(kBandsDown, m)
                     : wide    ? band_of(kBandsGateUp, m)
@@ -978,6 +1110,16 @@ GemmPlan plan_gemm(int m, int n, int k) {
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
     GemmPlan p{};
     p.cfg = cfg;
+    if (cfg == kNarrowCfg) {
+        // waves per work-group: each takes a whole number of 32-wide k slices
+        int ks = 8;
+        while (ks > 1 && k % (32 * ks)) ks /= 2;
+        p.ks = ks;
+        p.bm = m <= 16 ? 16 : 32;
+        p.bn = 16;
+        p.splits = 1;
+        return p;
+    }
     if (cfg == kSkinnyCfg) {
         // Four waves slice k inside a work-group (fewer when k is short); k is
         // also split across work-groups until there are 384 of them (three
@@ -1007,7 +1149,7 @@ GemmPlan plan_with_cfg(int cfg, int m, int n, int k) {
 
 GemmPlan plan_stream_k(int cfg, int m, int n, int k) {
     GemmPlan p = plan_with_cfg(cfg, m, n, k);
-    if (cfg == kSkinnyCfg) return p;
+    if (cfg == kSkinnyCfg || cfg == kNarrowCfg) return p;
     const TileCfg& t = kCfgs[cfg];
     // work-groups a CU holds at once: one for eight waves or more than 80 KB of LDS
     const int lds = (t.ring == 0 ? 2 : t.ring) * (t.bm + t.bn) * t.bk * 2;
@@ -1026,6 +1168,8 @@ GemmPlan plan_stream_k(int cfg, int m, int n, int k) {
 }
 
 bool gemm_shape_ok(const GemmPlan& p, int n, int k) {
+    if (p.cfg == kNarrowCfg)  // m <= 32 is the caller's part; paired epilogues need 64-column tiles
+        return n % 64 == 0 && p.ks >= 1 && p.ks <= 8 && k % (32 * p.ks) == 0;
     if (p.cfg == kSkinnyCfg)  // m <= 32 is the caller's part (plan_gemm)
         return n % 64 == 0 && p.ks >= 1 && p.ks <= 4 && k % (64 * p.ks * p.splits) == 0;
     return p.cfg >= 0 && p.cfg < kNumCfgs && n % p.bn == 0 && k % (p.splits * BK_MAX) == 0;
@@ -1033,6 +1177,11 @@ bool gemm_shape_ok(const GemmPlan& p, int n, int k) {
 
 void launch_gemm(const GemmArgs& g, const GemmPlan& p, void* partial, hipStream_t s) {
     if (g.m <= 0) return;
+    if (p.cfg == kNarrowCfg) {  // plans cover m <= 32
+        if (g.m <= 16) launch_narrow<1>(g, p, s);
+        else launch_narrow<2>(g, p, s);
+        return;
+    }
     if (p.cfg == kSkinnyCfg) {
         launch_skinny<1>(g, p, partial, s);  // plans cover m <= 32
         return;

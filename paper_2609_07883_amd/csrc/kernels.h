@@ -47,6 +47,7 @@ struct GemmPlan {
 // CUs the stream-K schedule spreads its last round over (MI355X).
 constexpr int kStreamKCus = 256;
 constexpr int kSkinnyCfg = 99;
+constexpr int kNarrowCfg = 98;  // the narrow kernel (m <= 32, k split inside the work-group)
 GemmPlan plan_gemm(int m, int n, int k);
 // The plan for a given tile configuration (split-K chosen by tile count).
 GemmPlan plan_with_cfg(int cfg, int m, int n, int k);

@@ -118,6 +118,17 @@ def test_single_decode():
     _run(0, 0, [1500], seed=17)
 
 
+@pytest.mark.parametrize("B", [5, 8, 9, 16])
+def test_small_decode_batches(B):
+    """Decode-only batches at the narrow kernel's row limits: qkv, output and
+    down projections on it up to 8 rows, the output projection up to 16
+    (one 16-row token group, the last rows of it padding at 5 and 9)."""
+    ctx = synth.lognormal_lengths(B, 700, 0.8, 8192, seed=20 + B)
+    cfgs = [api.gemm_plan(B, n, k)["cfg"] for n, k in ((6144, 4096), (4096, 4096), (4096, 14336))]
+    assert api.GEMM_NARROW in cfgs
+    _run(0, 0, ctx, seed=30 + B)
+
+
 @functools.lru_cache(maxsize=None)
 def _plan_cover():
     """Row counts that together reach every GEMM variant (tile configuration,
