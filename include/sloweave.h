@@ -388,7 +388,7 @@ int slw_fill_normal(void* dst, size_t n, uint64_t seed, float mean, float std, v
  * (host only, touches no GPU), for callers and tests that need to know which
  * kernel variant a row count reaches.  out[0..5]: tile configuration (99:
  * the weight-streaming kernel for m <= 32; 98: the narrow kernel for
- * m <= 16, k split over the waves of a work-group), tile rows BM, tile columns BN,
+ * m <= 24, k split over the waves of a work-group), tile rows BM, tile columns BN,
  * k split factor (1: none), stream-K work-groups (0: not used), whole tiles
  * run before them.  m >= 1; n a multiple of 128 and k of 64, else SLW_EINVAL.
  */

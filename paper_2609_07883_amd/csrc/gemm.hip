@@ -1080,17 +1080,19 @@ const Band& band_of(const Band (&t)[N], int m) {
 }
 
 // The narrow kernel takes qkv, the output and the down projection up to 8
-// rows and the output projection up to 16 (8B layer, against the kernels
-// below: output -34% at 1 row, -18% at 16; down -22% at 1 row, -13% at 8;
-// qkv -12% at 1 row; it loses on gate/up and beyond those row counts, where
-// every work-group re-reads all the activation rows).  The weight-streaming
+// rows and the output projection up to 24 (8B layer, against the kernels
+// below: output -34% at 1 row, -18% at 16, -7% at 24; down -22% at 1 row,
+// -13% at 8; qkv -12% at 1 row; it loses on gate/up and beyond those row
+// counts, where every work-group re-reads all the activation rows; 64-column
+// work-groups, which re-read them a quarter as often, measured 1.5-3x slower
+// for want of work-groups).  The weight-streaming
 // kernel takes the other narrow projections up to 32 rows and gate/up up to
 // 16 (it won there by 10-20%; on qkv the tile kernels measured faster).
 // Shapes outside the 8B layer take the band of their projection class; n must
 // be a multiple of 128 and k of 64.
 GemmPlan plan_gemm(int m, int n, int k) {
     const bool wide = n >= 16384, qkv_like = n >= 6144 && !wide;
-    if (n % 64 == 0 && k % 32 == 0 && !wide && (m <= 8 || (m <= 16 && !qkv_like && k < 8192)))
+    if (n % 64 == 0 && k % 32 == 0 && !wide && (m <= 8 || (m <= 24 && !qkv_like && k < 8192)))
         return plan_with_cfg(kNarrowCfg, m, n, k);
     if (n % 64 == 0 && (wide ? m <= 16 : m <= 32 && !qkv_like)) return plan_with_cfg(kSkinnyCfg, m, n, k);
     const Band& b = k >= 8192 ? band_of(kBandsDown, m)

@@ -118,11 +118,12 @@ def test_single_decode():
     _run(0, 0, [1500], seed=17)
 
 
-@pytest.mark.parametrize("B", [5, 8, 9, 16])
+@pytest.mark.parametrize("B", [5, 8, 9, 16, 24])
 def test_small_decode_batches(B):
     """Decode-only batches at the narrow kernel's row limits: qkv, output and
-    down projections on it up to 8 rows, the output projection up to 16
-    (one 16-row token group, the last rows of it padding at 5 and 9)."""
+    down projections on it up to 8 rows, the output projection up to 24
+    (one 16-row token group up to 16 rows, two beyond; the last rows of a
+    group padding at 5, 9 and 24)."""
     ctx = synth.lognormal_lengths(B, 700, 0.8, 8192, seed=20 + B)
     cfgs = [api.gemm_plan(B, n, k)["cfg"] for n, k in ((6144, 4096), (4096, 4096), (4096, 14336))]
     assert api.GEMM_NARROW in cfgs

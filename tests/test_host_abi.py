@@ -291,7 +291,7 @@ def test_gemm_plan_is_valid_for_every_row_count(shape):
     """The planner's choice for every row count is a launchable plan: tile
     widths divide n, the k split divides k into whole 64-deep steps, stream-K
     only with whole tiles counted in rounds of 8 XCDs, the weight-streaming
-    kernel only up to 32 rows, the narrow kernel only up to 16 with k split
+    kernel only up to 32 rows, the narrow kernel only up to 24 with k split
     into whole 32-wide slices over at most eight waves."""
     sh = synth.LLAMA8B_LAYER if shape == "8b" else synth.TINY
     d, F = sh.d_model, sh.ffn_dim
@@ -306,7 +306,7 @@ def test_gemm_plan_is_valid_for_every_row_count(shape):
                 assert m <= 32
                 continue
             if p["cfg"] == api.GEMM_NARROW:
-                assert m <= 16 and n % 64 == 0 and k % 32 == 0 and p["bn"] == 16 and p["splits"] == 1
+                assert m <= 24 and n % 64 == 0 and k % 32 == 0 and p["bn"] == 16 and p["splits"] == 1
                 seen.add(p["cfg"])
                 continue
             assert n % p["bn"] == 0 and p["bm"] % 32 == 0
