@@ -1,19 +1,22 @@
 """GPU parity of the mixed iteration for the other attention shapes the
 kernels take: grouped-query attention with 2, 8 and 16 query heads per KV
-head (head dim 64) and MHA at head dim 128, every row against the float64
-oracle, slots and block tables bit-exact.
+head at head dims 64 and 128, and MHA at head dim 128 (the 8B layer's
+group of 4 and MHA at head dim 64 are covered elsewhere), every row against
+the float64 oracle, slots and block tables bit-exact.
 
 Each shape runs a chunk of 150 rows after a 100-token prefix beside three
 decodes (contexts 0, 37 and 1500, the last split over several
 work-groups), then a 300-row chunk of a fresh prompt beside the same
 decodes one token later (several query tiles), and a decode-only iteration.
 
-The q and k weights are scaled with 1/sqrt(d_model) (0.16 at d_model 256)
-so that every shape sees the same spread of attention scores: a fixed scale
-makes the scores grow with d_model, and near-hard attention turns the bf16
-rounding of q and k into output errors of the size of the bar itself (an
-exact CPU emulation of bf16 storage reaches 3.3e-2 elementwise at
-d_model 1024 with the scale left at 0.16).
+The q and k weights are scaled with 1/sqrt(d_model) and (64/head_dim)^(1/4)
+(0.16 at d_model 256, head dim 64) so that every shape sees the same spread
+of attention scores: a fixed scale makes the scores grow with d_model (and
+with sqrt(head_dim) after the 1/sqrt(head_dim) scaling), and near-hard
+attention turns the bf16 rounding of q and k into output errors of the size
+of the bar itself (an exact CPU emulation of bf16 storage reaches 3.3e-2
+elementwise at d_model 1024 with the scale left at 0.16; with these scales
+its floor stays at or below 2e-2 for every shape here).
 """
 import pytest
 
@@ -34,6 +37,12 @@ SHAPES = {
                              rms_eps=1e-5, rope_theta=10000.0, max_pos=4096),
     "mha_hd128": ModelShape(n_layers=1, d_model=256, n_q_heads=2, n_kv_heads=2, head_dim=128, ffn_dim=512,
                             rms_eps=1e-5, rope_theta=10000.0, max_pos=4096),
+    "gqa2_hd128": ModelShape(n_layers=1, d_model=512, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn_dim=512,
+                             rms_eps=1e-5, rope_theta=10000.0, max_pos=4096),
+    "gqa8_hd128": ModelShape(n_layers=1, d_model=1024, n_q_heads=8, n_kv_heads=1, head_dim=128, ffn_dim=768,
+                             rms_eps=1e-5, rope_theta=10000.0, max_pos=4096),
+    "gqa16_hd128": ModelShape(n_layers=1, d_model=2048, n_q_heads=16, n_kv_heads=1, head_dim=128, ffn_dim=1024,
+                              rms_eps=1e-5, rope_theta=10000.0, max_pos=4096),
 }
 
 
@@ -43,7 +52,8 @@ def test_attention_shapes(name):
         pytest.skip("no GPU")
     from paper_2609_07883_amd.runtime import Session
     shape = SHAPES[name]
-    sess = Session(shape, num_blocks=256, max_c=300, max_b=3, qk_std=0.16 * (256 / shape.d_model) ** 0.5)
+    qk_std = 0.16 * (256 / shape.d_model) ** 0.5 * (64 / shape.head_dim) ** 0.25
+    sess = Session(shape, num_blocks=256, max_c=300, max_b=3, qk_std=qk_std)
     mir = Mirror(sess, seed=7)
     dec, ctx = [21, 22, 23], [0, 37, 1500]
     for sid, L in zip(dec, ctx):

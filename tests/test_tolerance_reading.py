@@ -130,7 +130,9 @@ def test_elementwise_floor_grows_with_the_score_spread():
     bf16 rounding of the normed rows and of q/k alone moves the output past
     ELEMENTWISE_TOL; at the scale 0.16 sqrt(256 / d_model) (the spread of the
     d_model-256 cases) the same pipeline stays far inside it.  GPU cases of
-    other widths scale their q/k weights that way."""
+    other widths scale their q/k weights that way, and those at head dim 128
+    also by (64 / head_dim)^(1/4), since the scores grow with sqrt(head_dim)
+    after the 1/sqrt(head_dim) scaling."""
     from tests.test_gpu_gqa import SHAPES
     s = SHAPES["gqa16_hd64"]
     sh = oracle_shape(s)
