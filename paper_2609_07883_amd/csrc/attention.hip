@@ -133,7 +133,9 @@ __device__ __forceinline__ void decode_attn_wave(const DecodeAttnArgs& a, int sl
 // that part takes slot v % n_slots of kv head v / n_slots).  They start as
 // chunk work-groups leave CUs free, so the decodes fill the chunk part's
 // tail and any CUs a short chunk leaves idle, with no second stream to fork
-// and join.  Decode waves need no barrier; the chunk part's barriers see all
+// and join.  The decode wave's index is read as wave-uniform, so that its
+// work list and block-table entries come through the scalar cache as in the
+// decode kernel.  Decode waves need no barrier; the chunk part's barriers see all
 // eight waves of its work-groups, which come first in the grid, so the
 // hardware's round-robin over the XCDs sees them in order.  (The chunk code
 // stays in the kernel itself: compiled as a separate function and inlined,
@@ -143,7 +145,8 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
     if constexpr (DECODE) {
         const int n_chunk = a.n_slots * a.hkv;
         if (static_cast<int>(blockIdx.x) >= n_chunk) {
-            const int v = (static_cast<int>(blockIdx.x) - n_chunk) * 8 + static_cast<int>(threadIdx.x >> 6);
+            const int v = (static_cast<int>(blockIdx.x) - n_chunk) * 8 +
+                          __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
             if (v < da.n_slots * da.hkv) decode_attn_wave<HD>(da, v % da.n_slots, v / da.n_slots, threadIdx.x & 63);
             return;
         }
@@ -162,7 +165,11 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
     __shared__ __attribute__((aligned(16))) bf16 Ks[ST][4 * PAGE];
     __shared__ __attribute__((aligned(16))) bf16 Vs[ST][4 * PAGE];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // The wave index goes through readfirstlane so that the compiler knows it
+    // is wave-uniform: the per-wave tests of the tile loop (live rows, masked
+    // tile) then become scalar branches, where a per-lane reading put every
+    // score of every tile under an exec-mask branch of its own.
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = lane >> 4, col = lane & 15;
     // Work order: kv-head major, the runs of one head in key order.  All
     // runs of a head read that head's keys and values, and runs that start
@@ -302,7 +309,19 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                         for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
                     }
                 }
-                const bool need_mask = key0 + 63 > wave_qpos_lo || key0 + 63 >= ke;
+                // Only tiles that reach the wave's diagonal or the range end
+                // are masked: one wave-uniform branch around the whole mask.
+                if (key0 + 63 > wave_qpos_lo || key0 + 63 >= ke) {
+#pragma unroll
+                    for (int p = 0; p < 4; ++p)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int kpos = key0 + 32 * (p >> 1) + pair_key(4 * grp + e, p & 1);
+#pragma unroll
+                            for (int ct = 0; ct < CT; ++ct)
+                                sc[p][ct][e] = (kpos <= qpos_col[ct] && kpos < ke) ? sc[p][ct][e] : -INFINITY;
+                        }
+                }
                 float mx[CT];
                 bool grow = false;
 #pragma unroll
@@ -311,15 +330,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
 #pragma unroll
                     for (int p = 0; p < 4; ++p)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            float x = sc[p][ct][e];
-                            if (need_mask) {
-                                const int kpos = key0 + 32 * (p >> 1) + pair_key(4 * grp + e, p & 1);
-                                x = (kpos <= qpos_col[ct] && kpos < ke) ? x : -INFINITY;
-                                sc[p][ct][e] = x;
-                            }
-                            m = fmaxf(m, x);
-                        }
+                        for (int e = 0; e < 4; ++e) m = fmaxf(m, sc[p][ct][e]);
                     m = rows4_max(m);
                     mx[ct] = m * sl2;
                     grow |= mx[ct] > m_run[ct] + kSlack;
