@@ -78,7 +78,11 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // global->LDS loads issued ST - 1 tiles ahead (each lane fetches the 16-byte
 // chunk that belongs at its swizzled LDS slot; every wave issues the same
 // number of loads per tile, so a counted wait for its own loads plus a bare
-// barrier publishes a tile).  A work item covers one key range of one query
+// barrier publishes a tile).  Within a tile the LDS reads run one step ahead
+// of the MFMAs: the next score tile's K fragments and the next group's V
+// fragments are read while the current ones are multiplied.  On an item's
+// last tile the V values of keys past the range end are zeroed in LDS once,
+// so the P V loop carries no masking.  A work item covers one key range of one query
 // tile, and a work-group runs the items its slot lists one after the other
 // (the host gives each work-group whole query tiles when they balance, and
 // otherwise cuts the keys of all query tiles into equal runs).
@@ -121,6 +125,10 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Wait until this wave's LDS operations are complete (vector memory
+// operations may stay outstanding).
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
 // Workgroup barrier with no memory fence (the memory clobber keeps the
 // compiler from moving LDS or global accesses across it).
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
@@ -156,6 +164,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
     constexpr int PER_WAVE = SLABS / 8;        // loads each wave issues per tile
     static_assert(SLABS % 8 == 0, "tile loads must split evenly over the waves");
     static_assert(ST >= 2 && ST <= 4, "ring of two to four tiles");
+    static_assert(NT % 4 == 0, "V fragments are read four at a time");
     constexpr int CT = 2;                 // 16-row column tiles per wave (32 rows)
     constexpr int PW = 32 / GROUP;        // positions per wave (eight waves: a tile of 8 PW positions)
     // Lazy rescaling: a row keeps its running max until a tile exceeds it by
@@ -292,23 +301,81 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
             barrier_only();
             if (t + ST - 1 < n_tiles) issue(t + ST - 1);
             const int key0 = kb + t * 64;
+            // The item's last tile: keys at or past ke (unwritten slots of the
+            // last page, stand-in pages) get probability 0, and their V values
+            // are zeroed here once for all waves, so that whatever the pool
+            // holds there cannot turn 0 into NaN in the P V product.
+            if (key0 + 63 >= ke) {
+                for (int r = tid; r < 4 * HD; r += 512) {  // row r: page r / HD, dim r % HD
+                    const int pg = r / HD, d = r % HD;
+#pragma unroll
+                    for (int tt = 0; tt < 16; ++tt)
+                        if (key0 + 16 * pg + tt >= ke)
+                            Vs[buf][pg * PAGE + d * 16 + vswz(d, tt >> 3) * 8 + (tt & 7)] = bf16(0.0f);
+                }
+                wait_lgkmcnt0();
+                barrier_only();
+            }
             if (wave_live && key0 <= wave_qpos_hi) {
                 f32x4 sc[4][CT];  // [2 pair + tile][ct]
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
 #pragma unroll
                     for (int ct = 0; ct < CT; ++ct) sc[p][ct] = f32x4{};
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
+                // K fragments of score tile p + 1 are read while tile p's
+                // MFMAs run (two register sets); the scheduling groups below
+                // keep that order, which the compiler otherwise undoes by
+                // reading each fragment right before its MFMAs and waiting there.
+                bf16x8 kf[2][KK];
+                auto kread = [&](int p, bf16x8(&k)[KK]) {
                     const int key = pair_key(col, p & 1), tok = key & 15;
                     const int base = (2 * (p >> 1) + (key >> 4)) * PAGE + tok * 32 + kswz(tok, grp) * 8;
 #pragma unroll
-                    for (int kk = 0; kk < KK; ++kk) {
-                        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[buf][base + kk * 512]);
+                    for (int kk = 0; kk < KK; ++kk) k[kk] = *reinterpret_cast<const bf16x8*>(&Ks[buf][base + kk * 512]);
+                };
+                kread(0, kf[0]);
 #pragma unroll
-                        for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf, qf[ct][kk], sc[p][ct]);
-                    }
+                for (int p = 0; p < 4; ++p) {
+                    if (p + 1 < 4) kread(p + 1, kf[(p + 1) & 1]);
+#pragma unroll
+                    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+                        for (int ct = 0; ct < CT; ++ct) sc[p][ct] = mfma16(kf[p & 1][kk], qf[ct][kk], sc[p][ct]);
                 }
+                // V fragments in groups of four: group g covers page pair
+                // g / (NT / 4) (k slice grp = tokens 8 (grp % 2) .. + 7 of page
+                // 2 j + grp / 2) and output dims 16 n0 .. 16 n0 + 63,
+                // n0 = 4 (g % (NT / 4)).  The first group is read during the
+                // last score tile's MFMAs, each next one during the current
+                // one's P V MFMAs.
+                constexpr int VG = 2 * NT / 4;
+                bf16x8 vf[2][4];
+                auto vread = [&](int g, bf16x8(&v)[4]) {
+                    const int j = g / (NT / 4), n0 = (g % (NT / 4)) * 4;
+                    const int v_base = (2 * j + (grp >> 1)) * PAGE;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int d = (n0 + i) * 16 + col;
+                        v[i] = *reinterpret_cast<const bf16x8*>(&Vs[buf][v_base + d * 16 + vswz(d, grp & 1) * 8]);
+                    }
+                };
+                vread(0, vf[0]);
+                __builtin_amdgcn_sched_group_barrier(0x100, KK, 0);  // 0x100: LDS reads
+#pragma unroll
+                for (int p = 0; p < 3; ++p) {  // next score tile's K reads
+#pragma unroll
+                    for (int r = 0; r < KK; ++r) {
+                        __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);  // 0x8: MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    }
+                    if constexpr (KK * CT > KK) __builtin_amdgcn_sched_group_barrier(0x8, KK * CT - KK, 0);
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {  // the last score tile: V group 0's reads
+                    __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+                if constexpr (KK * CT > 4) __builtin_amdgcn_sched_group_barrier(0x8, KK * CT - 4, 0);
                 // Only tiles that reach the wave's diagonal or the range end
                 // are masked: one wave-uniform branch around the whole mask.
                 if (key0 + 63 > wave_qpos_lo || key0 + 63 >= ke) {
@@ -368,26 +435,31 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                 // key_lim >= ke, stand-in pages past ke) have probability 0; their
                 // V values are zeroed too so that whatever the pool holds there
                 // cannot turn 0 into NaN
-                const bool v_mask = key0 + 63 >= ke;
+                bf16x8 pf[2][CT];
 #pragma unroll
-                for (int j = 0; j < 2; ++j) {
-                    bf16x8 pf[CT];
+                for (int j = 0; j < 2; ++j)
 #pragma unroll
-                    for (int ct = 0; ct < CT; ++ct) pf[ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
-                    // k slice grp = tokens 8 (grp % 2) .. + 7 of page 2 j + grp / 2
-                    const int v_base = (2 * j + (grp >> 1)) * PAGE;
-                    const int k_lo = key0 + 32 * j + 8 * grp;
+                    for (int ct = 0; ct < CT; ++ct) pf[j][ct] = to_bf16x8(sc[2 * j][ct], sc[2 * j + 1][ct]);
 #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) {
-                        const int d = nt * 16 + col;
-                        bf16x8 vf = *reinterpret_cast<const bf16x8*>(&Vs[buf][v_base + d * 16 + vswz(d, grp & 1) * 8]);
-                        if (v_mask) {
+                for (int g = 0; g < VG; ++g) {
+                    const int j = g / (NT / 4), n0 = (g % (NT / 4)) * 4;
+                    if (g + 1 < VG) vread(g + 1, vf[(g + 1) & 1]);
 #pragma unroll
-                            for (int e = 0; e < 8; ++e)
-                                if (k_lo + e >= ke) vf[e] = bf16(0.0f);
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int ct = 0; ct < CT; ++ct) o[ct][n0 + i] = mfma16(pf[j][ct], vf[g & 1][i], o[ct][n0 + i]);
+                }
+#pragma unroll
+                for (int g = 0; g < VG; ++g) {
+                    if (g + 1 < VG) {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
+                            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                         }
-#pragma unroll
-                        for (int ct = 0; ct < CT; ++ct) o[ct][nt] = mfma16(pf[ct], vf, o[ct][nt]);
+                        if constexpr (4 * CT > 4) __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT - 4, 0);
+                    } else {
+                        __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT, 0);
                     }
                 }
             }
