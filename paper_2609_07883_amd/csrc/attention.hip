@@ -431,10 +431,8 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                         }
                     l_run[ct] += ls;
                 }
-                // keys at or past ke (the range end; unwritten slots lie past
-                // key_lim >= ke, stand-in pages past ke) have probability 0; their
-                // V values are zeroed too so that whatever the pool holds there
-                // cannot turn 0 into NaN
+                // P in bf16, the A operand of the P V MFMAs (keys 8 grp .. 8 grp + 7
+                // of page pair j in lane group grp)
                 bf16x8 pf[2][CT];
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
