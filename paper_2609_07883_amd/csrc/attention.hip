@@ -82,7 +82,10 @@ __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 lo, f32x4 hi) {
 // of the MFMAs: the next score tile's K fragments and the next group's V
 // fragments are read while the current ones are multiplied.  On an item's
 // last tile the V values of keys past the range end are zeroed in LDS once,
-// so the P V loop carries no masking.  A work item covers one key range of one query
+// so the P V loop carries no masking.  The row sums of the probabilities come
+// from the matrix cores (P times a column of ones, two MFMAs per page pair),
+// so they add the same bf16 values the P V product does and take no VALU
+// additions.  A work item covers one key range of one query
 // tile, and a work-group runs the items its slot lists one after the other
 // (the host gives each work-group whole query tiles when they balance, and
 // otherwise cuts the keys of all query tiles into equal runs).
@@ -189,6 +192,9 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
     const float sl2 = kLog2e / sqrtf(static_cast<float>(HD));
     const bf16* kpool = static_cast<const bf16*>(a.k_pool);
     const bf16* vpool = static_cast<const bf16*>(a.v_pool);
+    bf16x8 ones;  // the B operand of the row-sum MFMAs
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = bf16(1.0f);
 
     // Load j of a tile (j = wave + 8 i): 0 .. 4 KK - 1 are K slabs (page j / KK,
     // dims 32 (j % KK) ..), the rest V slabs (page, 32 dims of 16 tokens).
@@ -269,12 +275,15 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
         for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) o[ct][nt] = f32x4{};
-        float m_run[CT], l_run[CT];
+        float m_run[CT];
+        // Row sums of P on the matrix cores (P times a column of ones): lane
+        // (grp, col) holds the sums of rows 4 grp .. 4 grp + 3 of column tile ct.
+        f32x4 l_acc[CT];
         int qpos_col[CT];  // query position of row ct*16 + col
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
             m_run[ct] = -INFINITY;
-            l_run[ct] = 0.f;
+            l_acc[ct] = f32x4{};
             qpos_col[ct] = wave_qpos_lo + (ct * 16 + col) / GROUP;
         }
 
@@ -407,11 +416,11 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                     for (int ct = 0; ct < CT; ++ct) {
                         const float m_new = fmaxf(m_run[ct], mx[ct]);
                         const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[ct] - m_new);
-                        l_run[ct] *= alpha;
                         m_run[ct] = m_new;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             const float ae = __shfl(alpha, grp * 4 + e, 64);
+                            l_acc[ct][e] *= ae;
 #pragma unroll
                             for (int nt = 0; nt < NT; ++nt) o[ct][nt][e] *= ae;
                         }
@@ -420,16 +429,10 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct) {
                     const float m_use = m_run[ct] == -INFINITY ? 0.f : m_run[ct];
-                    float ls = 0.f;
 #pragma unroll
                     for (int p = 0; p < 4; ++p)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float v = fast_exp2(fmaf(sc[p][ct][e], sl2, -m_use));
-                            sc[p][ct][e] = v;
-                            ls += v;
-                        }
-                    l_run[ct] += ls;
+                        for (int e = 0; e < 4; ++e) sc[p][ct][e] = fast_exp2(fmaf(sc[p][ct][e], sl2, -m_use));
                 }
                 // P in bf16, the A operand of the P V MFMAs (keys 8 grp .. 8 grp + 7
                 // of page pair j in lane group grp)
@@ -446,6 +449,10 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                     for (int i = 0; i < 4; ++i)
 #pragma unroll
                         for (int ct = 0; ct < CT; ++ct) o[ct][n0 + i] = mfma16(pf[j][ct], vf[g & 1][i], o[ct][n0 + i]);
+                    if (n0 == 0) {
+#pragma unroll
+                        for (int ct = 0; ct < CT; ++ct) l_acc[ct] = mfma16(pf[j][ct], ones, l_acc[ct]);
+                    }
                 }
 #pragma unroll
                 for (int g = 0; g < VG; ++g) {
@@ -455,9 +462,11 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                             __builtin_amdgcn_sched_group_barrier(0x8, 1, 0);
                             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                         }
-                        if constexpr (4 * CT > 4) __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT - 4, 0);
+                        if (g % (NT / 4) == 0) __builtin_amdgcn_sched_group_barrier(0x8, 5 * CT - 4, 0);
+                        else __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT - 4, 0);
                     } else {
-                        __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT, 0);
+                        if (g % (NT / 4) == 0) __builtin_amdgcn_sched_group_barrier(0x8, 5 * CT, 0);
+                        else __builtin_amdgcn_sched_group_barrier(0x8, 4 * CT, 0);
                     }
                 }
             }
@@ -470,13 +479,12 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
 
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
-            float l = l_run[ct];
-            l = rows4_sum(l);
             if (!whole) {
                 const size_t rbase = (static_cast<size_t>(item) * a.hkv + kvh) * 256 + wave * 32 + ct * 16;
-                if (grp == 0) {
-                    a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
-                    a.part_ml[(rbase + col) * 2 + 1] = l;
+                if (grp == 0) a.part_ml[(rbase + col) * 2 + 0] = m_run[ct];
+                if (col == 0) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) a.part_ml[(rbase + grp * 4 + e) * 2 + 1] = l_acc[ct][e];
                 }
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
@@ -490,7 +498,7 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
                 for (int e = 0; e < 4; ++e) {
                     const int r = ct * 16 + grp * 4 + e;
                     const int j = j0 + r / GROUP, h = kvh * GROUP + r % GROUP;
-                    const float inv = 1.0f / __shfl(l, grp * 4 + e, 64);
+                    const float inv = 1.0f / l_acc[ct][e];
                     if (j < nrows) {
 #pragma unroll
                         for (int nt = 0; nt < NT; ++nt)
