@@ -198,8 +198,9 @@ __global__ __launch_bounds__(512) void chunk_attn_kernel(ChunkAttnArgs a, Decode
 
     // Load j of a tile (j = wave + 8 i): 0 .. 4 KK - 1 are K slabs (page j / KK,
     // dims 32 (j % KK) ..), the rest V slabs (page, 32 dims of 16 tokens).
-    // Pages past the key range load the range's last page instead (finite
-    // values whose scores are masked), so every wave issues PER_WAVE loads.
+    // Pages past the key range load the range's last page instead (their
+    // scores are masked and their values zeroed in LDS on the item's last
+    // tile), so every wave issues PER_WAVE loads.
     int l_page[PER_WAVE], l_elem[PER_WAVE], l_dst[PER_WAVE];
     bool l_isv[PER_WAVE];
 #pragma unroll
