@@ -28,7 +28,64 @@ def bits_to_tensor(bits: np.ndarray, device) -> torch.Tensor:
 
 
 def tensor_to_f64(t: torch.Tensor) -> np.ndarray:
-    return t.detach().float().cpu().numpy().astype(np.float64)
+    """A bf16 (or fp32) tensor as float64 numbers: copied to the host first,
+    converted there."""
+    return t.detach().cpu().float().numpy().astype(np.float64)
+
+
+def _page_bits(page: torch.Tensor) -> np.ndarray:
+    """One pool page (bf16, any device) as a writable host uint16 array."""
+    return page.view(torch.int16).cpu().numpy().view(np.uint16).copy()
+
+
+def write_pages(k_pool: torch.Tensor, v_pool: torch.Tensor, blk: np.ndarray, tok: np.ndarray,
+                k_bits: np.ndarray, v_bits: np.ndarray) -> None:
+    """Write K/V rows into one layer's pools, page by page through host copies.
+
+    k_pool is [blocks][Hkv][hd/32][16][32], v_pool [blocks][Hkv][hd][16]
+    (bf16); row i (k_bits/v_bits uint16 [n][Hkv][hd]) goes to token tok[i] of
+    block blk[i], and rows of one block are consecutive.  A page the rows fill
+    is written whole; one they cover in part is read, updated and written
+    back, so its other tokens keep what they held.  torch only moves memory.
+    """
+    n = len(blk)
+    hkv, slabs = k_pool.shape[1], k_pool.shape[2]
+    k = np.ascontiguousarray(k_bits, dtype=np.uint16).reshape(n, hkv, slabs, 32)
+    v = np.ascontiguousarray(v_bits, dtype=np.uint16).reshape(n, hkv, slabs * 32)
+    i = 0
+    while i < n:
+        b = int(blk[i])
+        j = i + 1
+        while j < n and blk[j] == b:
+            j += 1
+        t = np.asarray(tok[i:j], dtype=np.int64)
+        if j - i == 16 and np.array_equal(np.sort(t), np.arange(16)):
+            kpage = np.empty(tuple(k_pool.shape[1:]), dtype=np.uint16)
+            vpage = np.empty(tuple(v_pool.shape[1:]), dtype=np.uint16)
+        else:
+            kpage, vpage = _page_bits(k_pool[b]), _page_bits(v_pool[b])
+        kpage[:, :, t, :] = k[i:j].transpose(1, 2, 0, 3)
+        vpage[:, :, t] = v[i:j].transpose(1, 2, 0)
+        k_pool[b].copy_(torch.from_numpy(kpage.view(np.int16)).view(torch.bfloat16))
+        v_pool[b].copy_(torch.from_numpy(vpage.view(np.int16)).view(torch.bfloat16))
+        i = j
+
+
+def read_pages(k_pool: torch.Tensor, v_pool: torch.Tensor, blk: np.ndarray, tok: np.ndarray):
+    """(K, V) uint16 [n][Hkv][hd]: the rows at token tok[i] of block blk[i] of
+    one layer's pools (layouts as in write_pages), read page by page."""
+    n = len(blk)
+    hkv, slabs = k_pool.shape[1], k_pool.shape[2]
+    k = np.empty((n, hkv, slabs * 32), dtype=np.uint16)
+    v = np.empty((n, hkv, slabs * 32), dtype=np.uint16)
+    blk = np.asarray(blk, dtype=np.int64)
+    tok = np.asarray(tok, dtype=np.int64)
+    for b in np.unique(blk):
+        sel = np.nonzero(blk == b)[0]
+        kpage, vpage = _page_bits(k_pool[int(b)]), _page_bits(v_pool[int(b)])
+        k[sel] = kpage[:, :, tok[sel], :].transpose(2, 0, 1, 3).reshape(len(sel), hkv, slabs * 32)
+        v[sel] = vpage[:, :, tok[sel]].transpose(2, 0, 1)
+    return k, v
 
 
 class Session:
@@ -117,28 +174,20 @@ class Session:
         return tensor_to_f64(t)
 
     # -- cached K/V in the pool layout ---------------------------------------------
-    def _index(self, sid: int, positions):
+    def _pages(self, sid: int, positions):
+        """(block id, token in the block) of each position of sequence sid."""
         bt = np.asarray(self.ctx.block_table(sid), dtype=np.int64)
         pos = np.asarray(positions, dtype=np.int64)
-        blk = torch.from_numpy(bt[pos // 16]).to(self.dev)
-        t = torch.from_numpy(pos % 16).to(self.dev)
-        return blk, t
+        return bt[pos // 16], pos % 16
 
     def write_kv(self, layer: int, sid: int, k_bits: np.ndarray, v_bits: np.ndarray, start: int = 0):
         """Install K/V (uint16 [n][Hkv][hd]) at positions start..start+n-1 of sequence sid."""
-        s = self.shape
-        n = k_bits.shape[0]
-        blk, t = self._index(sid, np.arange(start, start + n))
-        k = bits_to_tensor(k_bits, self.dev).view(n, s.n_kv_heads, s.head_dim // 32, 32)
-        v = bits_to_tensor(v_bits, self.dev).view(n, s.n_kv_heads, s.head_dim)
-        self.k_pool[layer].permute(0, 3, 1, 2, 4)[blk, t] = k
-        self.v_pool[layer].permute(0, 3, 1, 2)[blk, t] = v
+        blk, tok = self._pages(sid, np.arange(start, start + k_bits.shape[0]))
+        write_pages(self.k_pool[layer], self.v_pool[layer], blk, tok, k_bits, v_bits)
 
     def read_kv(self, layer: int, sid: int, positions):
         """(K, V) float64 [n][Hkv][hd] at the given positions of sequence sid."""
-        s = self.shape
         torch.cuda.synchronize(self.dev)
-        blk, t = self._index(sid, positions)
-        k = self.k_pool[layer].permute(0, 3, 1, 2, 4)[blk, t].reshape(len(positions), s.n_kv_heads, s.head_dim)
-        v = self.v_pool[layer].permute(0, 3, 1, 2)[blk, t]
-        return tensor_to_f64(k), tensor_to_f64(v)
+        blk, tok = self._pages(sid, positions)
+        k, v = read_pages(self.k_pool[layer], self.v_pool[layer], blk, tok)
+        return synth.bf16_to_f64(k), synth.bf16_to_f64(v)
